@@ -1,0 +1,349 @@
+"""Pins for the fp64 oracle, independent of the oracle's own formula.
+
+The paper prints no worked numeric example, so every pin is a closed form, an
+invariant, a reduction to a simpler published rule, or brute force:
+
+* brute force with the dense transition matrices of Sec. 3.1 (paper's dv x dk
+  orientation) and the F/G expansion of Sec. 3.3;
+* the extended WY closed form proved in Appendix A;
+* DeltaNet (alpha == 1) through an independent implementation of the paper's
+  DeltaNet chunk equations (Eqs. "inverse", "wu=akv", "delta_chunk_h/o");
+* the online-learning objective of Table 1, minimised by autograd;
+* pure decay (beta == 0), whose outputs and gradients have closed forms;
+* write exactness of the delta rule (beta == 1, unit key);
+* linearity in (v, S0), independence of heads and packed sequences,
+  split-sequence carry;
+* central finite differences for all six gradients.
+"""
+import numpy as np
+import pytest
+import torch
+
+# ---------------------------------------------------------------- helpers
+
+
+def rand_unit(rng, shape):
+    x = rng.standard_normal(shape)
+    return x / np.linalg.norm(x, axis=-1, keepdims=True)
+
+
+def rand_problem(rng, B=1, T=7, H=2, dk=3, dv=4, h0=True, beta_scale=1.0, decay=1.0):
+    q = rand_unit(rng, (B, T, H, dk))
+    k = rand_unit(rng, (B, T, H, dk))
+    v = rng.standard_normal((B, T, H, dv))
+    beta = beta_scale / (1 + np.exp(-rng.standard_normal((B, T, H))))
+    log_alpha = -decay * np.log1p(np.exp(rng.standard_normal((B, T, H)))) * 0.5
+    S0 = rng.standard_normal((B, H, dk, dv)) * 0.3 if h0 else None
+    return q, k, v, beta, log_alpha, S0
+
+
+def brute_force_paper_orientation(q, k, v, beta, log_alpha, S0):
+    """One (sequence, head), paper orientation: S' (dv x dk),
+    S'_t = S'_{t-1} (alpha_t (I - beta_t k k^T)) + beta_t v k^T,  o_t = S'_t q_t."""
+    T, dk = q.shape
+    dv = v.shape[1]
+    Sp = np.zeros((dv, dk)) if S0 is None else S0.T.copy()
+    o = np.zeros((T, dv))
+    for t in range(T):
+        M = np.exp(log_alpha[t]) * (np.eye(dk) - beta[t] * np.outer(k[t], k[t]))
+        Sp = Sp @ M + beta[t] * np.outer(v[t], k[t])
+        o[t] = Sp @ q[t]
+    return o, Sp.T
+
+
+def fg_expansion(q, k, v, beta, log_alpha, S0):
+    """S'_r = S'_0 F_r + G_r with F_r = prod_{i<=r} M_i and
+    G_r = sum_i beta_i v_i k_i^T prod_{j=i+1..r} M_j (Sec. 3.3, first display)."""
+    T, dk = q.shape
+    dv = v.shape[1]
+    Ms = [np.exp(log_alpha[t]) * (np.eye(dk) - beta[t] * np.outer(k[t], k[t])) for t in range(T)]
+    S0p = np.zeros((dv, dk)) if S0 is None else S0.T
+    outs = []
+    for r in range(T):
+        F = np.eye(dk)
+        for i in range(r + 1):
+            F = F @ Ms[i]
+        G = np.zeros((dv, dk))
+        for i in range(r + 1):
+            Pr = np.eye(dk)
+            for j in range(i + 1, r + 1):
+                Pr = Pr @ Ms[j]
+            G += beta[i] * np.outer(v[i], k[i]) @ Pr
+        outs.append(S0p @ F + G)
+    o = np.stack([outs[r] @ q[r] for r in range(T)])
+    return o, outs[-1].T
+
+
+# ---------------------------------------------------------------- brute force
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_brute_force_transition_matrices(oracle_mod, seed):
+    rng = np.random.default_rng(seed)
+    q, k, v, beta, la, S0 = rand_problem(rng, B=2, T=8, H=2, dk=4, dv=3)
+    o, ht = oracle_mod.fwd(q, k, v, beta, la, h0=S0)
+    for b in range(2):
+        for h in range(2):
+            ob, Sb = brute_force_paper_orientation(q[b, :, h], k[b, :, h], v[b, :, h],
+                                                   beta[b, :, h], la[b, :, h], S0[b, h])
+            np.testing.assert_allclose(o[b, :, h], ob, rtol=0, atol=1e-13)
+            np.testing.assert_allclose(ht[b, h], Sb, rtol=0, atol=1e-13)
+            of, Sf = fg_expansion(q[b, :, h], k[b, :, h], v[b, :, h], beta[b, :, h],
+                                  la[b, :, h], S0[b, h])
+            np.testing.assert_allclose(o[b, :, h], of, rtol=0, atol=1e-13)
+            np.testing.assert_allclose(ht[b, h], Sf, rtol=0, atol=1e-13)
+
+
+def test_extended_wy_closed_form(oracle_mod):
+    """Appendix A: with S_0 = 0, S'_t = sum_i (gamma_t/gamma_i) u_i k_i^T where
+    u_t = beta_t (v_t - sum_{i<t} (gamma_t/gamma_i) u_i k_i^T k_t)."""
+    rng = np.random.default_rng(5)
+    q, k, v, beta, la, _ = rand_problem(rng, B=1, T=9, H=1, dk=5, dv=3, h0=False)
+    o, ht = oracle_mod.fwd(q, k, v, beta, la)
+    K, V, Q, b = k[0, :, 0], v[0, :, 0], q[0, :, 0], beta[0, :, 0]
+    lg = np.cumsum(la[0, :, 0])  # log gamma_t
+    T = K.shape[0]
+    u = np.zeros((T, V.shape[1]))
+    for t in range(T):
+        acc = V[t].copy()
+        for i in range(t):
+            acc -= np.exp(lg[t] - lg[i]) * u[i] * (K[i] @ K[t])
+        u[t] = b[t] * acc
+    for t in range(T):
+        Sp = sum(np.exp(lg[t] - lg[i]) * np.outer(u[i], K[i]) for i in range(t + 1))
+        np.testing.assert_allclose(o[0, t, 0], Sp @ Q[t], rtol=0, atol=1e-13)
+    np.testing.assert_allclose(ht[0, 0], Sp.T, rtol=0, atol=1e-13)
+
+
+# ---------------------------------------------------------------- DeltaNet (alpha == 1)
+
+
+def deltanet_chunk_paper(Q, K, V, beta, C, S0p):
+    """The paper's DeltaNet chunk algorithm (paper orientation S' dv x dk):
+    T = [I + strictLower(diag(beta) K K^T)]^-1 diag(beta); W = T K; U = T V;
+    S'_{next} = S' + (U - W S'^T)^T K;  O = Q S'^T + (Q K^T * M)(U - W S'^T)."""
+    L = Q.shape[0]
+    Sp = S0p.copy()
+    O = np.zeros((L, V.shape[1]))
+    for s in range(0, L, C):
+        e = min(L, s + C)
+        Qc, Kc, Vc, bc = Q[s:e], K[s:e], V[s:e], beta[s:e]
+        n = e - s
+        Tm = np.linalg.solve(np.eye(n) + np.tril(np.diag(bc) @ Kc @ Kc.T, -1), np.diag(bc))
+        W = Tm @ Kc
+        U = Tm @ Vc
+        R = U - W @ Sp.T
+        O[s:e] = Qc @ Sp.T + np.tril(Qc @ Kc.T) @ R
+        Sp = Sp + R.T @ Kc
+    return O, Sp
+
+
+@pytest.mark.parametrize("C", [1, 3, 4])
+def test_deltanet_special_case(oracle_mod, C):
+    rng = np.random.default_rng(11)
+    q, k, v, beta, la, S0 = rand_problem(rng, B=1, T=10, H=1, dk=4, dv=5)
+    la = np.zeros_like(la)  # alpha == 1
+    o, ht = oracle_mod.fwd(q, k, v, beta, la, h0=S0)
+    O, Sp = deltanet_chunk_paper(q[0, :, 0], k[0, :, 0], v[0, :, 0], beta[0, :, 0], C,
+                                 S0[0, 0].T)
+    np.testing.assert_allclose(o[0, :, 0], O, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(ht[0, 0], Sp.T, rtol=0, atol=1e-12)
+
+
+# ---------------------------------------------------------------- online-learning view
+
+
+def test_online_learning_objective_minimiser(oracle_mod):
+    """Table 1, Gated DeltaNet row: S'_t minimises
+    ||S - alpha S'_{t-1}||_F^2 - 2 <S k, beta (v - alpha S'_{t-1} k)>.
+    The objective is 1 * ||S||^2 + linear, so its minimiser is -grad(0)/2;
+    the gradient comes from autograd on the objective as printed."""
+    rng = np.random.default_rng(3)
+    q, k, v, beta, la, S0 = rand_problem(rng, B=1, T=1, H=1, dk=4, dv=3)
+    _, ht = oracle_mod.fwd(q, k, v, beta, la, h0=S0)
+    Sprev = torch.tensor(S0[0, 0].T)  # paper orientation dv x dk
+    kt = torch.tensor(k[0, 0, 0])
+    vt = torch.tensor(v[0, 0, 0])
+    a = float(np.exp(la[0, 0, 0]))
+    b = float(beta[0, 0, 0])
+    S = torch.zeros_like(Sprev, requires_grad=True)
+    obj = ((S - a * Sprev) ** 2).sum() - 2 * torch.dot(S @ kt, b * (vt - a * Sprev @ kt))
+    (grad0,) = torch.autograd.grad(obj, S)
+    minimiser = (-grad0 / 2).numpy()
+    np.testing.assert_allclose(ht[0, 0], minimiser.T, rtol=0, atol=1e-13)
+
+
+# ---------------------------------------------------------------- special cases
+
+
+def test_pure_decay_beta_zero_forward_and_gradients(oracle_mod):
+    """beta == 0: no writes, S_t = e^{G_t} S_0 with G_t = sum_{j<=t} log alpha_j."""
+    rng = np.random.default_rng(7)
+    q, k, v, beta, la, S0 = rand_problem(rng, B=1, T=6, H=1, dk=3, dv=4)
+    beta = np.zeros_like(beta)
+    dO = rng.standard_normal(v.shape)
+    dSf = rng.standard_normal(S0.shape)
+    r = oracle_mod.bwd(q, k, v, beta, la, dO, h0=S0, dht=dSf)
+    Q, K, V, L, S, dOo, dS = (q[0, :, 0], k[0, :, 0], v[0, :, 0], la[0, :, 0], S0[0, 0],
+                              dO[0, :, 0], dSf[0, 0])
+    G = np.cumsum(L)
+    T = len(L)
+    o_ref = np.stack([np.exp(G[t]) * S.T @ Q[t] for t in range(T)])
+    np.testing.assert_allclose(r["o"][0, :, 0], o_ref, atol=1e-13, rtol=0)
+    np.testing.assert_allclose(r["ht"][0, 0], np.exp(G[-1]) * S, atol=1e-13, rtol=0)
+    # gradients
+    np.testing.assert_allclose(r["dq"][0, :, 0],
+                               np.stack([np.exp(G[t]) * S @ dOo[t] for t in range(T)]),
+                               atol=1e-13, rtol=0)
+    np.testing.assert_allclose(r["dv"], 0.0, atol=0)
+    np.testing.assert_allclose(r["dk"], 0.0, atol=0)
+    per_t = (dOo * o_ref).sum(1)
+    fin = (dSf[0, 0] * np.exp(G[-1]) * S).sum()
+    dla = np.array([per_t[j:].sum() + fin for j in range(T)])
+    np.testing.assert_allclose(r["dlog_alpha"][0, :, 0], dla, atol=1e-12, rtol=0)
+    dh0 = sum(np.exp(G[t]) * np.outer(Q[t], dOo[t]) for t in range(T)) + np.exp(G[-1]) * dS
+    np.testing.assert_allclose(r["dh0"][0, 0], dh0, atol=1e-12, rtol=0)
+    # dbeta_t = (v_t - alpha_t S_{t-1}^T k_t) . (Gt^T k_t), Gt = dL/dS_t
+    for t in range(T):
+        Gt = sum(np.exp(G[s] - G[t]) * np.outer(Q[s], dOo[s]) for s in range(t, T))
+        Gt = Gt + np.exp(G[-1] - G[t]) * dS
+        Sprev = np.exp(G[t - 1]) * S if t > 0 else S
+        ref = (V[t] - np.exp(L[t]) * Sprev.T @ K[t]) @ (Gt.T @ K[t])
+        assert abs(r["dbeta"][0, t, 0] - ref) < 1e-12
+
+
+def test_identity_when_no_write_no_decay(oracle_mod):
+    """beta == 0 and alpha == 1: the state never changes; dbeta is still nonzero."""
+    rng = np.random.default_rng(8)
+    q, k, v, beta, la, S0 = rand_problem(rng, B=1, T=5, H=2, dk=3, dv=2)
+    beta[:] = 0
+    la[:] = 0
+    dO = rng.standard_normal(v.shape)
+    r = oracle_mod.bwd(q, k, v, beta, la, dO, h0=S0)
+    np.testing.assert_array_equal(r["ht"], S0)
+    for h in range(2):
+        np.testing.assert_allclose(r["o"][0, :, h], q[0, :, h] @ S0[0, h], atol=1e-14)
+        for t in range(5):
+            dSt = sum(np.outer(q[0, s, h], dO[0, s, h]) for s in range(t, 5))
+            ref = (v[0, t, h] - S0[0, h].T @ k[0, t, h]) @ (dSt.T @ k[0, t, h])
+            assert abs(r["dbeta"][0, t, h] - ref) < 1e-12
+    assert np.abs(r["dbeta"]).max() > 1e-3
+
+
+def test_write_exactness(oracle_mod):
+    """Delta rule as online regression (Sec. 3.1): with |k_t| = 1 and beta_t = 1
+    the new state recalls exactly v_t for k_t whatever alpha_t is; in general
+    S_t^T k_t = (1 - beta_t) alpha_t S_{t-1}^T k_t + beta_t v_t."""
+    rng = np.random.default_rng(9)
+    q, k, v, beta, la, S0 = rand_problem(rng, B=1, T=6, H=1, dk=5, dv=3)
+    _, h_prev = oracle_mod.fwd(q[:, :5], k[:, :5], v[:, :5], beta[:, :5], la[:, :5], h0=S0)
+    _, h_all = oracle_mod.fwd(q, k, v, beta, la, h0=S0)
+    kt, vt, bt, at = k[0, 5, 0], v[0, 5, 0], beta[0, 5, 0], np.exp(la[0, 5, 0])
+    np.testing.assert_allclose(h_all[0, 0].T @ kt,
+                               (1 - bt) * at * h_prev[0, 0].T @ kt + bt * vt, atol=1e-13)
+    beta1 = beta.copy()
+    beta1[0, 5, 0] = 1.0
+    _, h1 = oracle_mod.fwd(q, k, v, beta1, la, h0=S0)
+    np.testing.assert_allclose(h1[0, 0].T @ kt, vt, atol=1e-13)
+
+
+# ---------------------------------------------------------------- structure
+
+
+def test_linearity_in_v_and_state(oracle_mod):
+    rng = np.random.default_rng(12)
+    q, k, v1, beta, la, S1 = rand_problem(rng, B=1, T=9, H=2, dk=4, dv=3)
+    v2 = rng.standard_normal(v1.shape)
+    S2 = rng.standard_normal(S1.shape)
+    c = -0.7
+    o1, h1 = oracle_mod.fwd(q, k, v1, beta, la, h0=S1)
+    o2, h2 = oracle_mod.fwd(q, k, v2, beta, la, h0=S2)
+    o3, h3 = oracle_mod.fwd(q, k, v1 + c * v2, beta, la, h0=S1 + c * S2)
+    np.testing.assert_allclose(o3, o1 + c * o2, atol=1e-13)
+    np.testing.assert_allclose(h3, h1 + c * h2, atol=1e-13)
+
+
+def test_packed_equals_separate_and_heads_independent(oracle_mod):
+    rng = np.random.default_rng(13)
+    lens = [5, 0, 1, 9, 3]
+    Tt = sum(lens)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    q, k, v, beta, la, _ = rand_problem(rng, B=1, T=Tt, H=2, dk=3, dv=4, h0=False)
+    S0 = rng.standard_normal((len(lens), 2, 3, 4))
+    o, ht = oracle_mod.fwd(q, k, v, beta, la, h0=S0, cu_seqlens=cu)
+    for n, L in enumerate(lens):
+        s = cu[n]
+        if L == 0:
+            np.testing.assert_array_equal(ht[n], S0[n])
+            continue
+        for h in range(2):
+            sl = slice(s, s + L)
+            on, hn = oracle_mod.fwd(q[:, sl, h:h + 1], k[:, sl, h:h + 1], v[:, sl, h:h + 1],
+                                    beta[:, sl, h:h + 1], la[:, sl, h:h + 1],
+                                    h0=S0[n:n + 1, h:h + 1])
+            np.testing.assert_array_equal(o[s:s + L, h], on[0, :, 0])
+            np.testing.assert_array_equal(ht[n, h], hn[0, 0])
+
+
+def test_split_sequence_carry(oracle_mod):
+    rng = np.random.default_rng(14)
+    q, k, v, beta, la, S0 = rand_problem(rng, B=2, T=11, H=2, dk=3, dv=4)
+    o, ht = oracle_mod.fwd(q, k, v, beta, la, h0=S0)
+    oa, ha = oracle_mod.fwd(q[:, :4], k[:, :4], v[:, :4], beta[:, :4], la[:, :4], h0=S0)
+    ob, hb = oracle_mod.fwd(q[:, 4:], k[:, 4:], v[:, 4:], beta[:, 4:], la[:, 4:], h0=ha)
+    np.testing.assert_array_equal(np.concatenate([oa, ob], 1), o)
+    np.testing.assert_array_equal(hb, ht)
+
+
+def test_thread_count_does_not_change_results(oracle_mod):
+    rng = np.random.default_rng(15)
+    q, k, v, beta, la, S0 = rand_problem(rng, B=3, T=20, H=3, dk=4, dv=5)
+    dO = rng.standard_normal(v.shape)
+    r1 = oracle_mod.bwd(q, k, v, beta, la, dO, h0=S0, nthreads=1, seg=3)
+    r8 = oracle_mod.bwd(q, k, v, beta, la, dO, h0=S0, nthreads=8, seg=64)
+    for name in r1:
+        np.testing.assert_array_equal(r1[name], r8[name])
+
+
+def test_backward_forward_outputs_match_forward(oracle_mod):
+    rng = np.random.default_rng(16)
+    q, k, v, beta, la, S0 = rand_problem(rng, B=1, T=13, H=2, dk=4, dv=3)
+    dO = rng.standard_normal(v.shape)
+    o, ht = oracle_mod.fwd(q, k, v, beta, la, h0=S0)
+    r = oracle_mod.bwd(q, k, v, beta, la, dO, h0=S0, seg=4)
+    np.testing.assert_array_equal(r["o"], o)
+    np.testing.assert_array_equal(r["ht"], ht)
+
+
+# ---------------------------------------------------------------- finite differences
+
+
+@pytest.mark.parametrize("seed,beta_scale", [(21, 1.0), (22, 2.0)])
+def test_gradients_by_central_differences(oracle_mod, seed, beta_scale):
+    """Directional derivatives of L = <dO, o> + <dS_final, S_T> against the
+    oracle's VJP, for all six gradient tensors; beta in (0,2) too (no clamping)."""
+    rng = np.random.default_rng(seed)
+    q, k, v, beta, la, S0 = rand_problem(rng, B=2, T=7, H=2, dk=3, dv=4,
+                                         beta_scale=beta_scale)
+    dO = rng.standard_normal(v.shape)
+    dSf = rng.standard_normal(S0.shape)
+    r = oracle_mod.bwd(q, k, v, beta, la, dO, h0=S0, dht=dSf, seg=3)
+    base = dict(q=q, k=k, v=v, beta=beta, log_alpha=la, h0=S0)
+    grads = dict(q="dq", k="dk", v="dv", beta="dbeta", log_alpha="dlog_alpha", h0="dh0")
+
+    def loss(args):
+        o, ht = oracle_mod.fwd(args["q"], args["k"], args["v"], args["beta"],
+                               args["log_alpha"], h0=args["h0"])
+        return (o * dO).sum() + (ht * dSf).sum()
+
+    h = 1e-6
+    for name, gname in grads.items():
+        for trial in range(2):
+            d = rng.standard_normal(base[name].shape)
+            plus = dict(base)
+            minus = dict(base)
+            plus[name] = base[name] + h * d
+            minus[name] = base[name] - h * d
+            fd = (loss(plus) - loss(minus)) / (2 * h)
+            an = (r[gname] * d).sum()
+            assert abs(fd - an) <= 1e-7 * max(1.0, abs(an)), (name, fd, an)
