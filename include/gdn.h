@@ -1,0 +1,116 @@
+/*
+ * gdn.h - C ABI of the MI355X (gfx950) chunkwise gated delta rule.
+ *
+ * The operation (Gated DeltaNet, Sec. 3.1, Eq. "gated_delta_rule"): for each
+ * sequence and head, with the state stored as a dk x dv matrix S (the
+ * transpose of the paper's dv x dk state),
+ *
+ *     S_t = alpha_t (I - beta_t k_t k_t^T) S_{t-1} + beta_t k_t v_t^T,
+ *     o_t = S_t^T q_t,              alpha_t = exp(log_alpha_t),
+ *
+ * evaluated chunk by chunk (64 tokens) through the gate-decayed UT transform
+ * of Sec. 3.3 ("Hardware-efficient chunkwise training").  No query scale is
+ * applied (the paper's o_t = S_t q_t has none).  The backward returns the
+ * exact gradients of  L = sum_t <dO_t, o_t> + <dS_final, S_final>  with
+ * respect to q, k, v, beta, log_alpha and the initial state (the paper gives
+ * no backward; the gradient of the forward map is unique).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - All tensor pointers are DEVICE pointers, contiguous, innermost dim last:
+ *      q, k, dq, dk        [B, T, H, dk]   (dtype of the problem)
+ *      v, o, dO, dv        [B, T, H, dv]   (dtype of the problem)
+ *      beta, log_alpha,
+ *      dbeta, dlog_alpha   [B, T, H]       float32 always
+ *      h0, ht, dht, dh0    [Nseq, H, dk, dv] float32 always
+ *    Packed variable-length input: B == 1, T = total tokens, and
+ *    cu_seqlens[0..num_seqs] (int32, 0 = cu[0] <= ... <= cu[num_seqs] = T)
+ *    delimit the sequences; the state restarts at every sequence start
+ *    (h0[n] or zero) and chunks restart there too.  Dense input: Nseq = B.
+ *  - Value preconditions (not checked on the device): log_alpha <= 0
+ *    (alpha in (0, 1]); beta finite (nominally (0, 1); (0, 2) also works,
+ *    nothing is clamped); q and k are already L2-normalised if the caller
+ *    wants the paper's block semantics (the library does not normalise).
+ *  - Pointers must be 16-byte aligned.
+ *  - The library never allocates, frees or synchronises and keeps no state
+ *    between calls: the caller owns every buffer, including the workspace,
+ *    whose size the *_workspace_size queries return.  All work is enqueued on
+ *    `stream` (a hipStream_t; NULL = the default stream); outputs are valid
+ *    when the stream reaches them.  Calls on different streams with distinct
+ *    workspaces are independent.
+ *  - Every argument check runs on the host before the first launch; a failed
+ *    check returns its status and launches nothing.  A launch failure returns
+ *    GDN_ERR_HIP.  No C++ exception crosses this boundary.
+ *  - Supported head dims: (dk, dv) in {(64, 64), (128, 128), (256, 512)} for
+ *    bfloat16 (fp32 accumulation), and (64, 64) for float32.
+ */
+#ifndef GDN_H_
+#define GDN_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { GDN_F32 = 0, GDN_BF16 = 1 } gdn_dtype;
+
+typedef enum {
+  GDN_OK = 0,
+  GDN_ERR_NULL = 1,        /* a required pointer is NULL                     */
+  GDN_ERR_SHAPE = 2,       /* B, T, H < 1, or packed input with B != 1      */
+  GDN_ERR_UNSUPPORTED = 3, /* (dtype, dk, dv) combination not built         */
+  GDN_ERR_CU_SEQLENS = 4,  /* cu_seqlens_host malformed, or device copy NULL */
+  GDN_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than the query      */
+  GDN_ERR_HIP = 6,         /* a kernel launch failed                         */
+  GDN_ERR_ALIGN = 7        /* a pointer is not 16-byte aligned               */
+} gdn_status;
+
+typedef struct {
+  int32_t B, T, H, dk, dv;
+  /* Packed input: number of sequences N.  Ignored for dense input. */
+  int32_t num_seqs;
+  /* Packed input: device int32[N+1], or NULL for dense input.             */
+  const int32_t *cu_seqlens;
+  /* Packed input: the same N+1 values in host memory (used for validation
+   * and grid sizing without a device-to-host copy).  Required when
+   * cu_seqlens != NULL.                                                    */
+  const int32_t *cu_seqlens_host;
+  gdn_dtype dtype;
+} gdn_problem;
+
+/* Workspace bytes gdn_chunk_fwd / gdn_chunk_bwd need for this problem
+ * (0 if the problem itself is invalid). */
+size_t gdn_chunk_fwd_workspace_size(const gdn_problem *p);
+size_t gdn_chunk_bwd_workspace_size(const gdn_problem *p);
+
+/* Forward.  Sec. 3.3, the gated chunk state update and output equations
+ * (output mask read as the decay mask Gamma, with its diagonal).
+ *   in : q, k, v, beta, log_alpha; h0 = initial states or NULL (zero)
+ *   out: o; ht = final states, or NULL to skip. */
+gdn_status gdn_chunk_fwd(const gdn_problem *p, const void *q, const void *k,
+                         const void *v, const float *beta,
+                         const float *log_alpha, const float *h0, void *o,
+                         float *ht, void *workspace, size_t workspace_bytes,
+                         void *stream);
+
+/* Backward (stateless: recomputes the forward's chunk states itself).
+ *   in : the forward's inputs; dO = gradient of o; dht = gradient of the
+ *        final states or NULL (zero)
+ *   out: dq, dk, dv, dbeta, dlog_alpha; dh0 = gradient of the initial
+ *        states, or NULL to skip.  Every output is overwritten. */
+gdn_status gdn_chunk_bwd(const gdn_problem *p, const void *q, const void *k,
+                         const void *v, const float *beta,
+                         const float *log_alpha, const float *h0,
+                         const void *dO, const float *dht, void *dq, void *dk,
+                         void *dv, float *dbeta, float *dlog_alpha, float *dh0,
+                         void *workspace, size_t workspace_bytes, void *stream);
+
+/* Human-readable name of a status. */
+const char *gdn_status_string(gdn_status s);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GDN_H_ */

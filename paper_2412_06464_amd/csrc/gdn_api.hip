@@ -1,0 +1,215 @@
+// C ABI of libgdn: argument validation, workspace carve-up and launch
+// sequencing.  Every check runs before the first launch; nothing here
+// allocates, frees or synchronises.
+#include <stdint.h>
+#include <string.h>
+
+#include <new>
+
+#include "../../include/gdn.h"
+#include "gdn_kernels.h"
+
+namespace {
+
+using gdn::Args;
+using gdn::Dt;
+
+constexpr int CH = 64;
+constexpr size_t ALIGN = 256;
+
+size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+struct Shape {
+  int N = 0;      // sequences
+  long NC = 0;    // chunks
+  long Ttot = 0;  // tokens
+  size_t esz = 0; // element bytes of q/k/v
+};
+
+gdn_status check_problem(const gdn_problem* p, Shape* out) {
+  if (!p) return GDN_ERR_NULL;
+  if (p->dtype != GDN_F32 && p->dtype != GDN_BF16) return GDN_ERR_UNSUPPORTED;
+  if (p->B < 1 || p->T < 1 || p->H < 1) return GDN_ERR_SHAPE;
+  const bool ok_dims = (p->dtype == GDN_F32 && p->dk == 64 && p->dv == 64) ||
+                       (p->dtype == GDN_BF16 && ((p->dk == 64 && p->dv == 64) ||
+                                                 (p->dk == 128 && p->dv == 128) ||
+                                                 (p->dk == 256 && p->dv == 512)));
+  if (!ok_dims) return GDN_ERR_UNSUPPORTED;
+  const long Ttot = (long)p->B * p->T;
+  if (Ttot * (long)p->H * (p->dk > p->dv ? p->dk : p->dv) >= (1L << 40)) return GDN_ERR_SHAPE;
+  if (Ttot >= (1L << 31)) return GDN_ERR_SHAPE;
+  Shape s;
+  s.Ttot = Ttot;
+  s.esz = p->dtype == GDN_F32 ? 4 : 2;
+  if (p->cu_seqlens) {
+    if (p->B != 1) return GDN_ERR_SHAPE;
+    if (!p->cu_seqlens_host || p->num_seqs < 1) return GDN_ERR_CU_SEQLENS;
+    const int32_t* cu = p->cu_seqlens_host;
+    if (cu[0] != 0 || cu[p->num_seqs] != p->T) return GDN_ERR_CU_SEQLENS;
+    long nc = 0;
+    for (int n = 0; n < p->num_seqs; ++n) {
+      if (cu[n + 1] < cu[n]) return GDN_ERR_CU_SEQLENS;
+      nc += (cu[n + 1] - cu[n] + CH - 1) / CH;
+    }
+    s.N = p->num_seqs;
+    s.NC = nc;
+  } else {
+    if (p->cu_seqlens_host) return GDN_ERR_CU_SEQLENS;
+    s.N = p->B;
+    s.NC = (long)p->B * ((p->T + CH - 1) / CH);
+  }
+  if (s.NC >= (1L << 31) / CH) return GDN_ERR_SHAPE;
+  *out = s;
+  return GDN_OK;
+}
+
+// Workspace layout; `base` may be null to only compute the size.
+size_t carve(const gdn_problem* p, const Shape& s, bool backward, unsigned char* base,
+             Args* a) {
+  const size_t NC = (size_t)s.NC, H = (size_t)p->H;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    unsigned char* ptr = base ? base + off : nullptr;
+    off += up(bytes);
+    return ptr;
+  };
+  unsigned char* info = take(NC * sizeof(int4) + 16);
+  unsigned char* sc0 = take(((size_t)s.N + 1) * sizeof(int));
+  unsigned char* g = take(NC * H * CH * sizeof(float));
+  unsigned char* Tm = take(NC * H * CH * CH * sizeof(float));
+  unsigned char* Pm = take(NC * H * CH * CH * sizeof(float));
+  unsigned char* Ak = take(NC * H * CH * CH * sizeof(float));
+  unsigned char *Sc = nullptr, *Vp = nullptr, *dSc = nullptr, *dXb = nullptr;
+  if (backward) {
+    const size_t st = NC * H * (size_t)p->dk * p->dv * s.esz;
+    const size_t rows = NC * H * CH * (size_t)p->dv * s.esz;
+    Sc = take(st);
+    dSc = take(st);
+    Vp = take(rows);
+    dXb = take(rows);
+  }
+  if (a) {
+    a->info = (int4*)info;
+    a->seq_chunk0 = (int*)sc0;
+    a->g = (float*)g;
+    a->Tm = (float*)Tm;
+    a->Pm = (float*)Pm;
+    a->Ak = (float*)Ak;
+    a->Sc = Sc;
+    a->Vp = Vp;
+    a->dSc = dSc;
+    a->dXb = dXb;
+  }
+  return off;
+}
+
+void fill_common(const gdn_problem* p, const Shape& s, Args* a) {
+  a->H = p->H;
+  a->N = s.N;
+  a->NC = (int)s.NC;
+  a->T = p->cu_seqlens ? 0 : p->T;
+  a->cu = p->cu_seqlens;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t gdn_chunk_fwd_workspace_size(const gdn_problem* p) {
+  Shape s;
+  if (check_problem(p, &s) != GDN_OK) return 0;
+  return carve(p, s, false, nullptr, nullptr);
+}
+
+size_t gdn_chunk_bwd_workspace_size(const gdn_problem* p) {
+  Shape s;
+  if (check_problem(p, &s) != GDN_OK) return 0;
+  return carve(p, s, true, nullptr, nullptr);
+}
+
+gdn_status gdn_chunk_fwd(const gdn_problem* p, const void* q, const void* k, const void* v,
+                         const float* beta, const float* log_alpha, const float* h0, void* o,
+                         float* ht, void* workspace, size_t workspace_bytes, void* stream) {
+  Shape s;
+  gdn_status st = check_problem(p, &s);
+  if (st != GDN_OK) return st;
+  if (!q || !k || !v || !beta || !log_alpha || !o) return GDN_ERR_NULL;
+  const void* ptrs[] = {q, k, v, beta, log_alpha, h0, o, ht, workspace};
+  for (const void* x : ptrs)
+    if (x && !aligned16(x)) return GDN_ERR_ALIGN;
+  const size_t need = carve(p, s, false, nullptr, nullptr);
+  if (!workspace || workspace_bytes < need) return GDN_ERR_WORKSPACE;
+  Args a;
+  memset(&a, 0, sizeof a);
+  fill_common(p, s, &a);
+  carve(p, s, false, (unsigned char*)workspace, &a);
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.beta = beta;
+  a.log_alpha = log_alpha;
+  a.h0 = h0;
+  a.o = o;
+  a.ht = ht;
+  const hipError_t e = gdn::launch_fwd(p->dtype == GDN_F32 ? Dt::F32 : Dt::BF16, p->dk, p->dv, a,
+                                       (hipStream_t)stream);
+  return e == hipSuccess ? GDN_OK : GDN_ERR_HIP;
+}
+
+gdn_status gdn_chunk_bwd(const gdn_problem* p, const void* q, const void* k, const void* v,
+                         const float* beta, const float* log_alpha, const float* h0,
+                         const void* dO, const float* dht, void* dq, void* dk, void* dv,
+                         float* dbeta, float* dlog_alpha, float* dh0, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+  Shape s;
+  gdn_status st = check_problem(p, &s);
+  if (st != GDN_OK) return st;
+  if (!q || !k || !v || !beta || !log_alpha || !dO || !dq || !dk || !dv || !dbeta ||
+      !dlog_alpha)
+    return GDN_ERR_NULL;
+  const void* ptrs[] = {q, k, v, beta, log_alpha, h0, dO, dht, dq, dk, dv, dbeta, dlog_alpha,
+                        dh0, workspace};
+  for (const void* x : ptrs)
+    if (x && !aligned16(x)) return GDN_ERR_ALIGN;
+  const size_t need = carve(p, s, true, nullptr, nullptr);
+  if (!workspace || workspace_bytes < need) return GDN_ERR_WORKSPACE;
+  Args a;
+  memset(&a, 0, sizeof a);
+  fill_common(p, s, &a);
+  carve(p, s, true, (unsigned char*)workspace, &a);
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.beta = beta;
+  a.log_alpha = log_alpha;
+  a.h0 = h0;
+  a.dO = dO;
+  a.dht = dht;
+  a.dq = dq;
+  a.dk = dk;
+  a.dv = dv;
+  a.dbeta = dbeta;
+  a.dlog_alpha = dlog_alpha;
+  a.dh0 = dh0;
+  const hipError_t e = gdn::launch_bwd(p->dtype == GDN_F32 ? Dt::F32 : Dt::BF16, p->dk, p->dv, a,
+                                       (hipStream_t)stream);
+  return e == hipSuccess ? GDN_OK : GDN_ERR_HIP;
+}
+
+const char* gdn_status_string(gdn_status s) {
+  switch (s) {
+    case GDN_OK: return "GDN_OK";
+    case GDN_ERR_NULL: return "GDN_ERR_NULL: a required pointer is NULL";
+    case GDN_ERR_SHAPE: return "GDN_ERR_SHAPE: invalid B, T or H";
+    case GDN_ERR_UNSUPPORTED: return "GDN_ERR_UNSUPPORTED: (dtype, dk, dv) not supported";
+    case GDN_ERR_CU_SEQLENS: return "GDN_ERR_CU_SEQLENS: malformed cu_seqlens";
+    case GDN_ERR_WORKSPACE: return "GDN_ERR_WORKSPACE: workspace missing or too small";
+    case GDN_ERR_HIP: return "GDN_ERR_HIP: a kernel launch failed";
+    case GDN_ERR_ALIGN: return "GDN_ERR_ALIGN: pointer not 16-byte aligned";
+  }
+  return "GDN: unknown status";
+}
+
+}  // extern "C"

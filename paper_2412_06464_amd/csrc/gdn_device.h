@@ -1,0 +1,189 @@
+// Device helpers for the gfx950 gated-delta-rule kernels: MFMA fragments,
+// wave-level tile products from LDS, tile staging between HBM and LDS.
+//
+// MFMA conventions (16x16 output tiles, wave64):
+//   A operand   : lane l holds row (l & 15), KPL consecutive k starting at
+//                 (l >> 4) * KPL of the current k-step;
+//   B operand   : lane l holds column (l & 15), the same k range; we always
+//                 keep B transposed in memory ("Bt[n][k]"), so both operands
+//                 are read with the contraction index contiguous;
+//   accumulator : lane l holds rows 4*(l >> 4) + {0,1,2,3}, column (l & 15).
+// bf16 uses v_mfma_f32_16x16x32_bf16 (K = 32, 8 k per lane, fp32 accumulate);
+// fp32 uses v_mfma_f32_16x16x4_f32 (K = 4, 1 k per lane, full fp32).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace gdn {
+
+typedef __bf16 bf16;
+typedef bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int CH = 64;  // chunk length in tokens
+
+template <class E> struct Mfma;
+
+template <> struct Mfma<bf16> {
+  static constexpr int K = 32;
+  static constexpr int KPL = 8;
+  using frag = bf16x8;
+  __device__ static inline f32x4 mma(frag a, frag b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+  __device__ static inline frag load(const bf16* p) {
+    return *reinterpret_cast<const frag*>(p);
+  }
+};
+
+template <> struct Mfma<float> {
+  static constexpr int K = 4;
+  static constexpr int KPL = 1;
+  using frag = float;
+  __device__ static inline f32x4 mma(frag a, frag b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+  }
+  __device__ static inline frag load(const float* p) { return *p; }
+};
+
+template <class E> __device__ inline E to_e(float x);
+template <> __device__ inline float to_e<float>(float x) { return x; }
+template <> __device__ inline bf16 to_e<bf16>(float x) { return (bf16)x; }  // RNE
+
+__device__ inline float to_f(float x) { return x; }
+__device__ inline float to_f(bf16 x) { return (float)x; }
+
+__device__ inline int lane_id() { return threadIdx.x & 63; }
+__device__ inline int wave_id() { return threadIdx.x >> 6; }
+
+template <int MT, int NT>
+__device__ inline void zero_acc(f32x4 (&acc)[MT][NT]) {
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+}
+
+// acc[i][j] (+)= sum_k A[i*16 + m][k] * Bt[j*16 + n][k], k in [0, KDIM).
+// A and Bt point at the wave's first row; lda/ldb in elements.
+template <class E, int MT, int NT, int KDIM>
+__device__ inline void wave_mma_nt(f32x4 (&acc)[MT][NT], const E* A, int lda,
+                                   const E* Bt, int ldb) {
+  using M = Mfma<E>;
+  const int l = lane_id();
+  const int r = l & 15, kq = (l >> 4) * M::KPL;
+#pragma unroll
+  for (int k0 = 0; k0 < KDIM; k0 += M::K) {
+    typename M::frag a[MT], b[NT];
+#pragma unroll
+    for (int i = 0; i < MT; ++i) a[i] = M::load(A + (i * 16 + r) * lda + k0 + kq);
+#pragma unroll
+    for (int j = 0; j < NT; ++j) b[j] = M::load(Bt + (j * 16 + r) * ldb + k0 + kq);
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int j = 0; j < NT; ++j) acc[i][j] = M::mma(a[i], b[j], acc[i][j]);
+  }
+}
+
+// Row (within a 16x16 tile) of accumulator element e for this lane.
+__device__ inline int acc_row(int e) { return ((lane_id() >> 4) << 2) + e; }
+__device__ inline int acc_col() { return lane_id() & 15; }
+
+// Store an accumulator tile transposed into LDS: dstT[col][row0 + 4 rows].
+template <class E>
+__device__ inline void store_tile_T(E* dstT, int ld, const f32x4& a, int row0, int col0,
+                                    float s0 = 1.f, float s1 = 1.f, float s2 = 1.f,
+                                    float s3 = 1.f) {
+  const int c = col0 + acc_col();
+  const int r = row0 + acc_row(0);
+  E* p = dstT + c * ld + r;
+  p[0] = to_e<E>(a[0] * s0);
+  p[1] = to_e<E>(a[1] * s1);
+  p[2] = to_e<E>(a[2] * s2);
+  p[3] = to_e<E>(a[3] * s3);
+}
+
+// Copy rows [0, ROWS) x cols [0, W) of a row-major global tile (row stride
+// `rs` elements) into LDS with leading dimension LD.  Rows >= nvalid are
+// zero-filled.  16-byte vectors; W * sizeof(E) must be a multiple of 16.
+template <class E, int ROWS, int W, int LD, int NTH>
+__device__ inline void stage_rows(E* lds, const E* g, size_t rs, int nvalid) {
+  constexpr int EPV = 16 / sizeof(E);
+  constexpr int VPR = W / EPV;
+  static_assert(W % EPV == 0, "tile width must be a multiple of 16 bytes");
+#pragma unroll 4
+  for (int idx = threadIdx.x; idx < ROWS * VPR; idx += NTH) {
+    const int r = idx / VPR, cv = idx - r * VPR;
+    uint4 val = {0u, 0u, 0u, 0u};
+    if (r < nvalid) val = *reinterpret_cast<const uint4*>(g + (size_t)r * rs + cv * EPV);
+    *reinterpret_cast<uint4*>(lds + r * LD + cv * EPV) = val;
+  }
+}
+
+// Transposed staging of a [64 x W] row-major global tile into LDS
+// dstT[c][t] (leading dimension LDT), multiplying row t by scale[t] (LDS
+// array, may be null).  Rows >= nvalid are zero.  Consecutive lanes take
+// consecutive rows so that the 2-byte LDS scatter is bank-conflict free.
+template <class E, int W, int LDT, int NTH>
+__device__ inline void stage_rows_T(E* dstT, const E* g, size_t rs, int nvalid,
+                                    const float* scale) {
+  constexpr int EPV = 16 / sizeof(E);
+  constexpr int VPR = W / EPV;
+#pragma unroll 2
+  for (int idx = threadIdx.x; idx < CH * VPR; idx += NTH) {
+    const int t = idx & (CH - 1), cv = idx / CH;
+    union {
+      uint4 u;
+      E e[EPV];
+    } val;
+    val.u = uint4{0u, 0u, 0u, 0u};
+    if (t < nvalid) val.u = *reinterpret_cast<const uint4*>(g + (size_t)t * rs + cv * EPV);
+    const float s = scale ? scale[t] : 1.f;
+#pragma unroll
+    for (int j = 0; j < EPV; ++j) dstT[(cv * EPV + j) * LDT + t] = to_e<E>(to_f(val.e[j]) * s);
+  }
+}
+
+// Stage a 64x64 fp32 matrix from global into LDS as E, optionally transposed.
+template <class E, int LD, int NTH, bool TRANSPOSE>
+__device__ inline void stage_mat64(E* dst, const float* g) {
+#pragma unroll 4
+  for (int idx = threadIdx.x; idx < CH * CH / 4; idx += NTH) {
+    const int r = idx / (CH / 4), c4 = (idx - r * (CH / 4)) * 4;
+    const float4 x = *reinterpret_cast<const float4*>(g + r * CH + c4);
+    if (TRANSPOSE) {
+      dst[(c4 + 0) * LD + r] = to_e<E>(x.x);
+      dst[(c4 + 1) * LD + r] = to_e<E>(x.y);
+      dst[(c4 + 2) * LD + r] = to_e<E>(x.z);
+      dst[(c4 + 3) * LD + r] = to_e<E>(x.w);
+    } else {
+      E* p = dst + r * LD + c4;
+      p[0] = to_e<E>(x.x);
+      p[1] = to_e<E>(x.y);
+      p[2] = to_e<E>(x.z);
+      p[3] = to_e<E>(x.w);
+    }
+  }
+}
+
+// Inclusive prefix sum across the 64 lanes of a wave.
+__device__ inline float wave_incl_scan(float x) {
+  const int l = lane_id();
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const float y = __shfl_up(x, off, 64);
+    if (l >= off) x += y;
+  }
+  return x;
+}
+
+// Sum over the 16 lanes that share (l >> 4) (the columns of an accumulator tile).
+__device__ inline float reduce16(float x) {
+#pragma unroll
+  for (int off = 1; off < 16; off <<= 1) x += __shfl_xor(x, off, 64);
+  return x;
+}
+
+}  // namespace gdn

@@ -1,0 +1,166 @@
+"""Thin ctypes binding of libgdn (include/gdn.h).
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels of ``libgdn.so``.  PyTorch provides device memory and the current
+stream.  There is no fallback: if the library is missing, loading fails.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgdn.so")
+
+GDN_F32, GDN_BF16 = 0, 1
+STATUS = {0: "GDN_OK", 1: "GDN_ERR_NULL", 2: "GDN_ERR_SHAPE", 3: "GDN_ERR_UNSUPPORTED",
+          4: "GDN_ERR_CU_SEQLENS", 5: "GDN_ERR_WORKSPACE", 6: "GDN_ERR_HIP", 7: "GDN_ERR_ALIGN"}
+EXPORTS = ("gdn_chunk_fwd", "gdn_chunk_bwd", "gdn_chunk_fwd_workspace_size",
+           "gdn_chunk_bwd_workspace_size", "gdn_status_string")
+
+
+class Problem(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("T", ctypes.c_int32), ("H", ctypes.c_int32),
+                ("dk", ctypes.c_int32), ("dv", ctypes.c_int32), ("num_seqs", ctypes.c_int32),
+                ("cu_seqlens", ctypes.c_void_p), ("cu_seqlens_host", ctypes.c_void_p),
+                ("dtype", ctypes.c_int)]
+
+
+class GdnError(RuntimeError):
+    def __init__(self, code: int):
+        super().__init__(STATUS.get(code, "status %d" % code))
+        self.code = code
+
+
+_lib = None
+
+
+def load_library():
+    """Load libgdn.so (built by ``paper_2412_06464_amd.build``); raise if absent."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libgdn.so is not built (%s); run "
+                               "`python -m paper_2412_06464_amd.build`" % LIB_PATH)
+        lib = ctypes.CDLL(LIB_PATH)
+        P, S = ctypes.c_void_p, ctypes.c_size_t
+        pp = ctypes.POINTER(Problem)
+        lib.gdn_chunk_fwd_workspace_size.argtypes = [pp]
+        lib.gdn_chunk_fwd_workspace_size.restype = S
+        lib.gdn_chunk_bwd_workspace_size.argtypes = [pp]
+        lib.gdn_chunk_bwd_workspace_size.restype = S
+        lib.gdn_chunk_fwd.argtypes = [pp] + [P] * 8 + [P, S, P]
+        lib.gdn_chunk_fwd.restype = ctypes.c_int
+        lib.gdn_chunk_bwd.argtypes = [pp] + [P] * 14 + [P, S, P]
+        lib.gdn_chunk_bwd.restype = ctypes.c_int
+        lib.gdn_status_string.argtypes = [ctypes.c_int]
+        lib.gdn_status_string.restype = ctypes.c_char_p
+        _lib = lib
+    return _lib
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def make_problem(q: torch.Tensor, v: torch.Tensor, cu_seqlens=None, cu_seqlens_host=None):
+    """Build the gdn_problem for q [B,T,H,dk], v [B,T,H,dv].  Returns (problem, keepalive)."""
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    dt = {torch.float32: GDN_F32, torch.bfloat16: GDN_BF16}.get(q.dtype)
+    if dt is None:
+        raise TypeError("q must be float32 or bfloat16")
+    keep = []
+    p = Problem(B, T, H, dk, dv, 0, None, None, dt)
+    if cu_seqlens is not None:
+        if cu_seqlens_host is None:
+            cu_seqlens_host = cu_seqlens.to("cpu")
+        host = cu_seqlens_host.to(torch.int32).contiguous()
+        keep.append(host)
+        p.num_seqs = host.numel() - 1
+        p.cu_seqlens = cu_seqlens.data_ptr()
+        p.cu_seqlens_host = host.data_ptr()
+    return p, keep
+
+
+def gdn_chunk_fwd_workspace_size(p: Problem) -> int:
+    return int(load_library().gdn_chunk_fwd_workspace_size(ctypes.byref(p)))
+
+
+def gdn_chunk_bwd_workspace_size(p: Problem) -> int:
+    return int(load_library().gdn_chunk_bwd_workspace_size(ctypes.byref(p)))
+
+
+def gdn_status_string(code: int) -> str:
+    return load_library().gdn_status_string(code).decode()
+
+
+def _stream(device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _check(code: int):
+    if code != 0:
+        raise GdnError(code)
+
+
+def _nstate(q, cu_seqlens):
+    return q.shape[0] if cu_seqlens is None else cu_seqlens.numel() - 1
+
+
+def gdn_chunk_fwd(q, k, v, beta, log_alpha, h0=None, cu_seqlens=None, cu_seqlens_host=None,
+                  output_final_state=True, o=None, ht=None, workspace=None):
+    """Forward of the chunkwise gated delta rule on the current stream.
+
+    q, k [B,T,H,dk] and v [B,T,H,dv] (fp32 or bf16, same dtype), beta and
+    log_alpha [B,T,H] fp32, h0 [Nseq,H,dk,dv] fp32 or None; packed input
+    passes cu_seqlens (int32 [N+1], device) with B == 1.  Returns (o, ht).
+    """
+    lib = load_library()
+    p, keep = make_problem(q, v, cu_seqlens, cu_seqlens_host)
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    if o is None:
+        o = torch.empty((B, T, H, dv), dtype=q.dtype, device=q.device)
+    if ht is None and output_final_state:
+        ht = torch.empty((_nstate(q, cu_seqlens), H, dk, dv), dtype=torch.float32,
+                         device=q.device)
+    need = lib.gdn_chunk_fwd_workspace_size(ctypes.byref(p))
+    if need == 0:
+        _check(lib.gdn_chunk_fwd(ctypes.byref(p), *[None] * 8, None, 0, None))
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    _check(lib.gdn_chunk_fwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(beta),
+                             _ptr(log_alpha), _ptr(h0), _ptr(o), _ptr(ht), _ptr(workspace),
+                             workspace.numel(), _stream(q.device)))
+    del keep
+    return o, ht
+
+
+def gdn_chunk_bwd(q, k, v, beta, log_alpha, dO, h0=None, dht=None, cu_seqlens=None,
+                  cu_seqlens_host=None, need_dh0=True, workspace=None, out=None):
+    """Backward (stateless): returns dict dq, dk, dv, dbeta, dlog_alpha, dh0."""
+    lib = load_library()
+    p, keep = make_problem(q, v, cu_seqlens, cu_seqlens_host)
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    if out is None:
+        out = dict(dq=torch.empty_like(q), dk=torch.empty_like(k), dv=torch.empty_like(v),
+                   dbeta=torch.empty_like(beta), dlog_alpha=torch.empty_like(log_alpha),
+                   dh0=torch.empty((_nstate(q, cu_seqlens), H, dk, dv), dtype=torch.float32,
+                                   device=q.device) if need_dh0 else None)
+    need = lib.gdn_chunk_bwd_workspace_size(ctypes.byref(p))
+    if need == 0:
+        _check(lib.gdn_chunk_bwd(ctypes.byref(p), *[None] * 14, None, 0, None))
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    _check(lib.gdn_chunk_bwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(beta),
+                             _ptr(log_alpha), _ptr(h0), _ptr(dO), _ptr(dht), _ptr(out["dq"]),
+                             _ptr(out["dk"]), _ptr(out["dv"]), _ptr(out["dbeta"]),
+                             _ptr(out["dlog_alpha"]), _ptr(out["dh0"]), _ptr(workspace),
+                             workspace.numel(), _stream(q.device)))
+    del keep
+    return out

@@ -1,0 +1,122 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, sizes workspaces, and rejects bad arguments on the host
+before any launch."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2412_06464_amd import gdn
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gdn.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(gdn.LIB_PATH):
+        from paper_2412_06464_amd import build
+        build.build()
+    return gdn.load_library()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_]+\s*\*?\s*(gdn_[a-z_0-9]+)\s*\(",
+                                 text, re.M)))
+
+
+def test_header_declares_expected_entry_points():
+    assert declared_functions() == sorted(gdn.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def problem(B=2, T=100, H=3, dk=64, dv=64, dtype=gdn.GDN_BF16, cu=None):
+    p = gdn.Problem(B, T, H, dk, dv, 0, None, None, dtype)
+    keep = None
+    if cu is not None:
+        arr = (ctypes.c_int32 * len(cu))(*cu)
+        keep = arr
+        p.num_seqs = len(cu) - 1
+        p.cu_seqlens = 0x1000  # a device address is never dereferenced on the host
+        p.cu_seqlens_host = ctypes.addressof(arr)
+    return p, keep
+
+
+def test_status_strings(lib):
+    for code, name in gdn.STATUS.items():
+        assert gdn.gdn_status_string(code).startswith(name)
+
+
+def test_workspace_sizes(lib):
+    p, _ = problem()
+    f = gdn.gdn_chunk_fwd_workspace_size(p)
+    b = gdn.gdn_chunk_bwd_workspace_size(p)
+    NC = 2 * 2  # two sequences of 100 tokens -> 2 chunks each
+    assert f >= NC * 3 * 64 * 64 * 4 * 3  # T, P and Ak per chunk-head
+    # backward adds entry states, exit-state gradients, V' and dX
+    assert b - f >= NC * 3 * (2 * 64 * 64 * 2 + 2 * 64 * 64 * 2)
+    bad, _ = problem(dk=96)
+    assert gdn.gdn_chunk_fwd_workspace_size(bad) == 0
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dk=96), 3), (dict(dk=128, dv=64), 3), (dict(dtype=gdn.GDN_F32, dk=128, dv=128), 3),
+    (dict(B=0), 2), (dict(T=0), 2), (dict(H=0), 2), (dict(dtype=7), 3),
+])
+def test_bad_problem_rejected_before_launch(lib, kw, code):
+    p, _ = problem(**kw)
+    fake = ctypes.c_void_p(0x10000)
+    rc = lib.gdn_chunk_fwd(ctypes.byref(p), fake, fake, fake, fake, fake, None, fake, None,
+                           fake, 1 << 40, None)
+    assert rc == code
+    rc = lib.gdn_chunk_bwd(ctypes.byref(p), *([fake] * 5), None, fake, None, *([fake] * 5),
+                           None, fake, 1 << 40, None)
+    assert rc == code
+
+
+@pytest.mark.parametrize("cu,code", [
+    ([0, 50, 40, 100], 4),   # decreasing
+    ([0, 50, 99], 4),        # does not end at T
+    ([1, 50, 100], 4),       # does not start at 0
+])
+def test_bad_cu_seqlens(lib, cu, code):
+    p, keep = problem(B=1, cu=cu)
+    fake = ctypes.c_void_p(0x10000)
+    rc = lib.gdn_chunk_fwd(ctypes.byref(p), fake, fake, fake, fake, fake, None, fake, None,
+                           fake, 1 << 40, None)
+    assert rc == code
+    del keep
+
+
+def test_packed_needs_batch_one_and_host_copy(lib):
+    p, keep = problem(B=2, cu=[0, 100])
+    fake = ctypes.c_void_p(0x10000)
+    assert lib.gdn_chunk_fwd(ctypes.byref(p), fake, fake, fake, fake, fake, None, fake, None,
+                             fake, 1 << 40, None) == 2
+    p, keep = problem(B=1, T=100, cu=[0, 100])
+    p.cu_seqlens_host = None
+    assert lib.gdn_chunk_fwd(ctypes.byref(p), fake, fake, fake, fake, fake, None, fake, None,
+                             fake, 1 << 40, None) == 4
+
+
+def test_null_misaligned_and_small_workspace(lib):
+    p, _ = problem()
+    fake = ctypes.c_void_p(0x10000)
+    odd = ctypes.c_void_p(0x10008)
+    args = [fake] * 5 + [None, fake, None]
+    assert lib.gdn_chunk_fwd(ctypes.byref(p), None, *args[1:], fake, 1 << 40, None) == 1
+    assert lib.gdn_chunk_fwd(ctypes.byref(p), odd, *args[1:], fake, 1 << 40, None) == 7
+    need = gdn.gdn_chunk_fwd_workspace_size(p)
+    assert lib.gdn_chunk_fwd(ctypes.byref(p), *args, fake, need - 1, None) == 5
+    assert lib.gdn_chunk_fwd(ctypes.byref(p), *args, None, need, None) == 5
+    bargs = [fake] * 5 + [None, fake, None] + [fake] * 5 + [None]
+    needb = gdn.gdn_chunk_bwd_workspace_size(p)
+    assert lib.gdn_chunk_bwd(ctypes.byref(p), *bargs, fake, needb - 1, None) == 5
+    bargs[6] = None  # dO
+    assert lib.gdn_chunk_bwd(ctypes.byref(p), *bargs, fake, needb, None) == 1

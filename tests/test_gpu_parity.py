@@ -1,0 +1,275 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+Error metric (per output tensor, computed in fp64):
+    err(x, ref) = max_i |x_i - ref_i| / max_i |ref_i|
+Bar: <= 1e-4 for float32 inputs, <= 2e-2 for bfloat16 inputs with fp32
+accumulation.  The denominator has a floor of 1e-30: a reference tensor whose
+magnitude lies below what fp32 represents (a state decayed by e^-170, say)
+counts as zero, and then the result must be within 1e-30 * tol of it.  Both
+sides see the same (already rounded) inputs, so input
+quantisation is not counted as kernel error.
+"""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2412_06464_amd.inputs import WORKLOADS, make_inputs, workload_inputs
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def rel_err(x, ref):
+    x = np.asarray(x, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    den = max(float(np.abs(ref).max()), 1e-30)
+    return float(np.abs(x - ref).max() / den)
+
+
+def f64(t):
+    return t.detach().to("cpu", torch.float64).numpy()
+
+
+def say(*a):
+    print("[gpu-case]", *a, flush=True)
+
+
+@pytest.fixture(scope="module")
+def G():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2412_06464_amd import gdn
+    gdn.load_library()
+    return gdn
+
+
+def to_dev(inp):
+    return {k: (v.cuda() if isinstance(v, torch.Tensor) else v) for k, v in inp.items()}
+
+
+def run_fwd(G, d):
+    o, ht = G.gdn_chunk_fwd(d["q"], d["k"], d["v"], d["beta"], d["log_alpha"], h0=d.get("h0"),
+                            cu_seqlens=d.get("cu_seqlens"))
+    torch.cuda.synchronize()
+    return o, ht
+
+
+def run_bwd(G, d):
+    r = G.gdn_chunk_bwd(d["q"], d["k"], d["v"], d["beta"], d["log_alpha"], d["dO"],
+                        h0=d.get("h0"), dht=d.get("dht"), cu_seqlens=d.get("cu_seqlens"))
+    torch.cuda.synchronize()
+    return r
+
+
+def check_fwd(G, oracle_mod, inp, tol, label):
+    say(label, "fwd", tuple(inp["q"].shape), tuple(inp["v"].shape), inp["q"].dtype)
+    d = to_dev(inp)
+    o, ht = run_fwd(G, d)
+    ro, rht = oracle_mod.fwd(inp["q"], inp["k"], inp["v"], inp["beta"], inp["log_alpha"],
+                             h0=inp.get("h0"), cu_seqlens=inp.get("cu_seqlens"))
+    eo = rel_err(f64(o).reshape(ro.shape), ro)
+    eh = rel_err(f64(ht), rht)
+    say(label, "err o=%.3g ht=%.3g" % (eo, eh))
+    assert eo <= tol and eh <= tol, (eo, eh)
+    return o, ht
+
+
+def check_bwd(G, oracle_mod, inp, tol, label):
+    say(label, "bwd", tuple(inp["q"].shape), tuple(inp["v"].shape), inp["q"].dtype)
+    d = to_dev(inp)
+    r = run_bwd(G, d)
+    ref = oracle_mod.bwd(inp["q"], inp["k"], inp["v"], inp["beta"], inp["log_alpha"], inp["dO"],
+                         h0=inp.get("h0"), dht=inp.get("dht"), cu_seqlens=inp.get("cu_seqlens"))
+    errs = {}
+    for name in ("dq", "dk", "dv", "dbeta", "dlog_alpha", "dh0"):
+        errs[name] = rel_err(f64(r[name]).reshape(ref[name].shape), ref[name])
+    say(label, "errs", {k: "%.3g" % v for k, v in errs.items()})
+    bad = {k: v for k, v in errs.items() if not v <= tol}
+    assert not bad, bad
+    return r
+
+
+# ------------------------------------------------------------------ forward, small
+
+
+def test_fwd_f32_workload(G, oracle_mod):
+    check_fwd(G, oracle_mod, workload_inputs("fwd_f32_b1_t256_h2_d64"), TOL["f32"],
+              "fwd_f32_b1_t256_h2_d64")
+
+
+@pytest.mark.parametrize("dtype,dk,dv,B,T,H", [
+    ("f32", 64, 64, 2, 200, 3),
+    ("bf16", 64, 64, 2, 200, 3),
+    ("bf16", 128, 128, 2, 130, 2),
+    ("bf16", 256, 512, 1, 150, 2),
+])
+def test_fwd_ragged_with_initial_state(G, oracle_mod, dtype, dk, dv, B, T, H):
+    inp = make_inputs(B, T, H, dk, dv, dtype, seed=1, h0_std=0.05)
+    check_fwd(G, oracle_mod, inp, TOL[dtype], "fwd_%s_%d_%d_T%d" % (dtype, dk, dv, T))
+
+
+@pytest.mark.parametrize("label,kw", [
+    ("weak_decay", dict(log_alpha_scale=0.01)),
+    ("alpha_one", dict(log_alpha_value=0.0)),
+    ("beta_0_2", dict(beta_scale=2.0, log_alpha_scale=0.1)),
+    ("beta_zero", dict(beta_value=0.0, log_alpha_scale=0.05)),
+    ("beta_zero_full_decay", dict(beta_value=0.0)),
+    ("strong_decay", dict(log_alpha_scale=8.0)),
+])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_fwd_stress(G, oracle_mod, label, kw, dtype):
+    inp = make_inputs(1, 333, 2, 64, 64, dtype, seed=3, h0_std=0.05, **kw)
+    check_fwd(G, oracle_mod, inp, TOL[dtype], "fwd_stress_" + label)
+
+
+@pytest.mark.parametrize("dtype,dk,dv", [("f32", 64, 64), ("bf16", 128, 128),
+                                         ("bf16", 256, 512)])
+def test_fwd_packed(G, oracle_mod, dtype, dk, dv):
+    lens = [1, 0, 64, 65, 130, 7, 128]
+    cu = torch.tensor(np.concatenate([[0], np.cumsum(lens)]), dtype=torch.int32)
+    inp = make_inputs(1, int(cu[-1]), 2, dk, dv, dtype, seed=4, h0_std=0.05, cu_seqlens=cu)
+    check_fwd(G, oracle_mod, inp, TOL[dtype], "fwd_packed_%s_%d" % (dtype, dk))
+
+
+def test_fwd_split_carry(G):
+    inp = to_dev(make_inputs(2, 300, 2, 128, 128, "bf16", seed=5, h0_std=0.05))
+    o, ht = run_fwd(G, inp)
+    a = {k: (v[:, :100].contiguous() if k in ("q", "k", "v", "beta", "log_alpha") else v)
+         for k, v in inp.items()}
+    b = {k: (v[:, 100:].contiguous() if k in ("q", "k", "v", "beta", "log_alpha") else v)
+         for k, v in inp.items()}
+    oa, ha = run_fwd(G, a)
+    b["h0"] = ha
+    ob, hb = run_fwd(G, b)
+    o2 = torch.cat([oa, ob], 1)
+    assert rel_err(f64(o2), f64(o)) < 2e-2
+    assert rel_err(f64(hb), f64(ht)) < 2e-2
+
+
+def test_fwd_deterministic(G):
+    inp = to_dev(make_inputs(2, 257, 3, 256, 512, "bf16", seed=6, h0_std=0.02))
+    o1, h1 = run_fwd(G, inp)
+    o2, h2 = run_fwd(G, inp)
+    assert torch.equal(o1, o2) and torch.equal(h1, h2)
+
+
+# ------------------------------------------------------------------ backward, small
+
+
+@pytest.mark.parametrize("dtype,dk,dv,B,T,H", [
+    ("f32", 64, 64, 1, 256, 2),
+    ("f32", 64, 64, 2, 150, 2),
+    ("bf16", 64, 64, 2, 150, 2),
+    ("bf16", 128, 128, 1, 200, 2),
+    ("bf16", 256, 512, 1, 130, 2),
+])
+def test_bwd_ragged(G, oracle_mod, dtype, dk, dv, B, T, H):
+    inp = make_inputs(B, T, H, dk, dv, dtype, seed=7, h0_std=0.05, backward=True)
+    check_bwd(G, oracle_mod, inp, TOL[dtype], "bwd_%s_%d_%d_T%d" % (dtype, dk, dv, T))
+
+
+@pytest.mark.parametrize("label,kw", [
+    ("weak_decay", dict(log_alpha_scale=0.01)),
+    ("alpha_one", dict(log_alpha_value=0.0)),
+    ("beta_0_2", dict(beta_scale=2.0, log_alpha_scale=0.1)),
+    ("beta_zero", dict(beta_value=0.0, log_alpha_scale=0.05)),
+])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_bwd_stress(G, oracle_mod, label, kw, dtype):
+    inp = make_inputs(1, 200, 2, 64, 64, dtype, seed=8, h0_std=0.05, backward=True, **kw)
+    check_bwd(G, oracle_mod, inp, TOL[dtype], "bwd_stress_" + label)
+
+
+@pytest.mark.parametrize("dtype,dk,dv", [("f32", 64, 64), ("bf16", 128, 128),
+                                         ("bf16", 256, 512)])
+def test_bwd_packed(G, oracle_mod, dtype, dk, dv):
+    lens = [1, 0, 64, 65, 130, 7]
+    cu = torch.tensor(np.concatenate([[0], np.cumsum(lens)]), dtype=torch.int32)
+    inp = make_inputs(1, int(cu[-1]), 2, dk, dv, dtype, seed=9, h0_std=0.05, backward=True,
+                      cu_seqlens=cu)
+    check_bwd(G, oracle_mod, inp, TOL[dtype], "bwd_packed_%s_%d" % (dtype, dk))
+
+
+def test_bwd_deterministic(G):
+    inp = to_dev(make_inputs(1, 200, 2, 256, 512, "bf16", seed=10, backward=True))
+    r1 = run_bwd(G, inp)
+    r2 = run_bwd(G, inp)
+    for k in r1:
+        assert torch.equal(r1[k], r2[k]), k
+
+
+# ------------------------------------------------------------------ full-size workloads
+# The HIP path runs the whole workload exactly as the benchmark launches it;
+# the oracle recomputes a sample of independent (sequence, head) units.
+
+
+def sample_units(inp, units):
+    """Slice inputs to the listed (sequence, head) units, each as its own dense call."""
+    cu = inp.get("cu_seqlens")
+    out = []
+    for n, h in units:
+        if cu is None:
+            sl = lambda x: x[n:n + 1, :, h:h + 1]
+            st = lambda x: None if x is None else x[n:n + 1, h:h + 1]
+        else:
+            s, e = int(cu[n]), int(cu[n + 1])
+            sl = lambda x, s=s, e=e: x[:, s:e, h:h + 1]
+            st = lambda x: None if x is None else x[n:n + 1, h:h + 1]
+        d = {k: sl(inp[k]) for k in ("q", "k", "v", "beta", "log_alpha")}
+        d["h0"] = st(inp.get("h0"))
+        if "dO" in inp:
+            d["dO"] = sl(inp["dO"])
+            d["dht"] = st(inp.get("dht"))
+        out.append(((n, h), d))
+    return out
+
+
+@pytest.mark.parametrize("name", list(WORKLOADS))
+def test_full_workload_sampled(G, oracle_mod, name):
+    w = WORKLOADS[name]
+    inp = workload_inputs(name)
+    say(name, "full-size run")
+    d = to_dev(inp)
+    o, ht = run_fwd(G, d)
+    r = run_bwd(G, d) if w.backward else None
+    tol = TOL[w.dtype]
+    cu = inp.get("cu_seqlens")
+    N = w.B if cu is None else cu.numel() - 1
+    rng = np.random.default_rng(0)
+    units = [(int(rng.integers(N)), int(rng.integers(w.H))) for _ in range(2)]
+    if cu is not None:  # include the longest sequence
+        lens = (cu[1:] - cu[:-1]).numpy()
+        units[0] = (int(lens.argmax()), units[0][1])
+    for (n, h), s in sample_units(inp, units):
+        say(name, "oracle unit", (n, h))
+        if w.backward:
+            ref = oracle_mod.bwd(s["q"], s["k"], s["v"], s["beta"], s["log_alpha"], s["dO"],
+                                 h0=s["h0"], dht=s["dht"])
+        else:
+            ro, rh = oracle_mod.fwd(s["q"], s["k"], s["v"], s["beta"], s["log_alpha"],
+                                    h0=s["h0"])
+            ref = dict(o=ro, ht=rh)
+        if cu is None:
+            got = dict(o=o[n:n + 1, :, h:h + 1], ht=ht[n:n + 1, h:h + 1])
+            if r is not None:
+                got.update(dq=r["dq"][n:n + 1, :, h:h + 1], dk=r["dk"][n:n + 1, :, h:h + 1],
+                           dv=r["dv"][n:n + 1, :, h:h + 1],
+                           dbeta=r["dbeta"][n:n + 1, :, h:h + 1],
+                           dlog_alpha=r["dlog_alpha"][n:n + 1, :, h:h + 1],
+                           dh0=r["dh0"][n:n + 1, h:h + 1])
+        else:
+            s_, e_ = int(cu[n]), int(cu[n + 1])
+            got = dict(o=o[:, s_:e_, h:h + 1], ht=ht[n:n + 1, h:h + 1])
+            if r is not None:
+                got.update(dq=r["dq"][:, s_:e_, h:h + 1], dk=r["dk"][:, s_:e_, h:h + 1],
+                           dv=r["dv"][:, s_:e_, h:h + 1],
+                           dbeta=r["dbeta"][:, s_:e_, h:h + 1],
+                           dlog_alpha=r["dlog_alpha"][:, s_:e_, h:h + 1],
+                           dh0=r["dh0"][n:n + 1, h:h + 1])
+        errs = {k: rel_err(f64(v).reshape(ref[k].shape), ref[k]) for k, v in got.items()}
+        say(name, (n, h), {k: "%.3g" % v for k, v in errs.items()})
+        bad = {k: v for k, v in errs.items() if not v <= tol}
+        assert not bad, bad
