@@ -1,0 +1,331 @@
+#!/usr/bin/env python3
+"""Throughput of the chunkwise gated delta rule on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+One step = one pass of the whole hot path over one batch of synthetic input:
+gdn_chunk_fwd followed by gdn_chunk_bwd for forward+backward workloads, or
+gdn_chunk_fwd alone for forward-only ones.  Inputs, outputs and workspaces
+are resident in HBM before the timed region; the timed region is K steps
+between two device synchronisations.  Per-kernel durations come from HIP
+events that the library records around each of its launches on the same
+stream (the *_timed entry points), one event set per step.
+
+Prints one JSON line (rank 0; this build runs on one GPU only).
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+DEFAULT_WORKLOAD = "fwdbwd_bf16_b8_t4096_h6_dk256_dv512"
+METRIC = "tokens/sec gated-delta chunk fwd+bwd (1 GPU); % bf16 MFMA peak"
+PEAK_HBM = 8.0e12          # bytes/s, MI355X HBM3E
+PEAK_MFMA_BF16 = 2.5e15    # dense bf16 MFMA FLOP/s
+PEAK_MFMA_F32 = 157.3e12   # fp32 matrix FLOP/s
+CH = 64
+
+
+def path_flops(w, tokens_heads):
+    """Algorithmic FLOP of the path per step (full C x C products counted).
+    Forward 6 dk dv + 6 C dk + 4 C dv + C^2/3 per token-head; backward
+    12 dk dv + 12 C dk + 8 C dv + 4 C^2 (the stateless recompute not credited)."""
+    dk, dv, C = w.dk, w.dv, CH
+    f = 6 * dk * dv + 6 * C * dk + 4 * C * dv + C * C / 3
+    if w.backward:
+        f += 12 * dk * dv + 12 * C * dk + 8 * C * dv + 4 * C * C
+    return f * tokens_heads
+
+
+def path_bytes(w, tokens_heads, n_states, has_h0):
+    """Algorithmic HBM bytes per step: every call reads its inputs and writes
+    its outputs once.  Forward (2 dk + 2 dv) e + 8 per token-head (q, k, v, o,
+    beta, log_alpha); backward (4 dk + 3 dv) e + 16 (q, k, v, dO in; dq, dk, dv
+    out; gates in, gate gradients out); plus the fp32 states (ht, h0 if
+    given, and dht, dh0 for the backward)."""
+    e = 4 if w.dtype == "f32" else 2
+    dk, dv = w.dk, w.dv
+    st = n_states * dk * dv * 4
+    b = ((2 * dk + 2 * dv) * e + 8) * tokens_heads + st * (2 if has_h0 else 1)
+    if w.backward:
+        b += ((4 * dk + 3 * dv) * e + 16) * tokens_heads + st * (3 if has_h0 else 2)
+    return b
+
+
+def kernel_models(w, n_chunks_heads):
+    """Algorithmic work of each kernel launch: {name: (bytes, flops)}.
+
+    Bytes: the operands the kernel's step of the path must read and write
+    once (inputs, outputs and the per-chunk intermediates it hands over), per
+    chunk-head x number of chunk-heads.  Flops: its matrix products counted at
+    full 64 x 64 chunk size (2 M N K each).  e = element bytes of q/k/v."""
+    e = 4 if w.dtype == "f32" else 2
+    dk, dv, C = w.dk, w.dv, CH
+    f32 = 4
+    mat = C * C * f32                  # one 64 x 64 fp32 matrix (T, P, Ak)
+    kside, vside, st = C * dk * e, C * dv * e, dk * dv * e
+    prod_dk = 2 * C * C * dk           # 64 x 64 times 64 x dk
+    prod_dv = 2 * C * C * dv
+    prod_s = 2 * C * dk * dv           # chunk rows times a dk x dv state
+    per = {
+        # q, k, gates in; g, T, P, Ak out; K K^T, Q K^T, triangular inverse
+        "k_prep_a": (2 * kside + 8 * C + 4 * C + 3 * mat, 2 * prod_dk + C ** 3 / 3),
+        "fwd:k_prep_w": (2 * kside + 2 * mat + 8 * C + 3 * kside, 2 * prod_dk),
+        "bwd:k_prep_w": (2 * kside + mat + 8 * C + 4 * kside + C * C * e, prod_dk),
+        "fwd:k_prep_u": (vside + 2 * mat + 4 * C + 2 * vside, 2 * prod_dv),
+        "bwd:k_prep_u": (2 * vside + 2 * mat + 4 * C + 2 * vside, 2 * prod_dv),
+        "k_fwd_seq": (3 * kside + 3 * vside + 4 * C, 3 * prod_s),
+        "k_fwd_seq_store": (2 * kside + vside + st + vside + 4 * C, 2 * prod_s),
+        "k_bwd_seq": (3 * kside + C * C * e + 2 * vside + 8 * C + st + 2 * vside,
+                      3 * prod_s + prod_dv),
+        "k_grad": (2 * st + 2 * kside + 4 * vside + 2 * mat + 8 * C + 2 * kside + 8 * C,
+                   3 * prod_s + 2 * prod_dv + 3 * prod_dk),
+        "k_chunk_table": (0, 0),
+    }
+    return {k: (b * n_chunks_heads, f * n_chunks_heads) for k, (b, f) in per.items()}
+
+
+def model_for(models, name):
+    """Model of a timed launch named 'fwd:k' / 'bwd:k'."""
+    if name in models:
+        return models[name]
+    return models.get(name.split(":", 1)[-1], (0, 0))
+
+
+def cpu_baseline(inp, w, budget_s=20.0):
+    """Time the oracle (fp64, all host cores) on a bounded sample of the same
+    workload: a few whole (sequence, head) units, fwd (+bwd)."""
+    import torch
+
+    from oracle import oracle
+    threads = oracle.default_threads()
+    cu = inp.get("cu_seqlens")
+    N = w.B if cu is None else cu.numel() - 1
+    units = []
+    for n in range(N):
+        for h in range(w.H):
+            units.append((n, h))
+    # estimate: ~20 flop * dk * dv per token for fwd+bwd, ~6 for fwd, ~3 GFLOP/s a core
+    per_tok = (20 if w.backward else 6) * w.dk * w.dv
+    tok_per_unit = w.T if cu is None else w.T / N
+    per_unit_s = per_tok * tok_per_unit / 3e9
+    n_units = int(max(1, min(len(units), threads * max(1.0, budget_s / per_unit_s / 1.5))))
+    n_units = min(n_units, max(threads, 1) * 4)
+    sel = units[:n_units]
+    sl = {}
+    # pack the selected units as independent sequences of one head each
+    qs, ks, vs, bs, las, dOs, dhts, cus = [], [], [], [], [], [], [], [0]
+    for n, h in sel:
+        if cu is None:
+            s = (slice(n, n + 1), slice(None), slice(h, h + 1))
+        else:
+            s = (slice(0, 1), slice(int(cu[n]), int(cu[n + 1])), slice(h, h + 1))
+        qs.append(inp["q"][s][0])
+        ks.append(inp["k"][s][0])
+        vs.append(inp["v"][s][0])
+        bs.append(inp["beta"][s][0])
+        las.append(inp["log_alpha"][s][0])
+        if w.backward:
+            dOs.append(inp["dO"][s][0])
+            dhts.append(inp["dht"][n:n + 1, h:h + 1, :, :][0])
+        cus.append(cus[-1] + qs[-1].shape[0])
+    cat = lambda xs: torch.cat(xs, 0).unsqueeze(0)
+    sl = dict(q=cat(qs), k=cat(ks), v=cat(vs), beta=cat(bs), log_alpha=cat(las))
+    cu_s = torch.tensor(cus, dtype=torch.int64)
+    tokens = int(cus[-1])
+    t0 = time.perf_counter()
+    if w.backward:
+        dht = torch.stack(dhts, 0)
+        oracle.bwd(sl["q"], sl["k"], sl["v"], sl["beta"], sl["log_alpha"], cat(dOs), dht=dht,
+                   cu_seqlens=cu_s, nthreads=threads)
+    else:
+        oracle.fwd(sl["q"], sl["k"], sl["v"], sl["beta"], sl["log_alpha"], cu_seqlens=cu_s,
+                   nthreads=threads)
+    dt = time.perf_counter() - t0
+    # each token of the workload carries H heads; the sample covers `tokens`
+    # token-heads, i.e. tokens / H workload tokens
+    value = (tokens / w.H) / dt
+    return {"value": value, "unit": "tokens/s", "cores": min(threads, len(sel)),
+            "kind": "oracle",
+            "sample": "%d of %d (sequence, head) units, %d token-heads, %s, %.1f s" % (
+                len(sel), len(units), tokens, "fwd+bwd" if w.backward else "fwd", dt)}
+
+
+def kernel_source_digest():
+    """sha256 over the HIP sources, to tell whether recorded counters are stale."""
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2412_06464_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".h")):
+            h.update(name.encode())
+            h.update(open(os.path.join(csrc, name), "rb").read())
+    return h.hexdigest()
+
+
+def traffic_from_profiles(kernel, workload):
+    """HBM bytes per launch measured by rocprofv3 PMC (FETCH_SIZE + WRITE_SIZE,
+    scaled by a copy-kernel calibration), if recorded for the current kernel
+    source; otherwise None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+    except ValueError:
+        return None
+    digest = kernel_source_digest()
+    ent = rec.get(workload, {}).get(kernel)
+    if not ent or ent.get("kernel_source_sha256") != digest:
+        return None
+    return ent.get("bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a 1 GiB device copy 10 times (PMC calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs on one GPU only (no sharding, no collectives); "
+              "use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2412_06464_amd import gdn
+    from paper_2412_06464_amd.inputs import WORKLOADS, workload_inputs
+
+    if args.copy_calibration:
+        x = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        y = torch.empty_like(x)
+        x.fill_(1)
+        for _ in range(10):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": 1 << 30, "launches": 10}))
+        return
+
+    w = WORKLOADS[args.workload]
+    gdn.load_library()
+    inp = workload_inputs(args.workload, seed=0)
+    dev = torch.device("cuda", 0)
+    d = {k: (v.to(dev) if isinstance(v, torch.Tensor) else v) for k, v in inp.items()}
+    cu = d.get("cu_seqlens")
+    cu_host = inp.get("cu_seqlens")
+    n_states = w.B if cu is None else cu.numel() - 1
+
+    # everything allocated before the timed region
+    p, keep = gdn.make_problem(d["q"], d["v"], cu, cu_host)
+    ws_f = torch.empty(gdn.gdn_chunk_fwd_workspace_size(p), dtype=torch.uint8, device=dev)
+    o = torch.empty_like(d["v"])
+    ht = torch.empty((n_states, w.H, w.dk, w.dv), dtype=torch.float32, device=dev)
+    out_b = ws_b = None
+    if w.backward:
+        ws_b = torch.empty(gdn.gdn_chunk_bwd_workspace_size(p), dtype=torch.uint8, device=dev)
+        out_b = dict(dq=torch.empty_like(d["q"]), dk=torch.empty_like(d["k"]),
+                     dv=torch.empty_like(d["v"]), dbeta=torch.empty_like(d["beta"]),
+                     dlog_alpha=torch.empty_like(d["log_alpha"]),
+                     dh0=torch.empty_like(ht))
+
+    def step(timers=None):
+        gdn.gdn_chunk_fwd(d["q"], d["k"], d["v"], d["beta"], d["log_alpha"], h0=d.get("h0"),
+                          cu_seqlens=cu, cu_seqlens_host=cu_host, o=o, ht=ht, workspace=ws_f,
+                          timer=timers[0] if timers else None)
+        if w.backward:
+            gdn.gdn_chunk_bwd(d["q"], d["k"], d["v"], d["beta"], d["log_alpha"], d["dO"],
+                              h0=d.get("h0"), dht=d["dht"], cu_seqlens=cu,
+                              cu_seqlens_host=cu_host, workspace=ws_b, out=out_b,
+                              timer=timers[1] if timers else None)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    timers = [(gdn.LaunchTimer(8), gdn.LaunchTimer(8) if w.backward else None)
+              for _ in range(args.steps)]
+    stream = torch.cuda.current_stream(dev)
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for i in range(args.steps):
+        step(timers[i])
+    end.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / args.steps
+
+    # per-kernel durations over the timed region
+    per_kernel = {}
+    for tf, tb in timers:
+        for call, t in (("fwd", tf), ("bwd", tb)):
+            if t is None:
+                continue
+            for name, kms in t.durations_ms().items():
+                per_kernel.setdefault(call + ":" + name, []).append(kms)
+        tf.close()
+        if tb is not None:
+            tb.close()
+    kern_ms = {k: sum(v) / len(v) for k, v in per_kernel.items()}
+
+    tokens = w.B * w.T
+    tokens_heads = tokens * w.H
+    n_chunks = (w.B * ((w.T + CH - 1) // CH) if cu_host is None else
+                int(sum((int(cu_host[i + 1]) - int(cu_host[i]) + CH - 1) // CH
+                        for i in range(n_states))))
+    models = kernel_models(w, n_chunks * w.H)
+    dom = max(kern_ms, key=lambda k: kern_ms[k])
+    kb, kf = model_for(models, dom)
+    peak_mfma = PEAK_MFMA_F32 if w.dtype == "f32" else PEAK_MFMA_BF16
+    t_dom = kern_ms[dom] / 1e3
+    if kb / PEAK_HBM >= kf / peak_mfma:
+        roof = {"bound": "hbm", "achieved": kb / t_dom / 1e9, "peak": PEAK_HBM / 1e9,
+                "unit": "GB/s"}
+    else:
+        roof = {"bound": "mfma", "achieved": kf / t_dom / 1e12, "peak": peak_mfma / 1e12,
+                "unit": "TFLOP/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = traffic_from_profiles(dom, args.workload)
+    roof["kernel"] = dom
+    roof["kernel_ms"] = kern_ms[dom]
+
+    flops = path_flops(w, tokens_heads)
+    nbytes = path_bytes(w, tokens_heads, n_states, d.get("h0") is not None)
+    res = {
+        "metric": METRIC,
+        "value": tokens / (ms / 1e3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if w.dtype == "f32" else "bf16",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "B": w.B, "T": w.T, "H": w.H, "dk": w.dk,
+                   "dv": w.dv, "chunk": CH, "backward": w.backward,
+                   "num_seqs": n_states},
+        "mfma_frac": flops / (ms / 1e3) / peak_mfma,
+        "hbm_frac": nbytes / (ms / 1e3) / PEAK_HBM,
+        "path_gflop": flops / 1e9,
+        "path_gbytes": nbytes / 1e9,
+        "kernels_ms": kern_ms,
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(inp, w)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -107,6 +107,36 @@ gdn_status gdn_chunk_bwd(const gdn_problem *p, const void *q, const void *k,
                          void *dv, float *dbeta, float *dlog_alpha, float *dh0,
                          void *workspace, size_t workspace_bytes, void *stream);
 
+/* Optional launch timing, for benchmarks and profilers.  The caller creates
+ * and owns the events (hipEvent_t handles, e.g. from hipEventCreate).  A
+ * *_timed call records events[2i] just before and events[2i+1] just after
+ * its i-th kernel launch on `stream`, for the first capacity/2 launches, and
+ * reports how many launches it made and their kernel names (static strings
+ * owned by the library).  Durations are read with hipEventElapsedTime once
+ * the stream has passed the events.  With timing == NULL a *_timed call is
+ * exactly the plain call.  Same arguments, checks and statuses otherwise. */
+typedef struct {
+  void **events;        /* in : hipEvent_t handles                */
+  int32_t capacity;     /* in : number of handles in `events`     */
+  int32_t launched;     /* out: kernel launches made by the call  */
+  const char *names[8]; /* out: kernel name of launch i           */
+} gdn_timing;
+
+gdn_status gdn_chunk_fwd_timed(const gdn_problem *p, const void *q,
+                               const void *k, const void *v, const float *beta,
+                               const float *log_alpha, const float *h0, void *o,
+                               float *ht, void *workspace,
+                               size_t workspace_bytes, void *stream,
+                               gdn_timing *timing);
+gdn_status gdn_chunk_bwd_timed(const gdn_problem *p, const void *q,
+                               const void *k, const void *v, const float *beta,
+                               const float *log_alpha, const float *h0,
+                               const void *dO, const float *dht, void *dq,
+                               void *dk, void *dv, float *dbeta,
+                               float *dlog_alpha, float *dh0, void *workspace,
+                               size_t workspace_bytes, void *stream,
+                               gdn_timing *timing);
+
 /* Human-readable name of a status. */
 const char *gdn_status_string(gdn_status s);
 

@@ -81,14 +81,28 @@ size_t carve(const gdn_problem* p, const Shape& s, bool backward, unsigned char*
   unsigned char* Tm = take(NC * H * CH * CH * sizeof(float));
   unsigned char* Pm = take(NC * H * CH * CH * sizeof(float));
   unsigned char* Ak = take(NC * H * CH * CH * sizeof(float));
+  // per-chunk operands in fragment layouts (element type of the problem)
+  const size_t kside = NC * H * CH * (size_t)p->dk * s.esz;  // 64 x dk
+  const size_t vside = NC * H * CH * (size_t)p->dv * s.esz;  // 64 x dv
+  unsigned char* Wf = take(kside);
+  unsigned char* KbT = take(kside);
+  unsigned char* Uc = take(vside);
+  unsigned char *Qf = nullptr, *Oc = nullptr, *nWT = nullptr, *QgT = nullptr, *TT = nullptr,
+                *dVi = nullptr;
   unsigned char *Sc = nullptr, *Vp = nullptr, *dSc = nullptr, *dXb = nullptr;
-  if (backward) {
+  if (!backward) {
+    Qf = take(kside);
+    Oc = take(vside);
+  } else {
+    nWT = take(kside);
+    QgT = take(kside);
+    TT = take(NC * H * CH * CH * s.esz);
+    dVi = take(vside);
     const size_t st = NC * H * (size_t)p->dk * p->dv * s.esz;
-    const size_t rows = NC * H * CH * (size_t)p->dv * s.esz;
     Sc = take(st);
     dSc = take(st);
-    Vp = take(rows);
-    dXb = take(rows);
+    Vp = take(vside);
+    dXb = take(vside);
   }
   if (a) {
     a->info = (int4*)info;
@@ -97,6 +111,15 @@ size_t carve(const gdn_problem* p, const Shape& s, bool backward, unsigned char*
     a->Tm = (float*)Tm;
     a->Pm = (float*)Pm;
     a->Ak = (float*)Ak;
+    a->Wf = Wf;
+    a->KbT = KbT;
+    a->Uc = Uc;
+    a->Qf = Qf;
+    a->Oc = Oc;
+    a->nWT = nWT;
+    a->QgT = QgT;
+    a->TT = TT;
+    a->dVi = dVi;
     a->Sc = Sc;
     a->Vp = Vp;
     a->dSc = dSc;
@@ -104,6 +127,29 @@ size_t carve(const gdn_problem* p, const Shape& s, bool backward, unsigned char*
   }
   return off;
 }
+
+// Bridges the C timing struct to the launchers' view of it.
+class TimingGuard {
+ public:
+  explicit TimingGuard(gdn_timing* t) : t_(t) {
+    if (t_) {
+      t_->launched = 0;
+      for (auto& n : t_->names) n = nullptr;
+      impl_.events = (hipEvent_t*)t_->events;
+      impl_.capacity = t_->events ? t_->capacity : 0;
+      impl_.launched = 0;
+      impl_.names = t_->names;
+    }
+  }
+  ~TimingGuard() {
+    if (t_) t_->launched = impl_.launched;
+  }
+  gdn::Timing* get() { return t_ ? &impl_ : nullptr; }
+
+ private:
+  gdn_timing* t_;
+  gdn::Timing impl_{};
+};
 
 void fill_common(const gdn_problem* p, const Shape& s, Args* a) {
   a->H = p->H;
@@ -129,9 +175,10 @@ size_t gdn_chunk_bwd_workspace_size(const gdn_problem* p) {
   return carve(p, s, true, nullptr, nullptr);
 }
 
-gdn_status gdn_chunk_fwd(const gdn_problem* p, const void* q, const void* k, const void* v,
-                         const float* beta, const float* log_alpha, const float* h0, void* o,
-                         float* ht, void* workspace, size_t workspace_bytes, void* stream) {
+gdn_status gdn_chunk_fwd_timed(const gdn_problem* p, const void* q, const void* k,
+                               const void* v, const float* beta, const float* log_alpha,
+                               const float* h0, void* o, float* ht, void* workspace,
+                               size_t workspace_bytes, void* stream, gdn_timing* timing) {
   Shape s;
   gdn_status st = check_problem(p, &s);
   if (st != GDN_OK) return st;
@@ -153,16 +200,25 @@ gdn_status gdn_chunk_fwd(const gdn_problem* p, const void* q, const void* k, con
   a.h0 = h0;
   a.o = o;
   a.ht = ht;
+  TimingGuard tg(timing);
   const hipError_t e = gdn::launch_fwd(p->dtype == GDN_F32 ? Dt::F32 : Dt::BF16, p->dk, p->dv, a,
-                                       (hipStream_t)stream);
+                                       (hipStream_t)stream, tg.get());
   return e == hipSuccess ? GDN_OK : GDN_ERR_HIP;
 }
 
-gdn_status gdn_chunk_bwd(const gdn_problem* p, const void* q, const void* k, const void* v,
-                         const float* beta, const float* log_alpha, const float* h0,
-                         const void* dO, const float* dht, void* dq, void* dk, void* dv,
-                         float* dbeta, float* dlog_alpha, float* dh0, void* workspace,
-                         size_t workspace_bytes, void* stream) {
+gdn_status gdn_chunk_fwd(const gdn_problem* p, const void* q, const void* k, const void* v,
+                         const float* beta, const float* log_alpha, const float* h0, void* o,
+                         float* ht, void* workspace, size_t workspace_bytes, void* stream) {
+  return gdn_chunk_fwd_timed(p, q, k, v, beta, log_alpha, h0, o, ht, workspace, workspace_bytes,
+                             stream, nullptr);
+}
+
+gdn_status gdn_chunk_bwd_timed(const gdn_problem* p, const void* q, const void* k,
+                               const void* v, const float* beta, const float* log_alpha,
+                               const float* h0, const void* dO, const float* dht, void* dq,
+                               void* dk, void* dv, float* dbeta, float* dlog_alpha, float* dh0,
+                               void* workspace, size_t workspace_bytes, void* stream,
+                               gdn_timing* timing) {
   Shape s;
   gdn_status st = check_problem(p, &s);
   if (st != GDN_OK) return st;
@@ -193,9 +249,19 @@ gdn_status gdn_chunk_bwd(const gdn_problem* p, const void* q, const void* k, con
   a.dbeta = dbeta;
   a.dlog_alpha = dlog_alpha;
   a.dh0 = dh0;
+  TimingGuard tg(timing);
   const hipError_t e = gdn::launch_bwd(p->dtype == GDN_F32 ? Dt::F32 : Dt::BF16, p->dk, p->dv, a,
-                                       (hipStream_t)stream);
+                                       (hipStream_t)stream, tg.get());
   return e == hipSuccess ? GDN_OK : GDN_ERR_HIP;
+}
+
+gdn_status gdn_chunk_bwd(const gdn_problem* p, const void* q, const void* k, const void* v,
+                         const float* beta, const float* log_alpha, const float* h0,
+                         const void* dO, const float* dht, void* dq, void* dk, void* dv,
+                         float* dbeta, float* dlog_alpha, float* dh0, void* workspace,
+                         size_t workspace_bytes, void* stream) {
+  return gdn_chunk_bwd_timed(p, q, k, v, beta, log_alpha, h0, dO, dht, dq, dk, dv, dbeta,
+                             dlog_alpha, dh0, workspace, workspace_bytes, stream, nullptr);
 }
 
 const char* gdn_status_string(gdn_status s) {

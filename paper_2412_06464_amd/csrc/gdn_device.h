@@ -168,6 +168,99 @@ __device__ inline void stage_mat64(E* dst, const float* g) {
   }
 }
 
+// ---- operand layouts in HBM
+// A-fragment layout of an R x KD matrix M (logical row-major): the MFMA A
+// tile (mt, kt) covers rows 16mt.. and k = K*kt..; lane l's KPL elements
+// M[16mt + (l & 15)][K*kt + KPL*(l >> 4) + j] are stored contiguously at
+// ((mt * (KD / K) + kt) * 64 + l) * KPL, so a wave reads one tile with one
+// fully coalesced load (1 KiB for bf16).
+template <class E>
+__device__ inline size_t afrag_index(int mt, int kt, int KD) {
+  using M = Mfma<E>;
+  return ((size_t)(mt * (KD / M::K) + kt) * 64 + lane_id()) * M::KPL;
+}
+
+// C-fragment (accumulator) layout of an R x N matrix: tile (mt, nt), lane l
+// holds rows 16mt + 4(l >> 4) + e, column 16nt + (l & 15), stored at
+// ((mt * (N / 16) + nt) * 64 + l) * 4 + e.
+__device__ inline size_t cfrag_index(int mt, int nt, int N) {
+  return ((size_t)(mt * (N / 16) + nt) * 64 + lane_id()) * 4;
+}
+
+template <class E>
+__device__ inline f32x4 load4(const E* p);
+template <>
+__device__ inline f32x4 load4<float>(const float* p) {
+  const float4 x = *reinterpret_cast<const float4*>(p);
+  return f32x4{x.x, x.y, x.z, x.w};
+}
+template <>
+__device__ inline f32x4 load4<bf16>(const bf16* p) {
+  typedef bf16 bf16x4 __attribute__((ext_vector_type(4)));
+  const bf16x4 x = *reinterpret_cast<const bf16x4*>(p);
+  return f32x4{(float)x[0], (float)x[1], (float)x[2], (float)x[3]};
+}
+template <class E>
+__device__ inline void store4(E* p, f32x4 v) {
+  p[0] = to_e<E>(v[0]);
+  p[1] = to_e<E>(v[1]);
+  p[2] = to_e<E>(v[2]);
+  p[3] = to_e<E>(v[3]);
+}
+
+// Write an R x KD matrix in A-fragment layout; val(r, k) gives its elements.
+template <class E, int R, int KD, int NTH, class F>
+__device__ inline void export_afrag(E* dst, F&& val) {
+  using M = Mfma<E>;
+  constexpr int UNITS = R * KD / M::KPL;
+  for (int u = threadIdx.x; u < UNITS; u += NTH) {
+    const int tile = u >> 6, l = u & 63;
+    const int mt = tile / (KD / M::K), kt = tile - mt * (KD / M::K);
+    const int r = mt * 16 + (l & 15), k0 = kt * M::K + (l >> 4) * M::KPL;
+    union {
+      typename M::frag f;
+      E e[M::KPL];
+    } x;
+#pragma unroll
+    for (int j = 0; j < M::KPL; ++j) x.e[j] = to_e<E>(val(r, k0 + j));
+    *reinterpret_cast<typename M::frag*>(dst + (size_t)u * M::KPL) = x.f;
+  }
+}
+
+// acc[i][j] (+)= sum_k A_i[k] * Bt[j*16 + n][k] with the A operand already in
+// registers (a[i][kk] = fragment of row tile i, k-step kk) and Bt in LDS.
+template <class E, int MT, int NT, int NK>
+__device__ inline void mma_regA(f32x4 (&acc)[MT][NT], const typename Mfma<E>::frag (&a)[MT][NK],
+                                const E* Bt, int ldb) {
+  using M = Mfma<E>;
+  const int l = lane_id();
+  const int r = l & 15, kq = (l >> 4) * M::KPL;
+#pragma unroll
+  for (int kk = 0; kk < NK; ++kk) {
+    typename M::frag b[NT];
+#pragma unroll
+    for (int j = 0; j < NT; ++j) b[j] = M::load(Bt + (j * 16 + r) * ldb + kk * M::K + kq);
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int j = 0; j < NT; ++j) acc[i][j] = M::mma(a[i][kk], b[j], acc[i][j]);
+  }
+}
+
+// Copy a [ROWS][W] tile from LDS (leading dim LD) to global rows (stride rs),
+// 16-byte vectors, rows >= nvalid skipped.
+template <class E, int ROWS, int W, int LD, int NTH>
+__device__ inline void copy_out_rows(E* g, size_t rs, const E* lds, int nvalid) {
+  constexpr int EPV = 16 / sizeof(E);
+  constexpr int VPR = W / EPV;
+  for (int idx = threadIdx.x; idx < ROWS * VPR; idx += NTH) {
+    const int r = idx / VPR, cv = idx - r * VPR;
+    if (r < nvalid)
+      *reinterpret_cast<uint4*>(g + (size_t)r * rs + cv * EPV) =
+          *reinterpret_cast<const uint4*>(lds + r * LD + cv * EPV);
+  }
+}
+
 // Inclusive prefix sum across the 64 lanes of a wave.
 __device__ inline float wave_incl_scan(float x) {
   const int l = lane_id();

@@ -7,6 +7,7 @@
 namespace gdn {
 
 // One packed description of a call.  Device pointers unless noted.
+// Per-chunk buffers are indexed by ch = chunk * H + head.
 struct Args {
   int H;       // heads
   int N;       // sequences (dense: B)
@@ -19,24 +20,66 @@ struct Args {
   // outputs
   void *o, *dq, *dk, *dv;
   float *ht, *dbeta, *dlog_alpha, *dh0;
-  // workspace
+  // workspace: chunk table and per-chunk fp32 matrices
   int4* info;       // [NC] {sequence, first token row, length, 0}
   int* seq_chunk0;  // [N+1] first chunk of every sequence
-  float* g;         // [NC][H][64]     cumulative log gate inside the chunk
-  float* Tm;        // [NC][H][64][64] (I + A)^-1
-  float* Pm;        // [NC][H][64][64] Gamma * Q K^T (lower, with diagonal)
-  float* Ak;        // [NC][H][64][64] strictLower(Gamma * K K^T)
-  void* Sc;         // [NC][H][dk][dv] chunk entry states          (backward)
-  void* Vp;         // [NC][H][64][dv] V' = T X                    (backward)
-  void* dSc;        // [NC][H][dk][dv] gradient of each exit state (backward)
-  void* dXb;        // [NC][H][64][dv] dX = T^T dV'                (backward)
+  float* g;         // [ch][64]     cumulative log gate inside the chunk
+  float* Tm;        // [ch][64][64] T = (I + A)^-1
+  float* Pm;        // [ch][64][64] Gamma * Q K^T (lower, with diagonal)
+  float* Ak;        // [ch][64][64] strictLower(Gamma * K K^T)
+  // workspace: per-chunk operands in MFMA fragment layouts (dtype E)
+  void* Wf;   // W~ = T diag(b e^g) K            64 x dk, A layout (rows t)
+  void* KbT;  // Kbar^T = (diag(e^{gn-g}) K)^T    dk x 64, A layout (rows d)
+  void* Qf;   // Qeff = diag(e^g) Q - P W~        64 x dk, A layout   (forward)
+  void* nWT;  // -W~^T                            dk x 64, A layout   (backward)
+  void* QgT;  // (diag(e^g) Q)^T                  dk x 64, A layout   (backward)
+  void* TT;   // T^T                              64 x 64, A layout   (backward)
+  void* Uc;   // U~ = T diag(b) V                 64 x dv, C layout
+  void* Oc;   // P U~                             64 x dv, C layout   (forward)
+  void* dVi;  // P^T dO                           64 x dv, C layout   (backward)
+  // workspace: backward intermediates, row-major
+  void* Sc;   // [ch][dk][dv] chunk entry states
+  void* Vp;   // [ch][64][dv] V' = U~ - W~ S
+  void* dSc;  // [ch][dk][dv] gradient of each chunk's exit state
+  void* dXb;  // [ch][64][dv] dX = T^T dV'
 };
 
 enum class Dt { F32, BF16 };
 
-// Launch the forward / backward kernel sequence for one (dtype, dk, dv).
-// Return the first launch error (hipSuccess if none).
-hipError_t launch_fwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s);
-hipError_t launch_bwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s);
+// Optional event recording around every launch (caller-owned events).
+struct Timing {
+  hipEvent_t* events;
+  int capacity;
+  int launched;
+  const char** names;  // at least 8 entries
+};
+
+// Individual launches (each returns the launch status).
+hipError_t launch_chunk_table(const Args& a, hipStream_t s);
+hipError_t launch_prep_a(Dt dt, int dk, int dv, const Args& a, hipStream_t s);
+hipError_t launch_prep_w(Dt dt, int dk, int dv, bool fwd, const Args& a, hipStream_t s);
+hipError_t launch_prep_u(Dt dt, int dk, int dv, bool fwd, const Args& a, hipStream_t s);
+hipError_t launch_fwd_seq(Dt dt, int dk, int dv, bool store, const Args& a, hipStream_t s);
+hipError_t launch_bwd_seq(Dt dt, int dk, int dv, const Args& a, hipStream_t s);
+hipError_t launch_grad(Dt dt, int dk, int dv, const Args& a, hipStream_t s);
+
+// The forward / backward sequences, with optional timing.
+hipError_t launch_fwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t);
+hipError_t launch_bwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t);
+
+// Call a lambda templated on (element type, dk, dv) for the supported
+// shapes; returns hipErrorInvalidValue for anything else.
+#define GDN_DISPATCH(dt, dk, dv, f)                                                         \
+  do {                                                                                      \
+    if ((dt) == Dt::F32 && (dk) == 64 && (dv) == 64)                                        \
+      return (f).template operator()<float, 64, 64>();                                      \
+    if ((dt) == Dt::BF16 && (dk) == 64 && (dv) == 64)                                       \
+      return (f).template operator()<__bf16, 64, 64>();                                     \
+    if ((dt) == Dt::BF16 && (dk) == 128 && (dv) == 128)                                     \
+      return (f).template operator()<__bf16, 128, 128>();                                   \
+    if ((dt) == Dt::BF16 && (dk) == 256 && (dv) == 512)                                     \
+      return (f).template operator()<__bf16, 256, 512>();                                   \
+    return hipErrorInvalidValue;                                                            \
+  } while (0)
 
 }  // namespace gdn

@@ -1,0 +1,63 @@
+// Launch sequences of the forward and backward calls, with optional event
+// recording around every launch.
+#include "gdn_kernels.h"
+
+namespace gdn {
+
+namespace {
+
+// Run one launch, bracketed by the caller's timing events if any.
+template <class F>
+hipError_t timed(Timing* t, const char* name, hipStream_t s, F&& launch) {
+  const int i = t ? t->launched : 0;
+  const bool rec = t && 2 * i + 1 < t->capacity;
+  if (rec && hipEventRecord(t->events[2 * i], s) != hipSuccess) return hipErrorInvalidValue;
+  const hipError_t e = launch();
+  if (e != hipSuccess) return e;
+  if (rec && hipEventRecord(t->events[2 * i + 1], s) != hipSuccess) return hipErrorInvalidValue;
+  if (t) {
+    if (i < 8) t->names[i] = name;
+    t->launched = i + 1;
+  }
+  return hipSuccess;
+}
+
+}  // namespace
+
+hipError_t launch_fwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t) {
+  hipError_t e;
+  if ((e = timed(t, "k_chunk_table", s, [&] { return launch_chunk_table(a, s); })) != hipSuccess)
+    return e;
+  if ((e = timed(t, "k_prep_a", s, [&] { return launch_prep_a(dt, dk, dv, a, s); })) != hipSuccess)
+    return e;
+  if ((e = timed(t, "k_prep_w", s, [&] { return launch_prep_w(dt, dk, dv, true, a, s); })) !=
+      hipSuccess)
+    return e;
+  if ((e = timed(t, "k_prep_u", s, [&] { return launch_prep_u(dt, dk, dv, true, a, s); })) !=
+      hipSuccess)
+    return e;
+  return timed(t, "k_fwd_seq", s, [&] { return launch_fwd_seq(dt, dk, dv, false, a, s); });
+}
+
+hipError_t launch_bwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t) {
+  hipError_t e;
+  if ((e = timed(t, "k_chunk_table", s, [&] { return launch_chunk_table(a, s); })) != hipSuccess)
+    return e;
+  if ((e = timed(t, "k_prep_a", s, [&] { return launch_prep_a(dt, dk, dv, a, s); })) != hipSuccess)
+    return e;
+  if ((e = timed(t, "k_prep_w", s, [&] { return launch_prep_w(dt, dk, dv, false, a, s); })) !=
+      hipSuccess)
+    return e;
+  if ((e = timed(t, "k_prep_u", s, [&] { return launch_prep_u(dt, dk, dv, false, a, s); })) !=
+      hipSuccess)
+    return e;
+  if ((e = timed(t, "k_fwd_seq_store", s,
+                 [&] { return launch_fwd_seq(dt, dk, dv, true, a, s); })) != hipSuccess)
+    return e;
+  if ((e = timed(t, "k_bwd_seq", s, [&] { return launch_bwd_seq(dt, dk, dv, a, s); })) !=
+      hipSuccess)
+    return e;
+  return timed(t, "k_grad", s, [&] { return launch_grad(dt, dk, dv, a, s); });
+}
+
+}  // namespace gdn

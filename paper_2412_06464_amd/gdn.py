@@ -19,7 +19,8 @@ GDN_F32, GDN_BF16 = 0, 1
 STATUS = {0: "GDN_OK", 1: "GDN_ERR_NULL", 2: "GDN_ERR_SHAPE", 3: "GDN_ERR_UNSUPPORTED",
           4: "GDN_ERR_CU_SEQLENS", 5: "GDN_ERR_WORKSPACE", 6: "GDN_ERR_HIP", 7: "GDN_ERR_ALIGN"}
 EXPORTS = ("gdn_chunk_fwd", "gdn_chunk_bwd", "gdn_chunk_fwd_workspace_size",
-           "gdn_chunk_bwd_workspace_size", "gdn_status_string")
+           "gdn_chunk_bwd_workspace_size", "gdn_chunk_fwd_timed", "gdn_chunk_bwd_timed",
+           "gdn_status_string")
 
 
 class Problem(ctypes.Structure):
@@ -27,6 +28,47 @@ class Problem(ctypes.Structure):
                 ("dk", ctypes.c_int32), ("dv", ctypes.c_int32), ("num_seqs", ctypes.c_int32),
                 ("cu_seqlens", ctypes.c_void_p), ("cu_seqlens_host", ctypes.c_void_p),
                 ("dtype", ctypes.c_int)]
+
+
+class Timing(ctypes.Structure):
+    _fields_ = [("events", ctypes.POINTER(ctypes.c_void_p)), ("capacity", ctypes.c_int32),
+                ("launched", ctypes.c_int32), ("names", ctypes.c_char_p * 8)]
+
+
+class LaunchTimer:
+    """Caller-owned HIP events for the *_timed entry points (2 per launch)."""
+
+    def __init__(self, max_launches: int = 8):
+        self._hip = ctypes.CDLL("libamdhip64.so")
+        self._hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self._hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float),
+                                                  ctypes.c_void_p, ctypes.c_void_p]
+        self._hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        n = 2 * max_launches
+        self.events = (ctypes.c_void_p * n)()
+        for i in range(n):
+            ev = ctypes.c_void_p()
+            if self._hip.hipEventCreate(ctypes.byref(ev)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+            self.events[i] = ev.value
+        self.timing = Timing(ctypes.cast(self.events, ctypes.POINTER(ctypes.c_void_p)), n, 0)
+
+    def durations_ms(self):
+        """{kernel name: ms} of the last timed call (stream must have passed it)."""
+        out = {}
+        for i in range(min(self.timing.launched, len(self.events) // 2)):
+            ms = ctypes.c_float()
+            if self._hip.hipEventElapsedTime(ctypes.byref(ms), self.events[2 * i],
+                                             self.events[2 * i + 1]) != 0:
+                raise RuntimeError("hipEventElapsedTime failed")
+            out[self.timing.names[i].decode()] = ms.value
+        return out
+
+    def close(self):
+        for e in self.events:
+            if e:
+                self._hip.hipEventDestroy(e)
+        self.events = (ctypes.c_void_p * 0)()
 
 
 class GdnError(RuntimeError):
@@ -56,6 +98,11 @@ def load_library():
         lib.gdn_chunk_fwd.restype = ctypes.c_int
         lib.gdn_chunk_bwd.argtypes = [pp] + [P] * 14 + [P, S, P]
         lib.gdn_chunk_bwd.restype = ctypes.c_int
+        pt = ctypes.POINTER(Timing)
+        lib.gdn_chunk_fwd_timed.argtypes = [pp] + [P] * 8 + [P, S, P, pt]
+        lib.gdn_chunk_fwd_timed.restype = ctypes.c_int
+        lib.gdn_chunk_bwd_timed.argtypes = [pp] + [P] * 14 + [P, S, P, pt]
+        lib.gdn_chunk_bwd_timed.restype = ctypes.c_int
         lib.gdn_status_string.argtypes = [ctypes.c_int]
         lib.gdn_status_string.restype = ctypes.c_char_p
         _lib = lib
@@ -112,12 +159,13 @@ def _nstate(q, cu_seqlens):
 
 
 def gdn_chunk_fwd(q, k, v, beta, log_alpha, h0=None, cu_seqlens=None, cu_seqlens_host=None,
-                  output_final_state=True, o=None, ht=None, workspace=None):
+                  output_final_state=True, o=None, ht=None, workspace=None, timer=None):
     """Forward of the chunkwise gated delta rule on the current stream.
 
     q, k [B,T,H,dk] and v [B,T,H,dv] (fp32 or bf16, same dtype), beta and
     log_alpha [B,T,H] fp32, h0 [Nseq,H,dk,dv] fp32 or None; packed input
     passes cu_seqlens (int32 [N+1], device) with B == 1.  Returns (o, ht).
+    ``timer`` (a LaunchTimer) routes the call through gdn_chunk_fwd_timed.
     """
     lib = load_library()
     p, keep = make_problem(q, v, cu_seqlens, cu_seqlens_host)
@@ -133,16 +181,20 @@ def gdn_chunk_fwd(q, k, v, beta, log_alpha, h0=None, cu_seqlens=None, cu_seqlens
         _check(lib.gdn_chunk_fwd(ctypes.byref(p), *[None] * 8, None, 0, None))
     if workspace is None or workspace.numel() < need:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
-    _check(lib.gdn_chunk_fwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(beta),
-                             _ptr(log_alpha), _ptr(h0), _ptr(o), _ptr(ht), _ptr(workspace),
-                             workspace.numel(), _stream(q.device)))
+    args = (ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(beta), _ptr(log_alpha), _ptr(h0),
+            _ptr(o), _ptr(ht), _ptr(workspace), workspace.numel(), _stream(q.device))
+    if timer is None:
+        _check(lib.gdn_chunk_fwd(*args))
+    else:
+        _check(lib.gdn_chunk_fwd_timed(*args, ctypes.byref(timer.timing)))
     del keep
     return o, ht
 
 
 def gdn_chunk_bwd(q, k, v, beta, log_alpha, dO, h0=None, dht=None, cu_seqlens=None,
-                  cu_seqlens_host=None, need_dh0=True, workspace=None, out=None):
-    """Backward (stateless): returns dict dq, dk, dv, dbeta, dlog_alpha, dh0."""
+                  cu_seqlens_host=None, need_dh0=True, workspace=None, out=None, timer=None):
+    """Backward (stateless): returns dict dq, dk, dv, dbeta, dlog_alpha, dh0.
+    ``timer`` (a LaunchTimer) routes the call through gdn_chunk_bwd_timed."""
     lib = load_library()
     p, keep = make_problem(q, v, cu_seqlens, cu_seqlens_host)
     B, T, H, dk = q.shape
@@ -157,10 +209,13 @@ def gdn_chunk_bwd(q, k, v, beta, log_alpha, dO, h0=None, dht=None, cu_seqlens=No
         _check(lib.gdn_chunk_bwd(ctypes.byref(p), *[None] * 14, None, 0, None))
     if workspace is None or workspace.numel() < need:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
-    _check(lib.gdn_chunk_bwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(beta),
-                             _ptr(log_alpha), _ptr(h0), _ptr(dO), _ptr(dht), _ptr(out["dq"]),
-                             _ptr(out["dk"]), _ptr(out["dv"]), _ptr(out["dbeta"]),
-                             _ptr(out["dlog_alpha"]), _ptr(out["dh0"]), _ptr(workspace),
-                             workspace.numel(), _stream(q.device)))
+    args = (ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(beta), _ptr(log_alpha), _ptr(h0),
+            _ptr(dO), _ptr(dht), _ptr(out["dq"]), _ptr(out["dk"]), _ptr(out["dv"]),
+            _ptr(out["dbeta"]), _ptr(out["dlog_alpha"]), _ptr(out["dh0"]), _ptr(workspace),
+            workspace.numel(), _stream(q.device))
+    if timer is None:
+        _check(lib.gdn_chunk_bwd(*args))
+    else:
+        _check(lib.gdn_chunk_bwd_timed(*args, ctypes.byref(timer.timing)))
     del keep
     return out
