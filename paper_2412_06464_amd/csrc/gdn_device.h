@@ -54,6 +54,16 @@ template <> __device__ inline bf16 to_e<bf16>(float x) { return (bf16)x; }  // R
 __device__ inline float to_f(float x) { return x; }
 __device__ inline float to_f(bf16 x) { return (float)x; }
 
+// Workgroup barrier that orders LDS traffic only: each wave waits for its
+// own outstanding LDS operations and then meets the others.  Unlike
+// __syncthreads(), whose workgroup-scope fence also waits for every
+// outstanding global load, this leaves prefetched global loads in flight
+// across the barrier.  It must not be used to publish global-memory writes
+// to other threads of the workgroup.
+__device__ inline void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 __device__ inline int lane_id() { return threadIdx.x & 63; }
 __device__ inline int wave_id() { return threadIdx.x >> 6; }
 

@@ -100,7 +100,7 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
     stage_rows<E, CH, BVG, LDG, NTH>(sVp, (const E*)a.Vp + ch * CH * DV + v0, DV, CH);
     stage_rows<E, DK, BVG, LDG, NTH>(sS, (const E*)a.Sc + ch * DK * DV + v0, DV, DK);
     stage_rows<E, DK, BVG, LDG, NTH>(sdS, (const E*)a.dSc + ch * DK * DV + v0, DV, DK);
-    __syncthreads();
+    lds_barrier();
     const E* Arow = sdO + wr * RTW * 16 * LDG;
     const E* Brow = sS + wc * CTW * 16 * LDG;
     wave_mma_nt<E, RTW, CTW, BVG>(Gq, Arow, LDG, Brow, LDG);
@@ -118,7 +118,7 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
       for (int vv = part * (BVG / 8); vv < (part + 1) * (BVG / 8); ++vv)
         xvp += to_f(sdX[t * LDG + vv]) * to_f(sV[t * LDG + vv]);
     }
-    __syncthreads();
+    lds_barrier();
   }
 
   // reductions of <dS_next, S> and dX . V
@@ -135,7 +135,7 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
   }
   stage_rows_T<E, DK, LDC, NTH>(sKT, K + row0 * DK, (size_t)H * DK, len, nullptr);
   stage_rows_T<E, DK, LDC, NTH>(sQT, Q + row0 * DK, (size_t)H * DK, len, nullptr);
-  __syncthreads();
+  lds_barrier();
 
   // intra-chunk matrices
   float ea[4][4];
@@ -203,7 +203,7 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
         }
       }
   }
-  __syncthreads();
+  lds_barrier();
   if (pm == 1) {
 #pragma unroll
     for (int j = 0; j < 4; ++j)
@@ -213,7 +213,7 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
         sE[r * LDE + i] += ea[j][e];
       }
   }
-  __syncthreads();
+  lds_barrier();
   for (int idx = tid; idx < CH * CH; idx += NTH) {
     const int r = idx >> 6, i = idx & 63;
     sDD[r * LDC + i] = to_e<E>(sD[r * LDE + i] + sD[i * LDE + r]);
@@ -228,7 +228,7 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
     for (int j = 0; j < CH; ++j) s += sE[j * LDE + col];
     sEcol[col] = s;
   }
-  __syncthreads();
+  lds_barrier();
 
   // dQ and dK
 #pragma unroll

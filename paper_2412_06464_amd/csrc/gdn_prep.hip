@@ -78,7 +78,7 @@ __global__ __launch_bounds__(256) void k_prep_a(Args a) {
     sb[tid] = tid < len ? a.beta[row0 + (size_t)tid * H] : 0.f;
     a.g[ch * CH + tid] = g;
   }
-  __syncthreads();
+  lds_barrier();
 
   // Gram blocks: wave w owns rows 16w..16w+15 of K K^T and Q K^T.
   f32x4 kk[1][4], qk[1][4];
@@ -101,7 +101,7 @@ __global__ __launch_bounds__(256) void k_prep_a(Args a) {
       gP[r * CH + i] = p;
       sA[r * LDA + i] = sb[r] * ak;
     }
-  __syncthreads();
+  lds_barrier();
 
   // T = (I + A)^-1, A strictly lower.  Diagonal 16x16 blocks by forward
   // substitution (one column per thread), then the off-diagonal blocks in
@@ -120,7 +120,7 @@ __global__ __launch_bounds__(256) void k_prep_a(Args a) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) sT[(o + i) * LDA + o + j] = x[i];
   }
-  __syncthreads();
+  lds_barrier();
   for (int d = 1; d < 4; ++d) {
     const int i = tid >> 4, j = tid & 15;
     for (int J = 0; J + d < 4; ++J) {
@@ -132,7 +132,7 @@ __global__ __launch_bounds__(256) void k_prep_a(Args a) {
           y += sA[(16 * I + i) * LDA + 16 * m + l] * sT[(16 * m + l) * LDA + 16 * J + j];
       sY[J * 272 + i * 17 + j] = y;
     }
-    __syncthreads();
+    lds_barrier();
     for (int J = 0; J + d < 4; ++J) {
       const int I = J + d;
       float t = 0.f;
@@ -140,7 +140,7 @@ __global__ __launch_bounds__(256) void k_prep_a(Args a) {
       for (int l = 0; l < 16; ++l) t -= sT[(16 * I + i) * LDA + 16 * I + l] * sY[J * 272 + l * 17 + j];
       sT[(16 * I + i) * LDA + 16 * J + j] = t;
     }
-    __syncthreads();
+    lds_barrier();
   }
   float* gT = a.Tm + ch * CH * CH;
   for (int idx = tid; idx < CH * CH; idx += 256) {
@@ -187,7 +187,7 @@ __global__ __launch_bounds__(256) void k_prep_w(Args a) {
     sdec[tid] = __expf(gn - g);
     sbeg[tid] = b * eg;
   }
-  __syncthreads();
+  lds_barrier();
 
   export_afrag<E, DK, CH, 256>((E*)a.KbT + ch * DK * CH, [&](int d, int t) {
     return sdec[t] * to_f(sK[t * LDK + d]);
@@ -196,7 +196,7 @@ __global__ __launch_bounds__(256) void k_prep_w(Args a) {
     const int t = idx & (CH - 1), d = idx >> 6;
     sX[d * LDC + t] = to_e<E>(sbeg[t] * to_f(sK[t * LDK + d]));
   }
-  __syncthreads();
+  lds_barrier();
 
   // W~ = T (b e^g K): wave w owns rows 16w..16w+15
   f32x4 W[1][NCT];
@@ -209,12 +209,12 @@ __global__ __launch_bounds__(256) void k_prep_w(Args a) {
     for (int e = 0; e < 4; ++e)
       sK[(w * 16 + acc_row(e)) * LDK + j * 16 + acc_col()] = to_e<E>(W[0][j][e]);
   }
-  __syncthreads();
+  lds_barrier();
   export_afrag<E, CH, DK, 256>((E*)a.Wf + ch * CH * DK,
                                [&](int t, int d) { return to_f(sK[t * LDK + d]); });
   if (FWD) {
     stage_rows<E, CH, DK, LDK, 256>(sX, Q, (size_t)H * DK, len);
-    __syncthreads();
+    lds_barrier();
     f32x4 Qe[1][NCT];
     zero_acc(Qe);
     wave_mma_nt<E, 1, NCT, CH>(Qe, sPe + w * 16 * LDC, LDC, sWT, LDC);
@@ -226,7 +226,7 @@ __global__ __launch_bounds__(256) void k_prep_w(Args a) {
         E& x = sX[r * LDK + d];  // each lane rewrites exactly the elements it reads
         x = to_e<E>(seg[r] * to_f(x) - Qe[0][j][e]);
       }
-    __syncthreads();
+    lds_barrier();
     export_afrag<E, CH, DK, 256>((E*)a.Qf + ch * CH * DK,
                                  [&](int t, int d) { return to_f(sX[t * LDK + d]); });
   } else {
@@ -235,7 +235,7 @@ __global__ __launch_bounds__(256) void k_prep_w(Args a) {
     export_afrag<E, CH, CH, 256>((E*)a.TT + ch * CH * CH,
                                  [&](int t, int i) { return to_f(sTe[i * LDC + t]); });
     stage_rows<E, CH, DK, LDK, 256>(sX, Q, (size_t)H * DK, len);
-    __syncthreads();
+    lds_barrier();
     export_afrag<E, DK, CH, 256>((E*)a.QgT + ch * DK * CH, [&](int d, int t) {
       return seg[t] * to_f(sX[t * LDK + d]);
     });
@@ -270,12 +270,12 @@ __global__ __launch_bounds__(256) void k_prep_u(Args a) {
   else
     stage_mat64<E, LDC, 256, true>(sPx, a.Pm + ch * CH * CH);
   if (tid < CH) sb[tid] = tid < len ? a.beta[row0 + (size_t)tid * H] : 0.f;
-  __syncthreads();
+  lds_barrier();
   stage_rows_T<E, VB, LDC, 256>(sVT, (const E*)a.v + row0 * DV + v0, (size_t)H * DV, len, sb);
   if (!FWD)
     stage_rows_T<E, VB, LDC, 256>(sYT, (const E*)a.dO + row0 * DV + v0, (size_t)H * DV, len,
                                   nullptr);
-  __syncthreads();
+  lds_barrier();
   f32x4 U[1][4];
   zero_acc(U);
   wave_mma_nt<E, 1, 4, CH>(U, sTe + w * 16 * LDC, LDC, sVT, LDC);
@@ -287,7 +287,7 @@ __global__ __launch_bounds__(256) void k_prep_u(Args a) {
   if (FWD) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) store_tile_T<E>(sYT, LDC, U[0][j], w * 16, j * 16);
-    __syncthreads();
+    lds_barrier();
   }
   wave_mma_nt<E, 1, 4, CH>(Y, sPx + w * 16 * LDC, LDC, sYT, LDC);
   E* gY = (E*)(FWD ? a.Oc : a.dVi) + ch * CH * DV;

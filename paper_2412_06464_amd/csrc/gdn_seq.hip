@@ -124,7 +124,7 @@ __global__ __launch_bounds__(256) void k_fwd_seq(Args a) {
                 to_e<E>(S[i][j][e]);
         }
       }
-    __syncthreads();
+    lds_barrier();
 
     // (b) W~ S and Qeff S for the wave's 16 token rows
     if (STORE) copy_out_rows<E, DK, BV, LDV, 256>((E*)a.Sc + ch * DK * DV + v0, DV, sSs, DK);
@@ -146,7 +146,7 @@ __global__ __launch_bounds__(256) void k_fwd_seq(Args a) {
       for (int e = 0; e < 4; ++e) sOut[(w * 16 + acc_row(e)) * LDV + j * 16 + acc_col()] = to_e<E>(y[e]);
     }
     if (c + 1 < c1) load_rows_side(c + 1);
-    __syncthreads();
+    lds_barrier();
 
     // (d) S <- e^{g_n} S + Kbar^T V'; write the chunk's rows out
     const float egn = __expf(gn);
@@ -297,7 +297,7 @@ __global__ __launch_bounds__(256) void k_bwd_seq(Args a) {
       sdec[tid] = __expf(gn - pg);
       sb[c & 1][tid] = pb;
     }
-    __syncthreads();
+    lds_barrier();
 
     // (b) dV' = P^T dO + Kbar dS  (P^T dO precomputed per chunk)
     copy_out_rows<E, DK, BV, LDV, 256>((E*)a.dSc + ch * DK * DV + v0, DV, sSs, DK);
@@ -311,7 +311,7 @@ __global__ __launch_bounds__(256) void k_bwd_seq(Args a) {
       for (int e = 0; e < 4; ++e) y[e] = sdec[w * 16 + acc_row(e)] * X[0][j][e] + uD[j][e];
       store_tile_T<E>(sdVT, LDC, y, w * 16, j * 16);
     }
-    __syncthreads();
+    lds_barrier();
 
     // (c) dX = T^T dV'; dS <- e^{g_n} dS + (e^g Q)^T dO - W~^T dV'
     f32x4 dX[1][NTV];
@@ -330,7 +330,7 @@ __global__ __launch_bounds__(256) void k_bwd_seq(Args a) {
     mma_regA<E, MTS, NTV, NKC>(dS, fQ, sdOT, LDC);
     mma_regA<E, MTS, NTV, NKC>(dS, fW, sdVT, LDC);
     if (c - 1 >= c0) load_chunk(c - 1);
-    __syncthreads();
+    lds_barrier();
 
     // (d) dX rows (all 64) to the workspace, dv = b dX rows to the output
     copy_out_rows<E, CH, BV, LDV, 256>((E*)a.dXb + ch * CH * DV + v0, DV, sOut, CH);
