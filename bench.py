@@ -67,24 +67,29 @@ def kernel_models(w, n_chunks_heads):
     e = 4 if w.dtype == "f32" else 2
     dk, dv, C = w.dk, w.dv, CH
     f32 = 4
-    mat = C * C * f32                  # one 64 x 64 fp32 matrix (T, P, Ak)
     kside, vside, st = C * dk * e, C * dv * e, dk * dv * e
+    cc = C * C * e                     # one 64 x 64 operand in the element type
+    gates = 2 * C * f32
     prod_dk = 2 * C * C * dk           # 64 x 64 times 64 x dk
     prod_dv = 2 * C * C * dv
     prod_s = 2 * C * dk * dv           # chunk rows times a dk x dv state
     per = {
-        # q, k, gates in; g, T, P, Ak out; K K^T, Q K^T, triangular inverse
-        "k_prep_a": (2 * kside + 8 * C + 4 * C + 3 * mat, 2 * prod_dk + C ** 3 / 3),
-        "fwd:k_prep_w": (2 * kside + 2 * mat + 8 * C + 3 * kside, 2 * prod_dk),
-        "bwd:k_prep_w": (2 * kside + mat + 8 * C + 4 * kside + C * C * e, prod_dk),
-        "fwd:k_prep_u": (vside + 2 * mat + 4 * C + 2 * vside, 2 * prod_dv),
-        "bwd:k_prep_u": (2 * vside + 2 * mat + 4 * C + 2 * vside, 2 * prod_dv),
-        "k_fwd_seq": (3 * kside + 3 * vside + 4 * C, 3 * prod_s),
-        "k_fwd_seq_store": (2 * kside + vside + st + vside + 4 * C, 2 * prod_s),
-        "k_bwd_seq": (3 * kside + C * C * e + 2 * vside + 8 * C + st + 2 * vside,
-                      3 * prod_s + prod_dv),
-        "k_grad": (2 * st + 2 * kside + 4 * vside + 2 * mat + 8 * C + 2 * kside + 8 * C,
-                   3 * prod_s + 2 * prod_dv + 3 * prod_dk),
+        # q, k, v, gates in; g, W~, Kbar^T, U~, P out; Gram, inverse, W~, U~
+        "fwd:k_prep": (2 * kside + vside + gates + C * f32 + 2 * kside + vside + cc,
+                       3 * prod_dk + prod_dv + C ** 3 / 3),
+        # as forward, plus P^T, T^T, -W~^T, (e^g Q)^T, and P, Ak in fp32
+        "bwd:k_prep": (2 * kside + vside + gates + C * f32 + 4 * kside + vside + 2 * cc
+                       + 2 * C * C * f32, 4 * prod_dk + prod_dv + C ** 3 / 3),
+        # W~, q, Kbar^T, P, U~, g in; o out
+        "k_fwd_seq": (3 * kside + cc + vside + C * f32 + vside, 3 * prod_s + prod_dv),
+        # W~, Kbar^T, U~ in; chunk states and V' out
+        "k_fwd_seq_store": (2 * kside + vside + C * f32 + st + vside, 2 * prod_s),
+        # k, (e^g Q)^T, -W~^T, P^T, T^T, dO, g, beta in; dS, dX, dv out
+        "k_bwd_seq": (3 * kside + 2 * cc + vside + gates + st + 2 * vside,
+                      3 * prod_s + 2 * prod_dv),
+        # S, dS, q, k, v, dO, V', dX, P, Ak, gates in; dq, dk, dbeta, dlog_alpha out
+        "k_grad": (2 * st + 2 * kside + 4 * vside + 2 * C * C * f32 + 2 * gates
+                   + 2 * kside + gates, 3 * prod_s + 2 * prod_dv + 3 * prod_dk),
         "k_chunk_table": (0, 0),
     }
     return {k: (b * n_chunks_heads, f * n_chunks_heads) for k, (b, f) in per.items()}

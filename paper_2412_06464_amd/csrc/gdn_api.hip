@@ -78,26 +78,25 @@ size_t carve(const gdn_problem* p, const Shape& s, bool backward, unsigned char*
   unsigned char* info = take(NC * sizeof(int4) + 16);
   unsigned char* sc0 = take(((size_t)s.N + 1) * sizeof(int));
   unsigned char* g = take(NC * H * CH * sizeof(float));
-  unsigned char* Tm = take(NC * H * CH * CH * sizeof(float));
-  unsigned char* Pm = take(NC * H * CH * CH * sizeof(float));
-  unsigned char* Ak = take(NC * H * CH * CH * sizeof(float));
   // per-chunk operands in fragment layouts (element type of the problem)
   const size_t kside = NC * H * CH * (size_t)p->dk * s.esz;  // 64 x dk
   const size_t vside = NC * H * CH * (size_t)p->dv * s.esz;  // 64 x dv
+  const size_t cc = NC * H * CH * CH * s.esz;                // 64 x 64
   unsigned char* Wf = take(kside);
   unsigned char* KbT = take(kside);
   unsigned char* Uc = take(vside);
-  unsigned char *Qf = nullptr, *Oc = nullptr, *nWT = nullptr, *QgT = nullptr, *TT = nullptr,
-                *dVi = nullptr;
+  unsigned char *Pf = nullptr, *PTf = nullptr, *TTf = nullptr, *nWT = nullptr, *QgT = nullptr;
+  unsigned char *Pm = nullptr, *Ak = nullptr;
   unsigned char *Sc = nullptr, *Vp = nullptr, *dSc = nullptr, *dXb = nullptr;
   if (!backward) {
-    Qf = take(kside);
-    Oc = take(vside);
+    Pf = take(cc);
   } else {
+    PTf = take(cc);
+    TTf = take(cc);
     nWT = take(kside);
     QgT = take(kside);
-    TT = take(NC * H * CH * CH * s.esz);
-    dVi = take(vside);
+    Pm = take(NC * H * CH * CH * sizeof(float));
+    Ak = take(NC * H * CH * CH * sizeof(float));
     const size_t st = NC * H * (size_t)p->dk * p->dv * s.esz;
     Sc = take(st);
     dSc = take(st);
@@ -108,18 +107,16 @@ size_t carve(const gdn_problem* p, const Shape& s, bool backward, unsigned char*
     a->info = (int4*)info;
     a->seq_chunk0 = (int*)sc0;
     a->g = (float*)g;
-    a->Tm = (float*)Tm;
-    a->Pm = (float*)Pm;
-    a->Ak = (float*)Ak;
     a->Wf = Wf;
     a->KbT = KbT;
     a->Uc = Uc;
-    a->Qf = Qf;
-    a->Oc = Oc;
+    a->Pf = Pf;
+    a->PTf = PTf;
+    a->TTf = TTf;
     a->nWT = nWT;
     a->QgT = QgT;
-    a->TT = TT;
-    a->dVi = dVi;
+    a->Pm = (float*)Pm;
+    a->Ak = (float*)Ak;
     a->Sc = Sc;
     a->Vp = Vp;
     a->dSc = dSc;

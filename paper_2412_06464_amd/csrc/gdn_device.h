@@ -271,6 +271,150 @@ __device__ inline void copy_out_rows(E* g, size_t rs, const E* lds, int nvalid) 
   }
 }
 
+// ---- permuted contraction order
+// An MFMA sums over its K index in any order, provided both operands agree.
+// The kernels use an order in which the accumulator tiles of a matrix are
+// directly the B operand of a product that contracts over that matrix's
+// rows (and the A operand of one that contracts over the rows of its
+// transpose):
+//   bf16, k-step kt covers k in [32 kt, 32 kt + 32); lane group g = l >> 4,
+//         slot j holds k = 32 kt + 4 g + j (j < 4) or 32 kt + 12 + 4 g + j
+//         (j >= 4), i.e. rows 4g..4g+3 of the two 16-row accumulator tiles
+//         2 kt and 2 kt + 1;
+//   fp32, k-step kt holds k = 16 (kt >> 2) + 4 g + (kt & 3), i.e. element
+//         (kt & 3) of accumulator tile kt >> 2.
+// Every operand that meets such an accumulator-derived operand in a product
+// is stored (or loaded) in the same order.
+template <class E> __device__ inline int kperm(int kt, int g, int j);
+template <> __device__ inline int kperm<bf16>(int kt, int g, int j) {
+  return 32 * kt + (j < 4 ? 4 * g + j : 12 + 4 * g + j);
+}
+template <> __device__ inline int kperm<float>(int kt, int g, int) {
+  return 16 * (kt >> 2) + 4 * g + (kt & 3);
+}
+
+// Fragment buffers.  A "B buffer" holds the B operands of a K x N matrix
+// (N = 16 NT): fragment (kt, nt) of lane l at ((kt NT + nt) 64 + l) KPL.
+// An "A buffer" holds the A operands of an R x KD matrix: fragment (mt, kt)
+// of lane l at ((mt (KD / K) + kt) 64 + l) KPL.  Both are written from an
+// accumulator tile whose rows run along K (for an A buffer: the tile of the
+// transposed matrix), one 8-byte (bf16) or four 4-byte (fp32) stores per
+// lane, each wave store fully coalesced.
+__device__ inline size_t frag_slot_bf16(size_t frag, int i16) {
+  return (frag * 64 + lane_id()) * 8 + (i16 & 1) * 4;
+}
+template <class E> __device__ inline void bfrag_put(E* buf, int NT, int i16, int n, f32x4 v);
+template <> __device__ inline void bfrag_put<bf16>(bf16* buf, int NT, int i16, int n, f32x4 v) {
+  typedef bf16 bf16x4 __attribute__((ext_vector_type(4)));
+  const bf16x4 x = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3]};
+  *reinterpret_cast<bf16x4*>(buf + frag_slot_bf16((size_t)(i16 >> 1) * NT + n, i16)) = x;
+}
+template <> __device__ inline void bfrag_put<float>(float* buf, int NT, int i16, int n, f32x4 v) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) buf[((size_t)(4 * i16 + e) * NT + n) * 64 + lane_id()] = v[e];
+}
+template <class E>
+__device__ inline typename Mfma<E>::frag bfrag_get(const E* buf, int NT, int kt, int n) {
+  return Mfma<E>::load(buf + ((size_t)(kt * NT + n) * 64 + lane_id()) * Mfma<E>::KPL);
+}
+// A buffer of an R x KD matrix M from the accumulator tile of M^T that
+// covers k rows 16 i16.. and M rows 16 mt..
+template <class E> __device__ inline void afrag_put_T(E* dst, int KD, int mt, int i16, f32x4 v);
+template <> __device__ inline void afrag_put_T<bf16>(bf16* dst, int KD, int mt, int i16, f32x4 v) {
+  typedef bf16 bf16x4 __attribute__((ext_vector_type(4)));
+  const bf16x4 x = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3]};
+  *reinterpret_cast<bf16x4*>(dst + frag_slot_bf16((size_t)mt * (KD / 32) + (i16 >> 1), i16)) = x;
+}
+template <> __device__ inline void afrag_put_T<float>(float* dst, int KD, int mt, int i16, f32x4 v) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) dst[((size_t)mt * (KD / 4) + 4 * i16 + e) * 64 + lane_id()] = v[e];
+}
+
+// A operand, permuted order, read straight from a row-major row of a global
+// matrix (`row` points at the row, k-step kt); zero when !valid.
+template <class E>
+__device__ inline typename Mfma<E>::frag load_row_perm(const E* row, int kt, bool valid);
+template <>
+__device__ inline bf16x8 load_row_perm<bf16>(const bf16* row, int kt, bool valid) {
+  typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+  union {
+    bf16x8 f;
+    u32x2 h[2];
+  } x;
+  x.h[0] = u32x2{0u, 0u};
+  x.h[1] = u32x2{0u, 0u};
+  if (valid) {
+    const int g = lane_id() >> 4;
+    x.h[0] = *reinterpret_cast<const u32x2*>(row + 32 * kt + 4 * g);
+    x.h[1] = *reinterpret_cast<const u32x2*>(row + 32 * kt + 16 + 4 * g);
+  }
+  return x.f;
+}
+template <>
+__device__ inline float load_row_perm<float>(const float* row, int kt, bool valid) {
+  return valid ? row[kperm<float>(kt, lane_id() >> 4, 0)] : 0.f;
+}
+
+// Same, with `p` already pointing at the lane's first element of k-step 0
+// (row + 4 g for bf16, row + 4 g for fp32).
+template <class E>
+__device__ inline typename Mfma<E>::frag load_row_perm_at(const E* p, int kt, bool valid);
+template <>
+__device__ inline bf16x8 load_row_perm_at<bf16>(const bf16* p, int kt, bool valid) {
+  typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+  union {
+    bf16x8 f;
+    u32x2 h[2];
+  } x;
+  x.h[0] = u32x2{0u, 0u};
+  x.h[1] = u32x2{0u, 0u};
+  if (valid) {
+    x.h[0] = *reinterpret_cast<const u32x2*>(p + 32 * kt);
+    x.h[1] = *reinterpret_cast<const u32x2*>(p + 32 * kt + 16);
+  }
+  return x.f;
+}
+template <>
+__device__ inline float load_row_perm_at<float>(const float* p, int kt, bool valid) {
+  return valid ? p[16 * (kt >> 2) + (kt & 3)] : 0.f;
+}
+
+// Write the A buffer (permuted order) of an R x KD matrix whose elements are
+// val(r, k).
+template <class E, int R, int KD, int NTH, class F>
+__device__ inline void export_afrag_perm(E* dst, F&& val) {
+  using M = Mfma<E>;
+  constexpr int UNITS = R * KD / M::KPL;
+  for (int u = threadIdx.x; u < UNITS; u += NTH) {
+    const int tile = u >> 6, l = u & 63;
+    const int mt = tile / (KD / M::K), kt = tile - mt * (KD / M::K);
+    const int r = mt * 16 + (l & 15), g = l >> 4;
+    union {
+      typename M::frag f;
+      E e[M::KPL];
+    } x;
+#pragma unroll
+    for (int j = 0; j < M::KPL; ++j) x.e[j] = to_e<E>(val(r, kperm<E>(kt, g, j)));
+    *reinterpret_cast<typename M::frag*>(dst + (size_t)u * M::KPL) = x.f;
+  }
+}
+
+// A or B operand (standard order) of row `row` of an LDS matrix, k-step kt,
+// element k multiplied by sc[k].
+template <class E>
+__device__ inline typename Mfma<E>::frag load_frag_scaled(const E* row, int kt, const float* sc) {
+  using M = Mfma<E>;
+  const int k0 = kt * M::K + (lane_id() >> 4) * M::KPL;
+  union {
+    typename M::frag f;
+    E e[M::KPL];
+  } x;
+  x.f = M::load(row + k0);
+#pragma unroll
+  for (int j = 0; j < M::KPL; ++j) x.e[j] = to_e<E>(to_f(x.e[j]) * sc[k0 + j]);
+  return x.f;
+}
+
 // Inclusive prefix sum across the 64 lanes of a wave.
 __device__ inline float wave_incl_scan(float x) {
   const int l = lane_id();

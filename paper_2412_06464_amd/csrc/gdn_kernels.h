@@ -20,25 +20,24 @@ struct Args {
   // outputs
   void *o, *dq, *dk, *dv;
   float *ht, *dbeta, *dlog_alpha, *dh0;
-  // workspace: chunk table and per-chunk fp32 matrices
+  // workspace: chunk table and per-chunk gates
   int4* info;       // [NC] {sequence, first token row, length, 0}
   int* seq_chunk0;  // [N+1] first chunk of every sequence
   float* g;         // [ch][64]     cumulative log gate inside the chunk
-  float* Tm;        // [ch][64][64] T = (I + A)^-1
-  float* Pm;        // [ch][64][64] Gamma * Q K^T (lower, with diagonal)
-  float* Ak;        // [ch][64][64] strictLower(Gamma * K K^T)
-  // workspace: per-chunk operands in MFMA fragment layouts (dtype E)
-  void* Wf;   // W~ = T diag(b e^g) K            64 x dk, A layout (rows t)
-  void* KbT;  // Kbar^T = (diag(e^{gn-g}) K)^T    dk x 64, A layout (rows d)
-  void* Qf;   // Qeff = diag(e^g) Q - P W~        64 x dk, A layout   (forward)
-  void* nWT;  // -W~^T                            dk x 64, A layout   (backward)
-  void* QgT;  // (diag(e^g) Q)^T                  dk x 64, A layout   (backward)
-  void* TT;   // T^T                              64 x 64, A layout   (backward)
-  void* Uc;   // U~ = T diag(b) V                 64 x dv, C layout
-  void* Oc;   // P U~                             64 x dv, C layout   (forward)
-  void* dVi;  // P^T dO                           64 x dv, C layout   (backward)
-  // workspace: backward intermediates, row-major
-  void* Sc;   // [ch][dk][dv] chunk entry states
+  // workspace: per-chunk operands of the sequential passes (dtype E), as MFMA
+  // A operands in fragment order with the permuted contraction order
+  void* Wf;   // W~ = T diag(b e^g) K      rows t, k = d     64 x dk
+  void* KbT;  // Kbar^T                    rows d, k = t     dk x 64
+  void* Uc;   // U~ = T diag(b) V          accumulator layout 64 x dv
+  void* Pf;   // P                         rows t, k = t'    64 x 64  (forward)
+  void* PTf;  // P^T                       rows t', k = t    64 x 64  (backward)
+  void* TTf;  // T^T                       rows t', k = t    64 x 64  (backward)
+  void* nWT;  // -W~^T                     rows d, k = t     dk x 64  (backward)
+  void* QgT;  // (diag(e^g) Q)^T           rows d, k = t     dk x 64  (backward)
+  // workspace: backward intermediates for the gradient kernel
+  float* Pm;  // [ch][64][64] P, fp32
+  float* Ak;  // [ch][64][64] strictLower(Gamma * K K^T), fp32
+  void* Sc;   // [ch][dk][dv] chunk entry states (row-major)
   void* Vp;   // [ch][64][dv] V' = U~ - W~ S
   void* dSc;  // [ch][dk][dv] gradient of each chunk's exit state
   void* dXb;  // [ch][64][dv] dX = T^T dV'
@@ -56,9 +55,7 @@ struct Timing {
 
 // Individual launches (each returns the launch status).
 hipError_t launch_chunk_table(const Args& a, hipStream_t s);
-hipError_t launch_prep_a(Dt dt, int dk, int dv, const Args& a, hipStream_t s);
-hipError_t launch_prep_w(Dt dt, int dk, int dv, bool fwd, const Args& a, hipStream_t s);
-hipError_t launch_prep_u(Dt dt, int dk, int dv, bool fwd, const Args& a, hipStream_t s);
+hipError_t launch_prep(Dt dt, int dk, int dv, bool bwd, const Args& a, hipStream_t s);
 hipError_t launch_fwd_seq(Dt dt, int dk, int dv, bool store, const Args& a, hipStream_t s);
 hipError_t launch_bwd_seq(Dt dt, int dk, int dv, const Args& a, hipStream_t s);
 hipError_t launch_grad(Dt dt, int dk, int dv, const Args& a, hipStream_t s);

@@ -28,12 +28,7 @@ hipError_t launch_fwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timin
   hipError_t e;
   if ((e = timed(t, "k_chunk_table", s, [&] { return launch_chunk_table(a, s); })) != hipSuccess)
     return e;
-  if ((e = timed(t, "k_prep_a", s, [&] { return launch_prep_a(dt, dk, dv, a, s); })) != hipSuccess)
-    return e;
-  if ((e = timed(t, "k_prep_w", s, [&] { return launch_prep_w(dt, dk, dv, true, a, s); })) !=
-      hipSuccess)
-    return e;
-  if ((e = timed(t, "k_prep_u", s, [&] { return launch_prep_u(dt, dk, dv, true, a, s); })) !=
+  if ((e = timed(t, "k_prep", s, [&] { return launch_prep(dt, dk, dv, false, a, s); })) !=
       hipSuccess)
     return e;
   return timed(t, "k_fwd_seq", s, [&] { return launch_fwd_seq(dt, dk, dv, false, a, s); });
@@ -43,12 +38,7 @@ hipError_t launch_bwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timin
   hipError_t e;
   if ((e = timed(t, "k_chunk_table", s, [&] { return launch_chunk_table(a, s); })) != hipSuccess)
     return e;
-  if ((e = timed(t, "k_prep_a", s, [&] { return launch_prep_a(dt, dk, dv, a, s); })) != hipSuccess)
-    return e;
-  if ((e = timed(t, "k_prep_w", s, [&] { return launch_prep_w(dt, dk, dv, false, a, s); })) !=
-      hipSuccess)
-    return e;
-  if ((e = timed(t, "k_prep_u", s, [&] { return launch_prep_u(dt, dk, dv, false, a, s); })) !=
+  if ((e = timed(t, "k_prep", s, [&] { return launch_prep(dt, dk, dv, true, a, s); })) !=
       hipSuccess)
     return e;
   if ((e = timed(t, "k_fwd_seq_store", s,

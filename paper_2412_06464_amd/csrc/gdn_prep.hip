@@ -1,15 +1,14 @@
-// Parallel per-chunk preparation kernels (gfx950) of the chunkwise gated
-// delta rule.  Chunk algebra (Sec. 3.3 of the paper; state stored dk x dv,
-// the transpose of the paper's dv x dk state), for one chunk of n <= 64
-// tokens with beta b and cumulative log gate g (restarted at every chunk,
-// Sec. 2.1 footnote):
+// Parallel per-chunk preparation (gfx950) of the chunkwise gated delta rule.
+// Chunk algebra (Sec. 3.3 of the paper; state stored dk x dv, the transpose
+// of the paper's dv x dk state), for one chunk of n <= 64 tokens with beta b
+// and cumulative log gate g (restarted at every chunk, Sec. 2.1 footnote):
 //   Gamma_ri = exp(g_r - g_i) for i <= r          (decay-aware causal mask)
 //   A  = strictLower(diag(b) (Gamma * K K^T)),   T = (I + A)^-1
 //   W~ = T diag(b e^g) K,   U~ = T diag(b) V       (gated UT transform)
 //   P  = Gamma * Q K^T   (lower, with the diagonal)
 // With these, for entry state S:  V' = U~ - W~ S,
-//   O = diag(e^g) Q S + P V' = Qeff S + P U~   (Qeff = diag(e^g) Q - P W~),
-//   S_next = e^{g_n} S + Kbar^T V'             (Kbar = diag(e^{g_n - g}) K).
+//   O = diag(e^g) Q S + P V',   S_next = e^{g_n} S + Kbar^T V'
+//   (Kbar = diag(e^{g_n - g}) K).
 // W~ is the paper's decayed W (decay on the left of the ungated UT
 // transform) rewritten with the gated inverse: diag(e^g) (I + A_u)^-1 =
 // (I + A_g)^-1 diag(e^g) when A_g = diag(e^g) A_u diag(e^-g).  The output
@@ -17,16 +16,16 @@
 // does not reproduce the recurrence.
 //
 //   k_chunk_table  chunk -> (sequence, first row, length)
-//   k_prep_a       g, Ak, P, T per (chunk, head)                     (fp32)
-//   k_prep_w       W~, Kbar^T, and Qeff (forward) or -W~^T, (e^g Q)^T, T^T
-//                  (backward) in MFMA A-fragment layout
-//   k_prep_u       U~, and P U~ (forward) or P^T dO (backward) in
-//                  accumulator layout, per 64-wide block of dv
+//   k_prep         one workgroup per (chunk, head): g, Gram matrices, T in
+//                  LDS, then the operands of the sequential passes, streamed
+//                  over 64-wide slices of dk and dv.  Forward: W~, Kbar^T, U~,
+//                  P.  Backward (recompute): W~, Kbar^T, U~, and for the
+//                  reverse pass P^T, T^T, -W~^T, (e^g Q)^T, plus P and
+//                  strictLower(Gamma K K^T) in fp32 for the gradient kernel.
 #include "gdn_device.h"
 #include "gdn_kernels.h"
 
 namespace gdn {
-
 
 __global__ void k_chunk_table(const int32_t* cu, int N, int T, int4* info, int* seq_chunk0) {
   if (threadIdx.x == 0) {
@@ -48,19 +47,24 @@ __global__ void k_chunk_table(const int32_t* cu, int N, int T, int4* info, int* 
 }
 
 // ------------------------------------------------------------------ prep
-// Grid (NC, H), 256 threads.  Writes g, Ak, Pm and Tm of one chunk-head.
+// Grid (NC, H), 256 threads (4 waves).  LDS stays below 80 KB for bf16 so
+// that two workgroups share a CU: one streams while the other solves.
 
-template <class E, int DK>
-__global__ __launch_bounds__(256) void k_prep_a(Args a) {
+template <class E, int DK, int DV, bool BWD>
+__global__ __launch_bounds__(256, 2) void k_prep(Args a) {
+  using M = Mfma<E>;
   constexpr int PADE = 16 / sizeof(E);
-  constexpr int LDK = DK + PADE;
+  constexpr int LD = CH + PADE;  // rows of 64 elements
   constexpr int LDA = CH + 1;
-  __shared__ __align__(16) E sK[CH * LDK];
-  __shared__ __align__(16) E sQ[CH * LDK];
-  __shared__ float sA[CH * LDA];
-  __shared__ float sT[CH * LDA];
-  __shared__ float sY[3 * 16 * 17];
-  __shared__ float sg[CH], sb[CH];
+  constexpr int NKC = CH / M::K;
+  __shared__ __align__(16) E sX[CH * LD];  // K slice (Gram), then K_s^T or (b V_s)^T
+  __shared__ __align__(16) E sY[CH * LD];  // Q slice (Gram), then Q_s^T (backward)
+  __shared__ __align__(16) E sT[CH * LD];  // T, row-major
+  __shared__ __align__(16) E sP[CH * LD];  // P, row-major
+  __shared__ float sA[CH * LDA];           // diag(b) A
+  __shared__ float sTf[CH * LDA];          // T in fp32
+  __shared__ float sYb[3 * 16 * 17];
+  __shared__ float sg[CH], sb[CH], seg[CH], sdec[CH], sbeg[CH];
 
   const int c = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = wave_id();
   const int H = a.H;
@@ -68,26 +72,36 @@ __global__ __launch_bounds__(256) void k_prep_a(Args a) {
   const int start = ci.y, len = ci.z;
   const size_t ch = (size_t)c * H + h;
   const size_t row0 = (size_t)start * H + h;
+  const E* K = (const E*)a.k + row0 * DK;
+  const E* Q = (const E*)a.q + row0 * DK;
+  const E* V = (const E*)a.v + row0 * DV;
 
-  stage_rows<E, CH, DK, LDK, 256>(sK, (const E*)a.k + row0 * DK, (size_t)H * DK, len);
-  stage_rows<E, CH, DK, LDK, 256>(sQ, (const E*)a.q + row0 * DK, (size_t)H * DK, len);
   if (tid < CH) {
     const float la = tid < len ? a.log_alpha[row0 + (size_t)tid * H] : 0.f;
     const float g = wave_incl_scan(la);  // pads repeat g at the last token
+    const float gn = __shfl(g, CH - 1, 64);
+    const float b = tid < len ? a.beta[row0 + (size_t)tid * H] : 0.f;
     sg[tid] = g;
-    sb[tid] = tid < len ? a.beta[row0 + (size_t)tid * H] : 0.f;
+    sb[tid] = b;
+    seg[tid] = __expf(g);
+    sdec[tid] = __expf(gn - g);
+    sbeg[tid] = b * __expf(g);
     a.g[ch * CH + tid] = g;
   }
-  lds_barrier();
 
-  // Gram blocks: wave w owns rows 16w..16w+15 of K K^T and Q K^T.
+  // ---- Gram blocks K K^T and Q K^T over 64-wide slices of dk; wave w owns
+  // rows 16w..16w+15.
   f32x4 kk[1][4], qk[1][4];
   zero_acc(kk);
   zero_acc(qk);
-  wave_mma_nt<E, 1, 4, DK>(kk, sK + w * 16 * LDK, LDK, sK, LDK);
-  wave_mma_nt<E, 1, 4, DK>(qk, sQ + w * 16 * LDK, LDK, sK, LDK);
-  float* gAk = a.Ak + ch * CH * CH;
-  float* gP = a.Pm + ch * CH * CH;
+  for (int s = 0; s < DK / 64; ++s) {
+    stage_rows<E, CH, 64, LD, 256>(sX, K + 64 * s, (size_t)H * DK, len);
+    stage_rows<E, CH, 64, LD, 256>(sY, Q + 64 * s, (size_t)H * DK, len);
+    lds_barrier();
+    wave_mma_nt<E, 1, 4, 64>(kk, sX + w * 16 * LD, LD, sX, LD);
+    wave_mma_nt<E, 1, 4, 64>(qk, sY + w * 16 * LD, LD, sX, LD);
+    lds_barrier();
+  }
 #pragma unroll
   for (int j = 0; j < 4; ++j)
 #pragma unroll
@@ -97,13 +111,16 @@ __global__ __launch_bounds__(256) void k_prep_a(Args a) {
       const float gam = (i <= r) ? __expf(sg[r] - sg[i]) : 0.f;
       const float ak = (i < r) ? gam * kk[0][j][e] : 0.f;
       const float p = (i <= r) ? gam * qk[0][j][e] : 0.f;
-      gAk[r * CH + i] = ak;
-      gP[r * CH + i] = p;
       sA[r * LDA + i] = sb[r] * ak;
+      sP[r * LD + i] = to_e<E>(p);
+      if (BWD) {
+        a.Ak[ch * CH * CH + r * CH + i] = ak;
+        a.Pm[ch * CH * CH + r * CH + i] = p;
+      }
     }
   lds_barrier();
 
-  // T = (I + A)^-1, A strictly lower.  Diagonal 16x16 blocks by forward
+  // ---- T = (I + A)^-1, A strictly lower.  Diagonal 16x16 blocks by forward
   // substitution (one column per thread), then the off-diagonal blocks in
   // order of their distance from the diagonal:
   //   T_IJ = -T_II * sum_{m=J}^{I-1} A_Im T_mJ.
@@ -118,7 +135,7 @@ __global__ __launch_bounds__(256) void k_prep_a(Args a) {
       x[i] = s;
     }
 #pragma unroll
-    for (int i = 0; i < 16; ++i) sT[(o + i) * LDA + o + j] = x[i];
+    for (int i = 0; i < 16; ++i) sTf[(o + i) * LDA + o + j] = x[i];
   }
   lds_barrier();
   for (int d = 1; d < 4; ++d) {
@@ -129,170 +146,102 @@ __global__ __launch_bounds__(256) void k_prep_a(Args a) {
       for (int m = J; m < I; ++m)
 #pragma unroll
         for (int l = 0; l < 16; ++l)
-          y += sA[(16 * I + i) * LDA + 16 * m + l] * sT[(16 * m + l) * LDA + 16 * J + j];
-      sY[J * 272 + i * 17 + j] = y;
+          y += sA[(16 * I + i) * LDA + 16 * m + l] * sTf[(16 * m + l) * LDA + 16 * J + j];
+      sYb[J * 272 + i * 17 + j] = y;
     }
     lds_barrier();
     for (int J = 0; J + d < 4; ++J) {
       const int I = J + d;
       float t = 0.f;
 #pragma unroll
-      for (int l = 0; l < 16; ++l) t -= sT[(16 * I + i) * LDA + 16 * I + l] * sY[J * 272 + l * 17 + j];
-      sT[(16 * I + i) * LDA + 16 * J + j] = t;
+      for (int l = 0; l < 16; ++l)
+        t -= sTf[(16 * I + i) * LDA + 16 * I + l] * sYb[J * 272 + l * 17 + j];
+      sTf[(16 * I + i) * LDA + 16 * J + j] = t;
     }
     lds_barrier();
   }
-  float* gT = a.Tm + ch * CH * CH;
   for (int idx = tid; idx < CH * CH; idx += 256) {
     const int r = idx >> 6, i = idx & 63;
-    gT[idx] = ((i >> 4) > (r >> 4)) ? 0.f : sT[r * LDA + i];
-  }
-}
-
-// ------------------------------------------------------------------ W~ and friends
-// Grid (NC, H), 256 threads.
-
-template <class E, int DK, bool FWD>
-__global__ __launch_bounds__(256) void k_prep_w(Args a) {
-  constexpr int PADE = 16 / sizeof(E);
-  constexpr int LDK = DK + PADE;  // [64][LDK]: rows of K, Q, W~
-  constexpr int LDC = CH + PADE;  // [..][LDC]: token-indexed rows
-  constexpr int NCT = DK / 16;
-  constexpr int XSZ = (DK * LDC > CH * LDK) ? DK * LDC : CH * LDK;
-  __shared__ __align__(16) E sTe[CH * LDC];
-  __shared__ __align__(16) E sPe[FWD ? CH * LDC : 1];
-  __shared__ __align__(16) E sK[CH * LDK];  // K rows, later W~ rows
-  __shared__ __align__(16) E sX[XSZ];       // (b e^g K)^T, later Q rows (Qeff in place)
-  __shared__ __align__(16) E sWT[DK * LDC]; // W~^T
-  __shared__ float sdec[CH], sbeg[CH], seg[CH];
-
-  const int c = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = wave_id();
-  const int H = a.H;
-  const int4 ci = a.info[c];
-  const int start = ci.y, len = ci.z;
-  const size_t ch = (size_t)c * H + h;
-  const size_t row0 = (size_t)start * H + h;
-  const E* K = (const E*)a.k + row0 * DK;
-  const E* Q = (const E*)a.q + row0 * DK;
-
-  stage_rows<E, CH, DK, LDK, 256>(sK, K, (size_t)H * DK, len);
-  stage_mat64<E, LDC, 256, false>(sTe, a.Tm + ch * CH * CH);
-  if (FWD) stage_mat64<E, LDC, 256, false>(sPe, a.Pm + ch * CH * CH);
-  if (tid < CH) {
-    const float g = a.g[ch * CH + tid];
-    const float gn = __shfl(g, len - 1, 64);
-    const float b = tid < len ? a.beta[row0 + (size_t)tid * H] : 0.f;
-    const float eg = __expf(g);
-    seg[tid] = eg;
-    sdec[tid] = __expf(gn - g);
-    sbeg[tid] = b * eg;
+    sT[r * LD + i] = to_e<E>(((i >> 4) > (r >> 4)) ? 0.f : sTf[r * LDA + i]);
   }
   lds_barrier();
 
-  export_afrag<E, DK, CH, 256>((E*)a.KbT + ch * DK * CH, [&](int d, int t) {
-    return sdec[t] * to_f(sK[t * LDK + d]);
-  });
-  for (int idx = tid; idx < DK * CH; idx += 256) {
-    const int t = idx & (CH - 1), d = idx >> 6;
-    sX[d * LDC + t] = to_e<E>(sbeg[t] * to_f(sK[t * LDK + d]));
-  }
-  lds_barrier();
-
-  // W~ = T (b e^g K): wave w owns rows 16w..16w+15
-  f32x4 W[1][NCT];
-  zero_acc(W);
-  wave_mma_nt<E, 1, NCT, CH>(W, sTe + w * 16 * LDC, LDC, sX, LDC);
-#pragma unroll
-  for (int j = 0; j < NCT; ++j) {
-    store_tile_T<E>(sWT, LDC, W[0][j], w * 16, j * 16);
-#pragma unroll
-    for (int e = 0; e < 4; ++e)
-      sK[(w * 16 + acc_row(e)) * LDK + j * 16 + acc_col()] = to_e<E>(W[0][j][e]);
-  }
-  lds_barrier();
-  export_afrag<E, CH, DK, 256>((E*)a.Wf + ch * CH * DK,
-                               [&](int t, int d) { return to_f(sK[t * LDK + d]); });
-  if (FWD) {
-    stage_rows<E, CH, DK, LDK, 256>(sX, Q, (size_t)H * DK, len);
-    lds_barrier();
-    f32x4 Qe[1][NCT];
-    zero_acc(Qe);
-    wave_mma_nt<E, 1, NCT, CH>(Qe, sPe + w * 16 * LDC, LDC, sWT, LDC);
-#pragma unroll
-    for (int j = 0; j < NCT; ++j)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int r = w * 16 + acc_row(e), d = j * 16 + acc_col();
-        E& x = sX[r * LDK + d];  // each lane rewrites exactly the elements it reads
-        x = to_e<E>(seg[r] * to_f(x) - Qe[0][j][e]);
-      }
-    lds_barrier();
-    export_afrag<E, CH, DK, 256>((E*)a.Qf + ch * CH * DK,
-                                 [&](int t, int d) { return to_f(sX[t * LDK + d]); });
+  // ---- 64 x 64 operands
+  if (!BWD) {
+    export_afrag_perm<E, CH, CH, 256>((E*)a.Pf + ch * CH * CH,
+                                      [&](int t, int i) { return to_f(sP[t * LD + i]); });
   } else {
-    export_afrag<E, DK, CH, 256>((E*)a.nWT + ch * DK * CH,
-                                 [&](int d, int t) { return -to_f(sWT[d * LDC + t]); });
-    export_afrag<E, CH, CH, 256>((E*)a.TT + ch * CH * CH,
-                                 [&](int t, int i) { return to_f(sTe[i * LDC + t]); });
-    stage_rows<E, CH, DK, LDK, 256>(sX, Q, (size_t)H * DK, len);
-    lds_barrier();
-    export_afrag<E, DK, CH, 256>((E*)a.QgT + ch * DK * CH, [&](int d, int t) {
-      return seg[t] * to_f(sX[t * LDK + d]);
-    });
+    export_afrag_perm<E, CH, CH, 256>((E*)a.PTf + ch * CH * CH,
+                                      [&](int i, int t) { return to_f(sP[t * LD + i]); });
+    export_afrag_perm<E, CH, CH, 256>((E*)a.TTf + ch * CH * CH,
+                                      [&](int i, int t) { return to_f(sT[t * LD + i]); });
   }
-}
 
-// ------------------------------------------------------------------ U~ and friends
-// Grid (NC, H, DV / 64), 256 threads: one 64-wide block of dv.
-
-template <class E, int DV, bool FWD>
-__global__ __launch_bounds__(256) void k_prep_u(Args a) {
-  constexpr int PADE = 16 / sizeof(E);
-  constexpr int LDC = CH + PADE;
-  constexpr int VB = 64;
-  __shared__ __align__(16) E sTe[CH * LDC];
-  __shared__ __align__(16) E sPx[CH * LDC];  // P (forward) or P^T (backward)
-  __shared__ __align__(16) E sVT[VB * LDC];  // (b V)^T block
-  __shared__ __align__(16) E sYT[VB * LDC];  // U~^T (forward) or dO^T (backward)
-  __shared__ float sb[CH];
-
-  const int c = blockIdx.x, h = blockIdx.y, v0 = blockIdx.z * VB;
-  const int tid = threadIdx.x, w = wave_id();
-  const int H = a.H;
-  const int4 ci = a.info[c];
-  const int start = ci.y, len = ci.z;
-  const size_t ch = (size_t)c * H + h;
-  const size_t row0 = (size_t)start * H + h;
-
-  stage_mat64<E, LDC, 256, false>(sTe, a.Tm + ch * CH * CH);
-  if (FWD)
-    stage_mat64<E, LDC, 256, false>(sPx, a.Pm + ch * CH * CH);
-  else
-    stage_mat64<E, LDC, 256, true>(sPx, a.Pm + ch * CH * CH);
-  if (tid < CH) sb[tid] = tid < len ? a.beta[row0 + (size_t)tid * H] : 0.f;
-  lds_barrier();
-  stage_rows_T<E, VB, LDC, 256>(sVT, (const E*)a.v + row0 * DV + v0, (size_t)H * DV, len, sb);
-  if (!FWD)
-    stage_rows_T<E, VB, LDC, 256>(sYT, (const E*)a.dO + row0 * DV + v0, (size_t)H * DV, len,
-                                  nullptr);
-  lds_barrier();
-  f32x4 U[1][4];
-  zero_acc(U);
-  wave_mma_nt<E, 1, 4, CH>(U, sTe + w * 16 * LDC, LDC, sVT, LDC);
-  E* gU = (E*)a.Uc + ch * CH * DV;
+  // ---- dk slices: W~ (and -W~^T), Kbar^T, (e^g Q)^T
+  for (int s = 0; s < DK / 64; ++s) {
+    stage_rows_T<E, 64, LD, 256>(sX, K + 64 * s, (size_t)H * DK, len, nullptr);  // sX[d][t]
+    if (BWD) stage_rows_T<E, 64, LD, 256>(sY, Q + 64 * s, (size_t)H * DK, len, nullptr);
+    lds_barrier();
+    // W~^T (rows d of this wave, columns t'):  sum_t (b e^g K)^T[d][t] T[t'][t]
+    f32x4 Wt[4];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) store4<E>(gU + cfrag_index(w, v0 / 16 + j, DV), U[0][j]);
-  f32x4 Y[1][4];
-  zero_acc(Y);
-  if (FWD) {
+    for (int n = 0; n < 4; ++n) Wt[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const E* xrow = sX + (w * 16 + (lane_id() & 15)) * LD;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) store_tile_T<E>(sYT, LDC, U[0][j], w * 16, j * 16);
+    for (int kt = 0; kt < NKC; ++kt) {
+      const typename M::frag af = load_frag_scaled<E>(xrow, kt, sbeg);
+#pragma unroll
+      for (int n = 0; n < 4; ++n) {
+        const typename M::frag bf =
+            M::load(sT + (n * 16 + (lane_id() & 15)) * LD + kt * M::K + (lane_id() >> 4) * M::KPL);
+        Wt[n] = M::mma(af, bf, Wt[n]);
+      }
+    }
+    // W~ as A operands (rows t', k = d) for the state passes
+#pragma unroll
+    for (int n = 0; n < 4; ++n) afrag_put_T<E>((E*)a.Wf + ch * CH * DK, DK, n, 4 * s + w, Wt[n]);
+    // Kbar^T as A operands (rows d, k = t)
+    export_afrag_perm<E, 64, CH, 256>((E*)a.KbT + ch * DK * CH + (size_t)64 * s * CH,
+                                      [&](int d, int t) { return sdec[t] * to_f(sX[d * LD + t]); });
+    if (BWD) {
+      // W~ (rows t' of this wave, columns d):  sum_t T[t'][t] (b e^g K)[t][d]
+      f32x4 W[4];
+#pragma unroll
+      for (int n = 0; n < 4; ++n) W[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+      const E* trow = sT + (w * 16 + (lane_id() & 15)) * LD;
+#pragma unroll
+      for (int kt = 0; kt < NKC; ++kt) {
+        const typename M::frag af =
+            M::load(trow + kt * M::K + (lane_id() >> 4) * M::KPL);
+#pragma unroll
+        for (int n = 0; n < 4; ++n) {
+          const typename M::frag bf =
+              load_frag_scaled<E>(sX + (n * 16 + (lane_id() & 15)) * LD, kt, sbeg);
+          W[n] = M::mma(af, bf, W[n]);
+        }
+      }
+      // -W~^T as A operands (rows d, k = t')
+#pragma unroll
+      for (int n = 0; n < 4; ++n) afrag_put_T<E>((E*)a.nWT + ch * DK * CH, CH, 4 * s + n, w, -W[n]);
+      // (e^g Q)^T as A operands (rows d, k = t)
+      export_afrag_perm<E, 64, CH, 256>((E*)a.QgT + ch * DK * CH + (size_t)64 * s * CH,
+                                        [&](int d, int t) { return seg[t] * to_f(sY[d * LD + t]); });
+    }
     lds_barrier();
   }
-  wave_mma_nt<E, 1, 4, CH>(Y, sPx + w * 16 * LDC, LDC, sYT, LDC);
-  E* gY = (E*)(FWD ? a.Oc : a.dVi) + ch * CH * DV;
+
+  // ---- dv slices: U~ = T (b V), accumulator layout
+  for (int s = 0; s < DV / 64; ++s) {
+    stage_rows_T<E, 64, LD, 256>(sX, V + 64 * s, (size_t)H * DV, len, sb);  // sX[v][t] = b_t V
+    lds_barrier();
+    f32x4 U[1][4];
+    zero_acc(U);
+    wave_mma_nt<E, 1, 4, CH>(U, sT + w * 16 * LD, LD, sX, LD);
+    E* gU = (E*)a.Uc + ch * CH * DV;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) store4<E>(gY + cfrag_index(w, v0 / 16 + j, DV), Y[0][j]);
+    for (int n = 0; n < 4; ++n) store4<E>(gU + cfrag_index(w, 4 * s + n, DV), U[0][n]);
+    lds_barrier();
+  }
 }
 
 // ------------------------------------------------------------------ launchers
@@ -303,31 +252,12 @@ hipError_t launch_chunk_table(const Args& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_prep_a(Dt dt, int dk, int dv, const Args& a, hipStream_t s) {
+hipError_t launch_prep(Dt dt, int dk, int dv, bool bwd, const Args& a, hipStream_t s) {
   auto f = [&]<class E, int DK, int DV>() {
-    hipLaunchKernelGGL((k_prep_a<E, DK>), dim3(a.NC, a.H), dim3(256), 0, s, a);
-    return hipGetLastError();
-  };
-  GDN_DISPATCH(dt, dk, dv, f);
-}
-
-hipError_t launch_prep_w(Dt dt, int dk, int dv, bool fwd, const Args& a, hipStream_t s) {
-  auto f = [&]<class E, int DK, int DV>() {
-    if (fwd)
-      hipLaunchKernelGGL((k_prep_w<E, DK, true>), dim3(a.NC, a.H), dim3(256), 0, s, a);
+    if (bwd)
+      hipLaunchKernelGGL((k_prep<E, DK, DV, true>), dim3(a.NC, a.H), dim3(256), 0, s, a);
     else
-      hipLaunchKernelGGL((k_prep_w<E, DK, false>), dim3(a.NC, a.H), dim3(256), 0, s, a);
-    return hipGetLastError();
-  };
-  GDN_DISPATCH(dt, dk, dv, f);
-}
-
-hipError_t launch_prep_u(Dt dt, int dk, int dv, bool fwd, const Args& a, hipStream_t s) {
-  auto f = [&]<class E, int DK, int DV>() {
-    if (fwd)
-      hipLaunchKernelGGL((k_prep_u<E, DV, true>), dim3(a.NC, a.H, DV / 64), dim3(256), 0, s, a);
-    else
-      hipLaunchKernelGGL((k_prep_u<E, DV, false>), dim3(a.NC, a.H, DV / 64), dim3(256), 0, s, a);
+      hipLaunchKernelGGL((k_prep<E, DK, DV, false>), dim3(a.NC, a.H), dim3(256), 0, s, a);
     return hipGetLastError();
   };
   GDN_DISPATCH(dt, dk, dv, f);

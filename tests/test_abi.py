@@ -57,10 +57,13 @@ def test_workspace_sizes(lib):
     p, _ = problem()
     f = gdn.gdn_chunk_fwd_workspace_size(p)
     b = gdn.gdn_chunk_bwd_workspace_size(p)
-    NC = 2 * 2  # two sequences of 100 tokens -> 2 chunks each
-    assert f >= NC * 3 * 64 * 64 * 4 * 3  # T, P and Ak per chunk-head
-    # backward adds entry states, exit-state gradients, V' and dX
-    assert b - f >= NC * 3 * (2 * 64 * 64 * 2 + 2 * 64 * 64 * 2)
+    NCH = 2 * 2 * 3  # two sequences of 100 tokens -> 2 chunks each, 3 heads
+    e = 2
+    # forward: W~, Kbar^T (64 x dk), U~ (64 x dv), P (64 x 64) per chunk-head
+    assert f >= NCH * (2 * 64 * 64 * e + 64 * 64 * e + 64 * 64 * e)
+    # backward adds entry states and exit-state gradients (dk x dv), V' and dX
+    # (64 x dv), and P, strictLower(Gamma K K^T) in fp32
+    assert b - f >= NCH * (2 * 64 * 64 * e + 2 * 64 * 64 * e + 2 * 64 * 64 * 4)
     bad, _ = problem(dk=96)
     assert gdn.gdn_chunk_fwd_workspace_size(bad) == 0
 
