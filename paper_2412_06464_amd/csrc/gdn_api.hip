@@ -86,11 +86,14 @@ size_t carve(const gdn_problem* p, const Shape& s, bool backward, unsigned char*
   unsigned char* KbT = take(kside);
   unsigned char* Uc = take(vside);
   unsigned char *Pf = nullptr, *PTf = nullptr, *TTf = nullptr, *nWT = nullptr, *QgT = nullptr;
+  unsigned char *Qf = nullptr, *Kf = nullptr;
   unsigned char *Pm = nullptr, *Ak = nullptr;
   unsigned char *Sc = nullptr, *Vp = nullptr, *dSc = nullptr, *dXb = nullptr;
   if (!backward) {
     Pf = take(cc);
+    Qf = take(kside);
   } else {
+    Kf = take(kside);
     PTf = take(cc);
     TTf = take(cc);
     nWT = take(kside);
@@ -111,6 +114,8 @@ size_t carve(const gdn_problem* p, const Shape& s, bool backward, unsigned char*
     a->KbT = KbT;
     a->Uc = Uc;
     a->Pf = Pf;
+    a->Qf = Qf;
+    a->Kf = Kf;
     a->PTf = PTf;
     a->TTf = TTf;
     a->nWT = nWT;

@@ -47,6 +47,15 @@ template <> struct Mfma<float> {
   __device__ static inline frag load(const float* p) { return *p; }
 };
 
+// Four raw elements of an accumulator-layout tile (converted at use).
+template <class E> struct Raw4;
+template <> struct Raw4<bf16> {
+  typedef bf16 type __attribute__((ext_vector_type(4)));
+};
+template <> struct Raw4<float> {
+  typedef f32x4 type;
+};
+
 template <class E> __device__ inline E to_e(float x);
 template <> __device__ inline float to_e<float>(float x) { return x; }
 template <> __device__ inline bf16 to_e<bf16>(float x) { return (bf16)x; }  // RNE
@@ -399,6 +408,28 @@ __device__ inline void export_afrag_perm(E* dst, F&& val) {
   }
 }
 
+// Write the A-buffer fragments (permuted order) that cover k in [k0, k0 + KS)
+// of an R x KD matrix whose elements are val(r, k) (k relative to k0).
+template <class E, int R, int KD, int KS, int NTH, class F>
+__device__ inline void export_afrag_perm_kslice(E* dst, int k0, F&& val) {
+  using M = Mfma<E>;
+  constexpr int NKS = KS / M::K;
+  constexpr int UNITS = R * KS / M::KPL;
+  for (int u = threadIdx.x; u < UNITS; u += NTH) {
+    const int tile = u >> 6, l = u & 63;
+    const int mt = tile / NKS, ktl = tile - mt * NKS;
+    const int r = mt * 16 + (l & 15), g = l >> 4;
+    union {
+      typename M::frag f;
+      E e[M::KPL];
+    } x;
+#pragma unroll
+    for (int j = 0; j < M::KPL; ++j) x.e[j] = to_e<E>(val(r, kperm<E>(ktl, g, j)));
+    const size_t frag = (size_t)mt * (KD / M::K) + k0 / M::K + ktl;
+    *reinterpret_cast<typename M::frag*>(dst + (frag * 64 + l) * M::KPL) = x.f;
+  }
+}
+
 // A or B operand (standard order) of row `row` of an LDS matrix, k-step kt,
 // element k multiplied by sc[k].
 template <class E>
@@ -413,6 +444,21 @@ __device__ inline typename Mfma<E>::frag load_frag_scaled(const E* row, int kt, 
 #pragma unroll
   for (int j = 0; j < M::KPL; ++j) x.e[j] = to_e<E>(to_f(x.e[j]) * sc[k0 + j]);
   return x.f;
+}
+
+// Asynchronous copy of one fragment per lane from global memory straight
+// into LDS (gfx950 global_load_lds): lane l's KPL elements land at
+// lds_frag + l * KPL.  `lds_frag` must be the same for the whole wave.  The
+// copy is tracked by vmcnt; a wave may read back its own fragment once the
+// compiler-inserted wait for it has passed.
+template <class E> __device__ inline void frag_to_lds_async(const E* src_lane, E* lds_frag);
+template <> __device__ inline void frag_to_lds_async<bf16>(const bf16* src_lane, bf16* lds_frag) {
+  __builtin_amdgcn_global_load_lds((const void*)src_lane,
+                                   (__attribute__((address_space(3))) void*)lds_frag, 16, 0, 0);
+}
+template <> __device__ inline void frag_to_lds_async<float>(const float* src_lane, float* lds_frag) {
+  __builtin_amdgcn_global_load_lds((const void*)src_lane,
+                                   (__attribute__((address_space(3))) void*)lds_frag, 4, 0, 0);
 }
 
 // Inclusive prefix sum across the 64 lanes of a wave.

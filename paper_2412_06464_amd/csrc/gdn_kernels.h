@@ -30,6 +30,8 @@ struct Args {
   void* KbT;  // Kbar^T                    rows d, k = t     dk x 64
   void* Uc;   // U~ = T diag(b) V          accumulator layout 64 x dv
   void* Pf;   // P                         rows t, k = t'    64 x 64  (forward)
+  void* Qf;   // diag(e^g) Q               rows t, k = d     64 x dk  (forward)
+  void* Kf;   // K                         rows t, k = d     64 x dk  (backward)
   void* PTf;  // P^T                       rows t', k = t    64 x 64  (backward)
   void* TTf;  // T^T                       rows t', k = t    64 x 64  (backward)
   void* nWT;  // -W~^T                     rows d, k = t     dk x 64  (backward)

@@ -19,9 +19,9 @@
 //   k_prep         one workgroup per (chunk, head): g, Gram matrices, T in
 //                  LDS, then the operands of the sequential passes, streamed
 //                  over 64-wide slices of dk and dv.  Forward: W~, Kbar^T, U~,
-//                  P.  Backward (recompute): W~, Kbar^T, U~, and for the
-//                  reverse pass P^T, T^T, -W~^T, (e^g Q)^T, plus P and
-//                  strictLower(Gamma K K^T) in fp32 for the gradient kernel.
+//                  P, diag(e^g) Q.  Backward (recompute): W~, Kbar^T, U~, and
+//                  for the reverse pass K, P^T, T^T, -W~^T, (e^g Q)^T, plus P
+//                  and strictLower(Gamma K K^T) in fp32 for the gradient kernel.
 #include "gdn_device.h"
 #include "gdn_kernels.h"
 
@@ -100,6 +100,15 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
     lds_barrier();
     wave_mma_nt<E, 1, 4, 64>(kk, sX + w * 16 * LD, LD, sX, LD);
     wave_mma_nt<E, 1, 4, 64>(qk, sY + w * 16 * LD, LD, sX, LD);
+    if (!BWD) {
+      // diag(e^g) Q as A operands (rows t, k = d) for the output of the forward pass
+      export_afrag_perm_kslice<E, CH, DK, 64, 256>(
+          (E*)a.Qf + ch * CH * DK, 64 * s, [&](int t, int d) { return seg[t] * to_f(sY[t * LD + d]); });
+    } else {
+      // raw K as A operands (rows t, k = d) for K dS in the reverse pass
+      export_afrag_perm_kslice<E, CH, DK, 64, 256>(
+          (E*)a.Kf + ch * CH * DK, 64 * s, [&](int t, int d) { return to_f(sX[t * LD + d]); });
+    }
     lds_barrier();
   }
 #pragma unroll

@@ -9,7 +9,7 @@
 // fragment order (or, for raw q and k, in the same permuted order) and is
 // loaded into registers one chunk ahead of its use.  Two barriers per chunk.
 //
-// Forward, per chunk:   V' = U~ - W~ S,   O = diag(e^g) (Q S) + P V',
+// Forward, per chunk:   V' = U~ - W~ S,   O = (diag(e^g) Q) S + P V',
 //                       S <- e^{g_n} S + Kbar^T V'.
 // Backward, per chunk (reverse order), dS = gradient of the exit state:
 //                       dV' = P^T dO + diag(e^{g_n - g}) (K dS),
@@ -33,9 +33,21 @@ __device__ inline bool map_unit_tile(int ntiles, int nunits, int& unit, int& til
 
 inline int unit_tile_grid(int ntiles, int nunits) { return (nunits + 7) / 8 * 8 * ntiles; }
 
+// dv slice per workgroup and the workgroups per CU the register budget is
+// sized for.  The forward at dk = 256 takes 64-wide slices: every chunk moves
+// about 100 KB of dk-side A operands through each workgroup's vector memory
+// path, and a wider slice reuses them over twice the columns.
+#ifndef GDN_FWD_BV256
+#define GDN_FWD_BV256 64
+#endif
+#ifndef GDN_SEQ_MINB
+#define GDN_SEQ_MINB 2
+#endif
 template <class E, int DK, int DV>
 struct SeqCfg {
   static constexpr int BV = 32;
+  static constexpr int FWD_BV = DK == 256 ? GDN_FWD_BV256 : 32;
+  static constexpr int MINB = GDN_SEQ_MINB;
 };
 
 // ------------------------------------------------------------------ forward / recompute
@@ -44,10 +56,11 @@ struct SeqCfg {
 //                (row-major, for the gradient kernel).
 
 template <class E, int DK, int DV, bool STORE>
-__global__ __launch_bounds__(256, 2) void k_fwd_seq(Args a) {
+__global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_fwd_seq(Args a) {
   using M = Mfma<E>;
   using frag = typename M::frag;
-  constexpr int BV = SeqCfg<E, DK, DV>::BV;
+  using raw4 = typename Raw4<E>::type;
+  constexpr int BV = STORE ? SeqCfg<E, DK, DV>::BV : SeqCfg<E, DK, DV>::FWD_BV;
   constexpr int PADE = 16 / sizeof(E);
   constexpr int LDV = BV + PADE;
   constexpr int NTV = BV / 16, MTS = DK / 64;
@@ -65,7 +78,10 @@ __global__ __launch_bounds__(256, 2) void k_fwd_seq(Args a) {
   constexpr int FR = 64 * M::KPL;                  // elements of one fragment
   const unsigned lo = (unsigned)(l * M::KPL);      // lane offset inside a fragment
   const unsigned lc = (unsigned)(l * 4);           // lane offset inside an accumulator tile
-  const unsigned lq = (unsigned)((l & 15) * H * DK + 4 * g4);  // lane offset of raw q rows
+  // the sequence: first token, length, first chunk (no per-chunk table loads)
+  const int s0 = a.cu ? a.cu[n] : n * a.T;
+  const int L = a.cu ? a.cu[n + 1] - s0 : a.T;
+  const int c0 = a.seq_chunk0[n], nch = (L + CH - 1) / CH;
 
   f32x4 S[MTS][NTV];
   const size_t sbase = ((size_t)n * H + h) * DK * DV;
@@ -80,28 +96,31 @@ __global__ __launch_bounds__(256, 2) void k_fwd_seq(Args a) {
       }
 
   frag fW[NKD], fQ[NKD], fK[MTS][NKC], fP[NKC];
-  f32x4 uU[NTV];
-  // W~ rows of tile w: needed first in a chunk, loaded a full chunk ahead
-  auto load_w = [&](int c) {
-    const E* Wp = (const E*)a.Wf + ((size_t)c * H + h) * CH * DK + (size_t)w * NKD * FR;
+  raw4 uU[NTV];
+  float gl = 0.f;  // g of token l of the chunk
+  // Every operand is reloaded for the next chunk as soon as the current one
+  // has consumed it, in the order the next chunk needs them (vector memory
+  // returns in issue order): W~ and diag(e^g) Q rows of tile w after (b); U~
+  // after (c); Kbar^T rows of the wave's state rows, P rows of tile w and the
+  // gates after (d).  Nothing waits on a load right after issuing it.
+  auto load_wq = [&](int j) {
+    const E* Wp = (const E*)a.Wf + ((size_t)(c0 + j) * H + h) * CH * DK + (size_t)w * NKD * FR;
 #pragma unroll
     for (int kt = 0; kt < NKD; ++kt) fW[kt] = M::load(Wp + lo + kt * FR);
-  };
-  // raw q rows of tile w (permuted order of sSB), U~ tiles, Kbar^T rows of
-  // the wave's state rows, P rows of tile w: loaded once the current chunk
-  // has consumed its own (the register file holds one chunk of these)
-  auto load_rest = [&](int c) {
-    const size_t ch = (size_t)c * H + h;
     if (!STORE) {
-      const int4 ci = a.info[c];
-      const bool valid = w * 16 + (l & 15) < ci.z;
-      const E* qrow = (const E*)a.q + ((size_t)(ci.y + w * 16) * H + h) * DK + lq;
+      const E* Qp = (const E*)a.Qf + ((size_t)(c0 + j) * H + h) * CH * DK + (size_t)w * NKD * FR;
 #pragma unroll
-      for (int kt = 0; kt < NKD; ++kt) fQ[kt] = load_row_perm_at<E>(qrow, kt, valid);
+      for (int kt = 0; kt < NKD; ++kt) fQ[kt] = M::load(Qp + lo + kt * FR);
     }
-    const E* Up = (const E*)a.Uc + ch * CH * DV + ((size_t)w * (DV / 16) + v0 / 16) * 256;
+  };
+  auto load_u = [&](int j) {
+    const E* Up = (const E*)a.Uc + ((size_t)(c0 + j) * H + h) * CH * DV +
+                  ((size_t)w * (DV / 16) + v0 / 16) * 256;
 #pragma unroll
-    for (int j = 0; j < NTV; ++j) uU[j] = load4<E>(Up + lc + j * 256);
+    for (int jj = 0; jj < NTV; ++jj) uU[jj] = *reinterpret_cast<const raw4*>(Up + lc + jj * 256);
+  };
+  auto load_kp = [&](int j) {
+    const size_t ch = (size_t)(c0 + j) * H + h;
     const E* Kp = (const E*)a.KbT + ch * DK * CH + (size_t)w * MTS * NKC * FR;
 #pragma unroll
     for (int i = 0; i < MTS; ++i)
@@ -112,86 +131,87 @@ __global__ __launch_bounds__(256, 2) void k_fwd_seq(Args a) {
 #pragma unroll
       for (int kt = 0; kt < NKC; ++kt) fP[kt] = M::load(Pp + lo + kt * FR);
     }
+    gl = a.g[ch * CH + l];
   };
 
-  const int c0 = a.seq_chunk0[n], c1 = a.seq_chunk0[n + 1];
-  if (c0 < c1) {
-    load_w(c0);
-    load_rest(c0);
+  if (nch > 0) {
+    load_wq(0);
+    load_u(0);
+    load_kp(0);
   }
-  for (int c = c0; c < c1; ++c) {
-    const int4 ci = a.info[c];
-    const int start = ci.y, len = ci.z;
-    const size_t ch = (size_t)c * H + h;
-    const float gn = a.g[ch * CH + CH - 1];  // pads repeat g of the last token
+  for (int j = 0; j < nch; ++j) {
+    const int start = s0 + j * CH, len = min(CH, L - j * CH);
+    const size_t ch = (size_t)(c0 + j) * H + h;
 
     // (a) publish S as B operands (and as rows for the chunk-state store)
 #pragma unroll
     for (int i = 0; i < MTS; ++i)
 #pragma unroll
-      for (int j = 0; j < NTV; ++j) {
-        bfrag_put<E>(sSB, NTV, w * MTS + i, j, S[i][j]);
+      for (int jj = 0; jj < NTV; ++jj) {
+        bfrag_put<E>(sSB, NTV, w * MTS + i, jj, S[i][jj]);
         if (STORE) {
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            sSs[(w * (DK / 4) + i * 16 + acc_row(e)) * LDV + j * 16 + acc_col()] =
-                to_e<E>(S[i][j][e]);
+            sSs[(w * (DK / 4) + i * 16 + acc_row(e)) * LDV + jj * 16 + acc_col()] =
+                to_e<E>(S[i][jj][e]);
         }
       }
     lds_barrier();
 
-    // (b) W~ S and Q S for the wave's 16 token rows
+    // (b) W~ S and diag(e^g) Q S for the wave's 16 token rows
     if (STORE) copy_out_rows<E, DK, BV, LDV, 256>((E*)a.Sc + ch * DK * DV + v0, DV, sSs, DK);
     f32x4 P[NTV], Qs[NTV];
 #pragma unroll
-    for (int j = 0; j < NTV; ++j) P[j] = Qs[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int jj = 0; jj < NTV; ++jj) P[jj] = Qs[jj] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kt = 0; kt < NKD; ++kt)
 #pragma unroll
-      for (int j = 0; j < NTV; ++j) {
-        const frag b = bfrag_get<E>(sSB, NTV, kt, j);
-        P[j] = M::mma(fW[kt], b, P[j]);
-        if (!STORE) Qs[j] = M::mma(fQ[kt], b, Qs[j]);
+      for (int jj = 0; jj < NTV; ++jj) {
+        const frag b = bfrag_get<E>(sSB, NTV, kt, jj);
+        P[jj] = M::mma(fW[kt], b, P[jj]);
+        if (!STORE) Qs[jj] = M::mma(fQ[kt], b, Qs[jj]);
       }
-    if (c + 1 < c1) load_w(c + 1);
+    load_wq(min(j + 1, nch - 1));  // unconditional: keeps the load queue's shape static
 
     // (c) V' = U~ - W~ S
 #pragma unroll
-    for (int j = 0; j < NTV; ++j) {
-      const f32x4 vp = uU[j] - P[j];
-      bfrag_put<E>(sVB, NTV, w, j, vp);
+    for (int jj = 0; jj < NTV; ++jj) {
+      f32x4 vp;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) vp[e] = to_f(uU[jj][e]) - P[jj][e];
+      bfrag_put<E>(sVB, NTV, w, jj, vp);
       if (STORE) {
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          sOut[(w * 16 + acc_row(e)) * LDV + j * 16 + acc_col()] = to_e<E>(vp[e]);
+          sOut[(w * 16 + acc_row(e)) * LDV + jj * 16 + acc_col()] = to_e<E>(vp[e]);
       }
     }
+    load_u(min(j + 1, nch - 1));
     lds_barrier();
 
-    // (d) S <- e^{g_n} S + Kbar^T V';  O = diag(e^g) (Q S) + P V'
-    const float egn = __expf(gn);
+    // (d) S <- e^{g_n} S + Kbar^T V';  O = (diag(e^g) Q) S + P V'
+    const float egn = __expf(__shfl(gl, CH - 1, 64));  // pads repeat g of the last token
 #pragma unroll
     for (int i = 0; i < MTS; ++i)
 #pragma unroll
-      for (int j = 0; j < NTV; ++j) S[i][j] *= egn;
-    if (!STORE) {
-      const float4 gr = *reinterpret_cast<const float4*>(a.g + ch * CH + w * 16 + 4 * g4);
-      const float eg[4] = {__expf(gr.x), __expf(gr.y), __expf(gr.z), __expf(gr.w)};
+      for (int jj = 0; jj < NTV; ++jj) S[i][jj] *= egn;
+    frag fKc[MTS][NKC], fPc[NKC];
 #pragma unroll
-      for (int j = 0; j < NTV; ++j)
+    for (int i = 0; i < MTS; ++i)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) Qs[j][e] *= eg[e];
-    }
+      for (int kt = 0; kt < NKC; ++kt) fKc[i][kt] = fK[i][kt];
+#pragma unroll
+    for (int kt = 0; kt < NKC; ++kt) fPc[kt] = fP[kt];
 #pragma unroll
     for (int kt = 0; kt < NKC; ++kt)
 #pragma unroll
-      for (int j = 0; j < NTV; ++j) {
-        const frag b = bfrag_get<E>(sVB, NTV, kt, j);
+      for (int jj = 0; jj < NTV; ++jj) {
+        const frag b = bfrag_get<E>(sVB, NTV, kt, jj);
 #pragma unroll
-        for (int i = 0; i < MTS; ++i) S[i][j] = M::mma(fK[i][kt], b, S[i][j]);
-        if (!STORE) Qs[j] = M::mma(fP[kt], b, Qs[j]);
+        for (int i = 0; i < MTS; ++i) S[i][jj] = M::mma(fKc[i][kt], b, S[i][jj]);
+        if (!STORE) Qs[jj] = M::mma(fPc[kt], b, Qs[jj]);
       }
-    if (c + 1 < c1) load_rest(c + 1);
+    load_kp(min(j + 1, nch - 1));
     if (STORE) {
       copy_out_rows<E, CH, BV, LDV, 256>((E*)a.Vp + ch * CH * DV + v0, DV, sOut, CH);
     } else {
@@ -201,7 +221,7 @@ __global__ __launch_bounds__(256, 2) void k_fwd_seq(Args a) {
         const int t = w * 16 + acc_row(e);
         if (t < len) {
 #pragma unroll
-          for (int j = 0; j < NTV; ++j) orow[(size_t)t * H * DV + j * 16] = to_e<E>(Qs[j][e]);
+          for (int jj = 0; jj < NTV; ++jj) orow[(size_t)t * H * DV + jj * 16] = to_e<E>(Qs[jj][e]);
         }
       }
     }
@@ -211,11 +231,11 @@ __global__ __launch_bounds__(256, 2) void k_fwd_seq(Args a) {
 #pragma unroll
     for (int i = 0; i < MTS; ++i)
 #pragma unroll
-      for (int j = 0; j < NTV; ++j)
+      for (int jj = 0; jj < NTV; ++jj)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const int d = w * (DK / 4) + i * 16 + acc_row(e), vv = v0 + j * 16 + acc_col();
-          a.ht[sbase + (size_t)d * DV + vv] = S[i][j][e];
+          const int d = w * (DK / 4) + i * 16 + acc_row(e), vv = v0 + jj * 16 + acc_col();
+          a.ht[sbase + (size_t)d * DV + vv] = S[i][jj][e];
         }
   }
 }
@@ -236,7 +256,7 @@ template <> __device__ inline int bfrag_pos_t<float>(int t, int v, int NT) {
 }
 
 template <class E, int DK, int DV>
-__global__ __launch_bounds__(256, 2) void k_bwd_seq(Args a) {
+__global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
   using M = Mfma<E>;
   using frag = typename M::frag;
   constexpr int BV = SeqCfg<E, DK, DV>::BV;
@@ -262,7 +282,9 @@ __global__ __launch_bounds__(256, 2) void k_bwd_seq(Args a) {
   const E* dOin = (const E*)a.dO;
   constexpr int FR = 64 * M::KPL;                  // elements of one fragment
   const unsigned lo = (unsigned)(l * M::KPL);      // lane offset inside a fragment
-  const unsigned lk = (unsigned)((l & 15) * H * DK + 4 * g4);  // lane offset of raw k rows
+  const int s0 = a.cu ? a.cu[n] : n * a.T;
+  const int L = a.cu ? a.cu[n + 1] - s0 : a.T;
+  const int c0 = a.seq_chunk0[n], nch = (L + CH - 1) / CH;
 
   f32x4 dS[MTS][NTV];
   const size_t sbase = ((size_t)n * H + h) * DK * DV;
@@ -278,29 +300,37 @@ __global__ __launch_bounds__(256, 2) void k_bwd_seq(Args a) {
 
   frag fK[NKD], fPT[NKC], fT[NKC], fQ[MTS][NKC], fW[MTS][NKC];
   uint4 dov[DOV];
-  // raw K rows (permuted order) and P^T rows of tile w, dO tile
-  auto load_first = [&](int c) {
-    const int4 ci = a.info[c];
-    const size_t ch = (size_t)c * H + h;
-    const size_t row0 = (size_t)ci.y * H + h;
-    const bool valid = w * 16 + (l & 15) < ci.z;
-    const E* krow = (const E*)a.k + ((size_t)(ci.y + w * 16) * H + h) * DK + lk;
-#pragma unroll
-    for (int kt = 0; kt < NKD; ++kt) fK[kt] = load_row_perm_at<E>(krow, kt, valid);
-    const E* Pp = (const E*)a.PTf + ch * CH * CH + (size_t)w * NKC * FR;
-#pragma unroll
-    for (int kt = 0; kt < NKC; ++kt) fPT[kt] = M::load(Pp + lo + kt * FR);
+  float gl = 0.f, bl = 0.f;  // g and beta of token l of the chunk
+  // Loads for the next chunk (in reverse order) are issued once the current
+  // chunk has consumed the registers, in the order they are needed, and
+  // unconditionally (clamped at the first chunk) so that every wait on the
+  // in-order vector-memory counter stays partial.
+  // First group, needed in (a)/(b): dO tile, K rows and P^T rows of tile w,
+  // gates.
+  auto load_first = [&](int j) {
+    const int start = s0 + j * CH, len = min(CH, L - j * CH);
+    const size_t ch = (size_t)(c0 + j) * H + h;
+    const size_t row0 = (size_t)start * H + h;
 #pragma unroll
     for (int x = 0; x < DOV; ++x) {
       const int idx = tid + x * 256, tt = idx & (CH - 1), cv = idx >> 6;
-      dov[x] = uint4{0u, 0u, 0u, 0u};
-      if (tt < ci.z)
-        dov[x] = *reinterpret_cast<const uint4*>(dOin + (row0 + (size_t)tt * H) * DV + v0 + cv * EPV);
+      dov[x] = *reinterpret_cast<const uint4*>(dOin + (row0 + (size_t)min(tt, len - 1) * H) * DV +
+                                               v0 + cv * EPV);
+      if (tt >= len) dov[x] = uint4{0u, 0u, 0u, 0u};
     }
+    const E* Kp = (const E*)a.Kf + ch * CH * DK + (size_t)w * NKD * FR;
+#pragma unroll
+    for (int kt = 0; kt < NKD; ++kt) fK[kt] = M::load(Kp + lo + kt * FR);
+    const E* Pp = (const E*)a.PTf + ch * CH * CH + (size_t)w * NKC * FR;
+#pragma unroll
+    for (int kt = 0; kt < NKC; ++kt) fPT[kt] = M::load(Pp + lo + kt * FR);
+    gl = a.g[ch * CH + l];
+    bl = a.beta[row0 + (size_t)min(l, len - 1) * H];
   };
-  // T^T rows of tile w; (e^g Q)^T and -W~^T rows of the wave's state rows
-  auto load_second = [&](int c) {
-    const size_t ch = (size_t)c * H + h;
+  // Second group, needed in (c): T^T rows of tile w; (e^g Q)^T and -W~^T rows
+  // of the wave's state rows.
+  auto load_second = [&](int j) {
+    const size_t ch = (size_t)(c0 + j) * H + h;
     const E* Tp = (const E*)a.TTf + ch * CH * CH + (size_t)w * NKC * FR;
 #pragma unroll
     for (int kt = 0; kt < NKC; ++kt) fT[kt] = M::load(Tp + lo + kt * FR);
@@ -315,30 +345,26 @@ __global__ __launch_bounds__(256, 2) void k_bwd_seq(Args a) {
       }
   };
 
-  const int c0 = a.seq_chunk0[n], c1 = a.seq_chunk0[n + 1];
-  if (c0 < c1) {
-    load_first(c1 - 1);
-    load_second(c1 - 1);
+  if (nch > 0) {
+    load_first(nch - 1);
+    load_second(nch - 1);
   }
   size_t prev_ch = 0;  // chunk whose dX rows wait in sOut
-  bool pending = false;
-  for (int c = c1 - 1; c >= c0; --c) {
-    const int4 ci = a.info[c];
-    const int start = ci.y, len = ci.z;
-    const size_t ch = (size_t)c * H + h;
-    const float gn = a.g[ch * CH + CH - 1];  // pads repeat g of the last token
-    E* sdO = sdOB[c & 1];
+  for (int j = nch - 1; j >= 0; --j) {
+    const int start = s0 + j * CH, len = min(CH, L - j * CH);
+    const size_t ch = (size_t)(c0 + j) * H + h;
+    E* sdO = sdOB[j & 1];
 
     // (a) publish dS (B operands and rows), dO (B operands)
 #pragma unroll
     for (int i = 0; i < MTS; ++i)
 #pragma unroll
-      for (int j = 0; j < NTV; ++j) {
-        bfrag_put<E>(sdSB, NTV, w * MTS + i, j, dS[i][j]);
+      for (int jj = 0; jj < NTV; ++jj) {
+        bfrag_put<E>(sdSB, NTV, w * MTS + i, jj, dS[i][jj]);
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          sSs[(w * (DK / 4) + i * 16 + acc_row(e)) * LDV + j * 16 + acc_col()] =
-              to_e<E>(dS[i][j][e]);
+          sSs[(w * (DK / 4) + i * 16 + acc_row(e)) * LDV + jj * 16 + acc_col()] =
+              to_e<E>(dS[i][jj][e]);
       }
 #pragma unroll
     for (int x = 0; x < DOV; ++x) {
@@ -349,83 +375,83 @@ __global__ __launch_bounds__(256, 2) void k_bwd_seq(Args a) {
       } val;
       val.u = dov[x];
 #pragma unroll
-      for (int j = 0; j < EPV; ++j) sdO[bfrag_pos_t<E>(tt, cv * EPV + j, NTV)] = val.e[j];
+      for (int q = 0; q < EPV; ++q) sdO[bfrag_pos_t<E>(tt, cv * EPV + q, NTV)] = val.e[q];
     }
     lds_barrier();
 
     // (b) dV' = P^T dO + diag(e^{g_n - g}) (K dS); the stores of dS and of the
     //     previous chunk's dX rows
     copy_out_rows<E, DK, BV, LDV, 256>((E*)a.dSc + ch * DK * DV + v0, DV, sSs, DK);
-    if (pending) copy_out_rows<E, CH, BV, LDV, 256>((E*)a.dXb + prev_ch * CH * DV + v0, DV, sOut, CH);
+    if (j + 1 < nch)
+      copy_out_rows<E, CH, BV, LDV, 256>((E*)a.dXb + prev_ch * CH * DV + v0, DV, sOut, CH);
     f32x4 X1[NTV], X2[NTV];
 #pragma unroll
-    for (int j = 0; j < NTV; ++j) X1[j] = X2[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kt = 0; kt < NKD; ++kt)
-#pragma unroll
-      for (int j = 0; j < NTV; ++j) X1[j] = M::mma(fK[kt], bfrag_get<E>(sdSB, NTV, kt, j), X1[j]);
+    for (int jj = 0; jj < NTV; ++jj) X1[jj] = X2[jj] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kt = 0; kt < NKC; ++kt)
 #pragma unroll
-      for (int j = 0; j < NTV; ++j) X2[j] = M::mma(fPT[kt], bfrag_get<E>(sdO, NTV, kt, j), X2[j]);
-    {
-      const float4 gr = *reinterpret_cast<const float4*>(a.g + ch * CH + w * 16 + 4 * g4);
-      const float dec[4] = {__expf(gn - gr.x), __expf(gn - gr.y), __expf(gn - gr.z),
-                            __expf(gn - gr.w)};
+      for (int jj = 0; jj < NTV; ++jj) X2[jj] = M::mma(fPT[kt], bfrag_get<E>(sdO, NTV, kt, jj), X2[jj]);
 #pragma unroll
-      for (int j = 0; j < NTV; ++j) {
-        f32x4 y;
+    for (int kt = 0; kt < NKD; ++kt)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) y[e] = dec[e] * X1[j][e] + X2[j][e];
-        bfrag_put<E>(sdVB, NTV, w, j, y);
-      }
+      for (int jj = 0; jj < NTV; ++jj) X1[jj] = M::mma(fK[kt], bfrag_get<E>(sdSB, NTV, kt, jj), X1[jj]);
+    const float gn = __shfl(gl, CH - 1, 64);  // pads repeat g of the last token
+    float brow[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int r = w * 16 + acc_row(e);
+      const float dec = __expf(gn - __shfl(gl, r, 64));
+      const float br = __shfl(bl, r, 64);  // every lane takes part in the shuffle
+      brow[e] = r < len ? br : 0.f;
+#pragma unroll
+      for (int jj = 0; jj < NTV; ++jj) X1[jj][e] = dec * X1[jj][e] + X2[jj][e];
     }
-    if (c - 1 >= c0) load_first(c - 1);
+#pragma unroll
+    for (int jj = 0; jj < NTV; ++jj) bfrag_put<E>(sdVB, NTV, w, jj, X1[jj]);
+    load_first(max(j - 1, 0));
     lds_barrier();
 
     // (c) dX = T^T dV', dv = b dX;  dS <- e^{g_n} dS + (e^g Q)^T dO - W~^T dV'
     f32x4 dX[NTV];
 #pragma unroll
-    for (int j = 0; j < NTV; ++j) dX[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int jj = 0; jj < NTV; ++jj) dX[jj] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kt = 0; kt < NKC; ++kt)
 #pragma unroll
-      for (int j = 0; j < NTV; ++j) dX[j] = M::mma(fT[kt], bfrag_get<E>(sdVB, NTV, kt, j), dX[j]);
+      for (int jj = 0; jj < NTV; ++jj) dX[jj] = M::mma(fT[kt], bfrag_get<E>(sdVB, NTV, kt, jj), dX[jj]);
+    const float egn = __expf(gn);
+#pragma unroll
+    for (int i = 0; i < MTS; ++i)
+#pragma unroll
+      for (int jj = 0; jj < NTV; ++jj) dS[i][jj] *= egn;
+#pragma unroll
+    for (int kt = 0; kt < NKC; ++kt)
+#pragma unroll
+      for (int jj = 0; jj < NTV; ++jj) {
+        const frag bo = bfrag_get<E>(sdO, NTV, kt, jj);
+        const frag bv = bfrag_get<E>(sdVB, NTV, kt, jj);
+#pragma unroll
+        for (int i = 0; i < MTS; ++i) {
+          dS[i][jj] = M::mma(fQ[i][kt], bo, dS[i][jj]);
+          dS[i][jj] = M::mma(fW[i][kt], bv, dS[i][jj]);
+        }
+      }
+    load_second(max(j - 1, 0));
     {
       E* dvrow = (E*)a.dv + ((size_t)start * H + h) * DV + v0 + acc_col();
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int t = w * 16 + acc_row(e);
-        const float b = t < len ? a.beta[((size_t)start + t) * H + h] : 0.f;
 #pragma unroll
-        for (int j = 0; j < NTV; ++j) {
-          sOut[t * LDV + j * 16 + acc_col()] = to_e<E>(dX[j][e]);
-          if (t < len) dvrow[(size_t)t * H * DV + j * 16] = to_e<E>(b * dX[j][e]);
+        for (int jj = 0; jj < NTV; ++jj) {
+          sOut[t * LDV + jj * 16 + acc_col()] = to_e<E>(dX[jj][e]);
+          if (t < len) dvrow[(size_t)t * H * DV + jj * 16] = to_e<E>(brow[e] * dX[jj][e]);
         }
       }
     }
-    const float egn = __expf(gn);
-#pragma unroll
-    for (int i = 0; i < MTS; ++i)
-#pragma unroll
-      for (int j = 0; j < NTV; ++j) dS[i][j] *= egn;
-#pragma unroll
-    for (int kt = 0; kt < NKC; ++kt)
-#pragma unroll
-      for (int j = 0; j < NTV; ++j) {
-        const frag bo = bfrag_get<E>(sdO, NTV, kt, j);
-        const frag bv = bfrag_get<E>(sdVB, NTV, kt, j);
-#pragma unroll
-        for (int i = 0; i < MTS; ++i) {
-          dS[i][j] = M::mma(fQ[i][kt], bo, dS[i][j]);
-          dS[i][j] = M::mma(fW[i][kt], bv, dS[i][j]);
-        }
-      }
-    if (c - 1 >= c0) load_second(c - 1);
     prev_ch = ch;
-    pending = true;
   }
-  if (pending) {
+  if (nch > 0) {
     lds_barrier();
     copy_out_rows<E, CH, BV, LDV, 256>((E*)a.dXb + prev_ch * CH * DV + v0, DV, sOut, CH);
   }
@@ -434,11 +460,11 @@ __global__ __launch_bounds__(256, 2) void k_bwd_seq(Args a) {
 #pragma unroll
     for (int i = 0; i < MTS; ++i)
 #pragma unroll
-      for (int j = 0; j < NTV; ++j)
+      for (int jj = 0; jj < NTV; ++jj)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const int d = w * (DK / 4) + i * 16 + acc_row(e), vv = v0 + j * 16 + acc_col();
-          a.dh0[sbase + (size_t)d * DV + vv] = dS[i][j][e];
+          const int d = w * (DK / 4) + i * 16 + acc_row(e), vv = v0 + jj * 16 + acc_col();
+          a.dh0[sbase + (size_t)d * DV + vv] = dS[i][jj][e];
         }
   }
 }
@@ -447,12 +473,13 @@ __global__ __launch_bounds__(256, 2) void k_bwd_seq(Args a) {
 
 hipError_t launch_fwd_seq(Dt dt, int dk, int dv, bool store, const Args& a, hipStream_t s) {
   auto f = [&]<class E, int DK, int DV>() {
-    constexpr int BV = SeqCfg<E, DK, DV>::BV;
-    const dim3 grid(unit_tile_grid(DV / BV, a.N * a.H));
+    constexpr int BV = SeqCfg<E, DK, DV>::BV, FBV = SeqCfg<E, DK, DV>::FWD_BV;
     if (store)
-      hipLaunchKernelGGL((k_fwd_seq<E, DK, DV, true>), grid, dim3(256), 0, s, a);
+      hipLaunchKernelGGL((k_fwd_seq<E, DK, DV, true>), dim3(unit_tile_grid(DV / BV, a.N * a.H)),
+                         dim3(256), 0, s, a);
     else
-      hipLaunchKernelGGL((k_fwd_seq<E, DK, DV, false>), grid, dim3(256), 0, s, a);
+      hipLaunchKernelGGL((k_fwd_seq<E, DK, DV, false>), dim3(unit_tile_grid(DV / FBV, a.N * a.H)),
+                         dim3(256), 0, s, a);
     return hipGetLastError();
   };
   GDN_DISPATCH(dt, dk, dv, f);
