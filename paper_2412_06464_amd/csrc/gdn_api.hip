@@ -86,7 +86,7 @@ size_t carve(const gdn_problem* p, const Shape& s, bool backward, unsigned char*
   unsigned char* KbT = take(kside);
   unsigned char* Uc = take(vside);
   unsigned char *Pf = nullptr, *PTf = nullptr, *TTf = nullptr, *nWT = nullptr, *QgT = nullptr;
-  unsigned char *Qf = nullptr, *Kf = nullptr;
+  unsigned char *Qf = nullptr, *Kf = nullptr, *KTf = nullptr, *QTf = nullptr;
   unsigned char *Pm = nullptr, *Ak = nullptr;
   unsigned char *Sc = nullptr, *Vp = nullptr, *dSc = nullptr, *dXb = nullptr;
   if (!backward) {
@@ -98,6 +98,8 @@ size_t carve(const gdn_problem* p, const Shape& s, bool backward, unsigned char*
     TTf = take(cc);
     nWT = take(kside);
     QgT = take(kside);
+    KTf = take(kside);
+    QTf = take(kside);
     Pm = take(NC * H * CH * CH * sizeof(float));
     Ak = take(NC * H * CH * CH * sizeof(float));
     const size_t st = NC * H * (size_t)p->dk * p->dv * s.esz;
@@ -116,6 +118,8 @@ size_t carve(const gdn_problem* p, const Shape& s, bool backward, unsigned char*
     a->Pf = Pf;
     a->Qf = Qf;
     a->Kf = Kf;
+    a->KTf = KTf;
+    a->QTf = QTf;
     a->PTf = PTf;
     a->TTf = TTf;
     a->nWT = nWT;

@@ -461,6 +461,56 @@ template <> __device__ inline void frag_to_lds_async<float>(const float* src_lan
                                    (__attribute__((address_space(3))) void*)lds_frag, 4, 0, 0);
 }
 
+// Copy one MFMA fragment (KPL elements per lane, lane-contiguous) from global
+// memory straight into LDS with global_load_lds: lane l's elements land at
+// lds_frag + l * KPL.  `lds_frag` must be the same for the whole wave.  It is
+// issued from inline assembly so that the compiler does not wait on it: the
+// caller owns the vmcnt bookkeeping (s_waitcnt before reading the LDS, and
+// vmcnt(0) before the LDS is reused for anything else) and must issue no
+// other vector-memory loads whose waits it relies on in between.
+template <class E> __device__ inline void dma_frag(const E* src_lane, E* lds_frag);
+template <> __device__ inline void dma_frag<bf16>(const bf16* src_lane, bf16* lds_frag) {
+  const unsigned lds = (unsigned)(uintptr_t)lds_frag;
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(src_lane)
+               : "memory");
+}
+template <> __device__ inline void dma_frag<float>(const float* src_lane, float* lds_frag) {
+  const unsigned lds = (unsigned)(uintptr_t)lds_frag;
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off" ::"s"(lds), "v"(src_lane)
+               : "memory");
+}
+// Wait until at most N vector-memory operations of this wave are in flight.
+template <int N> __device__ inline void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Copy a [ROWS][BV] tile from LDS (leading dim LD; columns v0..v0+BV of an
+// R x N matrix) to global memory in MFMA fragment order over the columns:
+// fragment (row tile rt, k-step kt) of lane l (row rt*16 + (l & 15), columns
+// kt*K + KPL*(l >> 4) ..) at ((rt * NKT + kt) * 64 + l) * KPL, NKT = N / K.
+// A reader then loads one fragment as one contiguous 1 KiB (bf16) block.
+template <class E, int ROWS, int BV, int LD, int NTH>
+__device__ inline void copy_out_frags(E* g, int NKT, int v0, const E* lds) {
+  using M = Mfma<E>;
+  constexpr int EPV = 16 / sizeof(E);
+  constexpr int VPR = BV / EPV;
+  for (int idx = threadIdx.x; idx < ROWS * VPR; idx += NTH) {
+    const int r = idx / VPR, cv = idx - r * VPR;
+    const int v = v0 + cv * EPV;
+    if (sizeof(E) == 2) {
+      const int kt = v / M::K, lane = (r & 15) + 16 * ((v % M::K) / M::KPL);
+      *reinterpret_cast<uint4*>(g + ((size_t)((r >> 4) * NKT + kt) * 64 + lane) * M::KPL) =
+          *reinterpret_cast<const uint4*>(lds + r * LD + cv * EPV);
+    } else {
+#pragma unroll
+      for (int q = 0; q < EPV; ++q) {
+        const int vv = v + q, kt = vv / M::K, lane = (r & 15) + 16 * (vv % M::K);
+        g[(size_t)((r >> 4) * NKT + kt) * 64 + lane] = lds[r * LD + cv * EPV + q];
+      }
+    }
+  }
+}
+
 // Inclusive prefix sum across the 64 lanes of a wave.
 __device__ inline float wave_incl_scan(float x) {
   const int l = lane_id();

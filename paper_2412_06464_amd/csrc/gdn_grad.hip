@@ -1,292 +1,383 @@
 // Per-chunk gradient kernel (gfx950) of the chunkwise gated delta rule: the
 // parallel part of the backward, given every chunk's entry state S, exit-state
-// gradient dS_next, V' and dX from the two sequential passes.  The paper gives
-// no backward; these are the exact reverse-mode derivatives of its chunk
-// equations (Sec. 3.3, state stored dk x dv).
+// gradient dS (= dS_next of the chunk), V' and dX = T^T dV' from the two
+// sequential passes (all four stored in MFMA fragment order over dv).  The paper gives no backward; these are the exact
+// reverse-mode derivatives of its chunk equations (Sec. 3.3, state stored
+// dk x dv).  With dP = lower(dO V'^T) (with the diagonal), dA =
+// strictLower(-dX V'^T), M1 = dP * Gamma, D = diag(b) (dA * Gamma) and
+// E = dA * diag(b) Ak + dP * P (Ak = strictLower(Gamma * K K^T)):
+//   Gq = dO S^T,  Gk = dX S^T,  Gs = V' dS^T                     (64 x dk)
+//   dQ = diag(e^g) Gq + M1 K
+//   dK = M1^T Q + diag(e^{g_n-g}) Gs - diag(b e^g) Gk + (D + D^T) K
+//   dbeta_r = sum_i dA_ri Ak_ri + dX_r . V_r - e^{g_r} k_r . Gk_r
+//   dg_r = e^{g_r} q_r.Gq_r - b_r e^{g_r} k_r.Gk_r - e^{g_n-g_r} k_r.Gs_r
+//          + sum_i E_ri - sum_j E_jr
+//          (+ sum_r e^{g_n-g_r} k_r.Gs_r + e^{g_n} <dS, S> on the last token)
+//   dlog_alpha = reverse cumulative sum of dg inside the chunk.
+//
+// One workgroup per (chunk, head).  Streaming phase over dv: the dS/S
+// operands (the bulk of the bytes) are loaded straight from HBM as MFMA B
+// fragments, each wave owning a set of dk columns; dO, dX and V' (shared by
+// all waves as A operands) pass through a double-buffered LDS ring in
+// fragment order.  Finish phase: the 64 x 64 intra-chunk matrices go through
+// LDS, and K^T / Q^T come as ready-made fragments from the prep kernel.
 #include "gdn_device.h"
 #include "gdn_kernels.h"
 
 namespace gdn {
 
-// ------------------------------------------------------------------ gradient kernel
-// Grid (NC, H), 512 threads (8 waves).  Streams the dv dimension in tiles of
-// BVG and accumulates, for the chunk:
-//   Gq = dO S^T, Gk = dX S^T, Gs = V' dS_next^T       (64 x dk)
-//   dO V'^T, dX V'^T                                  (64 x 64)
-// then finishes
-//   dQ = diag(e^g) Gq + (dP * Gamma) K
-//   dK = (dP * Gamma)^T Q + diag(e^{g_n-g}) Gs - diag(b e^g) Gk + (D + D^T) K
-//   dbeta_r = sum_i dA_ri Ak_ri + dX_r . V_r - e^{g_r} k_r . Gk_r
-//   dg_r = e^{g_r} q_r.Gq_r - b_r e^{g_r} k_r.Gk_r - e^{g_n-g_r} k_r.Gs_r
-//          + sum_i E_ri - sum_j E_jr   (+ the g_n terms on the last token)
-//   dlog_alpha = reverse cumulative sum of dg inside the chunk
-// with dP = lower(dO V'^T), dA = strictLower(-dX V'^T), D = diag(b)(dA*Gamma),
-// E = dA * diag(b) Ak + dP * P.
-
-template <class E, int DK, int DV, int BVG>
-struct GradLds {
-  static constexpr int PADE = 16 / sizeof(E);
-  static constexpr int LDG = BVG + PADE;
-  static constexpr int LDC = CH + PADE;
-  static constexpr size_t stream_bytes = (size_t)(4 * CH * LDG + 2 * DK * LDG) * sizeof(E);
-  static constexpr size_t finish_e = (size_t)(2 * DK * LDC + 3 * CH * LDC) * sizeof(E);
-  static constexpr size_t finish_bytes = finish_e + 2 * CH * (CH + 1) * sizeof(float);
-  static constexpr size_t bytes = stream_bytes > finish_bytes ? stream_bytes : finish_bytes;
+template <class E, int DK>
+struct GradCfg {
+  static constexpr int NW = DK == 64 ? 4 : 8;  // waves
+  static constexpr int NTH = 64 * NW;
+  static constexpr int NDT = DK / 16 / NW;     // dk column tiles per wave
+  static constexpr int PAT = 32 / NW;          // tiles of [dO; dX] V'^T per wave
 };
 
-template <class E, int DK, int DV, int BVG>
+template <class E, int DK, int DV>
 __global__ __launch_bounds__(512) void k_grad(Args a) {
-  using L = GradLds<E, DK, DV, BVG>;
-  constexpr int LDG = L::LDG, LDC = L::LDC, LDE = CH + 1;
-  constexpr int NTH = 512;
-  constexpr int CT = DK / 16;
-  constexpr int CTW = CT >= 16 ? CT / 8 : 1;
-  constexpr int WC = CT / CTW;
-  constexpr int WR = 8 / WC;
-  constexpr int RTW = 4 / WR;
-  __shared__ __align__(16) unsigned char smem[L::bytes];
-  __shared__ float sg[CH], sb[CH], seg[CH], sdec[CH], sxv[CH], sdbA[CH];
-  __shared__ float sErow[CH], sEcol[CH];
-  __shared__ float srow[WC][3][CH];
-  __shared__ float sred[8];
+  using M = Mfma<E>;
+  using frag = typename M::frag;
+  using C = GradCfg<E, DK>;
+  constexpr int NW = C::NW, NTH = C::NTH, NDT = C::NDT, PAT = C::PAT;
+  constexpr int NKS = DV / M::K;         // MFMA k-steps over dv
+  constexpr int NDTOT = DK / 16;         // dk column tiles
+  constexpr int F = 16 + 2 * NDTOT;      // fragments per k-step: dO, dX, V' (4 each), V (4), S, dS
+  constexpr int PF = F / NW;             // fragments each wave copies per k-step
+  static_assert(F % NW == 0, "fragments do not divide over the waves");
+  constexpr int FR = 64 * M::KPL;        // elements of one fragment
+  constexpr int R = DK == 256 ? 3 : 4;   // ring depth in k-steps
+  constexpr int RING_BYTES = R * F * FR * (int)sizeof(E);
+  constexpr int PADE = 16 / sizeof(E);
+  constexpr int LD = CH + PADE;
+  constexpr int LDF = CH + 1;
+  constexpr int NKC = CH / M::K;
+  constexpr int FIN_BYTES = 3 * CH * LD * (int)sizeof(E) + CH * LDF * 4;
+  constexpr int SMEM = RING_BYTES > FIN_BYTES ? RING_BYTES : FIN_BYTES;
+  __shared__ __align__(16) unsigned char smem[SMEM];
+  __shared__ float sg[CH], sb[CH];
+  __shared__ float sdbA[CH], sxv[CH], sErow[2][CH], sEcol[2 * 4][CH];
+  __shared__ float srow[NW][3][CH];
+  __shared__ float sred[NW];
 
-  E* sdO = (E*)smem;
-  E* sdX = sdO + CH * LDG;
-  E* sVp = sdX + CH * LDG;
-  E* sV = sVp + CH * LDG;
-  E* sS = sV + CH * LDG;
-  E* sdS = sS + DK * LDG;
-  E* sKT = (E*)smem;
-  E* sQT = sKT + DK * LDC;
-  E* sM1 = sQT + DK * LDC;
-  E* sM1T = sM1 + CH * LDC;
-  E* sDD = sM1T + CH * LDC;
-  float* sD = (float*)(smem + L::finish_e);
-  float* sE = sD + CH * LDE;
+  E* ring = (E*)smem;                    // [R][F] fragments, filled by direct copies
+  E* sM1 = (E*)smem;                     // finish: M1 = dP * Gamma, row-major
+  E* sM1T = sM1 + CH * LD;               //         M1^T, row-major
+  E* sDD = sM1T + CH * LD;               //         D + D^T, row-major
+  float* sD = (float*)(sDD + CH * LD);   //         D, fp32
 
-  const int c = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = wave_id();
+  const int c = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, l = lane_id(), g4 = l >> 4;
+  const int w = __builtin_amdgcn_readfirstlane(wave_id());
   const int H = a.H;
   const int4 ci = a.info[c];
   const int start = ci.y, len = ci.z;
   const size_t ch = (size_t)c * H + h;
   const size_t row0 = (size_t)start * H + h;
-  const E* K = (const E*)a.k;
-  const E* Q = (const E*)a.q;
-  const E* V = (const E*)a.v;
-  const E* dO = (const E*)a.dO;
+  const E* dOin = (const E*)a.dO + row0 * DV;
+  const E* Vin = (const E*)a.v + row0 * DV;
+  const E* dXp = (const E*)a.dXb + ch * CH * DV;
+  const E* Vpp = (const E*)a.Vp + ch * CH * DV;
+  const E* Sp = (const E*)a.Sc + ch * DK * DV;
+  const E* dSp = (const E*)a.dSc + ch * DK * DV;
 
   if (tid < CH) {
-    const float g = a.g[ch * CH + tid];
-    const float gn = __shfl(g, len - 1, 64);
-    sg[tid] = g;
+    sg[tid] = a.g[ch * CH + tid];
     sb[tid] = tid < len ? a.beta[row0 + (size_t)tid * H] : 0.f;
-    seg[tid] = __expf(g);
-    sdec[tid] = __expf(gn - g);
   }
 
-  const int wc = w % WC, wr = w / WC;
-  const int pm = w >> 2, prt = w & 3;
-  f32x4 Gq[RTW][CTW], Gk[RTW][CTW], Gs[RTW][CTW], PA[1][4];
-  zero_acc(Gq);
-  zero_acc(Gk);
-  zero_acc(Gs);
-  zero_acc(PA);
-  float sdot = 0.f, xvp = 0.f;
+  // ---- streaming phase
+  // Every operand of the dv contraction goes HBM -> LDS by direct copies into
+  // a ring of R k-steps, each wave copying PF of a k-step's F fragments:
+  //   f in [0, 12): dO, dX, V' rows of t-tile f % 4 (A operands of all waves)
+  //   f in [12, 16): V rows of t-tile f - 12 (dX . V)
+  //   f in [16, F): S, then dS, columns of d-tile (B operands of their wave)
+  // Rows past the chunk's end read a valid row instead: every product they
+  // enter is multiplied by a zero row of dX, V', P, Q or beta, or lands in a
+  // row that is masked out.  Slot it % R holds logical k-step it (clamped to
+  // the last one, so every wave issues the same number of copies).
+  auto issue = [&](int it) {
+    const int ksd = min(it, NKS - 1);
+    E* slot = ring + (size_t)(it % R) * F * FR;
+    const int v = ksd * M::K + g4 * M::KPL;
+#pragma unroll
+    for (int i = 0; i < PF; ++i) {
+      const int f = w * PF + i;
+      const E* src;
+      // S, dS, dX and V' are stored in fragment order over dv: one
+      // contiguous fragment per copy
+      if (f < 4 || (f >= 12 && f < 16)) {
+        const int t = (f & 3) * 16 + (l & 15);
+        src = (f < 4 ? dOin : Vin) + (size_t)min(t, len - 1) * H * DV + v;
+      } else if (f < 12) {
+        src = (f < 8 ? dXp : Vpp) + ((size_t)((f & 3) * NKS + ksd) * 64 + l) * M::KPL;
+      } else {
+        const int j = f - 16, mat = j / NDTOT, dt = j - mat * NDTOT;
+        src = (mat ? dSp : Sp) + ((size_t)(dt * NKS + ksd) * 64 + l) * M::KPL;
+      }
+      dma_frag<E>(src, slot + f * FR);
+    }
+  };
 
-  for (int v0 = 0; v0 < DV; v0 += BVG) {
-    stage_rows<E, CH, BVG, LDG, NTH>(sdO, dO + row0 * DV + v0, (size_t)H * DV, len);
-    stage_rows<E, CH, BVG, LDG, NTH>(sV, V + row0 * DV + v0, (size_t)H * DV, len);
-    stage_rows<E, CH, BVG, LDG, NTH>(sdX, (const E*)a.dXb + ch * CH * DV + v0, DV, CH);
-    stage_rows<E, CH, BVG, LDG, NTH>(sVp, (const E*)a.Vp + ch * CH * DV + v0, DV, CH);
-    stage_rows<E, DK, BVG, LDG, NTH>(sS, (const E*)a.Sc + ch * DK * DV + v0, DV, DK);
-    stage_rows<E, DK, BVG, LDG, NTH>(sdS, (const E*)a.dSc + ch * DK * DV + v0, DV, DK);
-    lds_barrier();
-    const E* Arow = sdO + wr * RTW * 16 * LDG;
-    const E* Brow = sS + wc * CTW * 16 * LDG;
-    wave_mma_nt<E, RTW, CTW, BVG>(Gq, Arow, LDG, Brow, LDG);
-    wave_mma_nt<E, RTW, CTW, BVG>(Gk, sdX + wr * RTW * 16 * LDG, LDG, Brow, LDG);
-    wave_mma_nt<E, RTW, CTW, BVG>(Gs, sVp + wr * RTW * 16 * LDG, LDG,
-                                  sdS + wc * CTW * 16 * LDG, LDG);
-    wave_mma_nt<E, 1, 4, BVG>(PA, (pm ? sdX : sdO) + prt * 16 * LDG, LDG, sVp, LDG);
-    for (int idx = tid; idx < DK * BVG; idx += NTH) {
-      const int d = idx / BVG, vv = idx - d * BVG;
-      sdot += to_f(sS[d * LDG + vv]) * to_f(sdS[d * LDG + vv]);
+  f32x4 Gq[4][NDT], Gk[4][NDT], Gs[4][NDT], PA[PAT];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int n = 0; n < NDT; ++n) Gq[i][n] = Gk[i][n] = Gs[i][n] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int p = 0; p < PAT; ++p) PA[p] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float sdot = 0.f, xvp = 0.f;
+  const unsigned lo = (unsigned)(l * M::KPL);
+  constexpr int NPR = PAT / 4;  // (matrix, row tile) pairs of V'^T tiles per wave
+
+#pragma unroll
+  for (int it = 0; it < R - 1; ++it) issue(it);
+  for (int it = 0; it < NKS; ++it) {
+    wait_vmcnt<(R - 2) * PF>();  // this wave's copies of k-step it have landed
+    lds_barrier();               // ... and every wave's; slot (it - 1) % R is free
+    issue(it + R - 1);
+    const E* slot = ring + (size_t)(it % R) * F * FR;
+    frag bS[NDT], bD[NDT], fA[NPR];
+#pragma unroll
+    for (int n = 0; n < NDT; ++n) {
+      bS[n] = M::load(slot + (16 + w * NDT + n) * FR + lo);
+      bD[n] = M::load(slot + (16 + NDTOT + w * NDT + n) * FR + lo);
+    }
+#pragma unroll
+    for (int s2 = 0; s2 < NPR; ++s2) {
+      const int q = w * PAT + 4 * s2, m = q >> 4, rt = (q >> 2) & 3;
+      fA[s2] = M::load(slot + (m * 4 + rt) * FR + lo);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const frag fO = M::load(slot + (0 * 4 + i) * FR + lo);
+      const frag fX = M::load(slot + (1 * 4 + i) * FR + lo);
+      const frag fV = M::load(slot + (2 * 4 + i) * FR + lo);
+#pragma unroll
+      for (int n = 0; n < NDT; ++n) {
+        Gq[i][n] = M::mma(fO, bS[n], Gq[i][n]);
+        Gk[i][n] = M::mma(fX, bS[n], Gk[i][n]);
+        Gs[i][n] = M::mma(fV, bD[n], Gs[i][n]);
+      }
+#pragma unroll
+      for (int s2 = 0; s2 < NPR; ++s2) PA[4 * s2 + i] = M::mma(fA[s2], fV, PA[4 * s2 + i]);
     }
     {
-      const int t = tid >> 3, part = tid & 7;
+      union {
+        frag f;
+        E e[M::KPL];
+      } xs, xd, xv, xx;
 #pragma unroll
-      for (int vv = part * (BVG / 8); vv < (part + 1) * (BVG / 8); ++vv)
-        xvp += to_f(sdX[t * LDG + vv]) * to_f(sV[t * LDG + vv]);
+      for (int n = 0; n < NDT; ++n) {
+        xs.f = bS[n];
+        xd.f = bD[n];
+#pragma unroll
+        for (int j = 0; j < M::KPL; ++j) sdot += to_f(xs.e[j]) * to_f(xd.e[j]);
+      }
+      if (w < 4) {
+        xv.f = M::load(slot + (12 + w) * FR + lo);
+        xx.f = M::load(slot + (4 + w) * FR + lo);
+#pragma unroll
+        for (int j = 0; j < M::KPL; ++j) xvp += to_f(xv.e[j]) * to_f(xx.e[j]);
+      }
     }
-    lds_barrier();
   }
+  wait_vmcnt<0>();  // the clamped tail copies land before the LDS is reused
+  lds_barrier();
 
-  // reductions of <dS_next, S> and dX . V
+  // ---- finish phase (the staging ring is dead; its LDS is reused)
+  // (1) the [dO; dX] V'^T tiles: M1, D, and the parts of E and dbeta
   {
-    float x = xvp;
-    x += __shfl_xor(x, 1, 64);
-    x += __shfl_xor(x, 2, 64);
-    x += __shfl_xor(x, 4, 64);
-    if ((tid & 7) == 0) sxv[tid >> 3] = x;
+    const float* gP = a.Pm + ch * CH * CH;
+    const float* gA = a.Ak + ch * CH * CH;
+#pragma unroll
+    for (int p = 0; p < PAT; ++p) {
+      const int q = w * PAT + p, m = q >> 4, rt = (q >> 2) & 3, ct = q & 3;
+      const f32x4 side = *reinterpret_cast<const f32x4*>((m ? gA : gP) + cfrag_index(rt, ct, CH));
+      float rsum[4], csum = 0.f, dba[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int r = rt * 16 + acc_row(e), i = ct * 16 + acc_col();
+        const float gam = (i <= r) ? __expf(sg[r] - sg[i]) : 0.f;
+        float ev;
+        if (m == 0) {
+          const float dp = (i <= r) ? PA[p][e] : 0.f;
+          const float m1 = dp * gam;
+          sM1[r * LD + i] = to_e<E>(m1);
+          sM1T[i * LD + r] = to_e<E>(m1);
+          ev = dp * side[e];
+          dba[e] = 0.f;
+        } else {
+          const float da = (i < r) ? -PA[p][e] : 0.f;
+          sD[r * LDF + i] = sb[r] * da * gam;
+          ev = da * sb[r] * side[e];
+          dba[e] = da * side[e];
+        }
+        rsum[e] = ev;
+        csum += ev;
+      }
+      // row sums over the 16 columns of the tile, column sums over its 16 rows
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        rsum[e] = reduce16(rsum[e]);
+        dba[e] = reduce16(dba[e]);
+      }
+      csum += __shfl_xor(csum, 16, 64);
+      csum += __shfl_xor(csum, 32, 64);
+      // each (m, rt) row block is spread over 4 column tiles held by one wave:
+      // accumulate in registers across p, publish once per row block
+      if (acc_col() == 0) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = rt * 16 + acc_row(e);
+          if (ct == 0) {
+            sErow[m][r] = rsum[e];
+            if (m) sdbA[r] = dba[e];
+          } else {
+            sErow[m][r] += rsum[e];
+            if (m) sdbA[r] += dba[e];
+          }
+        }
+      }
+      if (l < 16) sEcol[m * 4 + rt][ct * 16 + l] = csum;
+    }
+  }
+  // partial row dots over this wave's columns, and <dS, S>
+  {
     float s = sdot;
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) s += __shfl_xor(s, off, 64);
-    if (lane_id() == 0) sred[w] = s;
-  }
-  stage_rows_T<E, DK, LDC, NTH>(sKT, K + row0 * DK, (size_t)H * DK, len, nullptr);
-  stage_rows_T<E, DK, LDC, NTH>(sQT, Q + row0 * DK, (size_t)H * DK, len, nullptr);
-  lds_barrier();
-
-  // intra-chunk matrices
-  float ea[4][4];
-  {
-    const float* gP = a.Pm + ch * CH * CH;
-    const float* gAk = a.Ak + ch * CH * CH;
-    float dbA[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int r = prt * 16 + acc_row(e), i = j * 16 + acc_col();
-        const float gam = (i <= r) ? __expf(sg[r] - sg[i]) : 0.f;
-        if (pm == 0) {
-          const float dp = (i <= r) ? PA[0][j][e] : 0.f;
-          const float m1 = dp * gam;
-          sM1[r * LDC + i] = to_e<E>(m1);
-          sM1T[i * LDC + r] = to_e<E>(m1);
-          sE[r * LDE + i] = dp * gP[r * CH + i];
-          ea[j][e] = 0.f;
-        } else {
-          const float da = (i < r) ? -PA[0][j][e] : 0.f;
-          const float ak = gAk[r * CH + i];
-          sD[r * LDE + i] = sb[r] * da * gam;
-          ea[j][e] = da * sb[r] * ak;
-          dbA[e] += da * ak;
-        }
-      }
-    if (pm == 1) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float s = reduce16(dbA[e]);
-        if (acc_col() == 0) sdbA[prt * 16 + acc_row(e)] = s;
-      }
+    if (l == 0) sred[w] = s;
+    if (w < 4) {
+      float x = xvp;
+      x += __shfl_xor(x, 16, 64);
+      x += __shfl_xor(x, 32, 64);
+      if (l < 16) sxv[w * 16 + l] = x;
     }
-  }
-  // row dot products of the raw accumulators
-  {
-    float pq[RTW][4], pk[RTW][4], ps[RTW][4];
-#pragma unroll
-    for (int i = 0; i < RTW; ++i)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        pq[i][e] = pk[i][e] = ps[i][e] = 0.f;
-        const int r = (wr * RTW + i) * 16 + acc_row(e);
-#pragma unroll
-        for (int j = 0; j < CTW; ++j) {
-          const int d = (wc * CTW + j) * 16 + acc_col();
-          const float qv = to_f(sQT[d * LDC + r]), kv = to_f(sKT[d * LDC + r]);
-          pq[i][e] += qv * Gq[i][j][e];
-          pk[i][e] += kv * Gk[i][j][e];
-          ps[i][e] += kv * Gs[i][j][e];
-        }
-      }
-#pragma unroll
-    for (int i = 0; i < RTW; ++i)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float a0 = reduce16(pq[i][e]), a1 = reduce16(pk[i][e]), a2 = reduce16(ps[i][e]);
-        if (acc_col() == 0) {
-          const int r = (wr * RTW + i) * 16 + acc_row(e);
-          srow[wc][0][r] = a0;
-          srow[wc][1][r] = a1;
-          srow[wc][2][r] = a2;
-        }
-      }
-  }
-  lds_barrier();
-  if (pm == 1) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int r = prt * 16 + acc_row(e), i = j * 16 + acc_col();
-        sE[r * LDE + i] += ea[j][e];
-      }
   }
   lds_barrier();
   for (int idx = tid; idx < CH * CH; idx += NTH) {
     const int r = idx >> 6, i = idx & 63;
-    sDD[r * LDC + i] = to_e<E>(sD[r * LDE + i] + sD[i * LDE + r]);
-  }
-  if (tid < CH) {
-    float s = 0.f;
-    for (int i = 0; i < CH; ++i) s += sE[tid * LDE + i];
-    sErow[tid] = s;
-  } else if (tid < 2 * CH) {
-    const int col = tid - CH;
-    float s = 0.f;
-    for (int j = 0; j < CH; ++j) s += sE[j * LDE + col];
-    sEcol[col] = s;
+    sDD[r * LD + i] = to_e<E>(sD[r * LDF + i] + sD[i * LDF + r]);
   }
   lds_barrier();
 
-  // dQ and dK
+  // (2) dQ and dK for this wave's dk columns
+  {
+    const E* KTp = (const E*)a.KTf + ch * DK * CH;
+    const E* QTp = (const E*)a.QTf + ch * DK * CH;
 #pragma unroll
-  for (int i = 0; i < RTW; ++i)
+    for (int n = 0; n < NDT; ++n) {
+      const int dt = w * NDT + n;
+      frag fk[NKC], fq[NKC];
 #pragma unroll
-    for (int j = 0; j < CTW; ++j)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int r = (wr * RTW + i) * 16 + acc_row(e);
-        Gq[i][j][e] *= seg[r];
-        Gk[i][j][e] = sdec[r] * Gs[i][j][e] - sb[r] * seg[r] * Gk[i][j][e];
+      for (int kt = 0; kt < NKC; ++kt) {
+        fk[kt] = M::load(KTp + (size_t)(dt * NKC + kt) * FR + l * M::KPL);
+        fq[kt] = M::load(QTp + (size_t)(dt * NKC + kt) * FR + l * M::KPL);
       }
-  {
-    const E* Bk = sKT + wc * CTW * 16 * LDC;
-    const E* Bq = sQT + wc * CTW * 16 * LDC;
-    wave_mma_nt<E, RTW, CTW, CH>(Gq, sM1 + wr * RTW * 16 * LDC, LDC, Bk, LDC);
-    wave_mma_nt<E, RTW, CTW, CH>(Gk, sM1T + wr * RTW * 16 * LDC, LDC, Bq, LDC);
-    wave_mma_nt<E, RTW, CTW, CH>(Gk, sDD + wr * RTW * 16 * LDC, LDC, Bk, LDC);
-  }
-  {
-    E* gdq = (E*)a.dq + row0 * DK;
-    E* gdk = (E*)a.dk + row0 * DK;
+      // row dots with the raw accumulators: element e of row tile i pairs with
+      // slot (i & 1) * 4 + e of k-step i >> 1 (bf16) or k-step 4 i + e (fp32)
 #pragma unroll
-    for (int i = 0; i < RTW; ++i)
-#pragma unroll
-      for (int j = 0; j < CTW; ++j)
+      for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const int r = (wr * RTW + i) * 16 + acc_row(e);
-          const int d = (wc * CTW + j) * 16 + acc_col();
-          if (r < len) {
-            gdq[(size_t)r * H * DK + d] = to_e<E>(Gq[i][j][e]);
-            gdk[(size_t)r * H * DK + d] = to_e<E>(Gk[i][j][e]);
+          union {
+            frag f;
+            E x[M::KPL];
+          } uk, uq;
+          float kv, qv;
+          if (sizeof(E) == 2) {
+            uk.f = fk[i >> 1];
+            uq.f = fq[i >> 1];
+            kv = to_f(uk.x[(i & 1) * 4 + e]);
+            qv = to_f(uq.x[(i & 1) * 4 + e]);
+          } else {
+            uk.f = fk[(4 * i + e) % NKC];
+            uq.f = fq[(4 * i + e) % NKC];
+            kv = to_f(uk.x[0]);
+            qv = to_f(uq.x[0]);
+          }
+          // this tile's share of the row dots, summed over its 16 columns and
+          // folded into the wave's slot (same lane, in program order)
+          const float a0 = reduce16(qv * Gq[i][n][e]);
+          const float a1 = reduce16(kv * Gk[i][n][e]);
+          const float a2 = reduce16(kv * Gs[i][n][e]);
+          if (acc_col() == 0) {
+            const int r = i * 16 + acc_row(e);
+            srow[w][0][r] = (n == 0 ? 0.f : srow[w][0][r]) + a0;
+            srow[w][1][r] = (n == 0 ? 0.f : srow[w][1][r]) + a1;
+            srow[w][2][r] = (n == 0 ? 0.f : srow[w][2][r]) + a2;
           }
         }
-  }
-
-  // dbeta, dg, dlog_alpha (one wave, one lane per chunk position)
-  if (w == 0) {
-    const int r = lane_id();
-    float pq = 0.f, pk = 0.f, ps = 0.f;
 #pragma unroll
-    for (int x = 0; x < WC; ++x) {
+      for (int i = 0; i < 4; ++i) {
+        f32x4 dq = Gq[i][n], dk;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = i * 16 + acc_row(e);
+          dq[e] *= __expf(sg[r]);
+          dk[e] = __expf(sg[CH - 1] - sg[r]) * Gs[i][n][e] - sb[r] * __expf(sg[r]) * Gk[i][n][e];
+        }
+        const E* m1row = sM1 + (i * 16 + (l & 15)) * LD;
+        const E* m1trow = sM1T + (i * 16 + (l & 15)) * LD;
+        const E* ddrow = sDD + (i * 16 + (l & 15)) * LD;
+#pragma unroll
+        for (int kt = 0; kt < NKC; ++kt) {
+          frag am, amt, add;
+          union {
+            frag f;
+            E x[M::KPL];
+          } u0, u1, u2;
+#pragma unroll
+          for (int j = 0; j < M::KPL; ++j) {
+            const int k = kperm<E>(kt, g4, j);
+            u0.x[j] = m1row[k];
+            u1.x[j] = m1trow[k];
+            u2.x[j] = ddrow[k];
+          }
+          am = u0.f;
+          amt = u1.f;
+          add = u2.f;
+          dq = M::mma(am, fk[kt], dq);
+          dk = M::mma(amt, fq[kt], dk);
+          dk = M::mma(add, fk[kt], dk);
+        }
+        E* gdq = (E*)a.dq + row0 * DK + dt * 16 + acc_col();
+        E* gdk = (E*)a.dk + row0 * DK + dt * 16 + acc_col();
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = i * 16 + acc_row(e);
+          if (r < len) {
+            gdq[(size_t)r * H * DK] = to_e<E>(dq[e]);
+            gdk[(size_t)r * H * DK] = to_e<E>(dk[e]);
+          }
+        }
+      }
+    }
+  }
+  lds_barrier();
+
+  // (3) dbeta, dg, dlog_alpha (one wave, one lane per chunk position)
+  if (w == 0) {
+    const int r = l;
+    float pq = 0.f, pk = 0.f, ps = 0.f, s_dot = 0.f;
+#pragma unroll
+    for (int x = 0; x < NW; ++x) {
       pq += srow[x][0][r];
       pk += srow[x][1][r];
       ps += srow[x][2][r];
+      s_dot += sred[x];
     }
-    float s_dot = 0.f;
+    float ecol = 0.f;
 #pragma unroll
-    for (int x = 0; x < 8; ++x) s_dot += sred[x];
+    for (int x = 0; x < 8; ++x) ecol += sEcol[x][r];
     const bool valid = r < len;
-    const float eg = seg[r], b = sb[r], dec = sdec[r];
-    float dg = eg * pq - b * eg * pk - dec * ps + sErow[r] - sEcol[r];
+    const float gn = sg[CH - 1];
+    const float eg = __expf(sg[r]), b = sb[r], dec = __expf(gn - sg[r]);
+    float dg = eg * pq - b * eg * pk - dec * ps + sErow[0][r] + sErow[1][r] - ecol;
     const float db = sdbA[r] + sxv[r] - eg * pk;
     float tail = valid ? dec * ps : 0.f;
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) tail += __shfl_xor(tail, off, 64);
-    const float gn = __shfl(sg[r], len - 1, 64);
     if (r == len - 1) dg += tail + __expf(gn) * s_dot;
     if (!valid) dg = 0.f;
     // reverse inclusive scan: lane r receives sum_{r' >= r} dg_r'
@@ -300,11 +391,9 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
   }
 }
 
-
 hipError_t launch_grad(Dt dt, int dk, int dv, const Args& a, hipStream_t s) {
   auto f = [&]<class E, int DK, int DV>() {
-    constexpr int BVG = (sizeof(E) == 2 && DK == 256) ? 32 : 64;
-    hipLaunchKernelGGL((k_grad<E, DK, DV, BVG>), dim3(a.NC, a.H), dim3(512), 0, s, a);
+    hipLaunchKernelGGL((k_grad<E, DK, DV>), dim3(a.NC, a.H), dim3(GradCfg<E, DK>::NTH), 0, s, a);
     return hipGetLastError();
   };
   GDN_DISPATCH(dt, dk, dv, f);

@@ -37,8 +37,10 @@ struct Args {
   void* nWT;  // -W~^T                     rows d, k = t     dk x 64  (backward)
   void* QgT;  // (diag(e^g) Q)^T           rows d, k = t     dk x 64  (backward)
   // workspace: backward intermediates for the gradient kernel
-  float* Pm;  // [ch][64][64] P, fp32
-  float* Ak;  // [ch][64][64] strictLower(Gamma * K K^T), fp32
+  void* KTf;  // K^T                       rows d, k = t     dk x 64  (backward)
+  void* QTf;  // Q^T                       rows d, k = t     dk x 64  (backward)
+  float* Pm;  // [ch] P, fp32, accumulator layout of a 64 x 64 matrix
+  float* Ak;  // [ch] strictLower(Gamma * K K^T), fp32, accumulator layout
   void* Sc;   // [ch][dk][dv] chunk entry states (row-major)
   void* Vp;   // [ch][64][dv] V' = U~ - W~ S
   void* dSc;  // [ch][dk][dv] gradient of each chunk's exit state

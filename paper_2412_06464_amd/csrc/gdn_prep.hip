@@ -20,8 +20,9 @@
 //                  LDS, then the operands of the sequential passes, streamed
 //                  over 64-wide slices of dk and dv.  Forward: W~, Kbar^T, U~,
 //                  P, diag(e^g) Q.  Backward (recompute): W~, Kbar^T, U~, and
-//                  for the reverse pass K, P^T, T^T, -W~^T, (e^g Q)^T, plus P
-//                  and strictLower(Gamma K K^T) in fp32 for the gradient kernel.
+//                  for the reverse pass K, P^T, T^T, -W~^T, (e^g Q)^T, plus
+//                  K^T, Q^T, and P and strictLower(Gamma K K^T) in fp32 for
+//                  the gradient kernel.
 #include "gdn_device.h"
 #include "gdn_kernels.h"
 
@@ -122,11 +123,17 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
       const float p = (i <= r) ? gam * qk[0][j][e] : 0.f;
       sA[r * LDA + i] = sb[r] * ak;
       sP[r * LD + i] = to_e<E>(p);
-      if (BWD) {
-        a.Ak[ch * CH * CH + r * CH + i] = ak;
-        a.Pm[ch * CH * CH + r * CH + i] = p;
-      }
+      kk[0][j][e] = ak;
+      qk[0][j][e] = p;
     }
+  if (BWD) {
+    // P and strictLower(Gamma K K^T) in fp32, accumulator layout
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      *reinterpret_cast<f32x4*>(a.Ak + ch * CH * CH + cfrag_index(w, j, CH)) = kk[0][j];
+      *reinterpret_cast<f32x4*>(a.Pm + ch * CH * CH + cfrag_index(w, j, CH)) = qk[0][j];
+    }
+  }
   lds_barrier();
 
   // ---- T = (I + A)^-1, A strictly lower.  Diagonal 16x16 blocks by forward
@@ -235,6 +242,11 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
       // (e^g Q)^T as A operands (rows d, k = t)
       export_afrag_perm<E, 64, CH, 256>((E*)a.QgT + ch * DK * CH + (size_t)64 * s * CH,
                                         [&](int d, int t) { return seg[t] * to_f(sY[d * LD + t]); });
+      // raw K^T and Q^T as A operands (rows d, k = t) for the gradient kernel
+      export_afrag_perm<E, 64, CH, 256>((E*)a.KTf + ch * DK * CH + (size_t)64 * s * CH,
+                                        [&](int d, int t) { return to_f(sX[d * LD + t]); });
+      export_afrag_perm<E, 64, CH, 256>((E*)a.QTf + ch * DK * CH + (size_t)64 * s * CH,
+                                        [&](int d, int t) { return to_f(sY[d * LD + t]); });
     }
     lds_barrier();
   }

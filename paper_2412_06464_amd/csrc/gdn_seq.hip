@@ -53,7 +53,7 @@ struct SeqCfg {
 // ------------------------------------------------------------------ forward / recompute
 // STORE = false: forward, writes O and ht.
 // STORE = true : backward recompute, writes each chunk's entry state and V'
-//                (row-major, for the gradient kernel).
+//                (in MFMA fragment order over dv, for the gradient kernel).
 
 template <class E, int DK, int DV, bool STORE>
 __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_fwd_seq(Args a) {
@@ -159,7 +159,7 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_fwd_seq(Args a) {
     lds_barrier();
 
     // (b) W~ S and diag(e^g) Q S for the wave's 16 token rows
-    if (STORE) copy_out_rows<E, DK, BV, LDV, 256>((E*)a.Sc + ch * DK * DV + v0, DV, sSs, DK);
+    if (STORE) copy_out_frags<E, DK, BV, LDV, 256>((E*)a.Sc + ch * DK * DV, DV / M::K, v0, sSs);
     f32x4 P[NTV], Qs[NTV];
 #pragma unroll
     for (int jj = 0; jj < NTV; ++jj) P[jj] = Qs[jj] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -213,7 +213,7 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_fwd_seq(Args a) {
       }
     load_kp(min(j + 1, nch - 1));
     if (STORE) {
-      copy_out_rows<E, CH, BV, LDV, 256>((E*)a.Vp + ch * CH * DV + v0, DV, sOut, CH);
+      copy_out_frags<E, CH, BV, LDV, 256>((E*)a.Vp + ch * CH * DV, DV / M::K, v0, sOut);
     } else {
       E* orow = (E*)a.o + ((size_t)start * H + h) * DV + v0 + acc_col();
 #pragma unroll
@@ -381,9 +381,9 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
 
     // (b) dV' = P^T dO + diag(e^{g_n - g}) (K dS); the stores of dS and of the
     //     previous chunk's dX rows
-    copy_out_rows<E, DK, BV, LDV, 256>((E*)a.dSc + ch * DK * DV + v0, DV, sSs, DK);
+    copy_out_frags<E, DK, BV, LDV, 256>((E*)a.dSc + ch * DK * DV, DV / M::K, v0, sSs);
     if (j + 1 < nch)
-      copy_out_rows<E, CH, BV, LDV, 256>((E*)a.dXb + prev_ch * CH * DV + v0, DV, sOut, CH);
+      copy_out_frags<E, CH, BV, LDV, 256>((E*)a.dXb + prev_ch * CH * DV, DV / M::K, v0, sOut);
     f32x4 X1[NTV], X2[NTV];
 #pragma unroll
     for (int jj = 0; jj < NTV; ++jj) X1[jj] = X2[jj] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -453,7 +453,7 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
   }
   if (nch > 0) {
     lds_barrier();
-    copy_out_rows<E, CH, BV, LDV, 256>((E*)a.dXb + prev_ch * CH * DV + v0, DV, sOut, CH);
+    copy_out_frags<E, CH, BV, LDV, 256>((E*)a.dXb + prev_ch * CH * DV, DV / M::K, v0, sOut);
   }
 
   if (a.dh0) {
