@@ -3,13 +3,17 @@
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 
-One step = one pass of the whole hot path over one batch of synthetic input:
-gdn_chunk_fwd followed by gdn_chunk_bwd for forward+backward workloads, or
-gdn_chunk_fwd alone for forward-only ones.  Inputs, outputs and workspaces
-are resident in HBM before the timed region; the timed region is K steps
-between two device synchronisations.  Per-kernel durations come from HIP
-events that the library records around each of its launches on the same
-stream (the *_timed entry points), one event set per step.
+One step = one pass of the whole hot path over one batch of synthetic input.
+For forward+backward workloads that is a training step: gdn_chunk_fwd_save
+(the forward, keeping what the backward needs) followed by
+gdn_chunk_bwd_saved; the stateless pair gdn_chunk_fwd + gdn_chunk_bwd (the
+backward recomputes the chunk states) is timed the same way afterwards and
+reported beside it.  Forward-only workloads run gdn_chunk_fwd.  Inputs,
+outputs, the saved buffer and the workspaces are resident in HBM before the
+timed region; the timed region is K steps between two device
+synchronisations.  Per-kernel durations come from HIP events that the
+library records around each of its launches on the same stream (the *_timed
+entry points), one event set per step.
 
 Prints one JSON line (rank 0; this build runs on one GPU only).
 """
@@ -80,8 +84,14 @@ def kernel_models(w, n_chunks_heads):
         # as forward, plus P^T, T^T, -W~^T, (e^g Q)^T, and P, Ak in fp32
         "bwd:k_prep": (2 * kside + vside + gates + C * f32 + 4 * kside + vside + 2 * cc
                        + 2 * C * C * f32, 4 * prod_dk + prod_dv + C ** 3 / 3),
+        # both of the above (P and P^T)
+        "fwd:k_prep_save": (2 * kside + vside + gates + C * f32 + 4 * kside + vside + 3 * cc
+                            + 2 * C * C * f32, 4 * prod_dk + prod_dv + C ** 3 / 3),
         # W~, q, Kbar^T, P, U~, g in; o out
         "k_fwd_seq": (3 * kside + cc + vside + C * f32 + vside, 3 * prod_s + prod_dv),
+        # as k_fwd_seq, plus chunk states and V' out
+        "k_fwd_seq_save": (3 * kside + cc + vside + C * f32 + vside + st + vside,
+                           3 * prod_s + prod_dv),
         # W~, Kbar^T, U~ in; chunk states and V' out
         "k_fwd_seq_store": (2 * kside + vside + C * f32 + st + vside, 2 * prod_s),
         # k, (e^g Q)^T, -W~^T, P^T, T^T, dO, g, beta in; dS, dX, dv out
@@ -197,6 +207,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--path", choices=("saved", "stateless"), default="saved",
+                    help="backward path of the headline step (the other is timed beside it)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy 10 times (PMC calibration)")
     args = ap.parse_args()
@@ -234,52 +246,75 @@ def main():
     ws_f = torch.empty(gdn.gdn_chunk_fwd_workspace_size(p), dtype=torch.uint8, device=dev)
     o = torch.empty_like(d["v"])
     ht = torch.empty((n_states, w.H, w.dk, w.dv), dtype=torch.float32, device=dev)
-    out_b = ws_b = None
+    out_b = ws_b = saved = ws_fs = ws_bs = None
     if w.backward:
         ws_b = torch.empty(gdn.gdn_chunk_bwd_workspace_size(p), dtype=torch.uint8, device=dev)
+        saved = torch.empty(gdn.gdn_chunk_saved_size(p), dtype=torch.uint8, device=dev)
+        ws_fs = torch.empty(gdn.gdn_chunk_fwd_save_workspace_size(p), dtype=torch.uint8,
+                            device=dev)
+        ws_bs = torch.empty(gdn.gdn_chunk_bwd_saved_workspace_size(p), dtype=torch.uint8,
+                            device=dev)
         out_b = dict(dq=torch.empty_like(d["q"]), dk=torch.empty_like(d["k"]),
                      dv=torch.empty_like(d["v"]), dbeta=torch.empty_like(d["beta"]),
                      dlog_alpha=torch.empty_like(d["log_alpha"]),
                      dh0=torch.empty_like(ht))
+    fwd_kw = dict(h0=d.get("h0"), cu_seqlens=cu, cu_seqlens_host=cu_host, o=o, ht=ht)
 
-    def step(timers=None):
-        gdn.gdn_chunk_fwd(d["q"], d["k"], d["v"], d["beta"], d["log_alpha"], h0=d.get("h0"),
-                          cu_seqlens=cu, cu_seqlens_host=cu_host, o=o, ht=ht, workspace=ws_f,
-                          timer=timers[0] if timers else None)
+    def step_stateless(timers=None):
+        gdn.gdn_chunk_fwd(d["q"], d["k"], d["v"], d["beta"], d["log_alpha"], workspace=ws_f,
+                          timer=timers[0] if timers else None, **fwd_kw)
         if w.backward:
             gdn.gdn_chunk_bwd(d["q"], d["k"], d["v"], d["beta"], d["log_alpha"], d["dO"],
                               h0=d.get("h0"), dht=d["dht"], cu_seqlens=cu,
                               cu_seqlens_host=cu_host, workspace=ws_b, out=out_b,
                               timer=timers[1] if timers else None)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    timers = [(gdn.LaunchTimer(8), gdn.LaunchTimer(8) if w.backward else None)
-              for _ in range(args.steps)]
-    stream = torch.cuda.current_stream(dev)
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record(stream)
-    for i in range(args.steps):
-        step(timers[i])
-    end.record(stream)
-    torch.cuda.synchronize()
-    ms = start.elapsed_time(end) / args.steps
+    def step_saved(timers=None):
+        gdn.gdn_chunk_fwd_save(d["q"], d["k"], d["v"], d["beta"], d["log_alpha"], saved=saved,
+                               workspace=ws_fs, timer=timers[0] if timers else None, **fwd_kw)
+        gdn.gdn_chunk_bwd_saved(d["q"], d["v"], d["beta"], d["dO"], saved, dht=d["dht"],
+                                cu_seqlens=cu, cu_seqlens_host=cu_host, workspace=ws_bs,
+                                out=out_b, timer=timers[1] if timers else None)
 
-    # per-kernel durations over the timed region
-    per_kernel = {}
-    for tf, tb in timers:
-        for call, t in (("fwd", tf), ("bwd", tb)):
-            if t is None:
-                continue
-            for name, kms in t.durations_ms().items():
-                per_kernel.setdefault(call + ":" + name, []).append(kms)
-        tf.close()
-        if tb is not None:
-            tb.close()
-    kern_ms = {k: sum(v) / len(v) for k, v in per_kernel.items()}
+    stream = torch.cuda.current_stream(dev)
+
+    def timed_run(step):
+        """Warm up, then time K steps; returns (ms per step, {kernel: mean ms})."""
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        timers = [(gdn.LaunchTimer(8), gdn.LaunchTimer(8) if w.backward else None)
+                  for _ in range(args.steps)]
+        start = torch.cuda.Event(enable_timing=True)
+        end = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record(stream)
+        for i in range(args.steps):
+            step(timers[i])
+        end.record(stream)
+        torch.cuda.synchronize()
+        per_kernel = {}
+        for tf, tb in timers:
+            for call, t in (("fwd", tf), ("bwd", tb)):
+                if t is None:
+                    continue
+                for name, kms in t.durations_ms().items():
+                    per_kernel.setdefault(call + ":" + name, []).append(kms)
+            tf.close()
+            if tb is not None:
+                tb.close()
+        return (start.elapsed_time(end) / args.steps,
+                {k: sum(v) / len(v) for k, v in per_kernel.items()})
+
+    path = args.path if w.backward else "stateless"
+    steps = {"saved": step_saved, "stateless": step_stateless}
+    ms, kern_ms = timed_run(steps[path])
+    other = None
+    if w.backward:
+        oname = "stateless" if path == "saved" else "saved"
+        oms, okern = timed_run(steps[oname])
+        other = {"path": oname, "ms_per_step": oms, "value": w.B * w.T / (oms / 1e3),
+                 "kernels_ms": okern}
 
     tokens = w.B * w.T
     tokens_heads = tokens * w.H
@@ -319,7 +354,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": args.workload, "B": w.B, "T": w.T, "H": w.H, "dk": w.dk,
                    "dv": w.dv, "chunk": CH, "backward": w.backward,
-                   "num_seqs": n_states},
+                   "num_seqs": n_states, "path": path},
         "mfma_frac": flops / (ms / 1e3) / peak_mfma,
         "hbm_frac": nbytes / (ms / 1e3) / PEAK_HBM,
         "path_gflop": flops / 1e9,
@@ -327,6 +362,8 @@ def main():
         "kernels_ms": kern_ms,
         "roofline": roof,
     }
+    if other is not None:
+        res["other_path"] = other
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(inp, w)
     print(json.dumps(res), flush=True)

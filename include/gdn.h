@@ -64,7 +64,8 @@ typedef enum {
   GDN_ERR_CU_SEQLENS = 4,  /* cu_seqlens_host malformed, or device copy NULL */
   GDN_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than the query      */
   GDN_ERR_HIP = 6,         /* a kernel launch failed                         */
-  GDN_ERR_ALIGN = 7        /* a pointer is not 16-byte aligned               */
+  GDN_ERR_ALIGN = 7,       /* a pointer is not 16-byte aligned               */
+  GDN_ERR_SAVED = 8        /* saved buffer NULL or smaller than the query    */
 } gdn_status;
 
 typedef struct {
@@ -107,6 +108,42 @@ gdn_status gdn_chunk_bwd(const gdn_problem *p, const void *q, const void *k,
                          void *dv, float *dbeta, float *dlog_alpha, float *dh0,
                          void *workspace, size_t workspace_bytes, void *stream);
 
+/* Forward that keeps what the backward needs (training).  Same operation
+ * and outputs as gdn_chunk_fwd (Sec. 3.3), and in addition fills `saved`
+ * (device memory of gdn_chunk_saved_size bytes, owned by the caller, opaque
+ * to it) with the per-chunk quantities the backward reads: the cumulative
+ * log-gates, each chunk's entry state S_[t], the pseudo-values
+ * V' = U~ - W~ S_[t] of the UT transform, and the chunk-local operands built
+ * from q, k, beta and the gates (P, T = (I + A)^-1, W~, their transposes).
+ * The layout of `saved` depends only on the problem; its content is valid
+ * for the inputs the call was made with until the caller overwrites it.
+ * `workspace` (gdn_chunk_fwd_save_workspace_size bytes) holds the call's
+ * temporaries only and may be reused as soon as the call has run. */
+size_t gdn_chunk_saved_size(const gdn_problem *p);
+size_t gdn_chunk_fwd_save_workspace_size(const gdn_problem *p);
+gdn_status gdn_chunk_fwd_save(const gdn_problem *p, const void *q,
+                              const void *k, const void *v, const float *beta,
+                              const float *log_alpha, const float *h0, void *o,
+                              float *ht, void *saved, size_t saved_bytes,
+                              void *workspace, size_t workspace_bytes,
+                              void *stream);
+
+/* Backward from a saving forward's buffer: the same gradients as
+ * gdn_chunk_bwd for the inputs gdn_chunk_fwd_save was called with, without
+ * rebuilding the chunk operands or recomputing the chunk states.  Reads v
+ * and beta (the delta-rule terms of dbeta), dO, dht (or NULL) and `saved`,
+ * which it leaves unchanged; q, k, log_alpha and h0 enter through `saved`.
+ * Same outputs as gdn_chunk_bwd.  `workspace` holds
+ * gdn_chunk_bwd_saved_workspace_size bytes. */
+size_t gdn_chunk_bwd_saved_workspace_size(const gdn_problem *p);
+gdn_status gdn_chunk_bwd_saved(const gdn_problem *p, const void *v,
+                               const float *beta, const void *dO,
+                               const float *dht, const void *saved,
+                               size_t saved_bytes, void *dq, void *dk,
+                               void *dv, float *dbeta, float *dlog_alpha,
+                               float *dh0, void *workspace,
+                               size_t workspace_bytes, void *stream);
+
 /* Optional launch timing, for benchmarks and profilers.  The caller creates
  * and owns the events (hipEvent_t handles, e.g. from hipEventCreate).  A
  * *_timed call records events[2i] just before and events[2i+1] just after
@@ -136,6 +173,21 @@ gdn_status gdn_chunk_bwd_timed(const gdn_problem *p, const void *q,
                                float *dlog_alpha, float *dh0, void *workspace,
                                size_t workspace_bytes, void *stream,
                                gdn_timing *timing);
+gdn_status gdn_chunk_fwd_save_timed(const gdn_problem *p, const void *q,
+                                    const void *k, const void *v,
+                                    const float *beta, const float *log_alpha,
+                                    const float *h0, void *o, float *ht,
+                                    void *saved, size_t saved_bytes,
+                                    void *workspace, size_t workspace_bytes,
+                                    void *stream, gdn_timing *timing);
+gdn_status gdn_chunk_bwd_saved_timed(const gdn_problem *p, const void *v,
+                                     const float *beta, const void *dO,
+                                     const float *dht, const void *saved,
+                                     size_t saved_bytes, void *dq, void *dk,
+                                     void *dv, float *dbeta, float *dlog_alpha,
+                                     float *dh0, void *workspace,
+                                     size_t workspace_bytes, void *stream,
+                                     gdn_timing *timing);
 
 /* Human-readable name of a status. */
 const char *gdn_status_string(gdn_status s);

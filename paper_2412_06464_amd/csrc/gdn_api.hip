@@ -65,73 +65,114 @@ gdn_status check_problem(const gdn_problem* p, Shape* out) {
   return GDN_OK;
 }
 
-// Workspace layout; `base` may be null to only compute the size.
-size_t carve(const gdn_problem* p, const Shape& s, bool backward, unsigned char* base,
-             Args* a) {
-  const size_t NC = (size_t)s.NC, H = (size_t)p->H;
+// Buffer layouts; `base` may be null to only compute the size.
+enum class Use { Fwd, Bwd, FwdSave, BwdSaved };
+
+struct Carver {
+  unsigned char* base;
   size_t off = 0;
-  auto take = [&](size_t bytes) {
+  unsigned char* take(size_t bytes) {
     unsigned char* ptr = base ? base + off : nullptr;
     off += up(bytes);
     return ptr;
-  };
-  unsigned char* info = take(NC * sizeof(int4) + 16);
-  unsigned char* sc0 = take(((size_t)s.N + 1) * sizeof(int));
-  unsigned char* g = take(NC * H * CH * sizeof(float));
-  // per-chunk operands in fragment layouts (element type of the problem)
-  const size_t kside = NC * H * CH * (size_t)p->dk * s.esz;  // 64 x dk
-  const size_t vside = NC * H * CH * (size_t)p->dv * s.esz;  // 64 x dv
-  const size_t cc = NC * H * CH * CH * s.esz;                // 64 x 64
-  unsigned char* Wf = take(kside);
-  unsigned char* KbT = take(kside);
-  unsigned char* Uc = take(vside);
-  unsigned char *Pf = nullptr, *PTf = nullptr, *TTf = nullptr, *nWT = nullptr, *QgT = nullptr;
-  unsigned char *Qf = nullptr, *Kf = nullptr, *KTf = nullptr, *QTf = nullptr;
-  unsigned char *Pm = nullptr, *Ak = nullptr;
-  unsigned char *Sc = nullptr, *Vp = nullptr, *dSc = nullptr, *dXb = nullptr;
-  if (!backward) {
-    Pf = take(cc);
-    Qf = take(kside);
-  } else {
-    Kf = take(kside);
-    PTf = take(cc);
-    TTf = take(cc);
-    nWT = take(kside);
-    QgT = take(kside);
-    KTf = take(kside);
-    QTf = take(kside);
-    Pm = take(NC * H * CH * CH * sizeof(float));
-    Ak = take(NC * H * CH * CH * sizeof(float));
-    const size_t st = NC * H * (size_t)p->dk * p->dv * s.esz;
-    Sc = take(st);
-    dSc = take(st);
-    Vp = take(vside);
-    dXb = take(vside);
   }
+};
+
+struct Sizes {
+  size_t kside, vside, cc, cf, st;
+  Sizes(const gdn_problem* p, const Shape& s) {
+    const size_t NC = (size_t)s.NC, H = (size_t)p->H;
+    kside = NC * H * CH * (size_t)p->dk * s.esz;        // 64 x dk per chunk
+    vside = NC * H * CH * (size_t)p->dv * s.esz;        // 64 x dv per chunk
+    cc = NC * H * CH * CH * s.esz;                      // 64 x 64 per chunk
+    cf = NC * H * CH * CH * sizeof(float);              // 64 x 64 fp32 per chunk
+    st = NC * H * (size_t)p->dk * p->dv * s.esz;        // dk x dv per chunk
+  }
+};
+
+// What the backward reads from the forward: the gates' cumulative sums, the
+// reverse pass's and gradient kernel's per-chunk operands, each chunk's entry
+// state and V'.  A saving forward writes it; the stateless backward keeps it
+// in its workspace.
+void carve_saved(const gdn_problem* p, const Shape& s, Carver& c, Args* a) {
+  const Sizes z(p, s);
+  unsigned char* g = c.take((size_t)s.NC * p->H * CH * sizeof(float));
+  unsigned char* Kf = c.take(z.kside);
+  unsigned char* PTf = c.take(z.cc);
+  unsigned char* TTf = c.take(z.cc);
+  unsigned char* nWT = c.take(z.kside);
+  unsigned char* QgT = c.take(z.kside);
+  unsigned char* KTf = c.take(z.kside);
+  unsigned char* QTf = c.take(z.kside);
+  unsigned char* Pm = c.take(z.cf);
+  unsigned char* Ak = c.take(z.cf);
+  unsigned char* Sc = c.take(z.st);
+  unsigned char* Vp = c.take(z.vside);
   if (a) {
-    a->info = (int4*)info;
-    a->seq_chunk0 = (int*)sc0;
     a->g = (float*)g;
-    a->Wf = Wf;
-    a->KbT = KbT;
-    a->Uc = Uc;
-    a->Pf = Pf;
-    a->Qf = Qf;
     a->Kf = Kf;
-    a->KTf = KTf;
-    a->QTf = QTf;
     a->PTf = PTf;
     a->TTf = TTf;
     a->nWT = nWT;
     a->QgT = QgT;
+    a->KTf = KTf;
+    a->QTf = QTf;
     a->Pm = (float*)Pm;
     a->Ak = (float*)Ak;
     a->Sc = Sc;
     a->Vp = Vp;
-    a->dSc = dSc;
-    a->dXb = dXb;
   }
-  return off;
+}
+
+size_t saved_bytes(const gdn_problem* p, const Shape& s) {
+  Carver c{nullptr};
+  carve_saved(p, s, c, nullptr);
+  return c.off;
+}
+
+// Workspace of one entry point: the chunk table, then what its kernels pass
+// between each other and the caller does not keep.
+size_t carve(const gdn_problem* p, const Shape& s, Use u, unsigned char* base, Args* a) {
+  const Sizes z(p, s);
+  Carver c{base};
+  unsigned char* info = c.take((size_t)s.NC * sizeof(int4) + 16);
+  unsigned char* sc0 = c.take(((size_t)s.N + 1) * sizeof(int));
+  if (a) {
+    a->info = (int4*)info;
+    a->seq_chunk0 = (int*)sc0;
+  }
+  if (u != Use::BwdSaved) {  // the forward pass's operands (the recompute's too)
+    unsigned char* Wf = c.take(z.kside);
+    unsigned char* KbT = c.take(z.kside);
+    unsigned char* Uc = c.take(z.vside);
+    if (a) {
+      a->Wf = Wf;
+      a->KbT = KbT;
+      a->Uc = Uc;
+    }
+  }
+  if (u == Use::Fwd || u == Use::FwdSave) {  // those only the output needs
+    unsigned char* Pf = c.take(z.cc);
+    unsigned char* Qf = c.take(z.kside);
+    if (a) {
+      a->Pf = Pf;
+      a->Qf = Qf;
+    }
+  }
+  if (u == Use::Fwd) {
+    unsigned char* g = c.take((size_t)s.NC * p->H * CH * sizeof(float));
+    if (a) a->g = (float*)g;
+  }
+  if (u == Use::Bwd) carve_saved(p, s, c, a);
+  if (u == Use::Bwd || u == Use::BwdSaved) {  // the reverse pass's chunk states and dX
+    unsigned char* dSc = c.take(z.st);
+    unsigned char* dXb = c.take(z.vside);
+    if (a) {
+      a->dSc = dSc;
+      a->dXb = dXb;
+    }
+  }
+  return c.off;
 }
 
 // Bridges the C timing struct to the launchers' view of it.
@@ -172,13 +213,13 @@ extern "C" {
 size_t gdn_chunk_fwd_workspace_size(const gdn_problem* p) {
   Shape s;
   if (check_problem(p, &s) != GDN_OK) return 0;
-  return carve(p, s, false, nullptr, nullptr);
+  return carve(p, s, Use::Fwd, nullptr, nullptr);
 }
 
 size_t gdn_chunk_bwd_workspace_size(const gdn_problem* p) {
   Shape s;
   if (check_problem(p, &s) != GDN_OK) return 0;
-  return carve(p, s, true, nullptr, nullptr);
+  return carve(p, s, Use::Bwd, nullptr, nullptr);
 }
 
 gdn_status gdn_chunk_fwd_timed(const gdn_problem* p, const void* q, const void* k,
@@ -192,12 +233,12 @@ gdn_status gdn_chunk_fwd_timed(const gdn_problem* p, const void* q, const void* 
   const void* ptrs[] = {q, k, v, beta, log_alpha, h0, o, ht, workspace};
   for (const void* x : ptrs)
     if (x && !aligned16(x)) return GDN_ERR_ALIGN;
-  const size_t need = carve(p, s, false, nullptr, nullptr);
+  const size_t need = carve(p, s, Use::Fwd, nullptr, nullptr);
   if (!workspace || workspace_bytes < need) return GDN_ERR_WORKSPACE;
   Args a;
   memset(&a, 0, sizeof a);
   fill_common(p, s, &a);
-  carve(p, s, false, (unsigned char*)workspace, &a);
+  carve(p, s, Use::Fwd, (unsigned char*)workspace, &a);
   a.q = q;
   a.k = k;
   a.v = v;
@@ -235,12 +276,12 @@ gdn_status gdn_chunk_bwd_timed(const gdn_problem* p, const void* q, const void* 
                         dh0, workspace};
   for (const void* x : ptrs)
     if (x && !aligned16(x)) return GDN_ERR_ALIGN;
-  const size_t need = carve(p, s, true, nullptr, nullptr);
+  const size_t need = carve(p, s, Use::Bwd, nullptr, nullptr);
   if (!workspace || workspace_bytes < need) return GDN_ERR_WORKSPACE;
   Args a;
   memset(&a, 0, sizeof a);
   fill_common(p, s, &a);
-  carve(p, s, true, (unsigned char*)workspace, &a);
+  carve(p, s, Use::Bwd, (unsigned char*)workspace, &a);
   a.q = q;
   a.k = k;
   a.v = v;
@@ -270,6 +311,114 @@ gdn_status gdn_chunk_bwd(const gdn_problem* p, const void* q, const void* k, con
                              dlog_alpha, dh0, workspace, workspace_bytes, stream, nullptr);
 }
 
+size_t gdn_chunk_saved_size(const gdn_problem* p) {
+  Shape s;
+  if (check_problem(p, &s) != GDN_OK) return 0;
+  return saved_bytes(p, s);
+}
+
+size_t gdn_chunk_fwd_save_workspace_size(const gdn_problem* p) {
+  Shape s;
+  if (check_problem(p, &s) != GDN_OK) return 0;
+  return carve(p, s, Use::FwdSave, nullptr, nullptr);
+}
+
+size_t gdn_chunk_bwd_saved_workspace_size(const gdn_problem* p) {
+  Shape s;
+  if (check_problem(p, &s) != GDN_OK) return 0;
+  return carve(p, s, Use::BwdSaved, nullptr, nullptr);
+}
+
+gdn_status gdn_chunk_fwd_save_timed(const gdn_problem* p, const void* q, const void* k,
+                                    const void* v, const float* beta, const float* log_alpha,
+                                    const float* h0, void* o, float* ht, void* saved,
+                                    size_t saved_bytes_, void* workspace, size_t workspace_bytes,
+                                    void* stream, gdn_timing* timing) {
+  Shape s;
+  gdn_status st = check_problem(p, &s);
+  if (st != GDN_OK) return st;
+  if (!q || !k || !v || !beta || !log_alpha || !o) return GDN_ERR_NULL;
+  const void* ptrs[] = {q, k, v, beta, log_alpha, h0, o, ht, saved, workspace};
+  for (const void* x : ptrs)
+    if (x && !aligned16(x)) return GDN_ERR_ALIGN;
+  if (!saved || saved_bytes_ < saved_bytes(p, s)) return GDN_ERR_SAVED;
+  if (!workspace || workspace_bytes < carve(p, s, Use::FwdSave, nullptr, nullptr))
+    return GDN_ERR_WORKSPACE;
+  Args a;
+  memset(&a, 0, sizeof a);
+  fill_common(p, s, &a);
+  carve(p, s, Use::FwdSave, (unsigned char*)workspace, &a);
+  Carver c{(unsigned char*)saved};
+  carve_saved(p, s, c, &a);
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.beta = beta;
+  a.log_alpha = log_alpha;
+  a.h0 = h0;
+  a.o = o;
+  a.ht = ht;
+  TimingGuard tg(timing);
+  const hipError_t e = gdn::launch_fwd_save(p->dtype == GDN_F32 ? Dt::F32 : Dt::BF16, p->dk,
+                                            p->dv, a, (hipStream_t)stream, tg.get());
+  return e == hipSuccess ? GDN_OK : GDN_ERR_HIP;
+}
+
+gdn_status gdn_chunk_fwd_save(const gdn_problem* p, const void* q, const void* k, const void* v,
+                              const float* beta, const float* log_alpha, const float* h0,
+                              void* o, float* ht, void* saved, size_t saved_bytes_,
+                              void* workspace, size_t workspace_bytes, void* stream) {
+  return gdn_chunk_fwd_save_timed(p, q, k, v, beta, log_alpha, h0, o, ht, saved, saved_bytes_,
+                                  workspace, workspace_bytes, stream, nullptr);
+}
+
+gdn_status gdn_chunk_bwd_saved_timed(const gdn_problem* p, const void* v, const float* beta,
+                                     const void* dO, const float* dht, const void* saved,
+                                     size_t saved_bytes_, void* dq, void* dk, void* dv,
+                                     float* dbeta, float* dlog_alpha, float* dh0,
+                                     void* workspace, size_t workspace_bytes, void* stream,
+                                     gdn_timing* timing) {
+  Shape s;
+  gdn_status st = check_problem(p, &s);
+  if (st != GDN_OK) return st;
+  if (!v || !beta || !dO || !dq || !dk || !dv || !dbeta || !dlog_alpha) return GDN_ERR_NULL;
+  const void* ptrs[] = {v, beta, dO, dht, saved, dq, dk, dv, dbeta, dlog_alpha, dh0, workspace};
+  for (const void* x : ptrs)
+    if (x && !aligned16(x)) return GDN_ERR_ALIGN;
+  if (!saved || saved_bytes_ < saved_bytes(p, s)) return GDN_ERR_SAVED;
+  if (!workspace || workspace_bytes < carve(p, s, Use::BwdSaved, nullptr, nullptr))
+    return GDN_ERR_WORKSPACE;
+  Args a;
+  memset(&a, 0, sizeof a);
+  fill_common(p, s, &a);
+  carve(p, s, Use::BwdSaved, (unsigned char*)workspace, &a);
+  Carver c{(unsigned char*)const_cast<void*>(saved)};
+  carve_saved(p, s, c, &a);
+  a.v = v;
+  a.beta = beta;
+  a.dO = dO;
+  a.dht = dht;
+  a.dq = dq;
+  a.dk = dk;
+  a.dv = dv;
+  a.dbeta = dbeta;
+  a.dlog_alpha = dlog_alpha;
+  a.dh0 = dh0;
+  TimingGuard tg(timing);
+  const hipError_t e = gdn::launch_bwd_saved(p->dtype == GDN_F32 ? Dt::F32 : Dt::BF16, p->dk,
+                                             p->dv, a, (hipStream_t)stream, tg.get());
+  return e == hipSuccess ? GDN_OK : GDN_ERR_HIP;
+}
+
+gdn_status gdn_chunk_bwd_saved(const gdn_problem* p, const void* v, const float* beta,
+                               const void* dO, const float* dht, const void* saved,
+                               size_t saved_bytes_, void* dq, void* dk, void* dv, float* dbeta,
+                               float* dlog_alpha, float* dh0, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+  return gdn_chunk_bwd_saved_timed(p, v, beta, dO, dht, saved, saved_bytes_, dq, dk, dv, dbeta,
+                                   dlog_alpha, dh0, workspace, workspace_bytes, stream, nullptr);
+}
+
 const char* gdn_status_string(gdn_status s) {
   switch (s) {
     case GDN_OK: return "GDN_OK";
@@ -280,6 +429,7 @@ const char* gdn_status_string(gdn_status s) {
     case GDN_ERR_WORKSPACE: return "GDN_ERR_WORKSPACE: workspace missing or too small";
     case GDN_ERR_HIP: return "GDN_ERR_HIP: a kernel launch failed";
     case GDN_ERR_ALIGN: return "GDN_ERR_ALIGN: pointer not 16-byte aligned";
+    case GDN_ERR_SAVED: return "GDN_ERR_SAVED: saved buffer missing or too small";
   }
   return "GDN: unknown status";
 }

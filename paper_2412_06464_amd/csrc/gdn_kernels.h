@@ -49,6 +49,14 @@ struct Args {
 
 enum class Dt { F32, BF16 };
 
+// What a prep launch writes: the forward pass's operands, the stateless
+// backward's (including those its forward recompute needs), or both (a
+// forward that saves what the backward needs).
+enum { PREP_FWD = 0, PREP_BWD = 1, PREP_SAVE = 2 };
+// What a forward state pass does: the forward (O, final state), the
+// backward's recompute (chunk states and V'), or both.
+enum { SEQ_FWD = 0, SEQ_STORE = 1, SEQ_SAVE = 2 };
+
 // Optional event recording around every launch (caller-owned events).
 struct Timing {
   hipEvent_t* events;
@@ -59,14 +67,16 @@ struct Timing {
 
 // Individual launches (each returns the launch status).
 hipError_t launch_chunk_table(const Args& a, hipStream_t s);
-hipError_t launch_prep(Dt dt, int dk, int dv, bool bwd, const Args& a, hipStream_t s);
-hipError_t launch_fwd_seq(Dt dt, int dk, int dv, bool store, const Args& a, hipStream_t s);
+hipError_t launch_prep(Dt dt, int dk, int dv, int mode, const Args& a, hipStream_t s);
+hipError_t launch_fwd_seq(Dt dt, int dk, int dv, int mode, const Args& a, hipStream_t s);
 hipError_t launch_bwd_seq(Dt dt, int dk, int dv, const Args& a, hipStream_t s);
 hipError_t launch_grad(Dt dt, int dk, int dv, const Args& a, hipStream_t s);
 
 // The forward / backward sequences, with optional timing.
 hipError_t launch_fwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t);
 hipError_t launch_bwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t);
+hipError_t launch_fwd_save(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t);
+hipError_t launch_bwd_saved(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t);
 
 // Call a lambda templated on (element type, dk, dv) for the supported
 // shapes; returns hipErrorInvalidValue for anything else.

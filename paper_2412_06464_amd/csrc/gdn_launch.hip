@@ -28,21 +28,45 @@ hipError_t launch_fwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timin
   hipError_t e;
   if ((e = timed(t, "k_chunk_table", s, [&] { return launch_chunk_table(a, s); })) != hipSuccess)
     return e;
-  if ((e = timed(t, "k_prep", s, [&] { return launch_prep(dt, dk, dv, false, a, s); })) !=
+  if ((e = timed(t, "k_prep", s, [&] { return launch_prep(dt, dk, dv, PREP_FWD, a, s); })) !=
       hipSuccess)
     return e;
-  return timed(t, "k_fwd_seq", s, [&] { return launch_fwd_seq(dt, dk, dv, false, a, s); });
+  return timed(t, "k_fwd_seq", s, [&] { return launch_fwd_seq(dt, dk, dv, SEQ_FWD, a, s); });
 }
 
 hipError_t launch_bwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t) {
   hipError_t e;
   if ((e = timed(t, "k_chunk_table", s, [&] { return launch_chunk_table(a, s); })) != hipSuccess)
     return e;
-  if ((e = timed(t, "k_prep", s, [&] { return launch_prep(dt, dk, dv, true, a, s); })) !=
+  if ((e = timed(t, "k_prep", s, [&] { return launch_prep(dt, dk, dv, PREP_BWD, a, s); })) !=
       hipSuccess)
     return e;
   if ((e = timed(t, "k_fwd_seq_store", s,
-                 [&] { return launch_fwd_seq(dt, dk, dv, true, a, s); })) != hipSuccess)
+                 [&] { return launch_fwd_seq(dt, dk, dv, SEQ_STORE, a, s); })) != hipSuccess)
+    return e;
+  if ((e = timed(t, "k_bwd_seq", s, [&] { return launch_bwd_seq(dt, dk, dv, a, s); })) !=
+      hipSuccess)
+    return e;
+  return timed(t, "k_grad", s, [&] { return launch_grad(dt, dk, dv, a, s); });
+}
+
+// Forward that keeps what the backward needs: the prep writes both operand
+// sets and the state pass stores chunk states and V' beside O.
+hipError_t launch_fwd_save(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t) {
+  hipError_t e;
+  if ((e = timed(t, "k_chunk_table", s, [&] { return launch_chunk_table(a, s); })) != hipSuccess)
+    return e;
+  if ((e = timed(t, "k_prep_save", s, [&] { return launch_prep(dt, dk, dv, PREP_SAVE, a, s); })) !=
+      hipSuccess)
+    return e;
+  return timed(t, "k_fwd_seq_save", s,
+               [&] { return launch_fwd_seq(dt, dk, dv, SEQ_SAVE, a, s); });
+}
+
+// Backward from a saving forward's buffer: no prep, no recompute.
+hipError_t launch_bwd_saved(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t) {
+  hipError_t e;
+  if ((e = timed(t, "k_chunk_table", s, [&] { return launch_chunk_table(a, s); })) != hipSuccess)
     return e;
   if ((e = timed(t, "k_bwd_seq", s, [&] { return launch_bwd_seq(dt, dk, dv, a, s); })) !=
       hipSuccess)

@@ -22,7 +22,7 @@
 //                  P, diag(e^g) Q.  Backward (recompute): W~, Kbar^T, U~, and
 //                  for the reverse pass K, P^T, T^T, -W~^T, (e^g Q)^T, plus
 //                  K^T, Q^T, and P and strictLower(Gamma K K^T) in fp32 for
-//                  the gradient kernel.
+//                  the gradient kernel.  Forward with save: both sets.
 #include "gdn_device.h"
 #include "gdn_kernels.h"
 
@@ -51,9 +51,12 @@ __global__ void k_chunk_table(const int32_t* cu, int N, int T, int4* info, int* 
 // Grid (NC, H), 256 threads (4 waves).  LDS stays below 80 KB for bf16 so
 // that two workgroups share a CU: one streams while the other solves.
 
-template <class E, int DK, int DV, bool BWD>
+template <class E, int DK, int DV, int MODE>
 __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
   using M = Mfma<E>;
+  // operands of the forward pass (diag(e^g) Q, P), of the reverse pass and
+  // gradient kernel (K, P^T, T^T, -W~^T, (e^g Q)^T, K^T, Q^T, P, Ak), or both
+  constexpr bool FOUT = MODE != PREP_BWD, BOUT = MODE != PREP_FWD;
   constexpr int PADE = 16 / sizeof(E);
   constexpr int LD = CH + PADE;  // rows of 64 elements
   constexpr int LDA = CH + 1;
@@ -101,11 +104,12 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
     lds_barrier();
     wave_mma_nt<E, 1, 4, 64>(kk, sX + w * 16 * LD, LD, sX, LD);
     wave_mma_nt<E, 1, 4, 64>(qk, sY + w * 16 * LD, LD, sX, LD);
-    if (!BWD) {
+    if (FOUT) {
       // diag(e^g) Q as A operands (rows t, k = d) for the output of the forward pass
       export_afrag_perm_kslice<E, CH, DK, 64, 256>(
           (E*)a.Qf + ch * CH * DK, 64 * s, [&](int t, int d) { return seg[t] * to_f(sY[t * LD + d]); });
-    } else {
+    }
+    if (BOUT) {
       // raw K as A operands (rows t, k = d) for K dS in the reverse pass
       export_afrag_perm_kslice<E, CH, DK, 64, 256>(
           (E*)a.Kf + ch * CH * DK, 64 * s, [&](int t, int d) { return to_f(sX[t * LD + d]); });
@@ -126,7 +130,7 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
       kk[0][j][e] = ak;
       qk[0][j][e] = p;
     }
-  if (BWD) {
+  if (BOUT) {
     // P and strictLower(Gamma K K^T) in fp32, accumulator layout
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -183,10 +187,11 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
   lds_barrier();
 
   // ---- 64 x 64 operands
-  if (!BWD) {
+  if (FOUT) {
     export_afrag_perm<E, CH, CH, 256>((E*)a.Pf + ch * CH * CH,
                                       [&](int t, int i) { return to_f(sP[t * LD + i]); });
-  } else {
+  }
+  if (BOUT) {
     export_afrag_perm<E, CH, CH, 256>((E*)a.PTf + ch * CH * CH,
                                       [&](int i, int t) { return to_f(sP[t * LD + i]); });
     export_afrag_perm<E, CH, CH, 256>((E*)a.TTf + ch * CH * CH,
@@ -196,7 +201,7 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
   // ---- dk slices: W~ (and -W~^T), Kbar^T, (e^g Q)^T
   for (int s = 0; s < DK / 64; ++s) {
     stage_rows_T<E, 64, LD, 256>(sX, K + 64 * s, (size_t)H * DK, len, nullptr);  // sX[d][t]
-    if (BWD) stage_rows_T<E, 64, LD, 256>(sY, Q + 64 * s, (size_t)H * DK, len, nullptr);
+    if (BOUT) stage_rows_T<E, 64, LD, 256>(sY, Q + 64 * s, (size_t)H * DK, len, nullptr);
     lds_barrier();
     // W~^T (rows d of this wave, columns t'):  sum_t (b e^g K)^T[d][t] T[t'][t]
     f32x4 Wt[4];
@@ -219,7 +224,7 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
     // Kbar^T as A operands (rows d, k = t)
     export_afrag_perm<E, 64, CH, 256>((E*)a.KbT + ch * DK * CH + (size_t)64 * s * CH,
                                       [&](int d, int t) { return sdec[t] * to_f(sX[d * LD + t]); });
-    if (BWD) {
+    if (BOUT) {
       // W~ (rows t' of this wave, columns d):  sum_t T[t'][t] (b e^g K)[t][d]
       f32x4 W[4];
 #pragma unroll
@@ -273,12 +278,14 @@ hipError_t launch_chunk_table(const Args& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_prep(Dt dt, int dk, int dv, bool bwd, const Args& a, hipStream_t s) {
+hipError_t launch_prep(Dt dt, int dk, int dv, int mode, const Args& a, hipStream_t s) {
   auto f = [&]<class E, int DK, int DV>() {
-    if (bwd)
-      hipLaunchKernelGGL((k_prep<E, DK, DV, true>), dim3(a.NC, a.H), dim3(256), 0, s, a);
+    if (mode == PREP_BWD)
+      hipLaunchKernelGGL((k_prep<E, DK, DV, PREP_BWD>), dim3(a.NC, a.H), dim3(256), 0, s, a);
+    else if (mode == PREP_SAVE)
+      hipLaunchKernelGGL((k_prep<E, DK, DV, PREP_SAVE>), dim3(a.NC, a.H), dim3(256), 0, s, a);
     else
-      hipLaunchKernelGGL((k_prep<E, DK, DV, false>), dim3(a.NC, a.H), dim3(256), 0, s, a);
+      hipLaunchKernelGGL((k_prep<E, DK, DV, PREP_FWD>), dim3(a.NC, a.H), dim3(256), 0, s, a);
     return hipGetLastError();
   };
   GDN_DISPATCH(dt, dk, dv, f);

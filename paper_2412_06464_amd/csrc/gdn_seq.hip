@@ -51,16 +51,19 @@ struct SeqCfg {
 };
 
 // ------------------------------------------------------------------ forward / recompute
-// STORE = false: forward, writes O and ht.
-// STORE = true : backward recompute, writes each chunk's entry state and V'
-//                (in MFMA fragment order over dv, for the gradient kernel).
+// SEQ_FWD  : forward, writes O and ht.
+// SEQ_STORE: backward recompute, writes each chunk's entry state and V' (in
+//            MFMA fragment order over dv, for the gradient kernel).
+// SEQ_SAVE : forward that also keeps what SEQ_STORE writes, for a backward
+//            that skips the recompute.
 
-template <class E, int DK, int DV, bool STORE>
+template <class E, int DK, int DV, int MODE>
 __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_fwd_seq(Args a) {
   using M = Mfma<E>;
   using frag = typename M::frag;
   using raw4 = typename Raw4<E>::type;
-  constexpr int BV = STORE ? SeqCfg<E, DK, DV>::BV : SeqCfg<E, DK, DV>::FWD_BV;
+  constexpr bool OUT = MODE != SEQ_STORE, STORE = MODE != SEQ_FWD;
+  constexpr int BV = MODE == SEQ_FWD ? SeqCfg<E, DK, DV>::FWD_BV : SeqCfg<E, DK, DV>::BV;
   constexpr int PADE = 16 / sizeof(E);
   constexpr int LDV = BV + PADE;
   constexpr int NTV = BV / 16, MTS = DK / 64;
@@ -107,7 +110,7 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_fwd_seq(Args a) {
     const E* Wp = (const E*)a.Wf + ((size_t)(c0 + j) * H + h) * CH * DK + (size_t)w * NKD * FR;
 #pragma unroll
     for (int kt = 0; kt < NKD; ++kt) fW[kt] = M::load(Wp + lo + kt * FR);
-    if (!STORE) {
+    if (OUT) {
       const E* Qp = (const E*)a.Qf + ((size_t)(c0 + j) * H + h) * CH * DK + (size_t)w * NKD * FR;
 #pragma unroll
       for (int kt = 0; kt < NKD; ++kt) fQ[kt] = M::load(Qp + lo + kt * FR);
@@ -126,7 +129,7 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_fwd_seq(Args a) {
     for (int i = 0; i < MTS; ++i)
 #pragma unroll
       for (int kt = 0; kt < NKC; ++kt) fK[i][kt] = M::load(Kp + lo + (i * NKC + kt) * FR);
-    if (!STORE) {
+    if (OUT) {
       const E* Pp = (const E*)a.Pf + ch * CH * CH + (size_t)w * NKC * FR;
 #pragma unroll
       for (int kt = 0; kt < NKC; ++kt) fP[kt] = M::load(Pp + lo + kt * FR);
@@ -169,7 +172,7 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_fwd_seq(Args a) {
       for (int jj = 0; jj < NTV; ++jj) {
         const frag b = bfrag_get<E>(sSB, NTV, kt, jj);
         P[jj] = M::mma(fW[kt], b, P[jj]);
-        if (!STORE) Qs[jj] = M::mma(fQ[kt], b, Qs[jj]);
+        if (OUT) Qs[jj] = M::mma(fQ[kt], b, Qs[jj]);
       }
     load_wq(min(j + 1, nch - 1));  // unconditional: keeps the load queue's shape static
 
@@ -209,12 +212,11 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_fwd_seq(Args a) {
         const frag b = bfrag_get<E>(sVB, NTV, kt, jj);
 #pragma unroll
         for (int i = 0; i < MTS; ++i) S[i][jj] = M::mma(fKc[i][kt], b, S[i][jj]);
-        if (!STORE) Qs[jj] = M::mma(fPc[kt], b, Qs[jj]);
+        if (OUT) Qs[jj] = M::mma(fPc[kt], b, Qs[jj]);
       }
     load_kp(min(j + 1, nch - 1));
-    if (STORE) {
-      copy_out_frags<E, CH, BV, LDV, 256>((E*)a.Vp + ch * CH * DV, DV / M::K, v0, sOut);
-    } else {
+    if (STORE) copy_out_frags<E, CH, BV, LDV, 256>((E*)a.Vp + ch * CH * DV, DV / M::K, v0, sOut);
+    if (OUT) {
       E* orow = (E*)a.o + ((size_t)start * H + h) * DV + v0 + acc_col();
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -227,7 +229,7 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_fwd_seq(Args a) {
     }
   }
 
-  if (!STORE && a.ht) {
+  if (OUT && a.ht) {
 #pragma unroll
     for (int i = 0; i < MTS; ++i)
 #pragma unroll
@@ -471,14 +473,17 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
 
 // ------------------------------------------------------------------ launchers
 
-hipError_t launch_fwd_seq(Dt dt, int dk, int dv, bool store, const Args& a, hipStream_t s) {
+hipError_t launch_fwd_seq(Dt dt, int dk, int dv, int mode, const Args& a, hipStream_t s) {
   auto f = [&]<class E, int DK, int DV>() {
     constexpr int BV = SeqCfg<E, DK, DV>::BV, FBV = SeqCfg<E, DK, DV>::FWD_BV;
-    if (store)
-      hipLaunchKernelGGL((k_fwd_seq<E, DK, DV, true>), dim3(unit_tile_grid(DV / BV, a.N * a.H)),
+    if (mode == SEQ_STORE)
+      hipLaunchKernelGGL((k_fwd_seq<E, DK, DV, SEQ_STORE>), dim3(unit_tile_grid(DV / BV, a.N * a.H)),
+                         dim3(256), 0, s, a);
+    else if (mode == SEQ_SAVE)
+      hipLaunchKernelGGL((k_fwd_seq<E, DK, DV, SEQ_SAVE>), dim3(unit_tile_grid(DV / BV, a.N * a.H)),
                          dim3(256), 0, s, a);
     else
-      hipLaunchKernelGGL((k_fwd_seq<E, DK, DV, false>), dim3(unit_tile_grid(DV / FBV, a.N * a.H)),
+      hipLaunchKernelGGL((k_fwd_seq<E, DK, DV, SEQ_FWD>), dim3(unit_tile_grid(DV / FBV, a.N * a.H)),
                          dim3(256), 0, s, a);
     return hipGetLastError();
   };

@@ -17,10 +17,13 @@ LIB_PATH = os.path.join(_HERE, "libgdn.so")
 
 GDN_F32, GDN_BF16 = 0, 1
 STATUS = {0: "GDN_OK", 1: "GDN_ERR_NULL", 2: "GDN_ERR_SHAPE", 3: "GDN_ERR_UNSUPPORTED",
-          4: "GDN_ERR_CU_SEQLENS", 5: "GDN_ERR_WORKSPACE", 6: "GDN_ERR_HIP", 7: "GDN_ERR_ALIGN"}
+          4: "GDN_ERR_CU_SEQLENS", 5: "GDN_ERR_WORKSPACE", 6: "GDN_ERR_HIP", 7: "GDN_ERR_ALIGN",
+          8: "GDN_ERR_SAVED"}
 EXPORTS = ("gdn_chunk_fwd", "gdn_chunk_bwd", "gdn_chunk_fwd_workspace_size",
            "gdn_chunk_bwd_workspace_size", "gdn_chunk_fwd_timed", "gdn_chunk_bwd_timed",
-           "gdn_status_string")
+           "gdn_chunk_saved_size", "gdn_chunk_fwd_save_workspace_size",
+           "gdn_chunk_bwd_saved_workspace_size", "gdn_chunk_fwd_save", "gdn_chunk_bwd_saved",
+           "gdn_chunk_fwd_save_timed", "gdn_chunk_bwd_saved_timed", "gdn_status_string")
 
 
 class Problem(ctypes.Structure):
@@ -103,6 +106,18 @@ def load_library():
         lib.gdn_chunk_fwd_timed.restype = ctypes.c_int
         lib.gdn_chunk_bwd_timed.argtypes = [pp] + [P] * 14 + [P, S, P, pt]
         lib.gdn_chunk_bwd_timed.restype = ctypes.c_int
+        for name in ("gdn_chunk_saved_size", "gdn_chunk_fwd_save_workspace_size",
+                     "gdn_chunk_bwd_saved_workspace_size"):
+            getattr(lib, name).argtypes = [pp]
+            getattr(lib, name).restype = S
+        lib.gdn_chunk_fwd_save.argtypes = [pp] + [P] * 8 + [P, S, P, S, P]
+        lib.gdn_chunk_fwd_save.restype = ctypes.c_int
+        lib.gdn_chunk_fwd_save_timed.argtypes = [pp] + [P] * 8 + [P, S, P, S, P, pt]
+        lib.gdn_chunk_fwd_save_timed.restype = ctypes.c_int
+        lib.gdn_chunk_bwd_saved.argtypes = [pp] + [P] * 5 + [S] + [P] * 6 + [P, S, P]
+        lib.gdn_chunk_bwd_saved.restype = ctypes.c_int
+        lib.gdn_chunk_bwd_saved_timed.argtypes = [pp] + [P] * 5 + [S] + [P] * 6 + [P, S, P, pt]
+        lib.gdn_chunk_bwd_saved_timed.restype = ctypes.c_int
         lib.gdn_status_string.argtypes = [ctypes.c_int]
         lib.gdn_status_string.restype = ctypes.c_char_p
         _lib = lib
@@ -139,6 +154,18 @@ def gdn_chunk_fwd_workspace_size(p: Problem) -> int:
 
 def gdn_chunk_bwd_workspace_size(p: Problem) -> int:
     return int(load_library().gdn_chunk_bwd_workspace_size(ctypes.byref(p)))
+
+
+def gdn_chunk_saved_size(p: Problem) -> int:
+    return int(load_library().gdn_chunk_saved_size(ctypes.byref(p)))
+
+
+def gdn_chunk_fwd_save_workspace_size(p: Problem) -> int:
+    return int(load_library().gdn_chunk_fwd_save_workspace_size(ctypes.byref(p)))
+
+
+def gdn_chunk_bwd_saved_workspace_size(p: Problem) -> int:
+    return int(load_library().gdn_chunk_bwd_saved_workspace_size(ctypes.byref(p)))
 
 
 def gdn_status_string(code: int) -> str:
@@ -217,5 +244,77 @@ def gdn_chunk_bwd(q, k, v, beta, log_alpha, dO, h0=None, dht=None, cu_seqlens=No
         _check(lib.gdn_chunk_bwd(*args))
     else:
         _check(lib.gdn_chunk_bwd_timed(*args, ctypes.byref(timer.timing)))
+    del keep
+    return out
+
+
+def gdn_chunk_fwd_save(q, k, v, beta, log_alpha, h0=None, cu_seqlens=None, cu_seqlens_host=None,
+                       output_final_state=True, o=None, ht=None, saved=None, workspace=None,
+                       timer=None):
+    """Forward that also fills the buffer the saved backward reads.
+
+    Same arguments and outputs as gdn_chunk_fwd; returns (o, ht, saved), where
+    ``saved`` is a uint8 device tensor of gdn_chunk_saved_size bytes (pass one
+    in to reuse it).  ``timer`` routes the call through gdn_chunk_fwd_save_timed.
+    """
+    lib = load_library()
+    p, keep = make_problem(q, v, cu_seqlens, cu_seqlens_host)
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    if o is None:
+        o = torch.empty((B, T, H, dv), dtype=q.dtype, device=q.device)
+    if ht is None and output_final_state:
+        ht = torch.empty((_nstate(q, cu_seqlens), H, dk, dv), dtype=torch.float32,
+                         device=q.device)
+    need = lib.gdn_chunk_fwd_save_workspace_size(ctypes.byref(p))
+    if need == 0:
+        _check(lib.gdn_chunk_fwd_save(ctypes.byref(p), *[None] * 8, None, 0, None, 0, None))
+    nsave = lib.gdn_chunk_saved_size(ctypes.byref(p))
+    if saved is None or saved.numel() < nsave:
+        saved = torch.empty(nsave, dtype=torch.uint8, device=q.device)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    args = (ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(beta), _ptr(log_alpha), _ptr(h0),
+            _ptr(o), _ptr(ht), _ptr(saved), saved.numel(), _ptr(workspace), workspace.numel(),
+            _stream(q.device))
+    if timer is None:
+        _check(lib.gdn_chunk_fwd_save(*args))
+    else:
+        _check(lib.gdn_chunk_fwd_save_timed(*args, ctypes.byref(timer.timing)))
+    del keep
+    return o, ht, saved
+
+
+def gdn_chunk_bwd_saved(q, v, beta, dO, saved, dht=None, cu_seqlens=None, cu_seqlens_host=None,
+                        need_dh0=True, workspace=None, out=None, timer=None):
+    """Backward from gdn_chunk_fwd_save's buffer: dict dq, dk, dv, dbeta, dlog_alpha, dh0.
+
+    ``q`` only gives the problem's shape and dtype (its values enter through
+    ``saved``); ``v`` and ``beta`` are read.  ``timer`` routes the call
+    through gdn_chunk_bwd_saved_timed.
+    """
+    lib = load_library()
+    p, keep = make_problem(q, v, cu_seqlens, cu_seqlens_host)
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    if out is None:
+        out = dict(dq=torch.empty_like(q), dk=torch.empty_like(q), dv=torch.empty_like(v),
+                   dbeta=torch.empty_like(beta), dlog_alpha=torch.empty_like(beta),
+                   dh0=torch.empty((_nstate(q, cu_seqlens), H, dk, dv), dtype=torch.float32,
+                                   device=q.device) if need_dh0 else None)
+    need = lib.gdn_chunk_bwd_saved_workspace_size(ctypes.byref(p))
+    if need == 0:
+        _check(lib.gdn_chunk_bwd_saved(ctypes.byref(p), *[None] * 5, 0, *[None] * 6, None, 0,
+                                       None))
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    args = (ctypes.byref(p), _ptr(v), _ptr(beta), _ptr(dO), _ptr(dht), _ptr(saved),
+            saved.numel(), _ptr(out["dq"]), _ptr(out["dk"]), _ptr(out["dv"]), _ptr(out["dbeta"]),
+            _ptr(out["dlog_alpha"]), _ptr(out["dh0"]), _ptr(workspace), workspace.numel(),
+            _stream(q.device))
+    if timer is None:
+        _check(lib.gdn_chunk_bwd_saved(*args))
+    else:
+        _check(lib.gdn_chunk_bwd_saved_timed(*args, ctypes.byref(timer.timing)))
     del keep
     return out

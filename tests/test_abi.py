@@ -123,3 +123,48 @@ def test_null_misaligned_and_small_workspace(lib):
     assert lib.gdn_chunk_bwd(ctypes.byref(p), *bargs, fake, needb - 1, None) == 5
     bargs[6] = None  # dO
     assert lib.gdn_chunk_bwd(ctypes.byref(p), *bargs, fake, needb, None) == 1
+
+
+def test_saved_path_sizes(lib):
+    p, _ = problem()
+    NCH = 2 * 2 * 3
+    e = 2
+    s = gdn.gdn_chunk_saved_size(p)
+    fw = gdn.gdn_chunk_fwd_save_workspace_size(p)
+    bw = gdn.gdn_chunk_bwd_saved_workspace_size(p)
+    # saved: entry states (dk x dv) and V' (64 x dv) per chunk-head, the
+    # gates' cumulative sums, P and strictLower(Gamma K K^T) in fp32
+    assert s >= NCH * (64 * 64 * e + 64 * 64 * e + 64 * 4 + 2 * 64 * 64 * 4)
+    # the stateless backward holds everything the saved path splits up
+    assert gdn.gdn_chunk_bwd_workspace_size(p) >= s + bw
+    assert fw >= NCH * (3 * 64 * 64 * e)  # at least W~, Kbar^T, U~
+    bad, _ = problem(dk=96)
+    for f in (gdn.gdn_chunk_saved_size, gdn.gdn_chunk_fwd_save_workspace_size,
+              gdn.gdn_chunk_bwd_saved_workspace_size):
+        assert f(bad) == 0
+
+
+def test_saved_path_rejects_bad_arguments(lib):
+    p, _ = problem()
+    fake = ctypes.c_void_p(0x10000)
+    odd = ctypes.c_void_p(0x10008)
+    ns = gdn.gdn_chunk_saved_size(p)
+    fw = gdn.gdn_chunk_fwd_save_workspace_size(p)
+    bw = gdn.gdn_chunk_bwd_saved_workspace_size(p)
+    fargs = [fake] * 5 + [None, fake, None]
+    assert lib.gdn_chunk_fwd_save(ctypes.byref(p), *fargs, fake, ns - 1, fake, fw, None) == 8
+    assert lib.gdn_chunk_fwd_save(ctypes.byref(p), *fargs, None, ns, fake, fw, None) == 8
+    assert lib.gdn_chunk_fwd_save(ctypes.byref(p), *fargs, fake, ns, fake, fw - 1, None) == 5
+    assert lib.gdn_chunk_fwd_save(ctypes.byref(p), *fargs, odd, ns, fake, fw, None) == 7
+    assert lib.gdn_chunk_fwd_save(ctypes.byref(p), None, *fargs[1:], fake, ns, fake, fw,
+                                  None) == 1
+    # v, beta, dO, dht, saved, saved_bytes, dq, dk, dv, dbeta, dlog_alpha, dh0
+    bargs = [fake, fake, fake, None, fake, ns, fake, fake, fake, fake, fake, None]
+    assert lib.gdn_chunk_bwd_saved(ctypes.byref(p), *bargs, fake, bw - 1, None) == 5
+    bargs[5] = ns - 1
+    assert lib.gdn_chunk_bwd_saved(ctypes.byref(p), *bargs, fake, bw, None) == 8
+    bargs[5] = ns
+    bargs[2] = None  # dO
+    assert lib.gdn_chunk_bwd_saved(ctypes.byref(p), *bargs, fake, bw, None) == 1
+    bad, _ = problem(dk=96)
+    assert lib.gdn_chunk_bwd_saved(ctypes.byref(bad), *bargs, fake, bw, None) == 3

@@ -201,6 +201,82 @@ def test_bwd_deterministic(G):
         assert torch.equal(r1[k], r2[k]), k
 
 
+# ------------------------------------------------------------------ saved-forward path
+
+
+def run_saved(G, d):
+    """Forward that saves, then the backward from its buffer; the buffer must
+    come back unchanged."""
+    o, ht, saved = G.gdn_chunk_fwd_save(d["q"], d["k"], d["v"], d["beta"], d["log_alpha"],
+                                        h0=d.get("h0"), cu_seqlens=d.get("cu_seqlens"))
+    torch.cuda.synchronize()
+    snap = saved.clone()
+    r = G.gdn_chunk_bwd_saved(d["q"], d["v"], d["beta"], d["dO"], saved, dht=d.get("dht"),
+                              cu_seqlens=d.get("cu_seqlens"))
+    torch.cuda.synchronize()
+    assert torch.equal(saved, snap), "the saved backward wrote to the saved buffer"
+    return o, ht, r
+
+
+def check_saved(G, oracle_mod, inp, tol, label):
+    say(label, "saved", tuple(inp["q"].shape), tuple(inp["v"].shape), inp["q"].dtype)
+    o, ht, r = run_saved(G, to_dev(inp))
+    kw = dict(h0=inp.get("h0"), cu_seqlens=inp.get("cu_seqlens"))
+    ro, rht = oracle_mod.fwd(inp["q"], inp["k"], inp["v"], inp["beta"], inp["log_alpha"], **kw)
+    ref = oracle_mod.bwd(inp["q"], inp["k"], inp["v"], inp["beta"], inp["log_alpha"], inp["dO"],
+                         dht=inp.get("dht"), **kw)
+    errs = dict(o=rel_err(f64(o).reshape(ro.shape), ro), ht=rel_err(f64(ht), rht))
+    for name in ("dq", "dk", "dv", "dbeta", "dlog_alpha", "dh0"):
+        errs[name] = rel_err(f64(r[name]).reshape(ref[name].shape), ref[name])
+    say(label, "errs", {k: "%.3g" % v for k, v in errs.items()})
+    bad = {k: v for k, v in errs.items() if not v <= tol}
+    assert not bad, bad
+
+
+@pytest.mark.parametrize("dtype,dk,dv,B,T,H", [
+    ("f32", 64, 64, 2, 150, 2),
+    ("bf16", 64, 64, 1, 256, 2),
+    ("bf16", 128, 128, 1, 200, 2),
+    ("bf16", 256, 512, 1, 130, 2),
+])
+def test_saved_ragged(G, oracle_mod, dtype, dk, dv, B, T, H):
+    inp = make_inputs(B, T, H, dk, dv, dtype, seed=11, h0_std=0.05, backward=True)
+    check_saved(G, oracle_mod, inp, TOL[dtype], "saved_%s_%d_%d_T%d" % (dtype, dk, dv, T))
+
+
+@pytest.mark.parametrize("label,kw", [
+    ("alpha_one", dict(log_alpha_value=0.0)),
+    ("beta_0_2", dict(beta_scale=2.0, log_alpha_scale=0.1)),
+])
+def test_saved_stress(G, oracle_mod, label, kw):
+    inp = make_inputs(1, 200, 2, 64, 64, "f32", seed=12, h0_std=0.05, backward=True, **kw)
+    check_saved(G, oracle_mod, inp, TOL["f32"], "saved_stress_" + label)
+
+
+@pytest.mark.parametrize("dtype,dk,dv", [("f32", 64, 64), ("bf16", 256, 512)])
+def test_saved_packed(G, oracle_mod, dtype, dk, dv):
+    lens = [1, 0, 64, 65, 130, 7]
+    cu = torch.tensor(np.concatenate([[0], np.cumsum(lens)]), dtype=torch.int32)
+    inp = make_inputs(1, int(cu[-1]), 2, dk, dv, dtype, seed=13, h0_std=0.05, backward=True,
+                      cu_seqlens=cu)
+    check_saved(G, oracle_mod, inp, TOL[dtype], "saved_packed_%s_%d" % (dtype, dk))
+
+
+@pytest.mark.parametrize("dtype,dk,dv", [("f32", 64, 64), ("bf16", 256, 512)])
+def test_saved_equals_stateless(G, dtype, dk, dv):
+    """Both backward paths evaluate the same expressions in the same order, so
+    their results agree bit for bit, and so do the two forwards."""
+    d = to_dev(make_inputs(1, 200, 2, dk, dv, dtype, seed=14, h0_std=0.05, backward=True))
+    say("saved_vs_stateless", dtype, dk, dv)
+    o, ht = run_fwd(G, d)
+    r = run_bwd(G, d)
+    o2, ht2, r2 = run_saved(G, d)
+    diff = {k: float((r[k].float() - r2[k].float()).abs().max()) for k in r}
+    diff.update(o=float((o.float() - o2.float()).abs().max()), ht=float((ht - ht2).abs().max()))
+    say("saved_vs_stateless max |diff|", diff)
+    assert all(v == 0.0 for v in diff.values()), diff
+
+
 # ------------------------------------------------------------------ full-size workloads
 # The HIP path runs the whole workload exactly as the benchmark launches it;
 # the oracle recomputes a sample of independent (sequence, head) units.
@@ -227,14 +303,22 @@ def sample_units(inp, units):
     return out
 
 
-@pytest.mark.parametrize("name", list(WORKLOADS))
-def test_full_workload_sampled(G, oracle_mod, name):
+FULL_CASES = [(name, "stateless") for name in WORKLOADS] + \
+    [(name, "saved") for name, w in WORKLOADS.items() if w.backward]
+
+
+@pytest.mark.parametrize("name,path", FULL_CASES)
+def test_full_workload_sampled(G, oracle_mod, name, path):
     w = WORKLOADS[name]
     inp = workload_inputs(name)
-    say(name, "full-size run")
+    say(name, path, "full-size run")
     d = to_dev(inp)
-    o, ht = run_fwd(G, d)
-    r = run_bwd(G, d) if w.backward else None
+    if path == "saved":
+        o, ht, r = run_saved(G, d)
+    else:
+        o, ht = run_fwd(G, d)
+        r = run_bwd(G, d) if w.backward else None
+    del d
     tol = TOL[w.dtype]
     cu = inp.get("cu_seqlens")
     N = w.B if cu is None else cu.numel() - 1
