@@ -1,9 +1,9 @@
 // Per-chunk gradient kernel (gfx950) of the chunkwise gated delta rule: the
 // parallel part of the backward, given every chunk's entry state S, exit-state
 // gradient dS (= dS_next of the chunk), V' and dX = T^T dV' from the two
-// sequential passes (all four stored in MFMA fragment order over dv).  The paper gives no backward; these are the exact
-// reverse-mode derivatives of its chunk equations (Sec. 3.3, state stored
-// dk x dv).  With dP = lower(dO V'^T) (with the diagonal), dA =
+// sequential passes (all four stored in MFMA fragment order over dv).  The
+// paper gives no backward; these are the exact reverse-mode derivatives of
+// its chunk equations (Sec. 3.3, state stored dk x dv).  With dP = lower(dO V'^T) (with the diagonal), dA =
 // strictLower(-dX V'^T), M1 = dP * Gamma, D = diag(b) (dA * Gamma) and
 // E = dA * diag(b) Ak + dP * P (Ak = strictLower(Gamma * K K^T)):
 //   Gq = dO S^T,  Gk = dX S^T,  Gs = V' dS^T                     (64 x dk)
@@ -15,12 +15,13 @@
 //          (+ sum_r e^{g_n-g_r} k_r.Gs_r + e^{g_n} <dS, S> on the last token)
 //   dlog_alpha = reverse cumulative sum of dg inside the chunk.
 //
-// One workgroup per (chunk, head).  Streaming phase over dv: the dS/S
-// operands (the bulk of the bytes) are loaded straight from HBM as MFMA B
-// fragments, each wave owning a set of dk columns; dO, dX and V' (shared by
-// all waves as A operands) pass through a double-buffered LDS ring in
-// fragment order.  Finish phase: the 64 x 64 intra-chunk matrices go through
-// LDS, and K^T / Q^T come as ready-made fragments from the prep kernel.
+// One workgroup per (chunk, head).  Streaming phase over dv, one MFMA k-step
+// (32 columns) at a time: every operand of the step (dO, dX, V', V rows and
+// the S, dS fragments, the bulk of the bytes) is copied HBM -> LDS by
+// direct-to-LDS loads into a ring a few k-steps deep; each wave then owns a
+// set of dk columns (B operands) and reads the shared A operands.  Finish
+// phase: the 64 x 64 intra-chunk matrices go through LDS, and K^T / Q^T come
+// as ready-made fragments from the prep kernel.
 #include "gdn_device.h"
 #include "gdn_kernels.h"
 

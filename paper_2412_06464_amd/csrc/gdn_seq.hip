@@ -43,10 +43,17 @@ inline int unit_tile_grid(int ntiles, int nunits) { return (nunits + 7) / 8 * 8 
 #ifndef GDN_SEQ_MINB
 #define GDN_SEQ_MINB 2
 #endif
+#ifndef GDN_SAVE_BV256
+#define GDN_SAVE_BV256 32
+#endif
+#ifndef GDN_SAVE_MINB
+#define GDN_SAVE_MINB GDN_SEQ_MINB
+#endif
 template <class E, int DK, int DV>
 struct SeqCfg {
   static constexpr int BV = 32;
   static constexpr int FWD_BV = DK == 256 ? GDN_FWD_BV256 : 32;
+  static constexpr int SAVE_BV = DK == 256 ? GDN_SAVE_BV256 : 32;
   static constexpr int MINB = GDN_SEQ_MINB;
 };
 
@@ -58,12 +65,15 @@ struct SeqCfg {
 //            that skips the recompute.
 
 template <class E, int DK, int DV, int MODE>
-__global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_fwd_seq(Args a) {
+__global__ __launch_bounds__(256, (MODE == SEQ_SAVE ? GDN_SAVE_MINB : GDN_SEQ_MINB)) void k_fwd_seq(
+    Args a) {
   using M = Mfma<E>;
   using frag = typename M::frag;
   using raw4 = typename Raw4<E>::type;
   constexpr bool OUT = MODE != SEQ_STORE, STORE = MODE != SEQ_FWD;
-  constexpr int BV = MODE == SEQ_FWD ? SeqCfg<E, DK, DV>::FWD_BV : SeqCfg<E, DK, DV>::BV;
+  constexpr int BV = MODE == SEQ_FWD    ? SeqCfg<E, DK, DV>::FWD_BV
+                     : MODE == SEQ_SAVE ? SeqCfg<E, DK, DV>::SAVE_BV
+                                        : SeqCfg<E, DK, DV>::BV;
   constexpr int PADE = 16 / sizeof(E);
   constexpr int LDV = BV + PADE;
   constexpr int NTV = BV / 16, MTS = DK / 64;
@@ -476,11 +486,12 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
 hipError_t launch_fwd_seq(Dt dt, int dk, int dv, int mode, const Args& a, hipStream_t s) {
   auto f = [&]<class E, int DK, int DV>() {
     constexpr int BV = SeqCfg<E, DK, DV>::BV, FBV = SeqCfg<E, DK, DV>::FWD_BV;
+    constexpr int SBV = SeqCfg<E, DK, DV>::SAVE_BV;
     if (mode == SEQ_STORE)
       hipLaunchKernelGGL((k_fwd_seq<E, DK, DV, SEQ_STORE>), dim3(unit_tile_grid(DV / BV, a.N * a.H)),
                          dim3(256), 0, s, a);
     else if (mode == SEQ_SAVE)
-      hipLaunchKernelGGL((k_fwd_seq<E, DK, DV, SEQ_SAVE>), dim3(unit_tile_grid(DV / BV, a.N * a.H)),
+      hipLaunchKernelGGL((k_fwd_seq<E, DK, DV, SEQ_SAVE>), dim3(unit_tile_grid(DV / SBV, a.N * a.H)),
                          dim3(256), 0, s, a);
     else
       hipLaunchKernelGGL((k_fwd_seq<E, DK, DV, SEQ_FWD>), dim3(unit_tile_grid(DV / FBV, a.N * a.H)),
