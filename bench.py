@@ -259,18 +259,19 @@ def main():
                      dlog_alpha=torch.empty_like(d["log_alpha"]),
                      dh0=torch.empty_like(ht))
     fwd_kw = dict(h0=d.get("h0"), cu_seqlens=cu, cu_seqlens_host=cu_host, o=o, ht=ht)
+    la = d["log_alpha"] if w.gated else None  # None: alpha == 1, no gate arithmetic
 
     def step_stateless(timers=None):
-        gdn.gdn_chunk_fwd(d["q"], d["k"], d["v"], d["beta"], d["log_alpha"], workspace=ws_f,
+        gdn.gdn_chunk_fwd(d["q"], d["k"], d["v"], d["beta"], la, workspace=ws_f,
                           timer=timers[0] if timers else None, **fwd_kw)
         if w.backward:
-            gdn.gdn_chunk_bwd(d["q"], d["k"], d["v"], d["beta"], d["log_alpha"], d["dO"],
+            gdn.gdn_chunk_bwd(d["q"], d["k"], d["v"], d["beta"], la, d["dO"],
                               h0=d.get("h0"), dht=d["dht"], cu_seqlens=cu,
                               cu_seqlens_host=cu_host, workspace=ws_b, out=out_b,
                               timer=timers[1] if timers else None)
 
     def step_saved(timers=None):
-        gdn.gdn_chunk_fwd_save(d["q"], d["k"], d["v"], d["beta"], d["log_alpha"], saved=saved,
+        gdn.gdn_chunk_fwd_save(d["q"], d["k"], d["v"], d["beta"], la, saved=saved,
                                workspace=ws_fs, timer=timers[0] if timers else None, **fwd_kw)
         gdn.gdn_chunk_bwd_saved(d["q"], d["v"], d["beta"], d["dO"], saved, dht=d["dht"],
                                 cu_seqlens=cu, cu_seqlens_host=cu_host, workspace=ws_bs,

@@ -27,6 +27,11 @@
  *    cu_seqlens[0..num_seqs] (int32, 0 = cu[0] <= ... <= cu[num_seqs] = T)
  *    delimit the sequences; the state restarts at every sequence start
  *    (h0[n] or zero) and chunks restart there too.  Dense input: Nseq = B.
+ *  - log_alpha == NULL means alpha == 1 for every token: the ungated delta
+ *    rule of DeltaNet (Sec. 2.2), without any decay arithmetic.  A NULL
+ *    dlog_alpha skips the gate gradient (and the work only it needs); with
+ *    log_alpha == NULL and a non-NULL dlog_alpha, it receives the gradient at
+ *    log_alpha = 0.
  *  - Value preconditions (not checked on the device): log_alpha <= 0
  *    (alpha in (0, 1]); beta finite (nominally (0, 1); (0, 2) also works,
  *    nothing is clamped); q and k are already L2-normalised if the caller
@@ -88,7 +93,8 @@ size_t gdn_chunk_bwd_workspace_size(const gdn_problem *p);
 
 /* Forward.  Sec. 3.3, the gated chunk state update and output equations
  * (output mask read as the decay mask Gamma, with its diagonal).
- *   in : q, k, v, beta, log_alpha; h0 = initial states or NULL (zero)
+ *   in : q, k, v, beta; log_alpha or NULL (alpha == 1); h0 = initial
+ *        states or NULL (zero)
  *   out: o; ht = final states, or NULL to skip. */
 gdn_status gdn_chunk_fwd(const gdn_problem *p, const void *q, const void *k,
                          const void *v, const float *beta,
@@ -99,8 +105,9 @@ gdn_status gdn_chunk_fwd(const gdn_problem *p, const void *q, const void *k,
 /* Backward (stateless: recomputes the forward's chunk states itself).
  *   in : the forward's inputs; dO = gradient of o; dht = gradient of the
  *        final states or NULL (zero)
- *   out: dq, dk, dv, dbeta, dlog_alpha; dh0 = gradient of the initial
- *        states, or NULL to skip.  Every output is overwritten. */
+ *   out: dq, dk, dv, dbeta; dlog_alpha, or NULL to skip; dh0 = gradient
+ *        of the initial states, or NULL to skip.  Every output is
+ *        overwritten. */
 gdn_status gdn_chunk_bwd(const gdn_problem *p, const void *q, const void *k,
                          const void *v, const float *beta,
                          const float *log_alpha, const float *h0,

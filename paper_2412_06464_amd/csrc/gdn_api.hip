@@ -199,6 +199,7 @@ class TimingGuard {
 };
 
 void fill_common(const gdn_problem* p, const Shape& s, Args* a) {
+  a->gated = 1;
   a->H = p->H;
   a->N = s.N;
   a->NC = (int)s.NC;
@@ -229,7 +230,7 @@ gdn_status gdn_chunk_fwd_timed(const gdn_problem* p, const void* q, const void* 
   Shape s;
   gdn_status st = check_problem(p, &s);
   if (st != GDN_OK) return st;
-  if (!q || !k || !v || !beta || !log_alpha || !o) return GDN_ERR_NULL;
+  if (!q || !k || !v || !beta || !o) return GDN_ERR_NULL;
   const void* ptrs[] = {q, k, v, beta, log_alpha, h0, o, ht, workspace};
   for (const void* x : ptrs)
     if (x && !aligned16(x)) return GDN_ERR_ALIGN;
@@ -244,6 +245,7 @@ gdn_status gdn_chunk_fwd_timed(const gdn_problem* p, const void* q, const void* 
   a.v = v;
   a.beta = beta;
   a.log_alpha = log_alpha;
+  a.gated = log_alpha != nullptr;
   a.h0 = h0;
   a.o = o;
   a.ht = ht;
@@ -269,9 +271,7 @@ gdn_status gdn_chunk_bwd_timed(const gdn_problem* p, const void* q, const void* 
   Shape s;
   gdn_status st = check_problem(p, &s);
   if (st != GDN_OK) return st;
-  if (!q || !k || !v || !beta || !log_alpha || !dO || !dq || !dk || !dv || !dbeta ||
-      !dlog_alpha)
-    return GDN_ERR_NULL;
+  if (!q || !k || !v || !beta || !dO || !dq || !dk || !dv || !dbeta) return GDN_ERR_NULL;
   const void* ptrs[] = {q, k, v, beta, log_alpha, h0, dO, dht, dq, dk, dv, dbeta, dlog_alpha,
                         dh0, workspace};
   for (const void* x : ptrs)
@@ -287,6 +287,7 @@ gdn_status gdn_chunk_bwd_timed(const gdn_problem* p, const void* q, const void* 
   a.v = v;
   a.beta = beta;
   a.log_alpha = log_alpha;
+  a.gated = log_alpha != nullptr;
   a.h0 = h0;
   a.dO = dO;
   a.dht = dht;
@@ -337,7 +338,7 @@ gdn_status gdn_chunk_fwd_save_timed(const gdn_problem* p, const void* q, const v
   Shape s;
   gdn_status st = check_problem(p, &s);
   if (st != GDN_OK) return st;
-  if (!q || !k || !v || !beta || !log_alpha || !o) return GDN_ERR_NULL;
+  if (!q || !k || !v || !beta || !o) return GDN_ERR_NULL;
   const void* ptrs[] = {q, k, v, beta, log_alpha, h0, o, ht, saved, workspace};
   for (const void* x : ptrs)
     if (x && !aligned16(x)) return GDN_ERR_ALIGN;
@@ -355,6 +356,7 @@ gdn_status gdn_chunk_fwd_save_timed(const gdn_problem* p, const void* q, const v
   a.v = v;
   a.beta = beta;
   a.log_alpha = log_alpha;
+  a.gated = log_alpha != nullptr;
   a.h0 = h0;
   a.o = o;
   a.ht = ht;
@@ -381,7 +383,7 @@ gdn_status gdn_chunk_bwd_saved_timed(const gdn_problem* p, const void* v, const 
   Shape s;
   gdn_status st = check_problem(p, &s);
   if (st != GDN_OK) return st;
-  if (!v || !beta || !dO || !dq || !dk || !dv || !dbeta || !dlog_alpha) return GDN_ERR_NULL;
+  if (!v || !beta || !dO || !dq || !dk || !dv || !dbeta) return GDN_ERR_NULL;
   const void* ptrs[] = {v, beta, dO, dht, saved, dq, dk, dv, dbeta, dlog_alpha, dh0, workspace};
   for (const void* x : ptrs)
     if (x && !aligned16(x)) return GDN_ERR_ALIGN;

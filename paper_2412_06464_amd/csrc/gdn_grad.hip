@@ -81,8 +81,10 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
   const E* Sp = (const E*)a.Sc + ch * DK * DV;
   const E* dSp = (const E*)a.dSc + ch * DK * DV;
 
+  // alpha == 1 (DeltaNet): g = 0 and every decay factor is exp(0) = 1
+  // exactly; the finish phase keeps one code path for both
   if (tid < CH) {
-    sg[tid] = a.g[ch * CH + tid];
+    sg[tid] = a.gated ? a.g[ch * CH + tid] : 0.f;
     sb[tid] = tid < len ? a.beta[row0 + (size_t)tid * H] : 0.f;
   }
 
@@ -374,20 +376,20 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
     const bool valid = r < len;
     const float gn = sg[CH - 1];
     const float eg = __expf(sg[r]), b = sb[r], dec = __expf(gn - sg[r]);
-    float dg = eg * pq - b * eg * pk - dec * ps + sErow[0][r] + sErow[1][r] - ecol;
     const float db = sdbA[r] + sxv[r] - eg * pk;
-    float tail = valid ? dec * ps : 0.f;
+    if (valid) a.dbeta[row0 + (size_t)r * H] = db;
+    if (a.dlog_alpha) {  // the gate gradient is optional
+      float dg = eg * pq - b * eg * pk - dec * ps + sErow[0][r] + sErow[1][r] - ecol;
+      float tail = valid ? dec * ps : 0.f;
 #pragma unroll
-    for (int off = 1; off < 64; off <<= 1) tail += __shfl_xor(tail, off, 64);
-    if (r == len - 1) dg += tail + __expf(gn) * s_dot;
-    if (!valid) dg = 0.f;
-    // reverse inclusive scan: lane r receives sum_{r' >= r} dg_r'
-    const float rev = __shfl(dg, 63 - r, 64);
-    const float sc = wave_incl_scan(rev);
-    const float dla = __shfl(sc, 63 - r, 64);
-    if (valid) {
-      a.dbeta[row0 + (size_t)r * H] = db;
-      a.dlog_alpha[row0 + (size_t)r * H] = dla;
+      for (int off = 1; off < 64; off <<= 1) tail += __shfl_xor(tail, off, 64);
+      if (r == len - 1) dg += tail + __expf(gn) * s_dot;
+      if (!valid) dg = 0.f;
+      // reverse inclusive scan: lane r receives sum_{r' >= r} dg_r'
+      const float rev = __shfl(dg, 63 - r, 64);
+      const float sc = wave_incl_scan(rev);
+      const float dla = __shfl(sc, 63 - r, 64);
+      if (valid) a.dlog_alpha[row0 + (size_t)r * H] = dla;
     }
   }
 }

@@ -13,6 +13,7 @@ struct Args {
   int N;       // sequences (dense: B)
   int NC;      // total chunks over all sequences
   int T;       // dense sequence length (used when cu == nullptr)
+  int gated;   // 0: alpha == 1 (no log_alpha input): g = 0, no gate math
   const int32_t* cu;  // packed boundaries [N+1] or nullptr (dense)
   // inputs
   const void *q, *k, *v, *dO;
@@ -41,10 +42,12 @@ struct Args {
   void* QTf;  // Q^T                       rows d, k = t     dk x 64  (backward)
   float* Pm;  // [ch] P, fp32, accumulator layout of a 64 x 64 matrix
   float* Ak;  // [ch] strictLower(Gamma * K K^T), fp32, accumulator layout
-  void* Sc;   // [ch][dk][dv] chunk entry states (row-major)
-  void* Vp;   // [ch][64][dv] V' = U~ - W~ S
-  void* dSc;  // [ch][dk][dv] gradient of each chunk's exit state
-  void* dXb;  // [ch][64][dv] dX = T^T dV'
+  // per-chunk matrices over dv, B operands of the gradient kernel in
+  // fragment order over dv (fragment (16-row tile, k-step) of 64 lanes)
+  void* Sc;   // [ch] chunk entry states          dk x dv
+  void* Vp;   // [ch] V' = U~ - W~ S              64 x dv
+  void* dSc;  // [ch] gradient of each chunk's exit state  dk x dv
+  void* dXb;  // [ch] dX = T^T dV'                64 x dv
 };
 
 enum class Dt { F32, BF16 };

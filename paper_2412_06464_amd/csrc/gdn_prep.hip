@@ -80,17 +80,26 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
   const E* Q = (const E*)a.q + row0 * DK;
   const E* V = (const E*)a.v + row0 * DV;
 
+  const bool gated = a.gated;
   if (tid < CH) {
-    const float la = tid < len ? a.log_alpha[row0 + (size_t)tid * H] : 0.f;
-    const float g = wave_incl_scan(la);  // pads repeat g at the last token
-    const float gn = __shfl(g, CH - 1, 64);
     const float b = tid < len ? a.beta[row0 + (size_t)tid * H] : 0.f;
-    sg[tid] = g;
     sb[tid] = b;
-    seg[tid] = __expf(g);
-    sdec[tid] = __expf(gn - g);
-    sbeg[tid] = b * __expf(g);
-    a.g[ch * CH + tid] = g;
+    if (gated) {
+      const float la = tid < len ? a.log_alpha[row0 + (size_t)tid * H] : 0.f;
+      const float g = wave_incl_scan(la);  // pads repeat g at the last token
+      const float gn = __shfl(g, CH - 1, 64);
+      sg[tid] = g;
+      seg[tid] = __expf(g);
+      sdec[tid] = __expf(gn - g);
+      sbeg[tid] = b * __expf(g);
+      a.g[ch * CH + tid] = g;
+    } else {  // alpha == 1 (DeltaNet): no decay anywhere
+      sg[tid] = 0.f;
+      seg[tid] = 1.f;
+      sdec[tid] = 1.f;
+      sbeg[tid] = b;
+      a.g[ch * CH + tid] = 0.f;  // read by a backward from a saved buffer
+    }
   }
 
   // ---- Gram blocks K K^T and Q K^T over 64-wide slices of dk; wave w owns
@@ -122,7 +131,7 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
     for (int e = 0; e < 4; ++e) {
       const int r = w * 16 + acc_row(e), i = j * 16 + acc_col();
       // select, never multiply by an overflowed exp above the diagonal
-      const float gam = (i <= r) ? __expf(sg[r] - sg[i]) : 0.f;
+      const float gam = (i <= r) ? (gated ? __expf(sg[r] - sg[i]) : 1.f) : 0.f;
       const float ak = (i < r) ? gam * kk[0][j][e] : 0.f;
       const float p = (i <= r) ? gam * qk[0][j][e] : 0.f;
       sA[r * LDA + i] = sb[r] * ak;

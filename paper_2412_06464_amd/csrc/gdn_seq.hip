@@ -144,7 +144,7 @@ __global__ __launch_bounds__(256, (MODE == SEQ_SAVE ? GDN_SAVE_MINB : GDN_SEQ_MI
 #pragma unroll
       for (int kt = 0; kt < NKC; ++kt) fP[kt] = M::load(Pp + lo + kt * FR);
     }
-    gl = a.g[ch * CH + l];
+    if (a.gated) gl = a.g[ch * CH + l];
   };
 
   if (nch > 0) {
@@ -203,11 +203,13 @@ __global__ __launch_bounds__(256, (MODE == SEQ_SAVE ? GDN_SAVE_MINB : GDN_SEQ_MI
     lds_barrier();
 
     // (d) S <- e^{g_n} S + Kbar^T V';  O = (diag(e^g) Q) S + P V'
-    const float egn = __expf(__shfl(gl, CH - 1, 64));  // pads repeat g of the last token
+    if (a.gated) {
+      const float egn = __expf(__shfl(gl, CH - 1, 64));  // pads repeat g of the last token
 #pragma unroll
-    for (int i = 0; i < MTS; ++i)
+      for (int i = 0; i < MTS; ++i)
 #pragma unroll
-      for (int jj = 0; jj < NTV; ++jj) S[i][jj] *= egn;
+        for (int jj = 0; jj < NTV; ++jj) S[i][jj] *= egn;
+    }
     frag fKc[MTS][NKC], fPc[NKC];
 #pragma unroll
     for (int i = 0; i < MTS; ++i)
@@ -336,7 +338,7 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
     const E* Pp = (const E*)a.PTf + ch * CH * CH + (size_t)w * NKC * FR;
 #pragma unroll
     for (int kt = 0; kt < NKC; ++kt) fPT[kt] = M::load(Pp + lo + kt * FR);
-    gl = a.g[ch * CH + l];
+    if (a.gated) gl = a.g[ch * CH + l];
     bl = a.beta[row0 + (size_t)min(l, len - 1) * H];
   };
   // Second group, needed in (c): T^T rows of tile w; (e^g Q)^T and -W~^T rows
@@ -412,7 +414,8 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int r = w * 16 + acc_row(e);
-      const float dec = __expf(gn - __shfl(gl, r, 64));
+      const float gr = __shfl(gl, r, 64);  // every lane takes part in the shuffle
+      const float dec = a.gated ? __expf(gn - gr) : 1.f;
       const float br = __shfl(bl, r, 64);  // every lane takes part in the shuffle
       brow[e] = r < len ? br : 0.f;
 #pragma unroll
@@ -431,11 +434,13 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
     for (int kt = 0; kt < NKC; ++kt)
 #pragma unroll
       for (int jj = 0; jj < NTV; ++jj) dX[jj] = M::mma(fT[kt], bfrag_get<E>(sdVB, NTV, kt, jj), dX[jj]);
-    const float egn = __expf(gn);
+    if (a.gated) {
+      const float egn = __expf(gn);
 #pragma unroll
-    for (int i = 0; i < MTS; ++i)
+      for (int i = 0; i < MTS; ++i)
 #pragma unroll
-      for (int jj = 0; jj < NTV; ++jj) dS[i][jj] *= egn;
+        for (int jj = 0; jj < NTV; ++jj) dS[i][jj] *= egn;
+    }
 #pragma unroll
     for (int kt = 0; kt < NKC; ++kt)
 #pragma unroll

@@ -190,7 +190,8 @@ def gdn_chunk_fwd(q, k, v, beta, log_alpha, h0=None, cu_seqlens=None, cu_seqlens
     """Forward of the chunkwise gated delta rule on the current stream.
 
     q, k [B,T,H,dk] and v [B,T,H,dv] (fp32 or bf16, same dtype), beta and
-    log_alpha [B,T,H] fp32, h0 [Nseq,H,dk,dv] fp32 or None; packed input
+    log_alpha [B,T,H] fp32 (log_alpha None: alpha == 1, the ungated rule),
+    h0 [Nseq,H,dk,dv] fp32 or None; packed input
     passes cu_seqlens (int32 [N+1], device) with B == 1.  Returns (o, ht).
     ``timer`` (a LaunchTimer) routes the call through gdn_chunk_fwd_timed.
     """
@@ -219,16 +220,20 @@ def gdn_chunk_fwd(q, k, v, beta, log_alpha, h0=None, cu_seqlens=None, cu_seqlens
 
 
 def gdn_chunk_bwd(q, k, v, beta, log_alpha, dO, h0=None, dht=None, cu_seqlens=None,
-                  cu_seqlens_host=None, need_dh0=True, workspace=None, out=None, timer=None):
+                  cu_seqlens_host=None, need_dh0=True, need_dlog_alpha=True, workspace=None,
+                  out=None, timer=None):
     """Backward (stateless): returns dict dq, dk, dv, dbeta, dlog_alpha, dh0.
-    ``timer`` (a LaunchTimer) routes the call through gdn_chunk_bwd_timed."""
+    ``log_alpha`` None means alpha == 1; ``need_dlog_alpha`` False skips the
+    gate gradient (dlog_alpha None).  ``timer`` (a LaunchTimer) routes the
+    call through gdn_chunk_bwd_timed."""
     lib = load_library()
     p, keep = make_problem(q, v, cu_seqlens, cu_seqlens_host)
     B, T, H, dk = q.shape
     dv = v.shape[-1]
     if out is None:
         out = dict(dq=torch.empty_like(q), dk=torch.empty_like(k), dv=torch.empty_like(v),
-                   dbeta=torch.empty_like(beta), dlog_alpha=torch.empty_like(log_alpha),
+                   dbeta=torch.empty_like(beta),
+                   dlog_alpha=torch.empty_like(beta) if need_dlog_alpha else None,
                    dh0=torch.empty((_nstate(q, cu_seqlens), H, dk, dv), dtype=torch.float32,
                                    device=q.device) if need_dh0 else None)
     need = lib.gdn_chunk_bwd_workspace_size(ctypes.byref(p))
@@ -286,11 +291,13 @@ def gdn_chunk_fwd_save(q, k, v, beta, log_alpha, h0=None, cu_seqlens=None, cu_se
 
 
 def gdn_chunk_bwd_saved(q, v, beta, dO, saved, dht=None, cu_seqlens=None, cu_seqlens_host=None,
-                        need_dh0=True, workspace=None, out=None, timer=None):
+                        need_dh0=True, need_dlog_alpha=True, workspace=None, out=None,
+                        timer=None):
     """Backward from gdn_chunk_fwd_save's buffer: dict dq, dk, dv, dbeta, dlog_alpha, dh0.
 
     ``q`` only gives the problem's shape and dtype (its values enter through
-    ``saved``); ``v`` and ``beta`` are read.  ``timer`` routes the call
+    ``saved``); ``v`` and ``beta`` are read.  ``need_dlog_alpha`` False skips
+    the gate gradient.  ``timer`` routes the call
     through gdn_chunk_bwd_saved_timed.
     """
     lib = load_library()
@@ -299,7 +306,8 @@ def gdn_chunk_bwd_saved(q, v, beta, dO, saved, dht=None, cu_seqlens=None, cu_seq
     dv = v.shape[-1]
     if out is None:
         out = dict(dq=torch.empty_like(q), dk=torch.empty_like(q), dv=torch.empty_like(v),
-                   dbeta=torch.empty_like(beta), dlog_alpha=torch.empty_like(beta),
+                   dbeta=torch.empty_like(beta),
+                   dlog_alpha=torch.empty_like(beta) if need_dlog_alpha else None,
                    dh0=torch.empty((_nstate(q, cu_seqlens), H, dk, dv), dtype=torch.float32,
                                    device=q.device) if need_dh0 else None)
     need = lib.gdn_chunk_bwd_saved_workspace_size(ctypes.byref(p))

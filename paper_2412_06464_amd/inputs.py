@@ -41,6 +41,7 @@ class Workload:
     h0_std: Optional[float] = None      # None: no initial state (zero)
     packed_mean: Optional[int] = None   # geometric mean length of packed sequences
     packed_min: int = 64
+    gated: bool = True                  # False: alpha == 1 (no log_alpha input)
 
     @property
     def tokens(self) -> int:
@@ -57,6 +58,8 @@ WORKLOADS = {
                  h0_std=0.02),
         Workload("fwd_bf16_b8_t4096_h6_dk256_dv512", 8, 4096, 6, 256, 512, "bf16", False),
         Workload("fwdbwd_bf16_b8_t4096_h6_dk256_dv512", 8, 4096, 6, 256, 512, "bf16", True),
+        Workload("fwdbwd_bf16_b8_t4096_h6_dk256_dv512_alpha1", 8, 4096, 6, 256, 512, "bf16",
+                 True, gated=False),
         Workload("fwdbwd_bf16_packed65536_h16_d128", 1, 65536, 16, 128, 128, "bf16", True,
                  packed_mean=4096, packed_min=64),
     )
@@ -89,7 +92,8 @@ def cu_from_lengths(lens):
 
 def make_inputs(B, T, H, dk, dv, dtype="bf16", seed=0, h0_std=None, backward=False,
                 cu_seqlens=None, packed_mean=None, packed_min=64, dht_std=0.01,
-                log_alpha_scale=1.0, beta_scale=1.0, beta_value=None, log_alpha_value=None):
+                log_alpha_scale=1.0, beta_scale=1.0, beta_value=None, log_alpha_value=None,
+                gated=True):
     """Draw one set of inputs (CPU tensors).
 
     Dense: q [B,T,H,dk], v [B,T,H,dv], beta/log_alpha [B,T,H] fp32.
@@ -99,7 +103,10 @@ def make_inputs(B, T, H, dk, dv, dtype="bf16", seed=0, h0_std=None, backward=Fal
     Stress knobs (defaults reproduce the distributions above):
       log_alpha_scale multiplies log_alpha (0.01 = weak decay, 0 = alpha == 1);
       beta_scale multiplies beta (2.0 gives beta in (0, 2));
-      beta_value / log_alpha_value replace them by a constant.
+      beta_value / log_alpha_value replace them by a constant;
+      gated=False draws the gates as usual (same stream), then sets
+      log_alpha to zero and marks the inputs ``gated: False`` (callers pass
+      no log_alpha: alpha == 1).
     """
     gen = torch.Generator().manual_seed(seed)
     dt = DTYPES[dtype]
@@ -132,8 +139,10 @@ def make_inputs(B, T, H, dk, dv, dtype="bf16", seed=0, h0_std=None, backward=Fal
     h0 = None
     if h0_std is not None:
         h0 = torch.randn((nstate, H, dk, dv), generator=gen, dtype=torch.float32) * h0_std
+    if not gated:
+        log_alpha = torch.zeros_like(log_alpha)
     out = dict(q=q, k=k, v=v, beta=beta.contiguous(), log_alpha=log_alpha.contiguous(), h0=h0,
-               cu_seqlens=cu_seqlens)
+               cu_seqlens=cu_seqlens, gated=gated)
     if backward:
         out["dO"] = torch.randn((B, T, H, dv), generator=gen, dtype=torch.float32).to(dt)
         out["dht"] = torch.randn((nstate, H, dk, dv), generator=gen,
@@ -144,4 +153,5 @@ def make_inputs(B, T, H, dk, dv, dtype="bf16", seed=0, h0_std=None, backward=Fal
 def workload_inputs(name: str, seed: int = 0):
     w = WORKLOADS[name]
     return make_inputs(w.B, w.T, w.H, w.dk, w.dv, w.dtype, seed=seed, h0_std=w.h0_std,
-                       backward=w.backward, packed_mean=w.packed_mean, packed_min=w.packed_min)
+                       backward=w.backward, packed_mean=w.packed_mean, packed_min=w.packed_min,
+                       gated=w.gated)

@@ -168,3 +168,16 @@ def test_saved_path_rejects_bad_arguments(lib):
     assert lib.gdn_chunk_bwd_saved(ctypes.byref(p), *bargs, fake, bw, None) == 1
     bad, _ = problem(dk=96)
     assert lib.gdn_chunk_bwd_saved(ctypes.byref(bad), *bargs, fake, bw, None) == 3
+
+
+def test_null_gates_are_accepted(lib):
+    """log_alpha NULL (alpha == 1) and dlog_alpha NULL are valid: the calls
+    get as far as the workspace check."""
+    p, _ = problem()
+    fake = ctypes.c_void_p(0x10000)
+    need = gdn.gdn_chunk_fwd_workspace_size(p)
+    assert lib.gdn_chunk_fwd(ctypes.byref(p), fake, fake, fake, fake, None, None, fake, None,
+                             fake, need - 1, None) == 5
+    needb = gdn.gdn_chunk_bwd_workspace_size(p)
+    bargs = [fake] * 4 + [None, None, fake, None] + [fake] * 4 + [None, None]
+    assert lib.gdn_chunk_bwd(ctypes.byref(p), *bargs, fake, needb - 1, None) == 5

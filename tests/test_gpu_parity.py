@@ -50,15 +50,20 @@ def to_dev(inp):
     return {k: (v.cuda() if isinstance(v, torch.Tensor) else v) for k, v in inp.items()}
 
 
+def gates(d):
+    """log_alpha as the library takes it: None for ungated (alpha == 1) inputs."""
+    return d["log_alpha"] if d.get("gated", True) else None
+
+
 def run_fwd(G, d):
-    o, ht = G.gdn_chunk_fwd(d["q"], d["k"], d["v"], d["beta"], d["log_alpha"], h0=d.get("h0"),
+    o, ht = G.gdn_chunk_fwd(d["q"], d["k"], d["v"], d["beta"], gates(d), h0=d.get("h0"),
                             cu_seqlens=d.get("cu_seqlens"))
     torch.cuda.synchronize()
     return o, ht
 
 
 def run_bwd(G, d):
-    r = G.gdn_chunk_bwd(d["q"], d["k"], d["v"], d["beta"], d["log_alpha"], d["dO"],
+    r = G.gdn_chunk_bwd(d["q"], d["k"], d["v"], d["beta"], gates(d), d["dO"],
                         h0=d.get("h0"), dht=d.get("dht"), cu_seqlens=d.get("cu_seqlens"))
     torch.cuda.synchronize()
     return r
@@ -207,7 +212,7 @@ def test_bwd_deterministic(G):
 def run_saved(G, d):
     """Forward that saves, then the backward from its buffer; the buffer must
     come back unchanged."""
-    o, ht, saved = G.gdn_chunk_fwd_save(d["q"], d["k"], d["v"], d["beta"], d["log_alpha"],
+    o, ht, saved = G.gdn_chunk_fwd_save(d["q"], d["k"], d["v"], d["beta"], gates(d),
                                         h0=d.get("h0"), cu_seqlens=d.get("cu_seqlens"))
     torch.cuda.synchronize()
     snap = saved.clone()
@@ -275,6 +280,64 @@ def test_saved_equals_stateless(G, dtype, dk, dv):
     diff.update(o=float((o.float() - o2.float()).abs().max()), ht=float((ht - ht2).abs().max()))
     say("saved_vs_stateless max |diff|", diff)
     assert all(v == 0.0 for v in diff.values()), diff
+
+
+# ------------------------------------------------------------------ alpha == 1 (no gates)
+
+
+@pytest.mark.parametrize("dtype,dk,dv,B,T,H", [
+    ("f32", 64, 64, 2, 150, 2),
+    ("bf16", 128, 128, 1, 200, 2),
+    ("bf16", 256, 512, 1, 130, 2),
+])
+def test_ungated_matches_oracle(G, oracle_mod, dtype, dk, dv, B, T, H):
+    """log_alpha = NULL is the ungated rule (DeltaNet, Sec. 2.2): against the
+    oracle at log_alpha = 0, forward and backward, with and without the gate
+    gradient."""
+    inp = make_inputs(B, T, H, dk, dv, dtype, seed=15, h0_std=0.05, backward=True)
+    zero = torch.zeros_like(inp["log_alpha"])
+    label = "ungated_%s_%d_%d" % (dtype, dk, dv)
+    say(label)
+    d = to_dev(inp)
+    o, ht = G.gdn_chunk_fwd(d["q"], d["k"], d["v"], d["beta"], None, h0=d["h0"])
+    r = G.gdn_chunk_bwd(d["q"], d["k"], d["v"], d["beta"], None, d["dO"], h0=d["h0"],
+                        dht=d["dht"])
+    r2 = G.gdn_chunk_bwd(d["q"], d["k"], d["v"], d["beta"], None, d["dO"], h0=d["h0"],
+                         dht=d["dht"], need_dlog_alpha=False)
+    torch.cuda.synchronize()
+    ro, rht = oracle_mod.fwd(inp["q"], inp["k"], inp["v"], inp["beta"], zero, h0=inp["h0"])
+    ref = oracle_mod.bwd(inp["q"], inp["k"], inp["v"], inp["beta"], zero, inp["dO"],
+                         h0=inp["h0"], dht=inp["dht"])
+    errs = dict(o=rel_err(f64(o).reshape(ro.shape), ro), ht=rel_err(f64(ht), rht))
+    for name in ("dq", "dk", "dv", "dbeta", "dlog_alpha", "dh0"):
+        errs[name] = rel_err(f64(r[name]).reshape(ref[name].shape), ref[name])
+    say(label, "errs", {k: "%.3g" % v for k, v in errs.items()})
+    bad = {k: v for k, v in errs.items() if not v <= TOL[dtype]}
+    assert not bad, bad
+    assert r2["dlog_alpha"] is None
+    for name in ("dq", "dk", "dv", "dbeta", "dh0"):  # skipping dlog_alpha changes nothing else
+        assert torch.equal(r[name], r2[name]), name
+
+
+@pytest.mark.parametrize("dtype,dk,dv", [("f32", 64, 64), ("bf16", 256, 512)])
+def test_ungated_equals_zero_gates(G, dtype, dk, dv):
+    """Skipping the gate arithmetic gives exactly what log_alpha = 0 gives
+    (every skipped factor is exp(0) = 1), on the stateless and saved paths."""
+    d = to_dev(make_inputs(1, 200, 2, dk, dv, dtype, seed=16, h0_std=0.05, backward=True))
+    d["log_alpha"] = torch.zeros_like(d["log_alpha"])
+    say("ungated_vs_zero_gates", dtype, dk, dv)
+    o, ht = run_fwd(G, d)
+    r = run_bwd(G, d)
+    o2, ht2 = G.gdn_chunk_fwd(d["q"], d["k"], d["v"], d["beta"], None, h0=d["h0"])
+    r2 = G.gdn_chunk_bwd(d["q"], d["k"], d["v"], d["beta"], None, d["dO"], h0=d["h0"],
+                         dht=d["dht"])
+    o3, ht3, saved = G.gdn_chunk_fwd_save(d["q"], d["k"], d["v"], d["beta"], None, h0=d["h0"])
+    r3 = G.gdn_chunk_bwd_saved(d["q"], d["v"], d["beta"], d["dO"], saved, dht=d["dht"])
+    torch.cuda.synchronize()
+    for x, y, z, name in ((o, o2, o3, "o"), (ht, ht2, ht3, "ht")):
+        assert torch.equal(x, y) and torch.equal(x, z), name
+    for name in r:
+        assert torch.equal(r[name], r2[name]) and torch.equal(r[name], r3[name]), name
 
 
 # ------------------------------------------------------------------ full-size workloads
