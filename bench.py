@@ -29,9 +29,12 @@ sys.path.insert(0, ROOT)
 
 DEFAULT_WORKLOAD = "fwdbwd_bf16_b8_t4096_h6_dk256_dv512"
 METRIC = "tokens/sec gated-delta chunk fwd+bwd (1 GPU); % bf16 MFMA peak"
+METRIC_FWD = "tokens/sec gated-delta chunk fwd (1 GPU); % bf16 MFMA peak"
+METRIC_RECURRENT = "tokens/sec gated-delta recurrent step (1 GPU); % HBM peak"
 PEAK_HBM = 8.0e12          # bytes/s, MI355X HBM3E
 PEAK_MFMA_BF16 = 2.5e15    # dense bf16 MFMA FLOP/s
 PEAK_MFMA_F32 = 157.3e12   # fp32 matrix FLOP/s
+PEAK_VALU_F32 = 157.3e12   # fp32 vector FLOP/s (256 CUs x 2.4 GHz, packed FMA)
 CH = 64
 
 
@@ -103,6 +106,19 @@ def kernel_models(w, n_chunks_heads):
         "k_chunk_table": (0, 0),
     }
     return {k: (b * n_chunks_heads, f * n_chunks_heads) for k, (b, f) in per.items()}
+
+
+def recurrent_model(w, n_units):
+    """Algorithmic work of one token-by-token launch: {name: (bytes, flops)}.
+    Bytes: the fp32 state slice in and out once per (sequence, head), plus
+    q, k, v, o and the two gates per token.  Flops: S^T k, S^T q and the
+    rank-one update, 6 dk dv per token (vector ALU, not MFMA)."""
+    e = 4 if w.dtype == "f32" else 2
+    per_unit = 2 * w.dk * w.dv * 4
+    per_tok = (2 * w.dk + 2 * w.dv) * e + 8
+    tokens_heads = w.B * w.T * w.H
+    return {"fwd:k_recurrent": (per_unit * n_units + per_tok * tokens_heads,
+                                6 * w.dk * w.dv * tokens_heads)}
 
 
 def model_for(models, name):
@@ -261,6 +277,16 @@ def main():
     fwd_kw = dict(h0=d.get("h0"), cu_seqlens=cu, cu_seqlens_host=cu_host, o=o, ht=ht)
     la = d["log_alpha"] if w.gated else None  # None: alpha == 1, no gate arithmetic
 
+    state = torch.zeros((n_states, w.H, w.dk, w.dv), dtype=torch.float32, device=dev)
+    if d.get("h0") is not None:
+        state.copy_(d["h0"])
+
+    def step_recurrent(timers=None):
+        # one decode step per sequence, the state updated in place
+        gdn.gdn_recurrent_fwd(d["q"], d["k"], d["v"], d["beta"], la, h0=state, ht=state,
+                              cu_seqlens=cu, cu_seqlens_host=cu_host, o=o,
+                              timer=timers[0] if timers else None)
+
     def step_stateless(timers=None):
         gdn.gdn_chunk_fwd(d["q"], d["k"], d["v"], d["beta"], la, workspace=ws_f,
                           timer=timers[0] if timers else None, **fwd_kw)
@@ -307,8 +333,8 @@ def main():
         return (start.elapsed_time(end) / args.steps,
                 {k: sum(v) / len(v) for k, v in per_kernel.items()})
 
-    path = args.path if w.backward else "stateless"
-    steps = {"saved": step_saved, "stateless": step_stateless}
+    path = args.path if w.backward else ("recurrent" if w.recurrent else "stateless")
+    steps = {"saved": step_saved, "stateless": step_stateless, "recurrent": step_recurrent}
     ms, kern_ms = timed_run(steps[path])
     other = None
     if w.backward:
@@ -322,26 +348,32 @@ def main():
     n_chunks = (w.B * ((w.T + CH - 1) // CH) if cu_host is None else
                 int(sum((int(cu_host[i + 1]) - int(cu_host[i]) + CH - 1) // CH
                         for i in range(n_states))))
-    models = kernel_models(w, n_chunks * w.H)
+    models = (recurrent_model(w, n_states * w.H) if w.recurrent else
+              kernel_models(w, n_chunks * w.H))
     dom = max(kern_ms, key=lambda k: kern_ms[k])
     kb, kf = model_for(models, dom)
     peak_mfma = PEAK_MFMA_F32 if w.dtype == "f32" else PEAK_MFMA_BF16
+    # the token-by-token kernel computes on the vector ALU, the others on MFMA
+    peak_c, cbound = (PEAK_VALU_F32, "alu") if w.recurrent else (peak_mfma, "mfma")
     t_dom = kern_ms[dom] / 1e3
-    if kb / PEAK_HBM >= kf / peak_mfma:
+    if kb / PEAK_HBM >= kf / peak_c:
         roof = {"bound": "hbm", "achieved": kb / t_dom / 1e9, "peak": PEAK_HBM / 1e9,
                 "unit": "GB/s"}
     else:
-        roof = {"bound": "mfma", "achieved": kf / t_dom / 1e12, "peak": peak_mfma / 1e12,
+        roof = {"bound": cbound, "achieved": kf / t_dom / 1e12, "peak": peak_c / 1e12,
                 "unit": "TFLOP/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
     roof["traffic"] = traffic_from_profiles(dom, args.workload)
     roof["kernel"] = dom
     roof["kernel_ms"] = kern_ms[dom]
 
-    flops = path_flops(w, tokens_heads)
-    nbytes = path_bytes(w, tokens_heads, n_states, d.get("h0") is not None)
+    if w.recurrent:
+        nbytes, flops = models["fwd:k_recurrent"]
+    else:
+        flops = path_flops(w, tokens_heads)
+        nbytes = path_bytes(w, tokens_heads, n_states, d.get("h0") is not None)
     res = {
-        "metric": METRIC,
+        "metric": METRIC if w.backward else (METRIC_RECURRENT if w.recurrent else METRIC_FWD),
         "value": tokens / (ms / 1e3),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -356,7 +388,7 @@ def main():
         "config": {"workload": args.workload, "B": w.B, "T": w.T, "H": w.H, "dk": w.dk,
                    "dv": w.dv, "chunk": CH, "backward": w.backward,
                    "num_seqs": n_states, "path": path},
-        "mfma_frac": flops / (ms / 1e3) / peak_mfma,
+        "mfma_frac": None if w.recurrent else flops / (ms / 1e3) / peak_mfma,
         "hbm_frac": nbytes / (ms / 1e3) / PEAK_HBM,
         "path_gflop": flops / 1e9,
         "path_gbytes": nbytes / 1e9,

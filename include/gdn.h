@@ -151,6 +151,21 @@ gdn_status gdn_chunk_bwd_saved(const gdn_problem *p, const void *v,
                                float *dh0, void *workspace,
                                size_t workspace_bytes, void *stream);
 
+/* Token-by-token (recurrent) form, for inference: Sec. 3.1, Eq.
+ * gated_delta_rule applied one token at a time,
+ *     S <- alpha_t (I - beta_t k_t k_t^T) S + beta_t k_t v_t^T,   o_t = S^T q_t,
+ * for every sequence and head, over all T tokens of the call (T = 1 is one
+ * decode step).  Same problem description, inputs, outputs, value
+ * conventions and statuses as gdn_chunk_fwd; the result equals the chunked
+ * forward's up to rounding.  No workspace.  The state may be updated in
+ * place: h0 == ht is allowed (h0 NULL still means a zero initial state).
+ * The state is read once and written once per call, whatever T; per token
+ * the call is latency-bound, so long prompts belong on gdn_chunk_fwd. */
+gdn_status gdn_recurrent_fwd(const gdn_problem *p, const void *q,
+                             const void *k, const void *v, const float *beta,
+                             const float *log_alpha, const float *h0, void *o,
+                             float *ht, void *stream);
+
 /* Optional launch timing, for benchmarks and profilers.  The caller creates
  * and owns the events (hipEvent_t handles, e.g. from hipEventCreate).  A
  * *_timed call records events[2i] just before and events[2i+1] just after
@@ -195,6 +210,12 @@ gdn_status gdn_chunk_bwd_saved_timed(const gdn_problem *p, const void *v,
                                      float *dh0, void *workspace,
                                      size_t workspace_bytes, void *stream,
                                      gdn_timing *timing);
+
+gdn_status gdn_recurrent_fwd_timed(const gdn_problem *p, const void *q,
+                                   const void *k, const void *v,
+                                   const float *beta, const float *log_alpha,
+                                   const float *h0, void *o, float *ht,
+                                   void *stream, gdn_timing *timing);
 
 /* Human-readable name of a status. */
 const char *gdn_status_string(gdn_status s);

@@ -421,6 +421,41 @@ gdn_status gdn_chunk_bwd_saved(const gdn_problem* p, const void* v, const float*
                                    dlog_alpha, dh0, workspace, workspace_bytes, stream, nullptr);
 }
 
+gdn_status gdn_recurrent_fwd_timed(const gdn_problem* p, const void* q, const void* k,
+                                   const void* v, const float* beta, const float* log_alpha,
+                                   const float* h0, void* o, float* ht, void* stream,
+                                   gdn_timing* timing) {
+  Shape s;
+  gdn_status st = check_problem(p, &s);
+  if (st != GDN_OK) return st;
+  if (!q || !k || !v || !beta || !o) return GDN_ERR_NULL;
+  const void* ptrs[] = {q, k, v, beta, log_alpha, h0, o, ht};
+  for (const void* x : ptrs)
+    if (x && !aligned16(x)) return GDN_ERR_ALIGN;
+  Args a;
+  memset(&a, 0, sizeof a);
+  fill_common(p, s, &a);
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.beta = beta;
+  a.log_alpha = log_alpha;
+  a.gated = log_alpha != nullptr;
+  a.h0 = h0;
+  a.o = o;
+  a.ht = ht;
+  TimingGuard tg(timing);
+  const hipError_t e = gdn::launch_recurrent_fwd(p->dtype == GDN_F32 ? Dt::F32 : Dt::BF16, p->dk,
+                                                 p->dv, a, (hipStream_t)stream, tg.get());
+  return e == hipSuccess ? GDN_OK : GDN_ERR_HIP;
+}
+
+gdn_status gdn_recurrent_fwd(const gdn_problem* p, const void* q, const void* k, const void* v,
+                             const float* beta, const float* log_alpha, const float* h0, void* o,
+                             float* ht, void* stream) {
+  return gdn_recurrent_fwd_timed(p, q, k, v, beta, log_alpha, h0, o, ht, stream, nullptr);
+}
+
 const char* gdn_status_string(gdn_status s) {
   switch (s) {
     case GDN_OK: return "GDN_OK";

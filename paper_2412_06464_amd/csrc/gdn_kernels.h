@@ -74,12 +74,14 @@ hipError_t launch_prep(Dt dt, int dk, int dv, int mode, const Args& a, hipStream
 hipError_t launch_fwd_seq(Dt dt, int dk, int dv, int mode, const Args& a, hipStream_t s);
 hipError_t launch_bwd_seq(Dt dt, int dk, int dv, const Args& a, hipStream_t s);
 hipError_t launch_grad(Dt dt, int dk, int dv, const Args& a, hipStream_t s);
+hipError_t launch_recurrent(Dt dt, int dk, int dv, const Args& a, hipStream_t s);
 
 // The forward / backward sequences, with optional timing.
 hipError_t launch_fwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t);
 hipError_t launch_bwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t);
 hipError_t launch_fwd_save(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t);
 hipError_t launch_bwd_saved(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t);
+hipError_t launch_recurrent_fwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t);
 
 // Call a lambda templated on (element type, dk, dv) for the supported
 // shapes; returns hipErrorInvalidValue for anything else.

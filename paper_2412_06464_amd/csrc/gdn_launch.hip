@@ -74,4 +74,9 @@ hipError_t launch_bwd_saved(Dt dt, int dk, int dv, const Args& a, hipStream_t s,
   return timed(t, "k_grad", s, [&] { return launch_grad(dt, dk, dv, a, s); });
 }
 
+// Token-by-token form: one launch, no workspace.
+hipError_t launch_recurrent_fwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t) {
+  return timed(t, "k_recurrent", s, [&] { return launch_recurrent(dt, dk, dv, a, s); });
+}
+
 }  // namespace gdn

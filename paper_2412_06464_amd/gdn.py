@@ -23,7 +23,8 @@ EXPORTS = ("gdn_chunk_fwd", "gdn_chunk_bwd", "gdn_chunk_fwd_workspace_size",
            "gdn_chunk_bwd_workspace_size", "gdn_chunk_fwd_timed", "gdn_chunk_bwd_timed",
            "gdn_chunk_saved_size", "gdn_chunk_fwd_save_workspace_size",
            "gdn_chunk_bwd_saved_workspace_size", "gdn_chunk_fwd_save", "gdn_chunk_bwd_saved",
-           "gdn_chunk_fwd_save_timed", "gdn_chunk_bwd_saved_timed", "gdn_status_string")
+           "gdn_chunk_fwd_save_timed", "gdn_chunk_bwd_saved_timed", "gdn_recurrent_fwd",
+           "gdn_recurrent_fwd_timed", "gdn_status_string")
 
 
 class Problem(ctypes.Structure):
@@ -118,6 +119,10 @@ def load_library():
         lib.gdn_chunk_bwd_saved.restype = ctypes.c_int
         lib.gdn_chunk_bwd_saved_timed.argtypes = [pp] + [P] * 5 + [S] + [P] * 6 + [P, S, P, pt]
         lib.gdn_chunk_bwd_saved_timed.restype = ctypes.c_int
+        lib.gdn_recurrent_fwd.argtypes = [pp] + [P] * 8 + [P]
+        lib.gdn_recurrent_fwd.restype = ctypes.c_int
+        lib.gdn_recurrent_fwd_timed.argtypes = [pp] + [P] * 8 + [P, pt]
+        lib.gdn_recurrent_fwd_timed.restype = ctypes.c_int
         lib.gdn_status_string.argtypes = [ctypes.c_int]
         lib.gdn_status_string.restype = ctypes.c_char_p
         _lib = lib
@@ -326,3 +331,30 @@ def gdn_chunk_bwd_saved(q, v, beta, dO, saved, dht=None, cu_seqlens=None, cu_seq
         _check(lib.gdn_chunk_bwd_saved_timed(*args, ctypes.byref(timer.timing)))
     del keep
     return out
+
+
+def gdn_recurrent_fwd(q, k, v, beta, log_alpha, h0=None, cu_seqlens=None, cu_seqlens_host=None,
+                      output_final_state=True, o=None, ht=None, timer=None):
+    """Token-by-token forward (inference; T = 1 is one decode step).
+
+    Same arguments and results as gdn_chunk_fwd, without a workspace.  Pass
+    ``ht=h0`` to update the state in place.  ``timer`` routes the call
+    through gdn_recurrent_fwd_timed.
+    """
+    lib = load_library()
+    p, keep = make_problem(q, v, cu_seqlens, cu_seqlens_host)
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    if o is None:
+        o = torch.empty((B, T, H, dv), dtype=q.dtype, device=q.device)
+    if ht is None and output_final_state:
+        ht = torch.empty((_nstate(q, cu_seqlens), H, dk, dv), dtype=torch.float32,
+                         device=q.device)
+    args = (ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(beta), _ptr(log_alpha), _ptr(h0),
+            _ptr(o), _ptr(ht), _stream(q.device))
+    if timer is None:
+        _check(lib.gdn_recurrent_fwd(*args))
+    else:
+        _check(lib.gdn_recurrent_fwd_timed(*args, ctypes.byref(timer.timing)))
+    del keep
+    return o, ht

@@ -42,6 +42,7 @@ class Workload:
     packed_mean: Optional[int] = None   # geometric mean length of packed sequences
     packed_min: int = 64
     gated: bool = True                  # False: alpha == 1 (no log_alpha input)
+    recurrent: bool = False             # token-by-token form (inference), not chunked
 
     @property
     def tokens(self) -> int:
@@ -60,6 +61,9 @@ WORKLOADS = {
         Workload("fwdbwd_bf16_b8_t4096_h6_dk256_dv512", 8, 4096, 6, 256, 512, "bf16", True),
         Workload("fwdbwd_bf16_b8_t4096_h6_dk256_dv512_alpha1", 8, 4096, 6, 256, 512, "bf16",
                  True, gated=False),
+        # one decode step for a serving batch, from a state left by a prefill
+        Workload("decode_bf16_b256_h6_dk256_dv512", 256, 1, 6, 256, 512, "bf16", False,
+                 h0_std=0.02, recurrent=True),
         Workload("fwdbwd_bf16_packed65536_h16_d128", 1, 65536, 16, 128, 128, "bf16", True,
                  packed_mean=4096, packed_min=64),
     )

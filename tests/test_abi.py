@@ -181,3 +181,16 @@ def test_null_gates_are_accepted(lib):
     needb = gdn.gdn_chunk_bwd_workspace_size(p)
     bargs = [fake] * 4 + [None, None, fake, None] + [fake] * 4 + [None, None]
     assert lib.gdn_chunk_bwd(ctypes.byref(p), *bargs, fake, needb - 1, None) == 5
+
+
+def test_recurrent_rejects_bad_arguments(lib):
+    p, _ = problem()
+    fake = ctypes.c_void_p(0x10000)
+    odd = ctypes.c_void_p(0x10008)
+    args = [fake] * 5 + [None, fake, None]
+    assert lib.gdn_recurrent_fwd(ctypes.byref(p), None, *args[1:], None) == 1
+    assert lib.gdn_recurrent_fwd(ctypes.byref(p), odd, *args[1:], None) == 7
+    bad, _ = problem(dk=96)
+    assert lib.gdn_recurrent_fwd(ctypes.byref(bad), *args, None) == 3
+    badcu, keep = problem(B=1, cu=[0, 60, 50, 100])
+    assert lib.gdn_recurrent_fwd(ctypes.byref(badcu), *args, None) == 4

@@ -340,6 +340,84 @@ def test_ungated_equals_zero_gates(G, dtype, dk, dv):
         assert torch.equal(r[name], r2[name]) and torch.equal(r[name], r3[name]), name
 
 
+# ------------------------------------------------------------------ token-by-token form
+
+
+def run_recurrent(G, d, **kw):
+    o, ht = G.gdn_recurrent_fwd(d["q"], d["k"], d["v"], d["beta"], gates(d), h0=d.get("h0"),
+                                cu_seqlens=d.get("cu_seqlens"), **kw)
+    torch.cuda.synchronize()
+    return o, ht
+
+
+def check_recurrent(G, oracle_mod, inp, tol, label):
+    say(label, "recurrent", tuple(inp["q"].shape), tuple(inp["v"].shape), inp["q"].dtype)
+    o, ht = run_recurrent(G, to_dev(inp))
+    ro, rht = oracle_mod.fwd(inp["q"], inp["k"], inp["v"], inp["beta"], inp["log_alpha"],
+                             h0=inp.get("h0"), cu_seqlens=inp.get("cu_seqlens"))
+    eo = rel_err(f64(o).reshape(ro.shape), ro)
+    eh = rel_err(f64(ht), rht)
+    say(label, "err o=%.3g ht=%.3g" % (eo, eh))
+    assert eo <= tol and eh <= tol, (eo, eh)
+
+
+@pytest.mark.parametrize("dtype,dk,dv,B,T,H", [
+    ("f32", 64, 64, 2, 150, 2),
+    ("bf16", 64, 64, 1, 1, 3),
+    ("bf16", 128, 128, 2, 37, 2),
+    ("bf16", 256, 512, 1, 70, 2),
+])
+def test_recurrent_matches_oracle(G, oracle_mod, dtype, dk, dv, B, T, H):
+    inp = make_inputs(B, T, H, dk, dv, dtype, seed=17, h0_std=0.05)
+    check_recurrent(G, oracle_mod, inp, TOL[dtype], "recurrent_%s_%d_%d_T%d" % (dtype, dk, dv, T))
+
+
+@pytest.mark.parametrize("label,kw", [
+    ("beta_0_2", dict(beta_scale=2.0)),
+    ("alpha_one", dict(gated=False)),
+    ("weak_decay", dict(log_alpha_scale=0.01)),
+])
+def test_recurrent_stress(G, oracle_mod, label, kw):
+    inp = make_inputs(2, 40, 2, 64, 64, "f32", seed=18, h0_std=0.05, **kw)
+    check_recurrent(G, oracle_mod, inp, TOL["f32"], "recurrent_stress_" + label)
+
+
+def test_recurrent_packed(G, oracle_mod):
+    lens = [1, 0, 64, 65, 7]
+    cu = torch.tensor(np.concatenate([[0], np.cumsum(lens)]), dtype=torch.int32)
+    inp = make_inputs(1, int(cu[-1]), 2, 128, 128, "bf16", seed=19, h0_std=0.05, cu_seqlens=cu)
+    check_recurrent(G, oracle_mod, inp, TOL["bf16"], "recurrent_packed")
+
+
+@pytest.mark.parametrize("dtype,dk,dv", [("f32", 64, 64), ("bf16", 256, 512)])
+def test_decode_continues_prefill(G, oracle_mod, dtype, dk, dv):
+    """Prefill with the chunked forward, then single-token decode steps that
+    update the state in place: every step's output and the final state match
+    the oracle run over the whole sequence."""
+    T0, steps = 130, 3
+    inp = make_inputs(2, T0 + steps, 2, dk, dv, dtype, seed=20, h0_std=0.05)
+    say("decode_after_prefill", dtype, dk, dv)
+    d = to_dev(inp)
+    pre = {k: (v[:, :T0].contiguous() if isinstance(v, torch.Tensor) and k != "h0" else v)
+           for k, v in d.items()}
+    _, state = run_fwd(G, pre)
+    outs = []
+    for t in range(T0, T0 + steps):
+        one = {k: v[:, t:t + 1].contiguous() for k, v in d.items()
+               if k in ("q", "k", "v", "beta", "log_alpha")}
+        o, st = G.gdn_recurrent_fwd(one["q"], one["k"], one["v"], one["beta"], one["log_alpha"],
+                                    h0=state, ht=state)
+        assert st is state
+        outs.append(o)
+    torch.cuda.synchronize()
+    ro, rht = oracle_mod.fwd(inp["q"], inp["k"], inp["v"], inp["beta"], inp["log_alpha"],
+                             h0=inp["h0"])
+    eo = rel_err(f64(torch.cat(outs, dim=1)), ro[:, T0:])
+    eh = rel_err(f64(state), rht)
+    say("decode_after_prefill err o=%.3g ht=%.3g" % (eo, eh))
+    assert eo <= TOL[dtype] and eh <= TOL[dtype], (eo, eh)
+
+
 # ------------------------------------------------------------------ full-size workloads
 # The HIP path runs the whole workload exactly as the benchmark launches it;
 # the oracle recomputes a sample of independent (sequence, head) units.
@@ -378,6 +456,9 @@ def test_full_workload_sampled(G, oracle_mod, name, path):
     d = to_dev(inp)
     if path == "saved":
         o, ht, r = run_saved(G, d)
+    elif w.recurrent:
+        o, ht = run_recurrent(G, d)
+        r = None
     else:
         o, ht = run_fwd(G, d)
         r = run_bwd(G, d) if w.backward else None
