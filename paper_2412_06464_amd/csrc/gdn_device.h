@@ -15,6 +15,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace gdn {
 
 typedef __bf16 bf16;
@@ -522,10 +524,34 @@ __device__ inline float wave_incl_scan(float x) {
   return x;
 }
 
-// Sum over the 16 lanes that share (l >> 4) (the columns of an accumulator tile).
+// f(std::integral_constant<int, i>) for i = I .. N-1, unrolled at compile
+// time (for code whose constants depend on the iteration, such as wait counts).
+template <int I, int N, class F>
+__device__ inline void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<I + 1, N>(f);
+  }
+}
+
+// x of another lane of the same 16-lane row, by a DPP lane pattern.
+template <int CTRL>
+__device__ inline float dpp_row(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), CTRL,
+                                                            0xF, 0xF, true));
+}
+
+// Sum over the 16 lanes that share (l >> 4) (the columns of an accumulator
+// tile): pairs (lane ^ 1), then (lane ^ 2), then the two quads of each half
+// row (mirror within 8 lanes), then the two halves (mirror within 16).  Four
+// VALU adds with DPP operands, no LDS traffic; every lane ends with the same
+// sum, formed in the same order as an xor butterfly.  All 64 lanes must be
+// active.
 __device__ inline float reduce16(float x) {
-#pragma unroll
-  for (int off = 1; off < 16; off <<= 1) x += __shfl_xor(x, off, 64);
+  x += dpp_row<0xB1>(x);   // quad_perm [1, 0, 3, 2]
+  x += dpp_row<0x4E>(x);   // quad_perm [2, 3, 0, 1]
+  x += dpp_row<0x141>(x);  // row_half_mirror
+  x += dpp_row<0x140>(x);  // row_mirror
   return x;
 }
 

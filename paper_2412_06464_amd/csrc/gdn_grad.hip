@@ -132,12 +132,8 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
   const unsigned lo = (unsigned)(l * M::KPL);
   constexpr int NPR = PAT / 4;  // (matrix, row tile) pairs of V'^T tiles per wave
 
-#pragma unroll
-  for (int it = 0; it < R - 1; ++it) issue(it);
-  for (int it = 0; it < NKS; ++it) {
-    wait_vmcnt<(R - 2) * PF>();  // this wave's copies of k-step it have landed
-    lds_barrier();               // ... and every wave's; slot (it - 1) % R is free
-    issue(it + R - 1);
+  // One k-step of the contraction over dv, from ring slot it % R.
+  auto step = [&](int it) {
     const E* slot = ring + (size_t)(it % R) * F * FR;
     frag bS[NDT], bD[NDT], fA[NPR];
 #pragma unroll
@@ -183,19 +179,56 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
         for (int j = 0; j < M::KPL; ++j) xvp += to_f(xv.e[j]) * to_f(xx.e[j]);
       }
     }
-  }
-  wait_vmcnt<0>();  // the clamped tail copies land before the LDS is reused
-  lds_barrier();
+  };
 
-  // ---- finish phase (the staging ring is dead; its LDS is reused)
-  // (1) the [dO; dX] V'^T tiles: M1, D, and the parts of E and dbeta
+  // Copies run NPRO k-steps ahead.  The last NPRO steps issue none; before
+  // them each wave loads the finish phase's global operands into registers
+  // (the P / Ak tiles of its [dO; dX] V'^T tiles, its K^T and Q^T
+  // fragments), so their latency hides behind those steps.
+  constexpr int NPRO = R - 1 < NKS ? R - 1 : NKS;
+#pragma unroll
+  for (int it = 0; it < NPRO; ++it) issue(it);
+  for (int it = 0; it < NKS - NPRO; ++it) {
+    wait_vmcnt<(NPRO - 1) * PF>();  // this wave's copies of k-step it have landed
+    lds_barrier();                  // ... and every wave's; slot (it - 1) % R is free
+    issue(it + NPRO);
+    step(it);
+  }
+  f32x4 side[PAT];
+  frag fkp[NDT][NKC], fqp[NDT][NKC];
   {
     const float* gP = a.Pm + ch * CH * CH;
     const float* gA = a.Ak + ch * CH * CH;
 #pragma unroll
     for (int p = 0; p < PAT; ++p) {
       const int q = w * PAT + p, m = q >> 4, rt = (q >> 2) & 3, ct = q & 3;
-      const f32x4 side = *reinterpret_cast<const f32x4*>((m ? gA : gP) + cfrag_index(rt, ct, CH));
+      side[p] = *reinterpret_cast<const f32x4*>((m ? gA : gP) + cfrag_index(rt, ct, CH));
+    }
+    const E* KTp = (const E*)a.KTf + ch * DK * CH;
+    const E* QTp = (const E*)a.QTf + ch * DK * CH;
+#pragma unroll
+    for (int n = 0; n < NDT; ++n)
+#pragma unroll
+      for (int kt = 0; kt < NKC; ++kt) {
+        const int dt = w * NDT + n;
+        fkp[n][kt] = M::load(KTp + (size_t)(dt * NKC + kt) * FR + l * M::KPL);
+        fqp[n][kt] = M::load(QTp + (size_t)(dt * NKC + kt) * FR + l * M::KPL);
+      }
+  }
+  constexpr int NP = PAT + 2 * NDT * NKC;  // loads issued after the last copies
+  static_for<0, NPRO>([&](auto tt) {
+    wait_vmcnt<(NPRO - 1 - decltype(tt)::value) * PF + NP>();
+    lds_barrier();
+    step(NKS - NPRO + decltype(tt)::value);
+  });
+  lds_barrier();  // every wave is done with the ring before its LDS is reused
+
+  // ---- finish phase (the staging ring is dead; its LDS is reused)
+  // (1) the [dO; dX] V'^T tiles: M1, D, and the parts of E and dbeta
+  {
+#pragma unroll
+    for (int p = 0; p < PAT; ++p) {
+      const int q = w * PAT + p, m = q >> 4, rt = (q >> 2) & 3, ct = q & 3;
       float rsum[4], csum = 0.f, dba[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -207,13 +240,13 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
           const float m1 = dp * gam;
           sM1[r * LD + i] = to_e<E>(m1);
           sM1T[i * LD + r] = to_e<E>(m1);
-          ev = dp * side[e];
+          ev = dp * side[p][e];
           dba[e] = 0.f;
         } else {
           const float da = (i < r) ? -PA[p][e] : 0.f;
           sD[r * LDF + i] = sb[r] * da * gam;
-          ev = da * sb[r] * side[e];
-          dba[e] = da * side[e];
+          ev = da * sb[r] * side[p][e];
+          dba[e] = da * side[p][e];
         }
         rsum[e] = ev;
         csum += ev;
@@ -266,17 +299,11 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
 
   // (2) dQ and dK for this wave's dk columns
   {
-    const E* KTp = (const E*)a.KTf + ch * DK * CH;
-    const E* QTp = (const E*)a.QTf + ch * DK * CH;
 #pragma unroll
     for (int n = 0; n < NDT; ++n) {
       const int dt = w * NDT + n;
-      frag fk[NKC], fq[NKC];
-#pragma unroll
-      for (int kt = 0; kt < NKC; ++kt) {
-        fk[kt] = M::load(KTp + (size_t)(dt * NKC + kt) * FR + l * M::KPL);
-        fq[kt] = M::load(QTp + (size_t)(dt * NKC + kt) * FR + l * M::KPL);
-      }
+      const frag(&fk)[NKC] = fkp[n];
+      const frag(&fq)[NKC] = fqp[n];
       // row dots with the raw accumulators: element e of row tile i pairs with
       // slot (i & 1) * 4 + e of k-step i >> 1 (bf16) or k-step 4 i + e (fp32)
 #pragma unroll
