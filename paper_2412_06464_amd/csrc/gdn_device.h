@@ -229,6 +229,28 @@ __device__ inline void store4(E* p, f32x4 v) {
   p[3] = to_e<E>(v[3]);
 }
 
+// 16-byte store of data that this kernel does not read back (a streamed
+// output or an intermediate for a later kernel): non-temporal, so it does
+// not displace operands that other workgroups are about to read.
+__device__ inline void store_stream(void* p, const uint4& v) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  __builtin_nontemporal_store(*reinterpret_cast<const u32x4*>(&v), reinterpret_cast<u32x4*>(p));
+}
+// The same for one MFMA fragment (16 bytes for bf16, 4 for fp32) or 8 bytes.
+template <class T>
+__device__ inline void store_stream_small(void* p, const T& v) {
+  static_assert(sizeof(T) == 16 || sizeof(T) == 8 || sizeof(T) == 4, "unsupported size");
+  if constexpr (sizeof(T) == 16) {
+    store_stream(p, *reinterpret_cast<const uint4*>(&v));
+  } else if constexpr (sizeof(T) == 8) {
+    typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+    __builtin_nontemporal_store(*reinterpret_cast<const u32x2*>(&v), reinterpret_cast<u32x2*>(p));
+  } else {
+    __builtin_nontemporal_store(*reinterpret_cast<const unsigned*>(&v), reinterpret_cast<unsigned*>(p));
+  }
+}
+
+
 // Write an R x KD matrix in A-fragment layout; val(r, k) gives its elements.
 template <class E, int R, int KD, int NTH, class F>
 __device__ inline void export_afrag(E* dst, F&& val) {
@@ -244,7 +266,7 @@ __device__ inline void export_afrag(E* dst, F&& val) {
     } x;
 #pragma unroll
     for (int j = 0; j < M::KPL; ++j) x.e[j] = to_e<E>(val(r, k0 + j));
-    *reinterpret_cast<typename M::frag*>(dst + (size_t)u * M::KPL) = x.f;
+    store_stream_small(dst + (size_t)u * M::KPL, x.f);
   }
 }
 
@@ -334,7 +356,7 @@ template <class E> __device__ inline void afrag_put_T(E* dst, int KD, int mt, in
 template <> __device__ inline void afrag_put_T<bf16>(bf16* dst, int KD, int mt, int i16, f32x4 v) {
   typedef bf16 bf16x4 __attribute__((ext_vector_type(4)));
   const bf16x4 x = {(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3]};
-  *reinterpret_cast<bf16x4*>(dst + frag_slot_bf16((size_t)mt * (KD / 32) + (i16 >> 1), i16)) = x;
+  store_stream_small(dst + frag_slot_bf16((size_t)mt * (KD / 32) + (i16 >> 1), i16), x);
 }
 template <> __device__ inline void afrag_put_T<float>(float* dst, int KD, int mt, int i16, f32x4 v) {
 #pragma unroll
@@ -406,7 +428,7 @@ __device__ inline void export_afrag_perm(E* dst, F&& val) {
     } x;
 #pragma unroll
     for (int j = 0; j < M::KPL; ++j) x.e[j] = to_e<E>(val(r, kperm<E>(kt, g, j)));
-    *reinterpret_cast<typename M::frag*>(dst + (size_t)u * M::KPL) = x.f;
+    store_stream_small(dst + (size_t)u * M::KPL, x.f);
   }
 }
 
@@ -428,7 +450,7 @@ __device__ inline void export_afrag_perm_kslice(E* dst, int k0, F&& val) {
 #pragma unroll
     for (int j = 0; j < M::KPL; ++j) x.e[j] = to_e<E>(val(r, kperm<E>(ktl, g, j)));
     const size_t frag = (size_t)mt * (KD / M::K) + k0 / M::K + ktl;
-    *reinterpret_cast<typename M::frag*>(dst + (frag * 64 + l) * M::KPL) = x.f;
+    store_stream_small(dst + (frag * 64 + l) * M::KPL, x.f);
   }
 }
 
@@ -491,25 +513,66 @@ template <int N> __device__ inline void wait_vmcnt() {
 // fragment (row tile rt, k-step kt) of lane l (row rt*16 + (l & 15), columns
 // kt*K + KPL*(l >> 4) ..) at ((rt * NKT + kt) * 64 + l) * KPL, NKT = N / K.
 // A reader then loads one fragment as one contiguous 1 KiB (bf16) block.
-template <class E, int ROWS, int BV, int LD, int NTH>
+// Unrolled: all of a thread's LDS reads are issued before its stores, so no
+// store waits on its own read.  ROLLED: one piece per loop trip, which keeps
+// registers low.
+template <class E, int ROWS, int BV, int LD, int NTH, bool ROLLED = false>
 __device__ inline void copy_out_frags(E* g, int NKT, int v0, const E* lds) {
   using M = Mfma<E>;
   constexpr int EPV = 16 / sizeof(E);
   constexpr int VPR = BV / EPV;
-  for (int idx = threadIdx.x; idx < ROWS * VPR; idx += NTH) {
+  constexpr int PER = ROWS * VPR / NTH;  // 16-byte pieces per thread
+  static_assert(ROWS * VPR % NTH == 0, "tile does not divide over the threads");
+  auto put = [&](int idx, const uint4& val) {
     const int r = idx / VPR, cv = idx - r * VPR;
     const int v = v0 + cv * EPV;
     if (sizeof(E) == 2) {
       const int kt = v / M::K, lane = (r & 15) + 16 * ((v % M::K) / M::KPL);
-      *reinterpret_cast<uint4*>(g + ((size_t)((r >> 4) * NKT + kt) * 64 + lane) * M::KPL) =
-          *reinterpret_cast<const uint4*>(lds + r * LD + cv * EPV);
+      store_stream(g + ((size_t)((r >> 4) * NKT + kt) * 64 + lane) * M::KPL, val);
     } else {
+      const E* x = reinterpret_cast<const E*>(&val);
 #pragma unroll
       for (int q = 0; q < EPV; ++q) {
         const int vv = v + q, kt = vv / M::K, lane = (r & 15) + 16 * (vv % M::K);
-        g[(size_t)((r >> 4) * NKT + kt) * 64 + lane] = lds[r * LD + cv * EPV + q];
+        g[(size_t)((r >> 4) * NKT + kt) * 64 + lane] = x[q];
       }
     }
+  };
+  auto get = [&](int idx) {
+    const int r = idx / VPR, cv = idx - r * VPR;
+    return *reinterpret_cast<const uint4*>(lds + r * LD + cv * EPV);
+  };
+  if constexpr (ROLLED) {
+    for (int idx = threadIdx.x; idx < ROWS * VPR; idx += NTH) put(idx, get(idx));
+  } else {
+    uint4 val[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) val[i] = get(threadIdx.x + i * NTH);
+#pragma unroll
+    for (int i = 0; i < PER; ++i) put(threadIdx.x + i * NTH, val[i]);
+  }
+}
+
+// One wave writes its 16 rows of a 64 x BV tile staged in LDS (row-major, row
+// stride LD, rows 16 w ..) to global rows of stride rs, 16 bytes per lane and
+// store; rows at or past nvalid are skipped.
+template <class E, int BV, int LD>
+__device__ inline void wave_rows_out(E* g, size_t rs, const E* lds, int w, int nvalid) {
+  constexpr int EPV = 16 / sizeof(E);
+  constexpr int VPR = BV / EPV;          // 16-byte pieces per row
+  constexpr int PER = 16 * VPR / 64;     // pieces per lane
+  static_assert(16 * VPR % 64 == 0, "rows do not divide over the lanes");
+  const int l = threadIdx.x & 63;
+  uint4 val[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int idx = l + 64 * i, r = 16 * w + idx / VPR, cv = idx % VPR;
+    val[i] = *reinterpret_cast<const uint4*>(lds + r * LD + cv * EPV);
+  }
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int idx = l + 64 * i, r = 16 * w + idx / VPR, cv = idx % VPR;
+    if (r < nvalid) store_stream(g + (size_t)r * rs + cv * EPV, val[i]);
   }
 }
 

@@ -80,8 +80,9 @@ __global__ __launch_bounds__(256, (MODE == SEQ_SAVE ? GDN_SAVE_MINB : GDN_SEQ_MI
   constexpr int NKD = DK / M::K, NKC = CH / M::K;
   __shared__ __align__(16) E sSB[DK * BV];  // S as B operands (k = d)
   __shared__ __align__(16) E sVB[CH * BV];  // V' as B operands (k = t)
-  __shared__ __align__(16) E sSs[STORE ? DK * LDV : 1];
-  __shared__ __align__(16) E sOut[STORE ? CH * LDV : 1];
+  __shared__ __align__(16) E sSs[STORE ? 2 * DK * LDV : 1];  // state rows, by chunk parity
+  __shared__ __align__(16) E sOut[STORE ? CH * LDV : 1];  // V' rows for the store
+  __shared__ __align__(16) E sO[OUT ? CH * LDV : 1];      // O rows for the store
 
   int unit, tile;
   if (!map_unit_tile(DV / BV, a.N * a.H, unit, tile)) return;
@@ -165,14 +166,13 @@ __global__ __launch_bounds__(256, (MODE == SEQ_SAVE ? GDN_SAVE_MINB : GDN_SEQ_MI
         if (STORE) {
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            sSs[(w * (DK / 4) + i * 16 + acc_row(e)) * LDV + jj * 16 + acc_col()] =
-                to_e<E>(S[i][jj][e]);
+            sSs[(j & 1) * DK * LDV + (w * (DK / 4) + i * 16 + acc_row(e)) * LDV + jj * 16 +
+                acc_col()] = to_e<E>(S[i][jj][e]);
         }
       }
     lds_barrier();
 
     // (b) W~ S and diag(e^g) Q S for the wave's 16 token rows
-    if (STORE) copy_out_frags<E, DK, BV, LDV, 256>((E*)a.Sc + ch * DK * DV, DV / M::K, v0, sSs);
     f32x4 P[NTV], Qs[NTV];
 #pragma unroll
     for (int jj = 0; jj < NTV; ++jj) P[jj] = Qs[jj] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -227,17 +227,23 @@ __global__ __launch_bounds__(256, (MODE == SEQ_SAVE ? GDN_SAVE_MINB : GDN_SEQ_MI
         if (OUT) Qs[jj] = M::mma(fPc[kt], b, Qs[jj]);
       }
     load_kp(min(j + 1, nch - 1));
-    if (STORE) copy_out_frags<E, CH, BV, LDV, 256>((E*)a.Vp + ch * CH * DV, DV / M::K, v0, sOut);
-    if (OUT) {
-      E* orow = (E*)a.o + ((size_t)start * H + h) * DV + v0 + acc_col();
+    // The chunk's outputs are stored last, after every load of the next chunk
+    // has been issued: vector memory completes in issue order, so a load
+    // queued behind a store also waits for the store.  The state rows are
+    // double-buffered by chunk parity and read here, one barrier after the
+    // next chunk starts writing the other buffer.
+    if (STORE) {
+      copy_out_frags<E, DK, BV, LDV, 256>((E*)a.Sc + ch * DK * DV, DV / M::K, v0,
+                                          sSs + (j & 1) * DK * LDV);
+      copy_out_frags<E, CH, BV, LDV, 256>((E*)a.Vp + ch * CH * DV, DV / M::K, v0, sOut);
+    }
+    if (OUT) {  // O rows through LDS: one 16-byte store per lane and piece
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int t = w * 16 + acc_row(e);
-        if (t < len) {
+      for (int jj = 0; jj < NTV; ++jj)
 #pragma unroll
-          for (int jj = 0; jj < NTV; ++jj) orow[(size_t)t * H * DV + jj * 16] = to_e<E>(Qs[jj][e]);
-        }
-      }
+        for (int e = 0; e < 4; ++e) sO[(w * 16 + acc_row(e)) * LDV + jj * 16 + acc_col()] = to_e<E>(Qs[jj][e]);
+      wave_rows_out<E, BV, LDV>((E*)a.o + ((size_t)start * H + h) * DV + v0, (size_t)H * DV, sO, w,
+                                len);
     }
   }
 
@@ -395,9 +401,9 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
 
     // (b) dV' = P^T dO + diag(e^{g_n - g}) (K dS); the stores of dS and of the
     //     previous chunk's dX rows
-    copy_out_frags<E, DK, BV, LDV, 256>((E*)a.dSc + ch * DK * DV, DV / M::K, v0, sSs);
+    copy_out_frags<E, DK, BV, LDV, 256, true>((E*)a.dSc + ch * DK * DV, DV / M::K, v0, sSs);
     if (j + 1 < nch)
-      copy_out_frags<E, CH, BV, LDV, 256>((E*)a.dXb + prev_ch * CH * DV, DV / M::K, v0, sOut);
+      copy_out_frags<E, CH, BV, LDV, 256, true>((E*)a.dXb + prev_ch * CH * DV, DV / M::K, v0, sOut);
     f32x4 X1[NTV], X2[NTV];
 #pragma unroll
     for (int jj = 0; jj < NTV; ++jj) X1[jj] = X2[jj] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -470,7 +476,7 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
   }
   if (nch > 0) {
     lds_barrier();
-    copy_out_frags<E, CH, BV, LDV, 256>((E*)a.dXb + prev_ch * CH * DV, DV / M::K, v0, sOut);
+    copy_out_frags<E, CH, BV, LDV, 256, true>((E*)a.dXb + prev_ch * CH * DV, DV / M::K, v0, sOut);
   }
 
   if (a.dh0) {
