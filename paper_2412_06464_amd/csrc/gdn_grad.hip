@@ -54,7 +54,10 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
   constexpr int LDF = CH + 1;
   constexpr int NKC = CH / M::K;
   constexpr int FIN_BYTES = 3 * CH * LD * (int)sizeof(E) + CH * LDF * 4;
-  constexpr int SMEM = RING_BYTES > FIN_BYTES ? RING_BYTES : FIN_BYTES;
+  constexpr int LDQ = NDT * 16 + PADE;   // row stride of a wave's dq / dk staging
+  constexpr int STG_BYTES = 2 * NW * CH * LDQ * (int)sizeof(E);
+  constexpr int FIN_ALL = FIN_BYTES + STG_BYTES;
+  constexpr int SMEM = RING_BYTES > FIN_ALL ? RING_BYTES : FIN_ALL;
   __shared__ __align__(16) unsigned char smem[SMEM];
   __shared__ float sg[CH], sb[CH];
   __shared__ float sdbA[CH], sxv[CH], sErow[2][CH], sEcol[2 * 4][CH];
@@ -66,6 +69,8 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
   E* sM1T = sM1 + CH * LD;               //         M1^T, row-major
   E* sDD = sM1T + CH * LD;               //         D + D^T, row-major
   float* sD = (float*)(sDD + CH * LD);   //         D, fp32
+  E* sQst = (E*)(smem + FIN_BYTES) + (size_t)2 * wave_id() * CH * LDQ;  // this wave's dq rows
+  E* sKst = sQst + CH * LDQ;                                             //           dk rows
 
   const int c = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, l = lane_id(), g4 = l >> 4;
   const int w = __builtin_amdgcn_readfirstlane(wave_id());
@@ -371,16 +376,26 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
           dk = M::mma(amt, fq[kt], dk);
           dk = M::mma(add, fk[kt], dk);
         }
-        E* gdq = (E*)a.dq + row0 * DK + dt * 16 + acc_col();
-        E* gdk = (E*)a.dk + row0 * DK + dt * 16 + acc_col();
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int r = i * 16 + acc_row(e);
-          if (r < len) {
-            gdq[(size_t)r * H * DK] = to_e<E>(dq[e]);
-            gdk[(size_t)r * H * DK] = to_e<E>(dk[e]);
-          }
+          sQst[r * LDQ + n * 16 + acc_col()] = to_e<E>(dq[e]);
+          sKst[r * LDQ + n * 16 + acc_col()] = to_e<E>(dk[e]);
         }
+      }
+    }
+    // the wave's dq and dk columns, row by row, 16 bytes per lane and store
+    constexpr int EPV = 16 / sizeof(E), VPR = NDT * 16 / EPV, PCS = CH * VPR / 64;
+    E* gq = (E*)a.dq + row0 * DK + w * NDT * 16;
+    E* gk = (E*)a.dk + row0 * DK + w * NDT * 16;
+#pragma unroll
+    for (int x = 0; x < PCS; ++x) {
+      const int idx = l + 64 * x, r = idx / VPR, cv = idx - r * VPR;
+      const uint4 vq = *reinterpret_cast<const uint4*>(sQst + r * LDQ + cv * EPV);
+      const uint4 vk = *reinterpret_cast<const uint4*>(sKst + r * LDQ + cv * EPV);
+      if (r < len) {
+        store_stream(gq + (size_t)r * H * DK + cv * EPV, vq);
+        store_stream(gk + (size_t)r * H * DK + cv * EPV, vk);
       }
     }
   }

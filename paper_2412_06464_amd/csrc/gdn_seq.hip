@@ -292,6 +292,7 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
   __shared__ __align__(16) E sdVB[CH * BV];     // dV' as B operands (k = t)
   __shared__ __align__(16) E sSs[DK * LDV];     // dS rows for the store
   __shared__ __align__(16) E sOut[CH * LDV];    // dX rows for the store
+  __shared__ __align__(16) E sDv[CH * LDV];     // dv rows for the store (per wave)
 
   int unit, tile;
   if (!map_unit_tile(DV / BV, a.N * a.H, unit, tile)) return;
@@ -460,17 +461,18 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
         }
       }
     load_second(max(j - 1, 0));
-    {
-      E* dvrow = (E*)a.dv + ((size_t)start * H + h) * DV + v0 + acc_col();
+    {  // dX rows (stored with the next chunk) and dv rows (through LDS, 16 bytes per lane)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int t = w * 16 + acc_row(e);
 #pragma unroll
         for (int jj = 0; jj < NTV; ++jj) {
           sOut[t * LDV + jj * 16 + acc_col()] = to_e<E>(dX[jj][e]);
-          if (t < len) dvrow[(size_t)t * H * DV + jj * 16] = to_e<E>(brow[e] * dX[jj][e]);
+          sDv[t * LDV + jj * 16 + acc_col()] = to_e<E>(brow[e] * dX[jj][e]);
         }
       }
+      wave_rows_out<E, BV, LDV>((E*)a.dv + ((size_t)start * H + h) * DV + v0, (size_t)H * DV, sDv,
+                                w, len);
     }
     prev_ch = ch;
   }
