@@ -71,6 +71,10 @@ __global__ __launch_bounds__(256, (MODE == SEQ_SAVE ? GDN_SAVE_MINB : GDN_SEQ_MI
   using frag = typename M::frag;
   using raw4 = typename Raw4<E>::type;
   constexpr bool OUT = MODE != SEQ_STORE, STORE = MODE != SEQ_FWD;
+  // where the chunk-state and V' stores go: between the (b) products of the
+  // next chunk (with O), or, without O (fewer products to hide them behind),
+  // S before the (b) products and V' at the end of the chunk
+  constexpr bool SPREAD = OUT;
   constexpr int BV = MODE == SEQ_FWD    ? SeqCfg<E, DK, DV>::FWD_BV
                      : MODE == SEQ_SAVE ? SeqCfg<E, DK, DV>::SAVE_BV
                                         : SeqCfg<E, DK, DV>::BV;
@@ -81,7 +85,7 @@ __global__ __launch_bounds__(256, (MODE == SEQ_SAVE ? GDN_SAVE_MINB : GDN_SEQ_MI
   __shared__ __align__(16) E sSB[DK * BV];  // S as B operands (k = d)
   __shared__ __align__(16) E sVB[CH * BV];  // V' as B operands (k = t)
   __shared__ __align__(16) E sSs[STORE ? 2 * DK * LDV : 1];  // state rows, by chunk parity
-  __shared__ __align__(16) E sOut[STORE ? CH * LDV : 1];  // V' rows for the store
+  __shared__ __align__(16) E sOut[STORE ? 2 * CH * LDV : 1];  // V' rows, by chunk parity
   __shared__ __align__(16) E sO[OUT ? CH * LDV : 1];      // O rows for the store
 
   int unit, tile;
@@ -148,6 +152,41 @@ __global__ __launch_bounds__(256, (MODE == SEQ_SAVE ? GDN_SAVE_MINB : GDN_SEQ_MI
     if (a.gated) gl = a.g[ch * CH + l];
   };
 
+  // Output pieces, 16 bytes per lane: chunk states and V' in fragment order
+  // over dv (from the parity buffers sSs, sOut), O rows (this wave's, sO).
+  constexpr int EPV = 16 / sizeof(E), VPR = BV / EPV;
+  constexpr int PS = STORE ? DK * VPR / 256 : 0;  // state pieces per thread
+  constexpr int PV = STORE ? CH * VPR / 256 : 0;  // V' pieces per thread
+  constexpr int PO = 16 * VPR / 64;               // O pieces per lane
+  static_assert(!STORE || (DK * VPR % 256 == 0 && CH * VPR % 256 == 0 && PS + PV <= NKD),
+                "store pieces do not fit the k-steps");
+  auto put_frag = [&](E* g, const E* lds, int idx) {
+    const int r = idx / VPR, cv = idx - r * VPR, v = v0 + cv * EPV;
+    const uint4 val = *reinterpret_cast<const uint4*>(lds + r * LDV + cv * EPV);
+    if (sizeof(E) == 2) {
+      const int kt = v / M::K, ln = (r & 15) + 16 * ((v % M::K) / M::KPL);
+      store_stream(g + ((size_t)((r >> 4) * (DV / M::K) + kt) * 64 + ln) * M::KPL, val);
+    } else {
+      const E* x = reinterpret_cast<const E*>(&val);
+#pragma unroll
+      for (int q = 0; q < EPV; ++q) {
+        const int vv = v + q, kt = vv / M::K, ln = (r & 15) + 16 * (vv % M::K);
+        g[(size_t)((r >> 4) * (DV / M::K) + kt) * 64 + ln] = x[q];
+      }
+    }
+  };
+  auto put_s = [&](int i, size_t chk, int jj) {
+    put_frag((E*)a.Sc + chk * DK * DV, sSs + (jj & 1) * DK * LDV, threadIdx.x + 256 * i);
+  };
+  auto put_v = [&](int i, size_t chk, int jj) {
+    put_frag((E*)a.Vp + chk * CH * DV, sOut + (jj & 1) * CH * LDV, threadIdx.x + 256 * i);
+  };
+  auto put_o = [&](int jj) {
+    const int st = s0 + jj * CH, ln = min(CH, L - jj * CH);
+    wave_rows_out<E, BV, LDV>((E*)a.o + ((size_t)st * H + h) * DV + v0, (size_t)H * DV, sO, w, ln);
+  };
+  (void)PO;
+
   if (nch > 0) {
     load_wq(0);
     load_u(0);
@@ -172,18 +211,34 @@ __global__ __launch_bounds__(256, (MODE == SEQ_SAVE ? GDN_SAVE_MINB : GDN_SEQ_MI
       }
     lds_barrier();
 
-    // (b) W~ S and diag(e^g) Q S for the wave's 16 token rows
+    // (b) W~ S and diag(e^g) Q S for the wave's 16 token rows.  The
+    // outputs pending from the previous steps (this chunk's entry state, the
+    // previous chunk's V' and O) are stored one piece per k-step between
+    // the products, so that the CU's store path is never hit by a burst.
+    if constexpr (STORE && !SPREAD)
+      copy_out_frags<E, DK, BV, LDV, 256, true>((E*)a.Sc + ch * DK * DV, DV / M::K, v0,
+                                                sSs + (j & 1) * DK * LDV);
     f32x4 P[NTV], Qs[NTV];
 #pragma unroll
     for (int jj = 0; jj < NTV; ++jj) P[jj] = Qs[jj] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kt = 0; kt < NKD; ++kt)
+    static_for<0, NKD>([&](auto ktc) {
+      constexpr int kt = decltype(ktc)::value;
 #pragma unroll
       for (int jj = 0; jj < NTV; ++jj) {
         const frag b = bfrag_get<E>(sSB, NTV, kt, jj);
         P[jj] = M::mma(fW[kt], b, P[jj]);
         if (OUT) Qs[jj] = M::mma(fQ[kt], b, Qs[jj]);
       }
+      if constexpr (STORE && SPREAD) {
+        if constexpr (kt < PS) put_s(kt, ch, j);
+        else if constexpr (kt < PS + PV) {
+          if (j > 0) put_v(kt - PS, ch - H, j - 1);
+        }
+      }
+      if constexpr (OUT && kt == NKD - 1) {
+        if (j > 0) put_o(j - 1);
+      }
+    });
     load_wq(min(j + 1, nch - 1));  // unconditional: keeps the load queue's shape static
 
     // (c) V' = U~ - W~ S
@@ -196,7 +251,8 @@ __global__ __launch_bounds__(256, (MODE == SEQ_SAVE ? GDN_SAVE_MINB : GDN_SEQ_MI
       if (STORE) {
 #pragma unroll
         for (int e = 0; e < 4; ++e)
-          sOut[(w * 16 + acc_row(e)) * LDV + jj * 16 + acc_col()] = to_e<E>(vp[e]);
+          sOut[(j & 1) * CH * LDV + (w * 16 + acc_row(e)) * LDV + jj * 16 + acc_col()] =
+              to_e<E>(vp[e]);
       }
     }
     load_u(min(j + 1, nch - 1));
@@ -227,24 +283,23 @@ __global__ __launch_bounds__(256, (MODE == SEQ_SAVE ? GDN_SAVE_MINB : GDN_SEQ_MI
         if (OUT) Qs[jj] = M::mma(fPc[kt], b, Qs[jj]);
       }
     load_kp(min(j + 1, nch - 1));
-    // The chunk's outputs are stored last, after every load of the next chunk
-    // has been issued: vector memory completes in issue order, so a load
-    // queued behind a store also waits for the store.  The state rows are
-    // double-buffered by chunk parity and read here, one barrier after the
-    // next chunk starts writing the other buffer.
-    if (STORE) {
-      copy_out_frags<E, DK, BV, LDV, 256>((E*)a.Sc + ch * DK * DV, DV / M::K, v0,
-                                          sSs + (j & 1) * DK * LDV);
-      copy_out_frags<E, CH, BV, LDV, 256>((E*)a.Vp + ch * CH * DV, DV / M::K, v0, sOut);
-    }
-    if (OUT) {  // O rows through LDS: one 16-byte store per lane and piece
+    if constexpr (STORE && !SPREAD)
+      copy_out_frags<E, CH, BV, LDV, 256, true>((E*)a.Vp + ch * CH * DV, DV / M::K, v0,
+                                                sOut + (j & 1) * CH * LDV);
+    if (OUT) {  // O rows wait in LDS (this wave's rows) until the next chunk's (b)
 #pragma unroll
       for (int jj = 0; jj < NTV; ++jj)
 #pragma unroll
-        for (int e = 0; e < 4; ++e) sO[(w * 16 + acc_row(e)) * LDV + jj * 16 + acc_col()] = to_e<E>(Qs[jj][e]);
-      wave_rows_out<E, BV, LDV>((E*)a.o + ((size_t)start * H + h) * DV + v0, (size_t)H * DV, sO, w,
-                                len);
+        for (int e = 0; e < 4; ++e)
+          sO[(w * 16 + acc_row(e)) * LDV + jj * 16 + acc_col()] = to_e<E>(Qs[jj][e]);
     }
+  }
+  // what the last chunk leaves pending
+  if (nch > 0) {
+    const size_t chl = (size_t)(c0 + nch - 1) * H + h;
+    if constexpr (STORE && SPREAD)
+      for (int i = 0; i < PV; ++i) put_v(i, chl, nch - 1);  // rows in LDS since (c)
+    if constexpr (OUT) put_o(nch - 1);
   }
 
   if (OUT && a.ht) {
