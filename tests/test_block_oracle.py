@@ -58,9 +58,6 @@ def test_conv_matches_banded_matrix_form():
     L, H, d, W = 7, 1, 2, 4
     x = RNG.standard_normal((1, L, H, d))
     w = RNG.standard_normal((H * d, W))
-    # silu is invertible on its range only numerically; compare the conv itself
-    # through l2norm=False and a kernel large enough to stay in silu's linear-ish
-    # region is not needed: invert silu by bisection instead.
     y = block.conv_silu(x, w, l2norm=False)
     u_ref = np.zeros((L, d))
     for c in range(d):
