@@ -70,7 +70,8 @@ typedef enum {
   GDN_ERR_WORKSPACE = 5,   /* workspace NULL or smaller than the query      */
   GDN_ERR_HIP = 6,         /* a kernel launch failed                         */
   GDN_ERR_ALIGN = 7,       /* a pointer is not 16-byte aligned               */
-  GDN_ERR_SAVED = 8        /* saved buffer NULL or smaller than the query    */
+  GDN_ERR_SAVED = 8,       /* saved buffer NULL or smaller than the query    */
+  GDN_ERR_VALUE = 9        /* a scalar argument (width, eps) out of range    */
 } gdn_status;
 
 typedef struct {
@@ -165,6 +166,48 @@ gdn_status gdn_recurrent_fwd(const gdn_problem *p, const void *q,
                              const void *k, const void *v, const float *beta,
                              const float *log_alpha, const float *h0, void *o,
                              float *ht, void *stream);
+
+/* Block prologue (Sec. 3.4 and the block-design figure): what turns the
+ * projections into the rule's q, k, v.  Per channel c of x [B, T, H, dim]
+ * (the problem's layout, dtype and sequences):
+ *     u_t[c] = sum_{i < width} w[c][i] * x_{t - width + 1 + i}[c]
+ * (a causal depthwise convolution over time that restarts with zeros at
+ * every sequence start), z_t = silu(u_t), and with l2norm != 0
+ * y_t = z_t / sqrt(|z_t|^2 + eps) over the dim channels of each (token, head)
+ * (q and k), else y_t = z_t (v).  dim is the problem's dk or dv; width is
+ * 1..4 (the paper says only "short"); w is fp32 [H * dim][width], tap
+ * width-1 multiplying the current token.  The backward returns dx and the
+ * weight gradient dw (fp32 [H * dim][width], summed over all tokens in a
+ * fixed order: deterministic).  Both need gdn_conv_silu_workspace_size
+ * bytes of workspace.  Errors as elsewhere; GDN_ERR_VALUE for width or eps
+ * out of range. */
+size_t gdn_conv_silu_workspace_size(const gdn_problem *p, int dim, int width);
+gdn_status gdn_conv_silu_fwd(const gdn_problem *p, int dim, int width,
+                             int l2norm, float eps, const void *x,
+                             const float *w, void *y, void *workspace,
+                             size_t workspace_bytes, void *stream);
+gdn_status gdn_conv_silu_bwd(const gdn_problem *p, int dim, int width,
+                             int l2norm, float eps, const void *x,
+                             const float *w, const void *dy, void *dx,
+                             float *dw, void *workspace,
+                             size_t workspace_bytes, void *stream);
+
+/* Block epilogue (Sec. 3.4: the output is normalised and gated before the
+ * output projection; the figure's caption gives the gate a SiLU).  Per
+ * (token, head) row of o [B, T, H, dv]:
+ *     y = o / sqrt(mean(o^2) + eps) * w * silu(g)
+ * with g [B, T, H, dv] (the gate projection, dtype of the problem) and w
+ * fp32 [dv] shared by the heads.  The backward returns dout (the gradient
+ * of o), dg and dw (fp32 [dv], deterministic); it needs
+ * gdn_norm_gate_workspace_size bytes of workspace, the forward none. */
+size_t gdn_norm_gate_workspace_size(const gdn_problem *p);
+gdn_status gdn_norm_gate_fwd(const gdn_problem *p, float eps, const void *o,
+                             const void *g, const float *w, void *y,
+                             void *stream);
+gdn_status gdn_norm_gate_bwd(const gdn_problem *p, float eps, const void *o,
+                             const void *g, const float *w, const void *dy,
+                             void *dout, void *dg, float *dw, void *workspace,
+                             size_t workspace_bytes, void *stream);
 
 /* Optional launch timing, for benchmarks and profilers.  The caller creates
  * and owns the events (hipEvent_t handles, e.g. from hipEventCreate).  A

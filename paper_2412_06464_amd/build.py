@@ -14,8 +14,8 @@ CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libgdn.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
-SOURCES = ["gdn_prep.hip", "gdn_seq.hip", "gdn_grad.hip", "gdn_recurrent.hip", "gdn_launch.hip",
-           "gdn_api.hip"]
+SOURCES = ["gdn_prep.hip", "gdn_seq.hip", "gdn_grad.hip", "gdn_recurrent.hip", "gdn_block.hip",
+           "gdn_launch.hip", "gdn_api.hip"]
 FLAGS = ["--offload-arch=" + ARCH, "-O3", "-std=c++20", "-fPIC",
          # keep the compiler from emitting packed fp32 math
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

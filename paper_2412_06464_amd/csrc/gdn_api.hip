@@ -4,6 +4,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <math.h>
+
 #include <new>
 
 #include "../../include/gdn.h"
@@ -197,6 +199,33 @@ class TimingGuard {
   gdn_timing* t_;
   gdn::Timing impl_{};
 };
+
+// Block prologue: argument checks and workspace (chunk table, then the
+// per-chunk partial weight gradients of the backward).
+gdn_status check_conv(const gdn_problem* p, int dim, int width, float eps, Shape* s) {
+  const gdn_status st = check_problem(p, s);
+  if (st != GDN_OK) return st;
+  if (dim != p->dk && dim != p->dv) return GDN_ERR_UNSUPPORTED;
+  if (width < 1 || width > 4 || !(eps >= 0.f) || !isfinite(eps)) return GDN_ERR_VALUE;
+  return GDN_OK;
+}
+
+size_t carve_conv(const gdn_problem* p, const Shape& s, int dim, int width, unsigned char* base,
+                  Args* t, gdn::ConvArgs* a) {
+  Carver c{base};
+  unsigned char* info = c.take((size_t)s.NC * sizeof(int4) + 16);
+  unsigned char* sc0 = c.take(((size_t)s.N + 1) * sizeof(int));
+  unsigned char* part = c.take((size_t)s.NC * p->H * dim * width * sizeof(float));
+  if (t) {
+    t->info = (int4*)info;
+    t->seq_chunk0 = (int*)sc0;
+  }
+  if (a) {
+    a->info = (const int4*)info;
+    a->part = (float*)part;
+  }
+  return c.off;
+}
 
 void fill_common(const gdn_problem* p, const Shape& s, Args* a) {
   a->gated = 1;
@@ -456,6 +485,123 @@ gdn_status gdn_recurrent_fwd(const gdn_problem* p, const void* q, const void* k,
   return gdn_recurrent_fwd_timed(p, q, k, v, beta, log_alpha, h0, o, ht, stream, nullptr);
 }
 
+size_t gdn_conv_silu_workspace_size(const gdn_problem* p, int dim, int width) {
+  Shape s;
+  if (check_conv(p, dim, width, 0.f, &s) != GDN_OK) return 0;
+  return carve_conv(p, s, dim, width, nullptr, nullptr, nullptr);
+}
+
+static gdn_status conv_call(const gdn_problem* p, int dim, int width, int l2norm, float eps,
+                            const void* x, const float* w, const void* dy, void* y, void* dx,
+                            float* dw, void* workspace, size_t workspace_bytes, void* stream,
+                            bool bwd) {
+  Shape s;
+  gdn_status st = check_conv(p, dim, width, eps, &s);
+  if (st != GDN_OK) return st;
+  if (!x || !w || (bwd ? (!dy || !dx || !dw) : !y)) return GDN_ERR_NULL;
+  const void* ptrs[] = {x, w, dy, y, dx, dw, workspace};
+  for (const void* q : ptrs)
+    if (q && !aligned16(q)) return GDN_ERR_ALIGN;
+  if (!workspace || workspace_bytes < carve_conv(p, s, dim, width, nullptr, nullptr, nullptr))
+    return GDN_ERR_WORKSPACE;
+  Args t;
+  memset(&t, 0, sizeof t);
+  fill_common(p, s, &t);
+  gdn::ConvArgs a;
+  memset(&a, 0, sizeof a);
+  carve_conv(p, s, dim, width, (unsigned char*)workspace, &t, &a);
+  a.H = p->H;
+  a.N = s.N;
+  a.NC = (int)s.NC;
+  a.T = t.T;
+  a.W = width;
+  a.l2 = l2norm ? 1 : 0;
+  a.eps = eps;
+  a.cu = p->cu_seqlens;
+  a.x = x;
+  a.w = w;
+  a.dy = dy;
+  a.y = y;
+  a.dx = dx;
+  a.dw = dw;
+  const Dt dt = p->dtype == GDN_F32 ? Dt::F32 : Dt::BF16;
+  hipError_t e = gdn::launch_chunk_table(t, (hipStream_t)stream);
+  if (e == hipSuccess)
+    e = bwd ? gdn::launch_conv_bwd(dt, dim, a, (hipStream_t)stream)
+            : gdn::launch_conv_fwd(dt, dim, a, (hipStream_t)stream);
+  return e == hipSuccess ? GDN_OK : GDN_ERR_HIP;
+}
+
+gdn_status gdn_conv_silu_fwd(const gdn_problem* p, int dim, int width, int l2norm, float eps,
+                             const void* x, const float* w, void* y, void* workspace,
+                             size_t workspace_bytes, void* stream) {
+  return conv_call(p, dim, width, l2norm, eps, x, w, nullptr, y, nullptr, nullptr, workspace,
+                   workspace_bytes, stream, false);
+}
+
+gdn_status gdn_conv_silu_bwd(const gdn_problem* p, int dim, int width, int l2norm, float eps,
+                             const void* x, const float* w, const void* dy, void* dx, float* dw,
+                             void* workspace, size_t workspace_bytes, void* stream) {
+  return conv_call(p, dim, width, l2norm, eps, x, w, dy, nullptr, dx, dw, workspace,
+                   workspace_bytes, stream, true);
+}
+
+static long norm_rows(const gdn_problem* p, const Shape& s) { return s.Ttot * p->H; }
+static int norm_blocks(long rows) { return (int)((rows + 63) / 64); }
+
+size_t gdn_norm_gate_workspace_size(const gdn_problem* p) {
+  Shape s;
+  if (check_problem(p, &s) != GDN_OK) return 0;
+  return up((size_t)norm_blocks(norm_rows(p, s)) * p->dv * sizeof(float));
+}
+
+static gdn_status norm_call(const gdn_problem* p, float eps, const void* o, const void* g,
+                            const float* w, const void* dy, void* y, void* dout, void* dg,
+                            float* dw, void* workspace, size_t workspace_bytes, void* stream,
+                            bool bwd) {
+  Shape s;
+  gdn_status st = check_problem(p, &s);
+  if (st != GDN_OK) return st;
+  if (!(eps >= 0.f) || !isfinite(eps)) return GDN_ERR_VALUE;
+  if (!o || !g || !w || (bwd ? (!dy || !dout || !dg || !dw) : !y)) return GDN_ERR_NULL;
+  const void* ptrs[] = {o, g, w, dy, y, dout, dg, dw, workspace};
+  for (const void* q : ptrs)
+    if (q && !aligned16(q)) return GDN_ERR_ALIGN;
+  gdn::NormArgs a;
+  memset(&a, 0, sizeof a);
+  a.rows = norm_rows(p, s);
+  a.nblk = norm_blocks(a.rows);
+  if (bwd && (!workspace || workspace_bytes < up((size_t)a.nblk * p->dv * sizeof(float))))
+    return GDN_ERR_WORKSPACE;
+  a.eps = eps;
+  a.o = o;
+  a.g = g;
+  a.dy = dy;
+  a.w = w;
+  a.y = y;
+  a.dout = dout;
+  a.dg = dg;
+  a.part = (float*)workspace;
+  a.dw = dw;
+  const Dt dt = p->dtype == GDN_F32 ? Dt::F32 : Dt::BF16;
+  const hipError_t e = bwd ? gdn::launch_norm_gate_bwd(dt, p->dv, a, (hipStream_t)stream)
+                           : gdn::launch_norm_gate_fwd(dt, p->dv, a, (hipStream_t)stream);
+  return e == hipSuccess ? GDN_OK : GDN_ERR_HIP;
+}
+
+gdn_status gdn_norm_gate_fwd(const gdn_problem* p, float eps, const void* o, const void* g,
+                             const float* w, void* y, void* stream) {
+  return norm_call(p, eps, o, g, w, nullptr, y, nullptr, nullptr, nullptr, nullptr, 0, stream,
+                   false);
+}
+
+gdn_status gdn_norm_gate_bwd(const gdn_problem* p, float eps, const void* o, const void* g,
+                             const float* w, const void* dy, void* dout, void* dg, float* dw,
+                             void* workspace, size_t workspace_bytes, void* stream) {
+  return norm_call(p, eps, o, g, w, dy, nullptr, dout, dg, dw, workspace, workspace_bytes, stream,
+                   true);
+}
+
 const char* gdn_status_string(gdn_status s) {
   switch (s) {
     case GDN_OK: return "GDN_OK";
@@ -467,6 +613,7 @@ const char* gdn_status_string(gdn_status s) {
     case GDN_ERR_HIP: return "GDN_ERR_HIP: a kernel launch failed";
     case GDN_ERR_ALIGN: return "GDN_ERR_ALIGN: pointer not 16-byte aligned";
     case GDN_ERR_SAVED: return "GDN_ERR_SAVED: saved buffer missing or too small";
+    case GDN_ERR_VALUE: return "GDN_ERR_VALUE: a scalar argument is out of range";
   }
   return "GDN: unknown status";
 }

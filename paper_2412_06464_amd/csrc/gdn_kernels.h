@@ -52,6 +52,34 @@ struct Args {
 
 enum class Dt { F32, BF16 };
 
+// Block prologue: short causal convolution + SiLU (+ L2) over [*, T, H, D].
+struct ConvArgs {
+  int H, N, NC, T;           // heads, sequences, chunks, dense length
+  int W, l2;                 // convolution width (1..4), L2 normalisation on/off
+  float eps;
+  const int32_t* cu;         // packed boundaries or nullptr
+  const int4* info;          // chunk table (sequence, first token, length)
+  const void* x;             // input  [*, T, H, D]
+  const float* w;            // weights [H * D][W]
+  const void* dy;            // gradient of the output
+  void* y;                   // output
+  void* dx;                  // gradient of the input
+  float* part;               // [NC][H][D][W] per-chunk partial weight gradients
+  float* dw;                 // weight gradient [H * D][W]
+};
+
+// Block epilogue: RMS normalisation x weight x SiLU gate over the dv channels.
+struct NormArgs {
+  long rows;                 // (token, head) rows
+  int nblk;                  // workgroups (64 rows each)
+  float eps;
+  const void *o, *g, *dy;    // [rows][dv]
+  const float* w;            // [dv]
+  void *y, *dout, *dg;       // [rows][dv]
+  float* part;               // [nblk][dv] partial weight gradients
+  float* dw;                 // [dv]
+};
+
 // What a prep launch writes: the forward pass's operands, the stateless
 // backward's (including those its forward recompute needs), or both (a
 // forward that saves what the backward needs).
@@ -75,6 +103,10 @@ hipError_t launch_fwd_seq(Dt dt, int dk, int dv, int mode, const Args& a, hipStr
 hipError_t launch_bwd_seq(Dt dt, int dk, int dv, const Args& a, hipStream_t s);
 hipError_t launch_grad(Dt dt, int dk, int dv, const Args& a, hipStream_t s);
 hipError_t launch_recurrent(Dt dt, int dk, int dv, const Args& a, hipStream_t s);
+hipError_t launch_conv_fwd(Dt dt, int d, const ConvArgs& a, hipStream_t s);
+hipError_t launch_conv_bwd(Dt dt, int d, const ConvArgs& a, hipStream_t s);
+hipError_t launch_norm_gate_fwd(Dt dt, int dv, const NormArgs& a, hipStream_t s);
+hipError_t launch_norm_gate_bwd(Dt dt, int dv, const NormArgs& a, hipStream_t s);
 
 // The forward / backward sequences, with optional timing.
 hipError_t launch_fwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t);

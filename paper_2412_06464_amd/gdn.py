@@ -18,13 +18,15 @@ LIB_PATH = os.path.join(_HERE, "libgdn.so")
 GDN_F32, GDN_BF16 = 0, 1
 STATUS = {0: "GDN_OK", 1: "GDN_ERR_NULL", 2: "GDN_ERR_SHAPE", 3: "GDN_ERR_UNSUPPORTED",
           4: "GDN_ERR_CU_SEQLENS", 5: "GDN_ERR_WORKSPACE", 6: "GDN_ERR_HIP", 7: "GDN_ERR_ALIGN",
-          8: "GDN_ERR_SAVED"}
+          8: "GDN_ERR_SAVED", 9: "GDN_ERR_VALUE"}
 EXPORTS = ("gdn_chunk_fwd", "gdn_chunk_bwd", "gdn_chunk_fwd_workspace_size",
            "gdn_chunk_bwd_workspace_size", "gdn_chunk_fwd_timed", "gdn_chunk_bwd_timed",
            "gdn_chunk_saved_size", "gdn_chunk_fwd_save_workspace_size",
            "gdn_chunk_bwd_saved_workspace_size", "gdn_chunk_fwd_save", "gdn_chunk_bwd_saved",
            "gdn_chunk_fwd_save_timed", "gdn_chunk_bwd_saved_timed", "gdn_recurrent_fwd",
-           "gdn_recurrent_fwd_timed", "gdn_status_string")
+           "gdn_recurrent_fwd_timed", "gdn_conv_silu_workspace_size", "gdn_conv_silu_fwd",
+           "gdn_conv_silu_bwd", "gdn_norm_gate_workspace_size", "gdn_norm_gate_fwd",
+           "gdn_norm_gate_bwd", "gdn_status_string")
 
 
 class Problem(ctypes.Structure):
@@ -123,6 +125,19 @@ def load_library():
         lib.gdn_recurrent_fwd.restype = ctypes.c_int
         lib.gdn_recurrent_fwd_timed.argtypes = [pp] + [P] * 8 + [P, pt]
         lib.gdn_recurrent_fwd_timed.restype = ctypes.c_int
+        I, F = ctypes.c_int, ctypes.c_float
+        lib.gdn_conv_silu_workspace_size.argtypes = [pp, I, I]
+        lib.gdn_conv_silu_workspace_size.restype = S
+        lib.gdn_conv_silu_fwd.argtypes = [pp, I, I, I, F, P, P, P, P, S, P]
+        lib.gdn_conv_silu_fwd.restype = ctypes.c_int
+        lib.gdn_conv_silu_bwd.argtypes = [pp, I, I, I, F, P, P, P, P, P, P, S, P]
+        lib.gdn_conv_silu_bwd.restype = ctypes.c_int
+        lib.gdn_norm_gate_workspace_size.argtypes = [pp]
+        lib.gdn_norm_gate_workspace_size.restype = S
+        lib.gdn_norm_gate_fwd.argtypes = [pp, F, P, P, P, P, P]
+        lib.gdn_norm_gate_fwd.restype = ctypes.c_int
+        lib.gdn_norm_gate_bwd.argtypes = [pp, F, P, P, P, P, P, P, P, P, S, P]
+        lib.gdn_norm_gate_bwd.restype = ctypes.c_int
         lib.gdn_status_string.argtypes = [ctypes.c_int]
         lib.gdn_status_string.restype = ctypes.c_char_p
         _lib = lib
@@ -358,3 +373,109 @@ def gdn_recurrent_fwd(q, k, v, beta, log_alpha, h0=None, cu_seqlens=None, cu_seq
         _check(lib.gdn_recurrent_fwd_timed(*args, ctypes.byref(timer.timing)))
     del keep
     return o, ht
+
+
+# ------------------------------------------------------------------ block prologue / epilogue
+
+# the (dk, dv) pair of a supported rule problem that has a given head dim
+_PAIR = {64: (64, 64), 128: (128, 128), 256: (256, 512), 512: (256, 512)}
+
+
+def block_problem(x: torch.Tensor, cu_seqlens=None, cu_seqlens_host=None):
+    """gdn_problem for a [B, T, H, d] tensor of the block (d is its dk or dv)."""
+    B, T, H, d = x.shape
+    if d not in _PAIR:
+        raise ValueError("unsupported head dim %d" % d)
+    dk, dv = _PAIR[d]
+    q = torch.empty((B, T, H, dk), dtype=x.dtype, device="meta")
+    v = torch.empty((B, T, H, dv), dtype=x.dtype, device="meta")
+    return make_problem_meta(q, v, cu_seqlens, cu_seqlens_host)
+
+
+def make_problem_meta(q, v, cu_seqlens=None, cu_seqlens_host=None):
+    """make_problem for shape-only tensors (no data pointer needed)."""
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    dt = {torch.float32: GDN_F32, torch.bfloat16: GDN_BF16}.get(q.dtype)
+    if dt is None:
+        raise TypeError("dtype must be float32 or bfloat16")
+    keep = []
+    p = Problem(B, T, H, dk, dv, 0, None, None, dt)
+    if cu_seqlens is not None:
+        if cu_seqlens_host is None:
+            cu_seqlens_host = cu_seqlens.to("cpu")
+        host = cu_seqlens_host.to(torch.int32).contiguous()
+        keep.append(host)
+        p.num_seqs = host.numel() - 1
+        p.cu_seqlens = cu_seqlens.data_ptr()
+        p.cu_seqlens_host = host.data_ptr()
+    return p, keep
+
+
+def gdn_conv_silu_fwd(x, w, l2norm=True, eps=1e-6, cu_seqlens=None, cu_seqlens_host=None, y=None,
+                      workspace=None):
+    """Short causal convolution + SiLU (+ L2 per row) of x [B, T, H, d]; w fp32 [H * d, W]."""
+    lib = load_library()
+    p, keep = block_problem(x, cu_seqlens, cu_seqlens_host)
+    d, W = x.shape[-1], w.shape[1]
+    if y is None:
+        y = torch.empty_like(x)
+    need = lib.gdn_conv_silu_workspace_size(ctypes.byref(p), d, W)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+    _check(lib.gdn_conv_silu_fwd(ctypes.byref(p), d, W, int(l2norm), eps, _ptr(x), _ptr(w),
+                                 _ptr(y), _ptr(workspace), workspace.numel(), _stream(x.device)))
+    del keep
+    return y
+
+
+def gdn_conv_silu_bwd(x, w, dy, l2norm=True, eps=1e-6, cu_seqlens=None, cu_seqlens_host=None,
+                      dx=None, dw=None, workspace=None):
+    """Backward of gdn_conv_silu_fwd: returns (dx, dw)."""
+    lib = load_library()
+    p, keep = block_problem(x, cu_seqlens, cu_seqlens_host)
+    d, W = x.shape[-1], w.shape[1]
+    if dx is None:
+        dx = torch.empty_like(x)
+    if dw is None:
+        dw = torch.empty_like(w)
+    need = lib.gdn_conv_silu_workspace_size(ctypes.byref(p), d, W)
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+    _check(lib.gdn_conv_silu_bwd(ctypes.byref(p), d, W, int(l2norm), eps, _ptr(x), _ptr(w),
+                                 _ptr(dy), _ptr(dx), _ptr(dw), _ptr(workspace),
+                                 workspace.numel(), _stream(x.device)))
+    del keep
+    return dx, dw
+
+
+def gdn_norm_gate_fwd(o, g, w, eps=1e-5, y=None):
+    """RMS normalisation of o [B, T, H, dv] per (token, head), times w [dv], times silu(g)."""
+    lib = load_library()
+    p, keep = block_problem(o)
+    if y is None:
+        y = torch.empty_like(o)
+    _check(lib.gdn_norm_gate_fwd(ctypes.byref(p), eps, _ptr(o), _ptr(g), _ptr(w), _ptr(y),
+                                 _stream(o.device)))
+    del keep
+    return y
+
+
+def gdn_norm_gate_bwd(o, g, w, dy, eps=1e-5, dout=None, dg=None, dw=None, workspace=None):
+    """Backward of gdn_norm_gate_fwd: returns (dout, dg, dw)."""
+    lib = load_library()
+    p, keep = block_problem(o)
+    if dout is None:
+        dout = torch.empty_like(o)
+    if dg is None:
+        dg = torch.empty_like(g)
+    if dw is None:
+        dw = torch.empty_like(w)
+    need = lib.gdn_norm_gate_workspace_size(ctypes.byref(p))
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=o.device)
+    _check(lib.gdn_norm_gate_bwd(ctypes.byref(p), eps, _ptr(o), _ptr(g), _ptr(w), _ptr(dy),
+                                 _ptr(dout), _ptr(dg), _ptr(dw), _ptr(workspace),
+                                 workspace.numel(), _stream(o.device)))
+    del keep
+    return dout, dg, dw

@@ -159,3 +159,29 @@ def workload_inputs(name: str, seed: int = 0):
     return make_inputs(w.B, w.T, w.H, w.dk, w.dv, w.dtype, seed=seed, h0_std=w.h0_std,
                        backward=w.backward, packed_mean=w.packed_mean, packed_min=w.packed_min,
                        gated=w.gated)
+
+
+def make_block_inputs(B, T, H, dk, dv, dtype="bf16", seed=0, width=4, cu_seqlens=None):
+    """Inputs of the block prologue and epilogue (CPU tensors).
+
+    Projections xq, xk [B, T, H, dk] and xv [B, T, H, dv] ~ N(0, 1); convolution
+    weights [H * d, width] ~ U(-1/sqrt(width), 1/sqrt(width)) fp32 (the default
+    range of a depthwise convolution with fan-in width); gradients of the
+    prologue outputs dq, dk, dv ~ N(0, 1); the rule's output o and the gate
+    projection g ~ N(0, 1), the normalisation weight 1 + N(0, 0.1) fp32 [dv],
+    the gradient of the block output dy ~ N(0, 1).  Draw order as listed.
+    """
+    gen = torch.Generator().manual_seed(seed)
+    dt = DTYPES[dtype]
+    n = lambda shape: torch.randn(shape, generator=gen, dtype=torch.float32).to(dt)
+    bound = 1.0 / width ** 0.5
+    u = lambda rows: (torch.rand((rows, width), generator=gen, dtype=torch.float32) * 2 - 1) * bound
+    out = dict(xq=n((B, T, H, dk)), xk=n((B, T, H, dk)), xv=n((B, T, H, dv)),
+               wq=u(H * dk), wk=u(H * dk), wv=u(H * dv),
+               dq=n((B, T, H, dk)), dk=n((B, T, H, dk)), dv=n((B, T, H, dv)),
+               o=n((B, T, H, dv)), g=n((B, T, H, dv)),
+               wo=1.0 + 0.1 * torch.randn((dv,), generator=gen, dtype=torch.float32),
+               dy=n((B, T, H, dv)))
+    if cu_seqlens is not None:
+        out["cu_seqlens"] = torch.as_tensor(cu_seqlens, dtype=torch.int32)
+    return out

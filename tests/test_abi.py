@@ -194,3 +194,30 @@ def test_recurrent_rejects_bad_arguments(lib):
     assert lib.gdn_recurrent_fwd(ctypes.byref(bad), *args, None) == 3
     badcu, keep = problem(B=1, cu=[0, 60, 50, 100])
     assert lib.gdn_recurrent_fwd(ctypes.byref(badcu), *args, None) == 4
+
+
+def test_block_ops_reject_bad_arguments(lib):
+    p, _ = problem(dk=256, dv=512)
+    fake = ctypes.c_void_p(0x10000)
+    odd = ctypes.c_void_p(0x10008)
+    need = lib.gdn_conv_silu_workspace_size(ctypes.byref(p), 256, 4)
+    assert need > 0
+    assert lib.gdn_conv_silu_workspace_size(ctypes.byref(p), 128, 4) == 0  # not dk or dv
+    f = lambda dim, W, eps, x, y, n: lib.gdn_conv_silu_fwd(ctypes.byref(p), dim, W, 1, eps, x,
+                                                           fake, y, fake, n, None)
+    assert f(256, 5, 1e-6, fake, fake, need) == 9
+    assert f(256, 0, 1e-6, fake, fake, need) == 9
+    assert f(256, 4, -1.0, fake, fake, need) == 9
+    assert f(128, 4, 1e-6, fake, fake, need) == 3
+    assert f(256, 4, 1e-6, None, fake, need) == 1
+    assert f(256, 4, 1e-6, fake, None, need) == 1
+    assert f(256, 4, 1e-6, odd, fake, need) == 7
+    assert f(256, 4, 1e-6, fake, fake, need - 1) == 5
+    assert lib.gdn_conv_silu_bwd(ctypes.byref(p), 512, 4, 0, 1e-6, fake, fake, fake, fake, None,
+                                 fake, need, None) == 1
+    nw = lib.gdn_norm_gate_workspace_size(ctypes.byref(p))
+    assert nw >= 200 // 64 * 512 * 4  # one partial dv-vector per 64 rows
+    assert lib.gdn_norm_gate_fwd(ctypes.byref(p), -1.0, fake, fake, fake, fake, None) == 9
+    assert lib.gdn_norm_gate_fwd(ctypes.byref(p), 1e-5, fake, None, fake, fake, None) == 1
+    assert lib.gdn_norm_gate_bwd(ctypes.byref(p), 1e-5, fake, fake, fake, fake, fake, fake, fake,
+                                 fake, nw - 1, None) == 5

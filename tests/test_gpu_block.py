@@ -1,0 +1,155 @@
+"""GPU parity of the block prologue and epilogue against the fp64 oracle.
+
+Same error metric and bar as tests/test_gpu_parity.py: per output tensor,
+max|x - ref| / max|ref| <= 1e-4 (fp32 inputs) or 2e-2 (bf16 inputs, fp32
+arithmetic); both sides see the same rounded inputs.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2412_06464_amd.inputs import make_block_inputs
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def rel_err(x, ref):
+    x = np.asarray(x, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    return float(np.abs(x - ref).max() / max(float(np.abs(ref).max()), 1e-30))
+
+
+def f64(t):
+    return t.detach().to("cpu", torch.float64).numpy()
+
+
+def say(*a):
+    print("[gpu-case]", *a, flush=True)
+
+
+@pytest.fixture(scope="module")
+def G():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2412_06464_amd import gdn
+    gdn.load_library()
+    return gdn
+
+
+@pytest.fixture(scope="module")
+def blk():
+    from oracle import block
+    return block
+
+
+def check_conv(G, blk, x, w, dy, l2norm, tol, label, cu=None):
+    say(label, tuple(x.shape), x.dtype, "W=%d" % w.shape[1], "l2=%d" % l2norm)
+    d = x.cuda()
+    cud = None if cu is None else cu.cuda()
+    y = G.gdn_conv_silu_fwd(d, w.cuda(), l2norm=l2norm, eps=1e-6, cu_seqlens=cud,
+                            cu_seqlens_host=cu)
+    dx, dw = G.gdn_conv_silu_bwd(d, w.cuda(), dy.cuda(), l2norm=l2norm, eps=1e-6,
+                                 cu_seqlens=cud, cu_seqlens_host=cu)
+    torch.cuda.synchronize()
+    ry = blk.conv_silu(x, w, cu, l2norm, 1e-6)
+    rdx, rdw = blk.conv_silu_vjp(x, w, dy, cu, l2norm, 1e-6)
+    errs = dict(y=rel_err(f64(y), ry), dx=rel_err(f64(dx), rdx), dw=rel_err(f64(dw), rdw))
+    say(label, {k: "%.3g" % v for k, v in errs.items()})
+    bad = {k: v for k, v in errs.items() if not v <= tol}
+    assert not bad, bad
+
+
+@pytest.mark.parametrize("dtype,d,B,T,H,W,l2", [
+    ("f32", 64, 2, 150, 2, 4, True),
+    ("f32", 64, 1, 70, 2, 1, False),
+    ("bf16", 128, 1, 200, 2, 3, True),
+    ("bf16", 256, 1, 130, 2, 4, True),
+    ("bf16", 256, 2, 64, 1, 2, True),
+    ("bf16", 512, 1, 70, 1, 4, False),
+])
+def test_conv_silu_matches_oracle(G, blk, dtype, d, B, T, H, W, l2):
+    dk, dv = (d, d) if d < 256 else (256, 512)
+    inp = make_block_inputs(B, T, H, dk, dv, dtype, seed=21, width=W)
+    x, w, dy = (inp["xq"], inp["wq"], inp["dq"]) if d == dk else (inp["xv"], inp["wv"], inp["dv"])
+    check_conv(G, blk, x, w, dy, l2, TOL[dtype], "conv_%s_%d_T%d" % (dtype, d, T))
+
+
+@pytest.mark.parametrize("dtype,d", [("f32", 64), ("bf16", 256)])
+def test_conv_silu_packed(G, blk, dtype, d):
+    lens = [1, 0, 2, 64, 65, 7]
+    cu = torch.tensor(np.concatenate([[0], np.cumsum(lens)]), dtype=torch.int32)
+    dk, dv = (d, d) if d < 256 else (256, 512)
+    inp = make_block_inputs(1, int(cu[-1]), 2, dk, dv, dtype, seed=22, width=4, cu_seqlens=cu)
+    check_conv(G, blk, inp["xk"], inp["wk"], inp["dk"], True, TOL[dtype],
+               "conv_packed_%s_%d" % (dtype, d), cu=cu)
+
+
+@pytest.mark.parametrize("dtype,dv,B,T,H", [
+    ("f32", 64, 2, 150, 2),
+    ("bf16", 128, 1, 77, 3),
+    ("bf16", 512, 2, 100, 2),
+])
+def test_norm_gate_matches_oracle(G, blk, dtype, dv, B, T, H):
+    dk = dv if dv < 512 else 256
+    inp = make_block_inputs(B, T, H, dk, dv, dtype, seed=23)
+    say("norm_gate", dtype, dv, B, T, H)
+    o, g, w, dy = inp["o"].cuda(), inp["g"].cuda(), inp["wo"].cuda(), inp["dy"].cuda()
+    y = G.gdn_norm_gate_fwd(o, g, w, eps=1e-5)
+    do, dg, dw = G.gdn_norm_gate_bwd(o, g, w, dy, eps=1e-5)
+    torch.cuda.synchronize()
+    ry = blk.norm_gate(inp["o"], inp["g"], inp["wo"], 1e-5)
+    rdo, rdg, rdw = blk.norm_gate_vjp(inp["o"], inp["g"], inp["wo"], inp["dy"], 1e-5)
+    errs = dict(y=rel_err(f64(y), ry), do=rel_err(f64(do), rdo), dg=rel_err(f64(dg), rdg),
+                dw=rel_err(f64(dw), rdw))
+    say("norm_gate", {k: "%.3g" % v for k, v in errs.items()})
+    bad = {k: v for k, v in errs.items() if not v <= TOL[dtype]}
+    assert not bad, bad
+
+
+def test_block_full_size_sampled(G, blk):
+    """The bench shape (B8 T4096 H6, dk 256, dv 512): the whole prologue and
+    epilogue on the GPU; the oracle recomputes one sequence (all heads) of
+    the q path and of the v path, and a sample of epilogue rows."""
+    B, T, H, dk, dv = 8, 4096, 6, 256, 512
+    inp = make_block_inputs(B, T, H, dk, dv, "bf16", seed=0)
+    d = {k: v.cuda() for k, v in inp.items()}
+    say("block full size")
+    q = G.gdn_conv_silu_fwd(d["xq"], d["wq"], l2norm=True)
+    dxq, dwq = G.gdn_conv_silu_bwd(d["xq"], d["wq"], d["dq"], l2norm=True)
+    v = G.gdn_conv_silu_fwd(d["xv"], d["wv"], l2norm=False)
+    dxv, dwv = G.gdn_conv_silu_bwd(d["xv"], d["wv"], d["dv"], l2norm=False)
+    y = G.gdn_norm_gate_fwd(d["o"], d["g"], d["wo"])
+    do, dg, dwo = G.gdn_norm_gate_bwd(d["o"], d["g"], d["wo"], d["dy"])
+    torch.cuda.synchronize()
+    tol = TOL["bf16"]
+    n = 5  # one whole sequence; dw is checked on the weight-gradient share of every sequence
+    for name, x, w, dy, out, dx, l2 in (("q", "xq", "wq", "dq", q, dxq, True),
+                                        ("v", "xv", "wv", "dv", v, dxv, False)):
+        sl = slice(n, n + 1)
+        ry = blk.conv_silu(inp[x][sl], inp[w], None, l2)
+        rdx, _ = blk.conv_silu_vjp(inp[x][sl], inp[w], inp[dy][sl], None, l2)
+        errs = dict(y=rel_err(f64(out[sl]), ry), dx=rel_err(f64(dx[sl]), rdx))
+        say("block", name, {k: "%.3g" % e for k, e in errs.items()})
+        assert all(e <= tol for e in errs.values()), errs
+    # the weight gradients over all sequences, checked on the v path's first
+    # 2 heads (fp64 oracle over the whole batch of those heads)
+    rdw = np.zeros((2 * dv, 4))
+    for b in range(B):
+        _, part = blk.conv_silu_vjp(inp["xv"][b:b + 1, :, :2], inp["wv"][:2 * dv],
+                                    inp["dv"][b:b + 1, :, :2], None, False)
+        rdw += part
+    e = rel_err(f64(dwv[:2 * dv]), rdw)
+    say("block dw_v heads 0-1 err %.3g" % e)
+    assert e <= tol
+    rows = np.random.default_rng(0).integers(0, B * T, 64)
+    o2 = inp["o"].reshape(B * T, H, dv)[rows]
+    g2 = inp["g"].reshape(B * T, H, dv)[rows]
+    ry = blk.norm_gate(o2, g2, inp["wo"])
+    rdo, rdg, _ = blk.norm_gate_vjp(o2, g2, inp["wo"], inp["dy"].reshape(B * T, H, dv)[rows])
+    errs = dict(y=rel_err(f64(y.reshape(B * T, H, dv)[rows]), ry),
+                do=rel_err(f64(do.reshape(B * T, H, dv)[rows]), rdo),
+                dg=rel_err(f64(dg.reshape(B * T, H, dv)[rows]), rdg))
+    say("block norm_gate rows", {k: "%.3g" % e for k, e in errs.items()})
+    assert all(e <= tol for e in errs.values()), errs
