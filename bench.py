@@ -31,6 +31,9 @@ DEFAULT_WORKLOAD = "fwdbwd_bf16_b8_t4096_h6_dk256_dv512"
 METRIC = "tokens/sec gated-delta chunk fwd+bwd (1 GPU); % bf16 MFMA peak"
 METRIC_FWD = "tokens/sec gated-delta chunk fwd (1 GPU); % bf16 MFMA peak"
 METRIC_RECURRENT = "tokens/sec gated-delta recurrent step (1 GPU); % HBM peak"
+METRIC_BLOCK = "tokens/sec gated-delta block prologue+epilogue fwd+bwd (1 GPU); % HBM peak"
+# block prologue / epilogue workloads: (B, T, H, dk, dv, conv width)
+BLOCK_WORKLOADS = {"block_bf16_b8_t4096_h6_dk256_dv512": (8, 4096, 6, 256, 512, 4)}
 PEAK_HBM = 8.0e12          # bytes/s, MI355X HBM3E
 PEAK_MFMA_BF16 = 2.5e15    # dense bf16 MFMA FLOP/s
 PEAK_MFMA_F32 = 157.3e12   # fp32 matrix FLOP/s
@@ -216,6 +219,131 @@ def traffic_from_profiles(kernel, workload):
     return ent.get("bytes_per_launch")
 
 
+def bench_block(args):
+    """One step = the block's prologue and epilogue, forward and backward:
+    conv+SiLU+L2 of q and k, conv+SiLU of v, RMS norm x gate of the output,
+    then the backward of each.  Every call is timed with events on the
+    stream the library launches on; the roofline is the slowest call's
+    algorithmic bytes (its inputs and outputs once) over its mean time."""
+    import torch
+
+    from paper_2412_06464_amd import gdn
+    from paper_2412_06464_amd.inputs import make_block_inputs
+
+    B, T, H, dk, dv, W = BLOCK_WORKLOADS[args.workload]
+    gdn.load_library()
+    inp = make_block_inputs(B, T, H, dk, dv, "bf16", seed=0, width=W)
+    d = {k: v.cuda() for k, v in inp.items()}
+    out = {k: torch.empty_like(d[k]) for k in ("xq", "xk", "xv", "o")}
+    grads = {k: torch.empty_like(d[k]) for k in ("xq", "xk", "xv", "o", "g")}
+    dws = {k: torch.empty_like(d[k]) for k in ("wq", "wk", "wv", "wo")}
+    pq, _ = gdn.block_problem(d["xq"])
+    ws = torch.empty(max(gdn.load_library().gdn_conv_silu_workspace_size(pq, dv, W),
+                         gdn.load_library().gdn_norm_gate_workspace_size(pq)), dtype=torch.uint8,
+                     device="cuda")
+    # C arguments prepared once: a step is eight library calls and nothing else
+    import ctypes
+    lib = gdn.load_library()
+    P = lambda t: ctypes.c_void_p(t.data_ptr())
+    st = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    probs = {}
+    for key in ("xq", "xv"):
+        probs[key], _ = gdn.block_problem(d[key])
+    pk, pv = ctypes.byref(probs["xq"]), ctypes.byref(probs["xv"])
+    wsp, wsn = P(ws), ws.numel()
+    eps_l2, eps_n = ctypes.c_float(1e-6), ctypes.c_float(1e-5)
+
+    def conv_fwd(pp, dim, l2, x, w, y):
+        args = (pp, dim, W, l2, eps_l2, P(d[x]), P(d[w]), P(out[y]), wsp, wsn, st)
+        return lambda: lib.gdn_conv_silu_fwd(*args)
+
+    def conv_bwd(pp, dim, l2, x, w, dy):
+        args = (pp, dim, W, l2, eps_l2, P(d[x]), P(d[w]), P(d[dy]), P(grads[x]), P(dws[w]),
+                wsp, wsn, st)
+        return lambda: lib.gdn_conv_silu_bwd(*args)
+
+    nf = (pv, eps_n, P(d["o"]), P(d["g"]), P(d["wo"]), P(out["o"]), st)
+    nb = (pv, eps_n, P(d["o"]), P(d["g"]), P(d["wo"]), P(d["dy"]), P(grads["o"]), P(grads["g"]),
+          P(dws["wo"]), wsp, wsn, st)
+    calls = [
+        ("conv_fwd_q", conv_fwd(pk, dk, 1, "xq", "wq", "xq"), 2 * dk),
+        ("conv_fwd_k", conv_fwd(pk, dk, 1, "xk", "wk", "xk"), 2 * dk),
+        ("conv_fwd_v", conv_fwd(pv, dv, 0, "xv", "wv", "xv"), 2 * dv),
+        ("norm_gate_fwd", lambda: lib.gdn_norm_gate_fwd(*nf), 3 * dv),
+        ("norm_gate_bwd", lambda: lib.gdn_norm_gate_bwd(*nb), 5 * dv),
+        ("conv_bwd_q", conv_bwd(pk, dk, 1, "xq", "wq", "dq"), 3 * dk),
+        ("conv_bwd_k", conv_bwd(pk, dk, 1, "xk", "wk", "dk"), 3 * dk),
+        ("conv_bwd_v", conv_bwd(pv, dv, 0, "xv", "wv", "dv"), 3 * dv),
+    ]
+    for name, f, _ in calls:  # one checked call each before timing
+        rc = f()
+        if rc != 0:
+            raise gdn.GdnError(rc)
+    stream = torch.cuda.current_stream()
+
+    def step(evs=None):
+        for i, (_, f, _) in enumerate(calls):
+            if evs:
+                evs[i][0].record(stream)
+            f()
+            if evs:
+                evs[i][1].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for _ in calls] for _ in range(args.steps)]
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for k in range(args.steps):
+        step(evs[k])
+    end.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / args.steps
+    call_ms = {name: sum(evs[k][i][0].elapsed_time(evs[k][i][1]) for k in range(args.steps))
+               / args.steps for i, (name, _, _) in enumerate(calls)}
+    th = B * T * H
+    nbytes = {name: per * 2 * th for name, _, per in calls}  # bf16 elements per token-head
+    dom = max(call_ms, key=lambda k: call_ms[k])
+    ach = nbytes[dom] / (call_ms[dom] / 1e3)
+    roof = {"bound": "hbm", "achieved": ach / 1e9, "peak": PEAK_HBM / 1e9, "unit": "GB/s",
+            "frac": ach / PEAK_HBM, "traffic": traffic_from_profiles(dom, args.workload),
+            "kernel": dom, "kernel_ms": call_ms[dom]}
+    total_bytes = sum(nbytes.values())
+    res = {
+        "metric": METRIC_BLOCK, "value": B * T / (ms / 1e3), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": args.workload, "B": B, "T": T, "H": H, "dk": dk, "dv": dv,
+                   "conv_width": W},
+        "hbm_frac": total_bytes / (ms / 1e3) / PEAK_HBM, "path_gbytes": total_bytes / 1e9,
+        "calls_ms": call_ms, "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        from oracle import block
+        t0 = time.perf_counter()
+        n = 0
+        while time.perf_counter() - t0 < 10.0 and n < B:
+            sl = slice(n, n + 1)
+            block.conv_silu(inp["xq"][sl], inp["wq"], None, True)
+            block.conv_silu(inp["xk"][sl], inp["wk"], None, True)
+            block.conv_silu(inp["xv"][sl], inp["wv"], None, False)
+            block.norm_gate(inp["o"][sl], inp["g"][sl], inp["wo"])
+            block.norm_gate_vjp(inp["o"][sl], inp["g"][sl], inp["wo"], inp["dy"][sl])
+            block.conv_silu_vjp(inp["xq"][sl], inp["wq"], inp["dq"][sl], None, True)
+            block.conv_silu_vjp(inp["xk"][sl], inp["wk"], inp["dk"][sl], None, True)
+            block.conv_silu_vjp(inp["xv"][sl], inp["wv"], inp["dv"][sl], None, False)
+            n += 1
+        dt = time.perf_counter() - t0
+        res["cpu_baseline"] = {"value": n * T / dt, "unit": "tokens/s", "cores": 1,
+                               "kind": "oracle",
+                               "sample": "%d of %d sequences, all heads, fwd+bwd, %.1f s" % (
+                                   n, B, dt)}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -238,6 +366,9 @@ def main():
     from paper_2412_06464_amd import gdn
     from paper_2412_06464_amd.inputs import WORKLOADS, workload_inputs
 
+    if args.workload in BLOCK_WORKLOADS:
+        bench_block(args)
+        return
     if args.copy_calibration:
         x = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
         y = torch.empty_like(x)

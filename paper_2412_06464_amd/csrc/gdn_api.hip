@@ -215,7 +215,9 @@ size_t carve_conv(const gdn_problem* p, const Shape& s, int dim, int width, unsi
   Carver c{base};
   unsigned char* info = c.take((size_t)s.NC * sizeof(int4) + 16);
   unsigned char* sc0 = c.take(((size_t)s.N + 1) * sizeof(int));
-  unsigned char* part = c.take((size_t)s.NC * p->H * dim * width * sizeof(float));
+  const size_t row = (size_t)p->H * dim * width * sizeof(float);
+  unsigned char* part = c.take((size_t)s.NC * row);
+  unsigned char* tmp = c.take((size_t)((s.NC + 255) / 256) * row);
   if (t) {
     t->info = (int4*)info;
     t->seq_chunk0 = (int*)sc0;
@@ -223,6 +225,7 @@ size_t carve_conv(const gdn_problem* p, const Shape& s, int dim, int width, unsi
   if (a) {
     a->info = (const int4*)info;
     a->part = (float*)part;
+    a->tmp = (float*)tmp;
   }
   return c.off;
 }
@@ -548,11 +551,16 @@ gdn_status gdn_conv_silu_bwd(const gdn_problem* p, int dim, int width, int l2nor
 
 static long norm_rows(const gdn_problem* p, const Shape& s) { return s.Ttot * p->H; }
 static int norm_blocks(long rows) { return (int)((rows + 63) / 64); }
+// partial dw rows, then their slice sums (256 rows a slice)
+static size_t norm_ws(const gdn_problem* p, int nblk) {
+  return up((size_t)nblk * p->dv * sizeof(float)) +
+         up((size_t)((nblk + 255) / 256) * p->dv * sizeof(float));
+}
 
 size_t gdn_norm_gate_workspace_size(const gdn_problem* p) {
   Shape s;
   if (check_problem(p, &s) != GDN_OK) return 0;
-  return up((size_t)norm_blocks(norm_rows(p, s)) * p->dv * sizeof(float));
+  return norm_ws(p, norm_blocks(norm_rows(p, s)));
 }
 
 static gdn_status norm_call(const gdn_problem* p, float eps, const void* o, const void* g,
@@ -571,8 +579,7 @@ static gdn_status norm_call(const gdn_problem* p, float eps, const void* o, cons
   memset(&a, 0, sizeof a);
   a.rows = norm_rows(p, s);
   a.nblk = norm_blocks(a.rows);
-  if (bwd && (!workspace || workspace_bytes < up((size_t)a.nblk * p->dv * sizeof(float))))
-    return GDN_ERR_WORKSPACE;
+  if (bwd && (!workspace || workspace_bytes < norm_ws(p, a.nblk))) return GDN_ERR_WORKSPACE;
   a.eps = eps;
   a.o = o;
   a.g = g;
@@ -582,6 +589,9 @@ static gdn_status norm_call(const gdn_problem* p, float eps, const void* o, cons
   a.dout = dout;
   a.dg = dg;
   a.part = (float*)workspace;
+  a.tmp = workspace ? (float*)((unsigned char*)workspace +
+                               up((size_t)a.nblk * p->dv * sizeof(float)))
+                    : nullptr;
   a.dw = dw;
   const Dt dt = p->dtype == GDN_F32 ? Dt::F32 : Dt::BF16;
   const hipError_t e = bwd ? gdn::launch_norm_gate_bwd(dt, p->dv, a, (hipStream_t)stream)

@@ -70,12 +70,8 @@ __device__ inline void store_piece(E* p, const float (&v)[N]) {
   } t;
 #pragma unroll
   for (int i = 0; i < N; ++i) t.e[i] = to_e<E>(v[i]);
-  if constexpr (sizeof(t) == 16) {
-    store_stream(p, *reinterpret_cast<const uint4*>(t.b));
-  } else if constexpr (sizeof(t) == 8) {
-    *reinterpret_cast<uint2*>(p) = *reinterpret_cast<const uint2*>(t.b);
-  } else if constexpr (sizeof(t) == 4) {
-    *reinterpret_cast<unsigned*>(p) = *reinterpret_cast<const unsigned*>(t.b);
+  if constexpr (sizeof(t) == 16 || sizeof(t) == 8 || sizeof(t) == 4) {
+    store_stream_small(p, t);
   } else {
 #pragma unroll
     for (int i = 0; i < N; ++i) p[i] = t.e[i];
@@ -90,7 +86,9 @@ __device__ inline float wave_sum(float x) {
   return x;
 }
 
-__device__ inline float sigmoidf(float x) { return 1.f / (1.f + __expf(-x)); }
+// 1 / (1 + e^-x) with the hardware reciprocal (1 ulp) instead of a full
+// IEEE division sequence
+__device__ inline float sigmoidf(float x) { return __builtin_amdgcn_rcpf(1.f + __expf(-x)); }
 
 }  // namespace
 
@@ -99,16 +97,18 @@ __device__ inline float sigmoidf(float x) { return 1.f / (1.f + __expf(-x)); }
 // One workgroup per (chunk, head); wave w owns rows 16 w .. 16 w + 15 of the
 // chunk.  The three rows before each wave's first row come from the previous
 // chunk of the same sequence (or are zero at the sequence start).
-template <class E, int D>
+// D: channels of the tensor; DL: channels of one workgroup (D, or a slice of
+// it when the rows need no L2 sum).
+template <class E, int D, int DL>
 __global__ __launch_bounds__(256) void k_conv_fwd(ConvArgs a) {
-  constexpr int CPL = D / 64, NR = 16 + 3;
+  constexpr int CPL = DL / 64, NR = 16 + 3;
   const int c = blockIdx.x, h = blockIdx.y, w = wave_id(), l = lane_id();
   const int4 ci = a.info[c];
   const int n = ci.x, start = ci.y, len = ci.z;
   const int s0 = a.cu ? a.cu[n] : n * a.T;
   const int pos0 = start - s0, r0 = 16 * w, H = a.H;
   if (r0 >= len) return;
-  const int ch = l * CPL;
+  const int ch = blockIdx.z * DL + l * CPL;
   float wl[CPL][4];  // weight of lag j (x_{t-j}); zero for j >= W
 #pragma unroll
   for (int k = 0; k < CPL; ++k)
@@ -160,19 +160,19 @@ __global__ __launch_bounds__(256) void k_conv_fwd(ConvArgs a) {
 // chunk of the same sequence), recomputing du_t, so that
 // dx_s = sum_j w_lag(j) du_{s+j} is complete for its own rows; dw is summed
 // over own rows only.  x, du: 4-row sliding windows; raw rows prefetched.
-template <class E, int D>
+template <class E, int D, int DL>
 __global__ __launch_bounds__(256) void k_conv_bwd(ConvArgs a) {
-  constexpr int CPL = D / 64;
-  constexpr int RP = D >= 512 ? 8 : 16;  // rows per pass
+  constexpr int CPL = DL / 64;
+  constexpr int RP = 8;  // rows per pass
   constexpr int NX = RP + 6, NG = RP + 3;
-  __shared__ float sdw[4][D][4];
+  __shared__ float sdw[4][DL][4];
   const int c = blockIdx.x, h = blockIdx.y, w = wave_id(), l = lane_id();
   const int4 ci = a.info[c];
   const int n = ci.x, start = ci.y, len = ci.z;
   const int s0 = a.cu ? a.cu[n] : n * a.T;
   const int L = a.cu ? a.cu[n + 1] - s0 : a.T;
   const int pos0 = start - s0, H = a.H;
-  const int ch = l * CPL;
+  const int cl = l * CPL, ch = blockIdx.z * DL + cl;
   float wl[CPL][4];
 #pragma unroll
   for (int k = 0; k < CPL; ++k)
@@ -264,32 +264,52 @@ __global__ __launch_bounds__(256) void k_conv_bwd(ConvArgs a) {
 #pragma unroll
   for (int k = 0; k < CPL; ++k)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) sdw[w][ch + k][j] = dwp[k][j];
+    for (int j = 0; j < 4; ++j) sdw[w][cl + k][j] = dwp[k][j];
   __syncthreads();
   // this workgroup's partial dw[h][ch][tap], in the order of the weights
-  float* part = a.part + ((size_t)c * H + h) * D * a.W;
-  for (int idx = threadIdx.x; idx < D * a.W; idx += 256) {
+  float* part = a.part + (((size_t)c * H + h) * D + blockIdx.z * DL) * a.W;
+  for (int idx = threadIdx.x; idx < DL * a.W; idx += 256) {
     const int cc = idx / a.W, tap = idx - cc * a.W, j = a.W - 1 - tap;
     part[idx] = sdw[0][cc][j] + sdw[1][cc][j] + sdw[2][cc][j] + sdw[3][cc][j];
   }
 }
 
-// out[m] = sum_{i < N} in[i * M + m], in a fixed order: thread (m, seg) sums
-// the rows seg, seg + 16, ..., then the 16 partial sums are added in order.
+// out[y * M + m] = sum of in[i * M + m] over the rows i of slice y (rows
+// [y * RS, (y + 1) * RS) of N), in a fixed order: thread (m, seg) sums rows
+// seg, seg + 16, ... of the slice, then the 16 partial sums are added in order.
+constexpr int SUM_RS = 256;  // rows per slice
 __global__ __launch_bounds__(256) void k_sum_rows(const float* in, int N, int M, float* out) {
   __shared__ float s[16][17];
   const int ml = threadIdx.x & 15, seg = threadIdx.x >> 4, m = blockIdx.x * 16 + ml;
+  const int i0 = blockIdx.y * SUM_RS, i1 = min(N, i0 + SUM_RS);
   float acc = 0.f;
   if (m < M)
-    for (int i = seg; i < N; i += 16) acc += in[(size_t)i * M + m];
+    for (int i = i0 + seg; i < i1; i += 16) acc += in[(size_t)i * M + m];
   s[seg][ml] = acc;
   __syncthreads();
   if (seg == 0 && m < M) {
     float t = 0.f;
 #pragma unroll
     for (int x = 0; x < 16; ++x) t += s[x][ml];
-    out[m] = t;
+    out[(size_t)blockIdx.y * M + m] = t;
   }
+}
+
+// dw = sum over the N rows of part [N][M]: slices of SUM_RS rows summed in
+// parallel into tmp [NS][M] (NS = slices), then the NS slice sums in order.
+// tmp may be null when N <= SUM_RS.  Deterministic for a given N.
+hipError_t launch_sum_rows(const float* part, int N, int M, float* tmp, float* out,
+                           hipStream_t s) {
+  const int NS = (N + SUM_RS - 1) / SUM_RS;
+  if (NS <= 1) {
+    hipLaunchKernelGGL(k_sum_rows, dim3((M + 15) / 16, 1), dim3(256), 0, s, part, N, M, out);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL(k_sum_rows, dim3((M + 15) / 16, NS), dim3(256), 0, s, part, N, M, tmp);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_sum_rows, dim3((M + 15) / 16, 1), dim3(256), 0, s, tmp, NS, M, out);
+  return hipGetLastError();
 }
 
 // ------------------------------------------------------------------ epilogue
@@ -303,12 +323,22 @@ __global__ __launch_bounds__(256) void k_norm_gate_fwd(NormArgs a) {
   const long r0 = (long)blockIdx.x * 64 + 16 * wave_id();
   RowPiece<float, CPL> wt;
   wt.load(a.w + ch);
-  for (int i = 0; i < 16; ++i) {
+  // one row ahead: the next row's loads are in flight while this one computes
+  const int nr = (int)min(16L, max(0L, a.rows - r0));
+  RowRaw<E, CPL> on, gn;
+  if (nr > 0) {
+    on.load((const E*)a.o + r0 * DV + ch);
+    gn.load((const E*)a.g + r0 * DV + ch);
+  }
+  for (int i = 0; i < nr; ++i) {
     const long r = r0 + i;
-    if (r >= a.rows) break;
     RowPiece<E, CPL> o, g;
-    o.load((const E*)a.o + r * DV + ch);
-    g.load((const E*)a.g + r * DV + ch);
+    on.to_float(o.v);
+    gn.to_float(g.v);
+    if (i + 1 < nr) {
+      on.load((const E*)a.o + (r + 1) * DV + ch);
+      gn.load((const E*)a.g + (r + 1) * DV + ch);
+    }
     float ss = 0.f;
 #pragma unroll
     for (int k = 0; k < CPL; ++k) ss += o.v[k] * o.v[k];
@@ -331,13 +361,25 @@ __global__ __launch_bounds__(256) void k_norm_gate_bwd(NormArgs a) {
   float dwp[CPL];
 #pragma unroll
   for (int k = 0; k < CPL; ++k) dwp[k] = 0.f;
-  for (int i = 0; i < 16; ++i) {
+  // one row ahead: the next row's loads are in flight while this one computes
+  const int nr = (int)min(16L, max(0L, a.rows - r0));
+  RowRaw<E, CPL> on, gn, dn;
+  if (nr > 0) {
+    on.load((const E*)a.o + r0 * DV + ch);
+    gn.load((const E*)a.g + r0 * DV + ch);
+    dn.load((const E*)a.dy + r0 * DV + ch);
+  }
+  for (int i = 0; i < nr; ++i) {
     const long r = r0 + i;
-    if (r >= a.rows) break;
     RowPiece<E, CPL> o, g, dy;
-    o.load((const E*)a.o + r * DV + ch);
-    g.load((const E*)a.g + r * DV + ch);
-    dy.load((const E*)a.dy + r * DV + ch);
+    on.to_float(o.v);
+    gn.to_float(g.v);
+    dn.to_float(dy.v);
+    if (i + 1 < nr) {
+      on.load((const E*)a.o + (r + 1) * DV + ch);
+      gn.load((const E*)a.g + (r + 1) * DV + ch);
+      dn.load((const E*)a.dy + (r + 1) * DV + ch);
+    }
     float ss = 0.f;
 #pragma unroll
     for (int k = 0; k < CPL; ++k) ss += o.v[k] * o.v[k];
@@ -379,9 +421,16 @@ __global__ __launch_bounds__(256) void k_norm_gate_bwd(NormArgs a) {
     return hipErrorInvalidValue;                                                           \
   } while (0)
 
+// Rows without the L2 sum are split over workgroups of at most 256 channels.
 hipError_t launch_conv_fwd(Dt dt, int d, const ConvArgs& a, hipStream_t s) {
   auto f = [&]<class E, int D>() {
-    hipLaunchKernelGGL((k_conv_fwd<E, D>), dim3(a.NC, a.H), dim3(256), 0, s, a);
+    if constexpr (D > 256) {
+      if (!a.l2) {
+        hipLaunchKernelGGL((k_conv_fwd<E, D, 256>), dim3(a.NC, a.H, D / 256), dim3(256), 0, s, a);
+        return hipGetLastError();
+      }
+    }
+    hipLaunchKernelGGL((k_conv_fwd<E, D, D>), dim3(a.NC, a.H), dim3(256), 0, s, a);
     return hipGetLastError();
   };
   GDN_BLOCK_DISPATCH(dt, d, f);
@@ -389,12 +438,17 @@ hipError_t launch_conv_fwd(Dt dt, int d, const ConvArgs& a, hipStream_t s) {
 
 hipError_t launch_conv_bwd(Dt dt, int d, const ConvArgs& a, hipStream_t s) {
   auto f = [&]<class E, int D>() {
-    hipLaunchKernelGGL((k_conv_bwd<E, D>), dim3(a.NC, a.H), dim3(256), 0, s, a);
+    bool split = false;
+    if constexpr (D > 256) split = !a.l2;
+    if constexpr (D > 256) {
+      if (split)
+        hipLaunchKernelGGL((k_conv_bwd<E, D, 256>), dim3(a.NC, a.H, D / 256), dim3(256), 0, s,
+                           a);
+    }
+    if (!split) hipLaunchKernelGGL((k_conv_bwd<E, D, D>), dim3(a.NC, a.H), dim3(256), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const int M = a.H * D * a.W;
-    hipLaunchKernelGGL(k_sum_rows, dim3((M + 15) / 16), dim3(256), 0, s, a.part, a.NC, M, a.dw);
-    return hipGetLastError();
+    return launch_sum_rows(a.part, a.NC, a.H * D * a.W, a.tmp, a.dw, s);
   };
   GDN_BLOCK_DISPATCH(dt, d, f);
 }
@@ -412,9 +466,7 @@ hipError_t launch_norm_gate_bwd(Dt dt, int dv, const NormArgs& a, hipStream_t s)
     hipLaunchKernelGGL((k_norm_gate_bwd<E, DV>), dim3(a.nblk), dim3(256), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_sum_rows, dim3((DV + 15) / 16), dim3(256), 0, s, a.part, a.nblk, DV,
-                       a.dw);
-    return hipGetLastError();
+    return launch_sum_rows(a.part, a.nblk, DV, a.tmp, a.dw, s);
   };
   GDN_BLOCK_DISPATCH(dt, dv, f);
 }

@@ -65,6 +65,7 @@ struct ConvArgs {
   void* y;                   // output
   void* dx;                  // gradient of the input
   float* part;               // [NC][H][D][W] per-chunk partial weight gradients
+  float* tmp;                // [ceil(NC / 256)][H][D][W] slice sums of part
   float* dw;                 // weight gradient [H * D][W]
 };
 
@@ -77,6 +78,7 @@ struct NormArgs {
   const float* w;            // [dv]
   void *y, *dout, *dg;       // [rows][dv]
   float* part;               // [nblk][dv] partial weight gradients
+  float* tmp;                // [ceil(nblk / 256)][dv] slice sums of part
   float* dw;                 // [dv]
 };
 
