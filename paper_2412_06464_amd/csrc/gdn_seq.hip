@@ -266,7 +266,7 @@ __global__ __launch_bounds__(256, (MODE == SEQ_SAVE ? GDN_SAVE_MINB : GDN_SEQ_MI
 #pragma unroll
         for (int jj = 0; jj < NTV; ++jj) S[i][jj] *= egn;
     }
-    frag fKc[MTS][NKC], fPc[NKC];
+    frag fKc[MTS][NKC], fPc[NKC];  // copies, so that the refills need not wait for the products
 #pragma unroll
     for (int i = 0; i < MTS; ++i)
 #pragma unroll
@@ -405,6 +405,49 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
   };
   // Second group, needed in (c): T^T rows of tile w; (e^g Q)^T and -W~^T rows
   // of the wave's state rows.
+  // The same loads one fragment group at a time, issued in the loop right
+  // after the last product that reads the register they refill (a refill
+  // of a register that queued products still read waits for them).
+  auto reload_K = [&](int j, int kt) {
+    const size_t ch = (size_t)(c0 + j) * H + h;
+    fK[kt] = M::load((const E*)a.Kf + ch * CH * DK + (size_t)w * NKD * FR + lo + kt * FR);
+  };
+  auto reload_PT = [&](int j) {
+    const size_t ch = (size_t)(c0 + j) * H + h;
+    const E* Pp = (const E*)a.PTf + ch * CH * CH + (size_t)w * NKC * FR;
+#pragma unroll
+    for (int kt = 0; kt < NKC; ++kt) fPT[kt] = M::load(Pp + lo + kt * FR);
+  };
+  auto reload_rest = [&](int j) {  // dO tile and gates
+    const int start = s0 + j * CH, len = min(CH, L - j * CH);
+    const size_t ch = (size_t)(c0 + j) * H + h;
+    const size_t row0 = (size_t)start * H + h;
+#pragma unroll
+    for (int x = 0; x < DOV; ++x) {
+      const int idx = tid + x * 256, tt = idx & (CH - 1), cv = idx >> 6;
+      dov[x] = *reinterpret_cast<const uint4*>(dOin + (row0 + (size_t)min(tt, len - 1) * H) * DV +
+                                               v0 + cv * EPV);
+      if (tt >= len) dov[x] = uint4{0u, 0u, 0u, 0u};
+    }
+    if (a.gated) gl = a.g[ch * CH + l];
+    bl = a.beta[row0 + (size_t)min(l, len - 1) * H];
+  };
+  auto reload_T = [&](int j) {
+    const size_t ch = (size_t)(c0 + j) * H + h;
+    const E* Tp = (const E*)a.TTf + ch * CH * CH + (size_t)w * NKC * FR;
+#pragma unroll
+    for (int kt = 0; kt < NKC; ++kt) fT[kt] = M::load(Tp + lo + kt * FR);
+  };
+  auto reload_QW = [&](int j, int kt) {
+    const size_t ch = (size_t)(c0 + j) * H + h;
+    const E* Qp = (const E*)a.QgT + ch * DK * CH + (size_t)w * MTS * NKC * FR;
+    const E* Wp = (const E*)a.nWT + ch * DK * CH + (size_t)w * MTS * NKC * FR;
+#pragma unroll
+    for (int i = 0; i < MTS; ++i) {
+      fQ[i][kt] = M::load(Qp + lo + (i * NKC + kt) * FR);
+      fW[i][kt] = M::load(Wp + lo + (i * NKC + kt) * FR);
+    }
+  };
   auto load_second = [&](int j) {
     const size_t ch = (size_t)(c0 + j) * H + h;
     const E* Tp = (const E*)a.TTf + ch * CH * CH + (size_t)w * NKC * FR;
@@ -463,14 +506,18 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
     f32x4 X1[NTV], X2[NTV];
 #pragma unroll
     for (int jj = 0; jj < NTV; ++jj) X1[jj] = X2[jj] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int jn = max(j - 1, 0);  // the chunk whose operands are loaded next
 #pragma unroll
     for (int kt = 0; kt < NKC; ++kt)
 #pragma unroll
       for (int jj = 0; jj < NTV; ++jj) X2[jj] = M::mma(fPT[kt], bfrag_get<E>(sdO, NTV, kt, jj), X2[jj]);
+    reload_PT(jn);
 #pragma unroll
-    for (int kt = 0; kt < NKD; ++kt)
+    for (int kt = 0; kt < NKD; ++kt) {
 #pragma unroll
       for (int jj = 0; jj < NTV; ++jj) X1[jj] = M::mma(fK[kt], bfrag_get<E>(sdSB, NTV, kt, jj), X1[jj]);
+      reload_K(jn, kt);
+    }
     const float gn = __shfl(gl, CH - 1, 64);  // pads repeat g of the last token
     float brow[4];
 #pragma unroll
@@ -485,7 +532,7 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
     }
 #pragma unroll
     for (int jj = 0; jj < NTV; ++jj) bfrag_put<E>(sdVB, NTV, w, jj, X1[jj]);
-    load_first(max(j - 1, 0));
+    reload_rest(jn);
     lds_barrier();
 
     // (c) dX = T^T dV', dv = b dX;  dS <- e^{g_n} dS + (e^g Q)^T dO - W~^T dV'
@@ -496,6 +543,7 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
     for (int kt = 0; kt < NKC; ++kt)
 #pragma unroll
       for (int jj = 0; jj < NTV; ++jj) dX[jj] = M::mma(fT[kt], bfrag_get<E>(sdVB, NTV, kt, jj), dX[jj]);
+    reload_T(jn);
     if (a.gated) {
       const float egn = __expf(gn);
 #pragma unroll
@@ -504,7 +552,7 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
         for (int jj = 0; jj < NTV; ++jj) dS[i][jj] *= egn;
     }
 #pragma unroll
-    for (int kt = 0; kt < NKC; ++kt)
+    for (int kt = 0; kt < NKC; ++kt) {
 #pragma unroll
       for (int jj = 0; jj < NTV; ++jj) {
         const frag bo = bfrag_get<E>(sdO, NTV, kt, jj);
@@ -515,7 +563,8 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
           dS[i][jj] = M::mma(fW[i][kt], bv, dS[i][jj]);
         }
       }
-    load_second(max(j - 1, 0));
+      reload_QW(jn, kt);
+    }
     {  // dX rows (stored with the next chunk) and dv rows (through LDS, 16 bytes per lane)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
