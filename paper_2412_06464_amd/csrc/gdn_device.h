@@ -112,20 +112,6 @@ __device__ inline void wave_mma_nt(f32x4 (&acc)[MT][NT], const E* A, int lda,
 __device__ inline int acc_row(int e) { return ((lane_id() >> 4) << 2) + e; }
 __device__ inline int acc_col() { return lane_id() & 15; }
 
-// Store an accumulator tile transposed into LDS: dstT[col][row0 + 4 rows].
-template <class E>
-__device__ inline void store_tile_T(E* dstT, int ld, const f32x4& a, int row0, int col0,
-                                    float s0 = 1.f, float s1 = 1.f, float s2 = 1.f,
-                                    float s3 = 1.f) {
-  const int c = col0 + acc_col();
-  const int r = row0 + acc_row(0);
-  E* p = dstT + c * ld + r;
-  p[0] = to_e<E>(a[0] * s0);
-  p[1] = to_e<E>(a[1] * s1);
-  p[2] = to_e<E>(a[2] * s2);
-  p[3] = to_e<E>(a[3] * s3);
-}
-
 // Copy rows [0, ROWS) x cols [0, W) of a row-major global tile (row stride
 // `rs` elements) into LDS with leading dimension LD.  Rows >= nvalid are
 // zero-filled.  16-byte vectors; W * sizeof(E) must be a multiple of 16.
@@ -167,39 +153,12 @@ __device__ inline void stage_rows_T(E* dstT, const E* g, size_t rs, int nvalid,
   }
 }
 
-// Stage a 64x64 fp32 matrix from global into LDS as E, optionally transposed.
-template <class E, int LD, int NTH, bool TRANSPOSE>
-__device__ inline void stage_mat64(E* dst, const float* g) {
-#pragma unroll 4
-  for (int idx = threadIdx.x; idx < CH * CH / 4; idx += NTH) {
-    const int r = idx / (CH / 4), c4 = (idx - r * (CH / 4)) * 4;
-    const float4 x = *reinterpret_cast<const float4*>(g + r * CH + c4);
-    if (TRANSPOSE) {
-      dst[(c4 + 0) * LD + r] = to_e<E>(x.x);
-      dst[(c4 + 1) * LD + r] = to_e<E>(x.y);
-      dst[(c4 + 2) * LD + r] = to_e<E>(x.z);
-      dst[(c4 + 3) * LD + r] = to_e<E>(x.w);
-    } else {
-      E* p = dst + r * LD + c4;
-      p[0] = to_e<E>(x.x);
-      p[1] = to_e<E>(x.y);
-      p[2] = to_e<E>(x.z);
-      p[3] = to_e<E>(x.w);
-    }
-  }
-}
-
 // ---- operand layouts in HBM
 // A-fragment layout of an R x KD matrix M (logical row-major): the MFMA A
 // tile (mt, kt) covers rows 16mt.. and k = K*kt..; lane l's KPL elements
 // M[16mt + (l & 15)][K*kt + KPL*(l >> 4) + j] are stored contiguously at
 // ((mt * (KD / K) + kt) * 64 + l) * KPL, so a wave reads one tile with one
 // fully coalesced load (1 KiB for bf16).
-template <class E>
-__device__ inline size_t afrag_index(int mt, int kt, int KD) {
-  using M = Mfma<E>;
-  return ((size_t)(mt * (KD / M::K) + kt) * 64 + lane_id()) * M::KPL;
-}
 
 // C-fragment (accumulator) layout of an R x N matrix: tile (mt, nt), lane l
 // holds rows 16mt + 4(l >> 4) + e, column 16nt + (l & 15), stored at
@@ -250,59 +209,6 @@ __device__ inline void store_stream_small(void* p, const T& v) {
   }
 }
 
-
-// Write an R x KD matrix in A-fragment layout; val(r, k) gives its elements.
-template <class E, int R, int KD, int NTH, class F>
-__device__ inline void export_afrag(E* dst, F&& val) {
-  using M = Mfma<E>;
-  constexpr int UNITS = R * KD / M::KPL;
-  for (int u = threadIdx.x; u < UNITS; u += NTH) {
-    const int tile = u >> 6, l = u & 63;
-    const int mt = tile / (KD / M::K), kt = tile - mt * (KD / M::K);
-    const int r = mt * 16 + (l & 15), k0 = kt * M::K + (l >> 4) * M::KPL;
-    union {
-      typename M::frag f;
-      E e[M::KPL];
-    } x;
-#pragma unroll
-    for (int j = 0; j < M::KPL; ++j) x.e[j] = to_e<E>(val(r, k0 + j));
-    store_stream_small(dst + (size_t)u * M::KPL, x.f);
-  }
-}
-
-// acc[i][j] (+)= sum_k A_i[k] * Bt[j*16 + n][k] with the A operand already in
-// registers (a[i][kk] = fragment of row tile i, k-step kk) and Bt in LDS.
-template <class E, int MT, int NT, int NK>
-__device__ inline void mma_regA(f32x4 (&acc)[MT][NT], const typename Mfma<E>::frag (&a)[MT][NK],
-                                const E* Bt, int ldb) {
-  using M = Mfma<E>;
-  const int l = lane_id();
-  const int r = l & 15, kq = (l >> 4) * M::KPL;
-#pragma unroll
-  for (int kk = 0; kk < NK; ++kk) {
-    typename M::frag b[NT];
-#pragma unroll
-    for (int j = 0; j < NT; ++j) b[j] = M::load(Bt + (j * 16 + r) * ldb + kk * M::K + kq);
-#pragma unroll
-    for (int i = 0; i < MT; ++i)
-#pragma unroll
-      for (int j = 0; j < NT; ++j) acc[i][j] = M::mma(a[i][kk], b[j], acc[i][j]);
-  }
-}
-
-// Copy a [ROWS][W] tile from LDS (leading dim LD) to global rows (stride rs),
-// 16-byte vectors, rows >= nvalid skipped.
-template <class E, int ROWS, int W, int LD, int NTH>
-__device__ inline void copy_out_rows(E* g, size_t rs, const E* lds, int nvalid) {
-  constexpr int EPV = 16 / sizeof(E);
-  constexpr int VPR = W / EPV;
-  for (int idx = threadIdx.x; idx < ROWS * VPR; idx += NTH) {
-    const int r = idx / VPR, cv = idx - r * VPR;
-    if (r < nvalid)
-      *reinterpret_cast<uint4*>(g + (size_t)r * rs + cv * EPV) =
-          *reinterpret_cast<const uint4*>(lds + r * LD + cv * EPV);
-  }
-}
 
 // ---- permuted contraction order
 // An MFMA sums over its K index in any order, provided both operands agree.
