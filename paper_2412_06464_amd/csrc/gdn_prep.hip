@@ -80,6 +80,53 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
   const E* Q = (const E*)a.q + row0 * DK;
   const E* V = (const E*)a.v + row0 * DV;
 
+  // The chunk's raw k, q and v rows, loaded once at the start and kept in
+  // registers for both the row-major and the transposed staging: lane = row
+  // t, 16-byte vectors cv = w + 4 i of each 64-wide column slice.
+  constexpr int EPV = 16 / sizeof(E), NI = 64 / EPV / 4;
+  constexpr int KS = DK / 64, VS = DV / 64;
+  uint4 rk[KS][NI], rq[KS][NI], rv[VS][NI];
+  {
+    const int t = lane_id();
+    const bool tv = t < len;
+    const size_t ko = (size_t)(tv ? t : 0) * H * DK, vo = (size_t)(tv ? t : 0) * H * DV;
+#pragma unroll
+    for (int sl = 0; sl < KS; ++sl)
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const int c = 64 * sl + (w + 4 * i) * EPV;
+        rk[sl][i] = tv ? *reinterpret_cast<const uint4*>(K + ko + c) : uint4{0u, 0u, 0u, 0u};
+        rq[sl][i] = tv ? *reinterpret_cast<const uint4*>(Q + ko + c) : uint4{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+    for (int sl = 0; sl < VS; ++sl)
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const int c = 64 * sl + (w + 4 * i) * EPV;
+        rv[sl][i] = tv ? *reinterpret_cast<const uint4*>(V + vo + c) : uint4{0u, 0u, 0u, 0u};
+      }
+  }
+  // a slice of raw rows into LDS, row-major (dst[t][c]) or transposed
+  // (dst[c][t], element scaled by scale)
+  auto put_rows = [&](E* dst, const uint4 (&r)[NI]) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+      *reinterpret_cast<uint4*>(dst + lane_id() * LD + (w + 4 * i) * EPV) = r[i];
+  };
+  auto put_T = [&](E* dstT, const uint4 (&r)[NI], float scale) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      union {
+        uint4 u;
+        E e[EPV];
+      } x;
+      x.u = r[i];
+#pragma unroll
+      for (int j = 0; j < EPV; ++j)
+        dstT[((w + 4 * i) * EPV + j) * LD + lane_id()] = to_e<E>(to_f(x.e[j]) * scale);
+    }
+  };
+
   const bool gated = a.gated;
   if (tid < CH) {
     const float b = tid < len ? a.beta[row0 + (size_t)tid * H] : 0.f;
@@ -107,9 +154,10 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
   f32x4 kk[1][4], qk[1][4];
   zero_acc(kk);
   zero_acc(qk);
-  for (int s = 0; s < DK / 64; ++s) {
-    stage_rows<E, CH, 64, LD, 256>(sX, K + 64 * s, (size_t)H * DK, len);
-    stage_rows<E, CH, 64, LD, 256>(sY, Q + 64 * s, (size_t)H * DK, len);
+  static_for<0, KS>([&](auto sc) {
+    constexpr int s = decltype(sc)::value;
+    put_rows(sX, rk[s]);
+    put_rows(sY, rq[s]);
     lds_barrier();
     wave_mma_nt<E, 1, 4, 64>(kk, sX + w * 16 * LD, LD, sX, LD);
     wave_mma_nt<E, 1, 4, 64>(qk, sY + w * 16 * LD, LD, sX, LD);
@@ -124,7 +172,7 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
           (E*)a.Kf + ch * CH * DK, 64 * s, [&](int t, int d) { return to_f(sX[t * LD + d]); });
     }
     lds_barrier();
-  }
+  });
 #pragma unroll
   for (int j = 0; j < 4; ++j)
 #pragma unroll
@@ -208,9 +256,10 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
   }
 
   // ---- dk slices: W~ (and -W~^T), Kbar^T, (e^g Q)^T
-  for (int s = 0; s < DK / 64; ++s) {
-    stage_rows_T<E, 64, LD, 256>(sX, K + 64 * s, (size_t)H * DK, len, nullptr);  // sX[d][t]
-    if (BOUT) stage_rows_T<E, 64, LD, 256>(sY, Q + 64 * s, (size_t)H * DK, len, nullptr);
+  static_for<0, KS>([&](auto sc) {
+    constexpr int s = decltype(sc)::value;
+    put_T(sX, rk[s], 1.f);  // sX[d][t]
+    if (BOUT) put_T(sY, rq[s], 1.f);
     lds_barrier();
     // W~^T (rows d of this wave, columns t'):  sum_t (b e^g K)^T[d][t] T[t'][t]
     f32x4 Wt[4];
@@ -263,11 +312,13 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
                                         [&](int d, int t) { return to_f(sY[d * LD + t]); });
     }
     lds_barrier();
-  }
+  });
 
   // ---- dv slices: U~ = T (b V), accumulator layout
-  for (int s = 0; s < DV / 64; ++s) {
-    stage_rows_T<E, 64, LD, 256>(sX, V + 64 * s, (size_t)H * DV, len, sb);  // sX[v][t] = b_t V
+  const float bt = sb[lane_id()];
+  static_for<0, VS>([&](auto sc) {
+    constexpr int s = decltype(sc)::value;
+    put_T(sX, rv[s], bt);  // sX[v][t] = b_t V
     lds_barrier();
     f32x4 U[1][4];
     zero_acc(U);
@@ -276,7 +327,7 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
 #pragma unroll
     for (int n = 0; n < 4; ++n) store4<E>(gU + cfrag_index(w, 4 * s + n, DV), U[0][n]);
     lds_barrier();
-  }
+  });
 }
 
 // ------------------------------------------------------------------ launchers
