@@ -112,47 +112,6 @@ __device__ inline void wave_mma_nt(f32x4 (&acc)[MT][NT], const E* A, int lda,
 __device__ inline int acc_row(int e) { return ((lane_id() >> 4) << 2) + e; }
 __device__ inline int acc_col() { return lane_id() & 15; }
 
-// Copy rows [0, ROWS) x cols [0, W) of a row-major global tile (row stride
-// `rs` elements) into LDS with leading dimension LD.  Rows >= nvalid are
-// zero-filled.  16-byte vectors; W * sizeof(E) must be a multiple of 16.
-template <class E, int ROWS, int W, int LD, int NTH>
-__device__ inline void stage_rows(E* lds, const E* g, size_t rs, int nvalid) {
-  constexpr int EPV = 16 / sizeof(E);
-  constexpr int VPR = W / EPV;
-  static_assert(W % EPV == 0, "tile width must be a multiple of 16 bytes");
-#pragma unroll 4
-  for (int idx = threadIdx.x; idx < ROWS * VPR; idx += NTH) {
-    const int r = idx / VPR, cv = idx - r * VPR;
-    uint4 val = {0u, 0u, 0u, 0u};
-    if (r < nvalid) val = *reinterpret_cast<const uint4*>(g + (size_t)r * rs + cv * EPV);
-    *reinterpret_cast<uint4*>(lds + r * LD + cv * EPV) = val;
-  }
-}
-
-// Transposed staging of a [64 x W] row-major global tile into LDS
-// dstT[c][t] (leading dimension LDT), multiplying row t by scale[t] (LDS
-// array, may be null).  Rows >= nvalid are zero.  Consecutive lanes take
-// consecutive rows so that the 2-byte LDS scatter is bank-conflict free.
-template <class E, int W, int LDT, int NTH>
-__device__ inline void stage_rows_T(E* dstT, const E* g, size_t rs, int nvalid,
-                                    const float* scale) {
-  constexpr int EPV = 16 / sizeof(E);
-  constexpr int VPR = W / EPV;
-#pragma unroll 2
-  for (int idx = threadIdx.x; idx < CH * VPR; idx += NTH) {
-    const int t = idx & (CH - 1), cv = idx / CH;
-    union {
-      uint4 u;
-      E e[EPV];
-    } val;
-    val.u = uint4{0u, 0u, 0u, 0u};
-    if (t < nvalid) val.u = *reinterpret_cast<const uint4*>(g + (size_t)t * rs + cv * EPV);
-    const float s = scale ? scale[t] : 1.f;
-#pragma unroll
-    for (int j = 0; j < EPV; ++j) dstT[(cv * EPV + j) * LDT + t] = to_e<E>(to_f(val.e[j]) * s);
-  }
-}
-
 // ---- operand layouts in HBM
 // A-fragment layout of an R x KD matrix M (logical row-major): the MFMA A
 // tile (mt, kt) covers rows 16mt.. and k = K*kt..; lane l's KPL elements
