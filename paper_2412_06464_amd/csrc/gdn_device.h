@@ -191,6 +191,19 @@ template <> __device__ inline int kperm<float>(int kt, int g, int) {
   return 16 * (kt >> 2) + 4 * g + (kt & 3);
 }
 
+// Element position, in a 64-column A buffer (permuted order), of element
+// (r, k) of the matrix: fragment (r / 16, kt), lane r % 16 + 16 g, slot j,
+// where kperm(kt, g, j) = k.
+template <class E> __device__ inline int afrag_pos64(int r, int k);
+template <> __device__ inline int afrag_pos64<bf16>(int r, int k) {
+  const int kk = k & 31;
+  return ((((r >> 4) << 1) + (k >> 5)) * 64 + (r & 15) + 16 * ((kk & 15) >> 2)) * 8 +
+         4 * (kk >> 4) + (kk & 3);
+}
+template <> __device__ inline int afrag_pos64<float>(int r, int k) {
+  return ((r >> 4) * 16 + 4 * (k >> 4) + (k & 3)) * 64 + (r & 15) + 16 * ((k & 15) >> 2);
+}
+
 // Fragment buffers.  A "B buffer" holds the B operands of a K x N matrix
 // (N = 16 NT): fragment (kt, nt) of lane l at ((kt NT + nt) 64 + l) KPL.
 // An "A buffer" holds the A operands of an R x KD matrix: fragment (mt, kt)

@@ -65,9 +65,9 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
   __shared__ float sred[NW];
 
   E* ring = (E*)smem;                    // [R][F] fragments, filled by direct copies
-  E* sM1 = (E*)smem;                     // finish: M1 = dP * Gamma, row-major
-  E* sM1T = sM1 + CH * LD;               //         M1^T, row-major
-  E* sDD = sM1T + CH * LD;               //         D + D^T, row-major
+  E* sM1 = (E*)smem;                     // finish: M1 = dP * Gamma, A buffer (permuted order)
+  E* sM1T = sM1 + CH * LD;               //         M1^T, A buffer
+  E* sDD = sM1T + CH * LD;               //         D + D^T, A buffer
   float* sD = (float*)(sDD + CH * LD);   //         D, fp32
   E* sQst = (E*)(smem + FIN_BYTES) + (size_t)2 * wave_id() * CH * LDQ;  // this wave's dq rows
   E* sKst = sQst + CH * LDQ;                                             //           dk rows
@@ -243,8 +243,8 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
         if (m == 0) {
           const float dp = (i <= r) ? PA[p][e] : 0.f;
           const float m1 = dp * gam;
-          sM1[r * LD + i] = to_e<E>(m1);
-          sM1T[i * LD + r] = to_e<E>(m1);
+          sM1[afrag_pos64<E>(r, i)] = to_e<E>(m1);
+          sM1T[afrag_pos64<E>(i, r)] = to_e<E>(m1);
           ev = dp * side[p][e];
           dba[e] = 0.f;
         } else {
@@ -298,7 +298,7 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
   lds_barrier();
   for (int idx = tid; idx < CH * CH; idx += NTH) {
     const int r = idx >> 6, i = idx & 63;
-    sDD[r * LD + i] = to_e<E>(sD[r * LDF + i] + sD[i * LDF + r]);
+    sDD[afrag_pos64<E>(r, i)] = to_e<E>(sD[r * LDF + i] + sD[i * LDF + r]);
   }
   lds_barrier();
 
@@ -352,26 +352,10 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
           dq[e] *= __expf(sg[r]);
           dk[e] = __expf(sg[CH - 1] - sg[r]) * Gs[i][n][e] - sb[r] * __expf(sg[r]) * Gk[i][n][e];
         }
-        const E* m1row = sM1 + (i * 16 + (l & 15)) * LD;
-        const E* m1trow = sM1T + (i * 16 + (l & 15)) * LD;
-        const E* ddrow = sDD + (i * 16 + (l & 15)) * LD;
 #pragma unroll
         for (int kt = 0; kt < NKC; ++kt) {
-          frag am, amt, add;
-          union {
-            frag f;
-            E x[M::KPL];
-          } u0, u1, u2;
-#pragma unroll
-          for (int j = 0; j < M::KPL; ++j) {
-            const int k = kperm<E>(kt, g4, j);
-            u0.x[j] = m1row[k];
-            u1.x[j] = m1trow[k];
-            u2.x[j] = ddrow[k];
-          }
-          am = u0.f;
-          amt = u1.f;
-          add = u2.f;
+          const int fo = ((i * NKC + kt) * 64 + l) * M::KPL;
+          const frag am = M::load(sM1 + fo), amt = M::load(sM1T + fo), add = M::load(sDD + fo);
           dq = M::mma(am, fk[kt], dq);
           dk = M::mma(amt, fq[kt], dk);
           dk = M::mma(add, fk[kt], dk);
