@@ -304,45 +304,49 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
 
   // (2) dQ and dK for this wave's dk columns
   {
+    // row dots over the wave's dk columns: element e of row tile i pairs
+    // with slot (i & 1) * 4 + e of k-step i >> 1 (bf16) or k-step 4 i + e
+    // (fp32) of the K^T / Q^T fragments; summed over the wave's tiles, then
+    // over each tile's 16 columns
 #pragma unroll
-    for (int n = 0; n < NDT; ++n) {
-      const int dt = w * NDT + n;
-      const frag(&fk)[NKC] = fkp[n];
-      const frag(&fq)[NKC] = fqp[n];
-      // row dots with the raw accumulators: element e of row tile i pairs with
-      // slot (i & 1) * 4 + e of k-step i >> 1 (bf16) or k-step 4 i + e (fp32)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int e = 0; e < 4; ++e) {
+        float s0 = 0.f, s1 = 0.f, s2 = 0.f;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
+        for (int n = 0; n < NDT; ++n) {
           union {
             frag f;
             E x[M::KPL];
           } uk, uq;
           float kv, qv;
           if (sizeof(E) == 2) {
-            uk.f = fk[i >> 1];
-            uq.f = fq[i >> 1];
+            uk.f = fkp[n][i >> 1];
+            uq.f = fqp[n][i >> 1];
             kv = to_f(uk.x[(i & 1) * 4 + e]);
             qv = to_f(uq.x[(i & 1) * 4 + e]);
           } else {
-            uk.f = fk[(4 * i + e) % NKC];
-            uq.f = fq[(4 * i + e) % NKC];
+            uk.f = fkp[n][(4 * i + e) % NKC];
+            uq.f = fqp[n][(4 * i + e) % NKC];
             kv = to_f(uk.x[0]);
             qv = to_f(uq.x[0]);
           }
-          // this tile's share of the row dots, summed over its 16 columns and
-          // folded into the wave's slot (same lane, in program order)
-          const float a0 = reduce16(qv * Gq[i][n][e]);
-          const float a1 = reduce16(kv * Gk[i][n][e]);
-          const float a2 = reduce16(kv * Gs[i][n][e]);
-          if (acc_col() == 0) {
-            const int r = i * 16 + acc_row(e);
-            srow[w][0][r] = (n == 0 ? 0.f : srow[w][0][r]) + a0;
-            srow[w][1][r] = (n == 0 ? 0.f : srow[w][1][r]) + a1;
-            srow[w][2][r] = (n == 0 ? 0.f : srow[w][2][r]) + a2;
-          }
+          s0 += qv * Gq[i][n][e];
+          s1 += kv * Gk[i][n][e];
+          s2 += kv * Gs[i][n][e];
         }
+        const float a0 = reduce16(s0), a1 = reduce16(s1), a2 = reduce16(s2);
+        if (acc_col() == 0) {
+          const int r = i * 16 + acc_row(e);
+          srow[w][0][r] = a0;
+          srow[w][1][r] = a1;
+          srow[w][2][r] = a2;
+        }
+      }
+#pragma unroll
+    for (int n = 0; n < NDT; ++n) {
+      const frag(&fk)[NKC] = fkp[n];
+      const frag(&fq)[NKC] = fqp[n];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         f32x4 dq = Gq[i][n], dk;
