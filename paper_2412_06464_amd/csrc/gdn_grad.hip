@@ -229,16 +229,28 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
   lds_barrier();  // every wave is done with the ring before its LDS is reused
 
   // ---- finish phase (the staging ring is dead; its LDS is reused)
-  // (1) the [dO; dX] V'^T tiles: M1, D, and the parts of E and dbeta
+  // (1) the [dO; dX] V'^T tiles: M1, D, and the parts of E and dbeta.  A
+  // wave's tiles come in runs of 4 that cover one (m, rt) row block, so its
+  // row sums stay in registers over the run and are reduced once.
   {
+    static_assert(PAT % 4 == 0, "a wave's tiles must cover whole row blocks");
+    float racc[4], dacc[4], sgr[4];
 #pragma unroll
     for (int p = 0; p < PAT; ++p) {
       const int q = w * PAT + p, m = q >> 4, rt = (q >> 2) & 3, ct = q & 3;
-      float rsum[4], csum = 0.f, dba[4];
+      if ((p & 3) == 0) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          racc[e] = dacc[e] = 0.f;
+          sgr[e] = sg[rt * 16 + acc_row(e)];
+        }
+      }
+      const float sgi = sg[ct * 16 + acc_col()];
+      float csum = 0.f;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int r = rt * 16 + acc_row(e), i = ct * 16 + acc_col();
-        const float gam = (i <= r) ? __expf(sg[r] - sg[i]) : 0.f;
+        const float gam = (i <= r) ? __expf(sgr[e] - sgi) : 0.f;
         float ev;
         if (m == 0) {
           const float dp = (i <= r) ? PA[p][e] : 0.f;
@@ -246,40 +258,32 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
           sM1[afrag_pos64<E>(r, i)] = to_e<E>(m1);
           sM1T[afrag_pos64<E>(i, r)] = to_e<E>(m1);
           ev = dp * side[p][e];
-          dba[e] = 0.f;
         } else {
           const float da = (i < r) ? -PA[p][e] : 0.f;
           sD[r * LDF + i] = sb[r] * da * gam;
           ev = da * sb[r] * side[p][e];
-          dba[e] = da * side[p][e];
+          dacc[e] += da * side[p][e];
         }
-        rsum[e] = ev;
+        racc[e] += ev;
         csum += ev;
       }
-      // row sums over the 16 columns of the tile, column sums over its 16 rows
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        rsum[e] = reduce16(rsum[e]);
-        dba[e] = reduce16(dba[e]);
-      }
+      // column sums over the tile's 16 rows
       csum += __shfl_xor(csum, 16, 64);
       csum += __shfl_xor(csum, 32, 64);
-      // each (m, rt) row block is spread over 4 column tiles held by one wave:
-      // accumulate in registers across p, publish once per row block
-      if (acc_col() == 0) {
+      if (l < 16) sEcol[m * 4 + rt][ct * 16 + l] = csum;
+      // row sums over the run's 64 columns
+      if ((p & 3) == 3) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const int r = rt * 16 + acc_row(e);
-          if (ct == 0) {
-            sErow[m][r] = rsum[e];
-            if (m) sdbA[r] = dba[e];
-          } else {
-            sErow[m][r] += rsum[e];
-            if (m) sdbA[r] += dba[e];
+          const float rs = reduce16(racc[e]);
+          const float db = m ? reduce16(dacc[e]) : 0.f;
+          if (acc_col() == 0) {
+            const int r = rt * 16 + acc_row(e);
+            sErow[m][r] = rs;
+            if (m) sdbA[r] = db;
           }
         }
       }
-      if (l < 16) sEcol[m * 4 + rt][ct * 16 + l] = csum;
     }
   }
   // partial row dots over this wave's columns, and <dS, S>
