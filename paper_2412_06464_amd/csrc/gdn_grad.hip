@@ -51,15 +51,14 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
   constexpr int RING_BYTES = R * F * FR * (int)sizeof(E);
   constexpr int PADE = 16 / sizeof(E);
   constexpr int LD = CH + PADE;
-  constexpr int LDF = CH + 1;
   constexpr int NKC = CH / M::K;
-  constexpr int FIN_BYTES = 3 * CH * LD * (int)sizeof(E) + CH * LDF * 4;
+  constexpr int FIN_BYTES = 4 * CH * LD * (int)sizeof(E);
   constexpr int LDQ = NDT * 16 + PADE;   // row stride of a wave's dq / dk staging
   constexpr int STG_BYTES = 2 * NW * CH * LDQ * (int)sizeof(E);
   constexpr int FIN_ALL = FIN_BYTES + STG_BYTES;
   constexpr int SMEM = RING_BYTES > FIN_ALL ? RING_BYTES : FIN_ALL;
   __shared__ __align__(16) unsigned char smem[SMEM];
-  __shared__ float sg[CH], sb[CH];
+  __shared__ float sg[CH], sb[CH], seg[CH], sdec[CH];
   __shared__ float sdbA[CH], sxv[CH], sErow[2][CH], sEcol[2 * 4][CH];
   __shared__ float srow[NW][3][CH];
   __shared__ float sred[NW];
@@ -67,8 +66,8 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
   E* ring = (E*)smem;                    // [R][F] fragments, filled by direct copies
   E* sM1 = (E*)smem;                     // finish: M1 = dP * Gamma, A buffer (permuted order)
   E* sM1T = sM1 + CH * LD;               //         M1^T, A buffer
-  E* sDD = sM1T + CH * LD;               //         D + D^T, A buffer
-  float* sD = (float*)(sDD + CH * LD);   //         D, fp32
+  E* sDA = sM1T + CH * LD;               //         D, A buffer
+  E* sDT = sDA + CH * LD;                //         D^T, A buffer
   E* sQst = (E*)(smem + FIN_BYTES) + (size_t)2 * wave_id() * CH * LDQ;  // this wave's dq rows
   E* sKst = sQst + CH * LDQ;                                             //           dk rows
 
@@ -88,8 +87,11 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
 
   // alpha == 1 (DeltaNet): g = 0 and every decay factor is exp(0) = 1
   // exactly; the finish phase keeps one code path for both
-  if (tid < CH) {
-    sg[tid] = a.gated ? a.g[ch * CH + tid] : 0.f;
+  if (tid < CH) {  // wave 0
+    const float g = a.gated ? a.g[ch * CH + tid] : 0.f;
+    sg[tid] = g;
+    seg[tid] = __expf(g);
+    sdec[tid] = __expf(__shfl(g, CH - 1, 64) - g);
     sb[tid] = tid < len ? a.beta[row0 + (size_t)tid * H] : 0.f;
   }
 
@@ -260,7 +262,9 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
           ev = dp * side[p][e];
         } else {
           const float da = (i < r) ? -PA[p][e] : 0.f;
-          sD[r * LDF + i] = sb[r] * da * gam;
+          const float dd = sb[r] * da * gam;
+          sDA[afrag_pos64<E>(r, i)] = to_e<E>(dd);
+          sDT[afrag_pos64<E>(i, r)] = to_e<E>(dd);
           ev = da * sb[r] * side[p][e];
           dacc[e] += da * side[p][e];
         }
@@ -298,11 +302,6 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
       x += __shfl_xor(x, 32, 64);
       if (l < 16) sxv[w * 16 + l] = x;
     }
-  }
-  lds_barrier();
-  for (int idx = tid; idx < CH * CH; idx += NTH) {
-    const int r = idx >> 6, i = idx & 63;
-    sDD[afrag_pos64<E>(r, i)] = to_e<E>(sD[r * LDF + i] + sD[i * LDF + r]);
   }
   lds_barrier();
 
@@ -357,16 +356,18 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int r = i * 16 + acc_row(e);
-          dq[e] *= __expf(sg[r]);
-          dk[e] = __expf(sg[CH - 1] - sg[r]) * Gs[i][n][e] - sb[r] * __expf(sg[r]) * Gk[i][n][e];
+          dq[e] *= seg[r];
+          dk[e] = sdec[r] * Gs[i][n][e] - sb[r] * seg[r] * Gk[i][n][e];
         }
 #pragma unroll
         for (int kt = 0; kt < NKC; ++kt) {
           const int fo = ((i * NKC + kt) * 64 + l) * M::KPL;
-          const frag am = M::load(sM1 + fo), amt = M::load(sM1T + fo), add = M::load(sDD + fo);
+          const frag am = M::load(sM1 + fo), amt = M::load(sM1T + fo);
+          const frag ad = M::load(sDA + fo), adt = M::load(sDT + fo);
           dq = M::mma(am, fk[kt], dq);
           dk = M::mma(amt, fq[kt], dk);
-          dk = M::mma(add, fk[kt], dk);
+          dk = M::mma(ad, fk[kt], dk);
+          dk = M::mma(adt, fk[kt], dk);
         }
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
