@@ -48,6 +48,34 @@ __global__ void k_chunk_table(const int32_t* cu, int N, int T, int4* info, int* 
 }
 
 // ------------------------------------------------------------------ prep
+
+// A buffers (permuted order) of a 64 x 64 LDS matrix src[r * ld + k]: the raw
+// values into dst_raw (skipped when null) and the values times scale[k] into
+// dst_scaled, from one LDS read per element.
+template <class E, int NTH>
+__device__ inline void export_afrag_perm_pair(E* dst_raw, E* dst_scaled, const E* src, int ld,
+                                              const float* scale) {
+  using M = Mfma<E>;
+  constexpr int NKT = CH / M::K, UNITS = CH * CH / M::KPL;
+  for (int u = threadIdx.x; u < UNITS; u += NTH) {
+    const int tile = u >> 6, l = u & 63;
+    const int mt = tile / NKT, kt = tile - mt * NKT;
+    const int r = mt * 16 + (l & 15), g = l >> 4;
+    union {
+      typename M::frag f;
+      E e[M::KPL];
+    } xr, xs;
+#pragma unroll
+    for (int j = 0; j < M::KPL; ++j) {
+      const int k = kperm<E>(kt, g, j);
+      const E x = src[r * ld + k];
+      xr.e[j] = x;
+      xs.e[j] = to_e<E>(to_f(x) * scale[k]);
+    }
+    if (dst_raw) store_stream_small(dst_raw + (size_t)u * M::KPL, xr.f);
+    store_stream_small(dst_scaled + (size_t)u * M::KPL, xs.f);
+  }
+}
 // Grid (NC, H), 256 threads (4 waves).  LDS stays below 80 KB for bf16 so
 // that two workgroups share a CU: one streams while the other solves.
 
@@ -279,9 +307,9 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
     // W~ as A operands (rows t', k = d) for the state passes
 #pragma unroll
     for (int n = 0; n < 4; ++n) afrag_put_T<E>((E*)a.Wf + ch * CH * DK, DK, n, 4 * s + w, Wt[n]);
-    // Kbar^T as A operands (rows d, k = t)
-    export_afrag_perm<E, 64, CH, 256>((E*)a.KbT + ch * DK * CH + (size_t)64 * s * CH,
-                                      [&](int d, int t) { return sdec[t] * to_f(sX[d * LD + t]); });
+    // Kbar^T as A operands (rows d, k = t), with raw K^T for the gradient kernel
+    export_afrag_perm_pair<E, 256>(BOUT ? (E*)a.KTf + ch * DK * CH + (size_t)64 * s * CH : nullptr,
+                                   (E*)a.KbT + ch * DK * CH + (size_t)64 * s * CH, sX, LD, sdec);
     if (BOUT) {
       // W~ (rows t' of this wave, columns d):  sum_t T[t'][t] (b e^g K)[t][d]
       f32x4 W[4];
@@ -302,14 +330,9 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
       // -W~^T as A operands (rows d, k = t')
 #pragma unroll
       for (int n = 0; n < 4; ++n) afrag_put_T<E>((E*)a.nWT + ch * DK * CH, CH, 4 * s + n, w, -W[n]);
-      // (e^g Q)^T as A operands (rows d, k = t)
-      export_afrag_perm<E, 64, CH, 256>((E*)a.QgT + ch * DK * CH + (size_t)64 * s * CH,
-                                        [&](int d, int t) { return seg[t] * to_f(sY[d * LD + t]); });
-      // raw K^T and Q^T as A operands (rows d, k = t) for the gradient kernel
-      export_afrag_perm<E, 64, CH, 256>((E*)a.KTf + ch * DK * CH + (size_t)64 * s * CH,
-                                        [&](int d, int t) { return to_f(sX[d * LD + t]); });
-      export_afrag_perm<E, 64, CH, 256>((E*)a.QTf + ch * DK * CH + (size_t)64 * s * CH,
-                                        [&](int d, int t) { return to_f(sY[d * LD + t]); });
+      // (e^g Q)^T as A operands (rows d, k = t), with raw Q^T for the gradient kernel
+      export_afrag_perm_pair<E, 256>((E*)a.QTf + ch * DK * CH + (size_t)64 * s * CH,
+                                     (E*)a.QgT + ch * DK * CH + (size_t)64 * s * CH, sY, LD, seg);
     }
     lds_barrier();
   });
