@@ -95,7 +95,7 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
   __shared__ __align__(16) E sP[CH * LD];  // P, row-major
   __shared__ float sA[CH * LDA];           // diag(b) A
   __shared__ float sTf[CH * LDA];          // T in fp32
-  __shared__ float sYb[3 * 16 * 17];
+  __shared__ float sYb[32 * 33];         // products of the block recursion
   __shared__ float sg[CH], sb[CH], seg[CH], sdec[CH], sbeg[CH];
 
   const int c = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = wave_id();
@@ -225,10 +225,12 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
   }
   lds_barrier();
 
-  // ---- T = (I + A)^-1, A strictly lower.  Diagonal 16x16 blocks by forward
-  // substitution (one column per thread), then the off-diagonal blocks in
-  // order of their distance from the diagonal:
-  //   T_IJ = -T_II * sum_{m=J}^{I-1} A_Im T_mJ.
+  // ---- T = (I + A)^-1, A strictly lower, by block recursion.  The 16x16
+  // diagonal blocks by forward substitution (one column per thread); then,
+  // with fp32 MFMA, the off-diagonal block of each 32x32 diagonal block and
+  // finally the lower-left 32x32 block, each as
+  //   T_21 = -T_22 (A_21 T_11)
+  // for a block lower-triangular [[T_11, 0], [T_21, T_22]].
   if (tid < CH) {
     const int blk = tid >> 4, j = tid & 15, o = blk * 16;
     float x[16];
@@ -243,28 +245,43 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
     for (int i = 0; i < 16; ++i) sTf[(o + i) * LDA + o + j] = x[i];
   }
   lds_barrier();
-  for (int d = 1; d < 4; ++d) {
-    const int i = tid >> 4, j = tid & 15;
-    for (int J = 0; J + d < 4; ++J) {
-      const int I = J + d;
-      float y = 0.f;
-      for (int m = J; m < I; ++m)
+  {
+    using MF = Mfma<float>;
+    const int lr = lane_id() & 15, lg = lane_id() >> 4;
+    // 16 x 16 x 16 product tile: acc += X[xr.., xc..] Y[yr.., yc..] (fp32 LDS, leading dims)
+    auto mm16 = [&](f32x4& acc, const float* X, int ldx, int xr, int xc, const float* Y, int ldy,
+                    int yr, int yc) {
 #pragma unroll
-        for (int l = 0; l < 16; ++l)
-          y += sA[(16 * I + i) * LDA + 16 * m + l] * sTf[(16 * m + l) * LDA + 16 * J + j];
-      sYb[J * 272 + i * 17 + j] = y;
+      for (int ks = 0; ks < 4; ++ks)
+        acc = MF::mma(X[(xr + lr) * ldx + xc + 4 * ks + lg], Y[(yr + 4 * ks + lg) * ldy + yc + lr], acc);
+    };
+    // 32x32 diagonal blocks (waves 0 and 1): T[o+16.., o..] = -T[o+16.., o+16..] (A[o+16.., o..] T[o.., o..])
+    if (w < 2) {
+      const int o = 32 * w;
+      float* yb = sYb + w * 16 * 17;
+      f32x4 y = {0.f, 0.f, 0.f, 0.f}, z = {0.f, 0.f, 0.f, 0.f};
+      mm16(y, sA, LDA, o + 16, o, sTf, LDA, o, o);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) yb[(4 * lg + e) * 17 + lr] = y[e];  // read back by this wave only
+      mm16(z, sTf, LDA, o + 16, o + 16, yb, 17, 0, 0);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sTf[(o + 16 + 4 * lg + e) * LDA + o + lr] = -z[e];
     }
     lds_barrier();
-    for (int J = 0; J + d < 4; ++J) {
-      const int I = J + d;
-      float t = 0.f;
+    // lower-left 32x32 block, one 16x16 tile (I, J) per wave:
+    //   Y = A[32.., 0..32] T[0..32, 0..32]  (T lower: k-blocks K >= J)
+    //   T[32 + 16 I.., 16 J..] = -sum_{K <= I} T[32 + 16 I.., 32 + 16 K..] Y[16 K.., 16 J..]
+    const int I = w >> 1, J = w & 1;
+    f32x4 y = {0.f, 0.f, 0.f, 0.f}, z = {0.f, 0.f, 0.f, 0.f};
+    for (int K = J; K < 2; ++K) mm16(y, sA, LDA, 32 + 16 * I, 16 * K, sTf, LDA, 16 * K, 16 * J);
 #pragma unroll
-      for (int l = 0; l < 16; ++l)
-        t -= sTf[(16 * I + i) * LDA + 16 * I + l] * sYb[J * 272 + l * 17 + j];
-      sTf[(16 * I + i) * LDA + 16 * J + j] = t;
-    }
+    for (int e = 0; e < 4; ++e) sYb[(16 * I + 4 * lg + e) * 33 + 16 * J + lr] = y[e];
     lds_barrier();
+    for (int K = 0; K <= I; ++K) mm16(z, sTf, LDA, 32 + 16 * I, 32 + 16 * K, sYb, 33, 16 * K, 16 * J);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sTf[(32 + 16 * I + 4 * lg + e) * LDA + 16 * J + lr] = -z[e];
   }
+  lds_barrier();
   for (int idx = tid; idx < CH * CH; idx += 256) {
     const int r = idx >> 6, i = idx & 63;
     sT[r * LD + i] = to_e<E>(((i >> 4) > (r >> 4)) ? 0.f : sTf[r * LDA + i]);
