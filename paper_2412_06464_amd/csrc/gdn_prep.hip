@@ -16,9 +16,10 @@
 // does not reproduce the recurrence.
 //
 //   k_chunk_table  chunk -> (sequence, first row, length)
-//   k_prep         one workgroup per (chunk, head): g, Gram matrices, T in
-//                  LDS, then the operands of the sequential passes, streamed
-//                  over 64-wide slices of dk and dv.  Forward: W~, Kbar^T, U~,
+//   k_prep         one workgroup per (chunk, head): the chunk's q, k, v rows
+//                  loaded once into registers, g, Gram matrices, T in LDS,
+//                  then the operands of the sequential passes, staged through
+//                  LDS in 64-wide slices of dk and dv.  Forward: W~, Kbar^T, U~,
 //                  P, diag(e^g) Q.  Backward (recompute): W~, Kbar^T, U~, and
 //                  for the reverse pass K, P^T, T^T, -W~^T, (e^g Q)^T, plus
 //                  K^T, Q^T, and P and strictLower(Gamma K K^T) in fp32 for
