@@ -25,6 +25,21 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int CH = 64;  // chunk length in tokens
 
+// Chunk c's {sequence, first token row, length}, and the first chunk of
+// sequence n.  Dense input (no cu_seqlens): B sequences of T tokens, each cut
+// into ceil(T / CH) consecutive chunks, so both are arithmetic; packed input
+// reads the chunk table.  (A is the kernels' argument struct.)
+template <class A>
+__device__ inline int4 chunk_info(const A& a, int c) {
+  if (a.cu) return a.info[c];
+  const int nch = (a.T + CH - 1) / CH, n = c / nch, j = c - n * nch;
+  return make_int4(n, n * a.T + j * CH, min(CH, a.T - j * CH), 0);
+}
+template <class A>
+__device__ inline int seq_first_chunk(const A& a, int n) {
+  return a.cu ? a.seq_chunk0[n] : n * ((a.T + CH - 1) / CH);
+}
+
 template <class E> struct Mfma;
 
 template <> struct Mfma<bf16> {

@@ -74,7 +74,7 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
   const int c = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, l = lane_id(), g4 = l >> 4;
   const int w = __builtin_amdgcn_readfirstlane(wave_id());
   const int H = a.H;
-  const int4 ci = a.info[c];
+  const int4 ci = chunk_info(a, c);
   const int start = ci.y, len = ci.z;
   const size_t ch = (size_t)c * H + h;
   const size_t row0 = (size_t)start * H + h;

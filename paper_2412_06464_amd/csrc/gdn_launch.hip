@@ -26,7 +26,9 @@ hipError_t timed(Timing* t, const char* name, hipStream_t s, F&& launch) {
 
 hipError_t launch_fwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t) {
   hipError_t e;
-  if ((e = timed(t, "k_chunk_table", s, [&] { return launch_chunk_table(a, s); })) != hipSuccess)
+  // the chunk table serves packed input only; dense chunks are arithmetic
+  if (a.cu && (e = timed(t, "k_chunk_table", s, [&] { return launch_chunk_table(a, s); })) !=
+                  hipSuccess)
     return e;
   if ((e = timed(t, "k_prep", s, [&] { return launch_prep(dt, dk, dv, PREP_FWD, a, s); })) !=
       hipSuccess)
@@ -36,7 +38,9 @@ hipError_t launch_fwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timin
 
 hipError_t launch_bwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t) {
   hipError_t e;
-  if ((e = timed(t, "k_chunk_table", s, [&] { return launch_chunk_table(a, s); })) != hipSuccess)
+  // the chunk table serves packed input only; dense chunks are arithmetic
+  if (a.cu && (e = timed(t, "k_chunk_table", s, [&] { return launch_chunk_table(a, s); })) !=
+                  hipSuccess)
     return e;
   if ((e = timed(t, "k_prep", s, [&] { return launch_prep(dt, dk, dv, PREP_BWD, a, s); })) !=
       hipSuccess)
@@ -54,7 +58,9 @@ hipError_t launch_bwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timin
 // sets and the state pass stores chunk states and V' beside O.
 hipError_t launch_fwd_save(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t) {
   hipError_t e;
-  if ((e = timed(t, "k_chunk_table", s, [&] { return launch_chunk_table(a, s); })) != hipSuccess)
+  // the chunk table serves packed input only; dense chunks are arithmetic
+  if (a.cu && (e = timed(t, "k_chunk_table", s, [&] { return launch_chunk_table(a, s); })) !=
+                  hipSuccess)
     return e;
   if ((e = timed(t, "k_prep_save", s, [&] { return launch_prep(dt, dk, dv, PREP_SAVE, a, s); })) !=
       hipSuccess)
@@ -66,7 +72,9 @@ hipError_t launch_fwd_save(Dt dt, int dk, int dv, const Args& a, hipStream_t s, 
 // Backward from a saving forward's buffer: no prep, no recompute.
 hipError_t launch_bwd_saved(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t) {
   hipError_t e;
-  if ((e = timed(t, "k_chunk_table", s, [&] { return launch_chunk_table(a, s); })) != hipSuccess)
+  // the chunk table serves packed input only; dense chunks are arithmetic
+  if (a.cu && (e = timed(t, "k_chunk_table", s, [&] { return launch_chunk_table(a, s); })) !=
+                  hipSuccess)
     return e;
   if ((e = timed(t, "k_bwd_seq", s, [&] { return launch_bwd_seq(dt, dk, dv, a, s); })) !=
       hipSuccess)

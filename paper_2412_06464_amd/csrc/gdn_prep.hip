@@ -101,7 +101,7 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
 
   const int c = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = wave_id();
   const int H = a.H;
-  const int4 ci = a.info[c];
+  const int4 ci = chunk_info(a, c);
   const int start = ci.y, len = ci.z;
   const size_t ch = (size_t)c * H + h;
   const size_t row0 = (size_t)start * H + h;

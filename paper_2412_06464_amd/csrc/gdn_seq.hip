@@ -99,7 +99,7 @@ __global__ __launch_bounds__(256, (MODE == SEQ_SAVE ? GDN_SAVE_MINB : GDN_SEQ_MI
   // the sequence: first token, length, first chunk (no per-chunk table loads)
   const int s0 = a.cu ? a.cu[n] : n * a.T;
   const int L = a.cu ? a.cu[n + 1] - s0 : a.T;
-  const int c0 = a.seq_chunk0[n], nch = (L + CH - 1) / CH;
+  const int c0 = seq_first_chunk(a, n), nch = (L + CH - 1) / CH;
 
   f32x4 S[MTS][NTV];
   const size_t sbase = ((size_t)n * H + h) * DK * DV;
@@ -360,7 +360,7 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
   const unsigned lo = (unsigned)(l * M::KPL);      // lane offset inside a fragment
   const int s0 = a.cu ? a.cu[n] : n * a.T;
   const int L = a.cu ? a.cu[n + 1] - s0 : a.T;
-  const int c0 = a.seq_chunk0[n], nch = (L + CH - 1) / CH;
+  const int c0 = seq_first_chunk(a, n), nch = (L + CH - 1) / CH;
 
   f32x4 dS[MTS][NTV];
   const size_t sbase = ((size_t)n * H + h) * DK * DV;
