@@ -268,6 +268,32 @@ def test_saved_packed(G, oracle_mod, dtype, dk, dv):
 
 
 @pytest.mark.parametrize("dtype,dk,dv", [("f32", 64, 64), ("bf16", 256, 512)])
+def test_dense_equals_packed(G, dtype, dk, dv):
+    """Dense input locates its chunks arithmetically, packed input through the
+    chunk table: the same two sequences given either way give the same bits,
+    in both backward paths."""
+    B, T, H = 2, 150, 2
+    d = to_dev(make_inputs(B, T, H, dk, dv, dtype, seed=16, h0_std=0.05, backward=True))
+    p = dict(d)
+    for key in ("q", "k", "v", "beta", "log_alpha", "dO"):
+        p[key] = d[key].reshape(1, B * T, *d[key].shape[2:]).contiguous()
+    p["cu_seqlens"] = torch.tensor([0, T, 2 * T], dtype=torch.int32, device="cuda")
+    say("dense_vs_packed", dtype, dk, dv)
+    out = {}
+    for name, x in (("dense", d), ("packed", p)):
+        o, ht = run_fwd(G, x)
+        r = run_bwd(G, x)
+        o2, ht2, r2 = run_saved(G, x)
+        out[name] = dict(o=o.reshape(B * T, -1), ht=ht, o2=o2.reshape(B * T, -1), ht2=ht2,
+                         **{k: v.reshape(-1) for k, v in r.items()},
+                         **{k + "_s": v.reshape(-1) for k, v in r2.items()})
+    diff = {k: float((out["dense"][k].float() - out["packed"][k].float()).abs().max())
+            for k in out["dense"]}
+    say("dense_vs_packed max |diff|", diff)
+    assert all(v == 0.0 for v in diff.values()), diff
+
+
+@pytest.mark.parametrize("dtype,dk,dv", [("f32", 64, 64), ("bf16", 256, 512)])
 def test_saved_equals_stateless(G, dtype, dk, dv):
     """Both backward paths evaluate the same expressions in the same order, so
     their results agree bit for bit, and so do the two forwards."""
