@@ -166,12 +166,15 @@ size_t carve(const gdn_problem* p, const Shape& s, Use u, unsigned char* base, A
     if (a) a->g = (float*)g;
   }
   if (u == Use::Bwd) carve_saved(p, s, c, a);
-  if (u == Use::Bwd || u == Use::BwdSaved) {  // the reverse pass's chunk states and dX
+  if (u == Use::Bwd || u == Use::BwdSaved) {  // the reverse pass's chunk states and dX,
+    // and the gradient kernel's partial sums
     unsigned char* dSc = c.take(z.st);
     unsigned char* dXb = c.take(z.vside);
+    unsigned char* gp = c.take((size_t)s.NC * p->H * gdn::GRAD_PART_FLOATS * sizeof(float));
     if (a) {
       a->dSc = dSc;
       a->dXb = dXb;
+      a->gpart = (float*)gp;
     }
   }
   return c.off;

@@ -15,48 +15,74 @@
 //          (+ sum_r e^{g_n-g_r} k_r.Gs_r + e^{g_n} <dS, S> on the last token)
 //   dlog_alpha = reverse cumulative sum of dg inside the chunk.
 //
-// One workgroup per (chunk, head).  Streaming phase over dv, one MFMA k-step
-// (32 columns) at a time: every operand of the step (dO, dX, V', V rows and
-// the S, dS fragments, the bulk of the bytes) is copied HBM -> LDS by
-// direct-to-LDS loads into a ring a few k-steps deep; each wave then owns a
-// set of dk columns (B operands) and reads the shared A operands.  Finish
-// phase: the 64 x 64 intra-chunk matrices go through LDS, and K^T / Q^T come
-// as ready-made fragments from the prep kernel.
+// One workgroup per (chunk, head), or two at dk = 128, each owning one half
+// of the dk columns.  Streaming phase over dv, one MFMA k-step (32 columns)
+// at a time: every operand of the step (dO, dX, V', V rows and the S, dS
+// fragments of the workgroup's dk columns, the bulk of the bytes) is copied
+// HBM -> LDS by direct-to-LDS loads into a ring of k-steps; each wave then
+// owns a set of dk columns (B operands) and reads the shared A operands.
+// Finish phase: the 64 x 64 intra-chunk matrices go through LDS, and K^T /
+// Q^T come as ready-made fragments from the prep kernel.  At dk <= 128 a
+// bf16 workgroup needs under 80 KB of LDS and 256 registers per lane, so two
+// share a CU and one's finish phase (no HBM reads) overlaps the other's
+// streaming.  The halves of a split chunk-head both form the dv-side
+// products ([dO; dX] V'^T, dX . V) in full.  The row sums over dk and
+// <dS, S> are written as partial sums per workgroup, which k_grad_gates adds
+// in a fixed order before the gate-gradient scan.
 #include "gdn_device.h"
 #include "gdn_kernels.h"
 
 namespace gdn {
 
+// Workgroups per (chunk, head): two at dk = 128, where the finish phase is a
+// large share of a workgroup's time and overlapping it with the other
+// workgroup's streaming pays for the second read of the dv-side operands
+// (packed dk = dv = 128: 1.08 against 1.20 ms); one at dk = 256, where the
+// two measured the same, and at dk = 64.
 template <class E, int DK>
 struct GradCfg {
-  static constexpr int NW = DK == 64 ? 4 : 8;  // waves
+  static constexpr int HV = DK == 128 ? 2 : 1;
+  static constexpr int NW = (HV == 1 && DK > 64) ? 8 : 4;  // waves
   static constexpr int NTH = 64 * NW;
-  static constexpr int NDT = DK / 16 / NW;     // dk column tiles per wave
-  static constexpr int PAT = 32 / NW;          // tiles of [dO; dX] V'^T per wave
+  static constexpr int NDH = DK / HV / 16;  // dk column tiles of a workgroup
+  static constexpr int NDT = NDH / NW;      // dk column tiles per wave
+  static constexpr int PAT = 32 / NW;       // tiles of [dO; dX] V'^T per wave
+  static constexpr int R = sizeof(E) == 4 ? 4 : 3;  // ring depth in k-steps
 };
 
+// Partial sums a gradient workgroup hands to k_grad_gates (Args::gpart), per
+// chunk-head, in blocks of CH floats: the row dots q.Gq, k.Gk, k.Gs over the
+// dk columns of half 0 (blocks 0-2) and half 1 (3-5); from half 0 the
+// dv-side row terms: E row sums for P and A (6, 7), E column sums (8),
+// sum_i dA Ak (9) and dX . V (10); <dS, S> of half h at block 11, element h.
+constexpr int GP_FLOATS = GRAD_PART_FLOATS;
+static_assert(GP_FLOATS == 12 * CH, "partial-sum blocks");
+
 template <class E, int DK, int DV>
-__global__ __launch_bounds__(512) void k_grad(Args a) {
+__global__ __attribute__((amdgpu_flat_work_group_size(1, GradCfg<E, DK>::NTH),
+                          amdgpu_waves_per_eu(sizeof(E) == 2 ? 2 : 1)))
+void k_grad(Args a) {
   using M = Mfma<E>;
   using frag = typename M::frag;
   using C = GradCfg<E, DK>;
-  constexpr int NW = C::NW, NTH = C::NTH, NDT = C::NDT, PAT = C::PAT;
+  constexpr int NW = C::NW, NDT = C::NDT, PAT = C::PAT, HV = C::HV, NDH = C::NDH;
   constexpr int NKS = DV / M::K;         // MFMA k-steps over dv
-  constexpr int NDTOT = DK / 16;         // dk column tiles
-  constexpr int F = 16 + 2 * NDTOT;      // fragments per k-step: dO, dX, V' (4 each), V (4), S, dS
+  constexpr int F = 16 + 2 * NDH;        // fragments per k-step: dO, dX, V' (4 each), V (4), S, dS
   constexpr int PF = F / NW;             // fragments each wave copies per k-step
   static_assert(F % NW == 0, "fragments do not divide over the waves");
   constexpr int FR = 64 * M::KPL;        // elements of one fragment
-  constexpr int R = DK == 256 ? 3 : 4;   // ring depth in k-steps
+  constexpr int R = C::R;
   constexpr int RING_BYTES = R * F * FR * (int)sizeof(E);
   constexpr int PADE = 16 / sizeof(E);
   constexpr int LD = CH + PADE;
   constexpr int NKC = CH / M::K;
   constexpr int FIN_BYTES = 4 * CH * LD * (int)sizeof(E);
   constexpr int LDQ = NDT * 16 + PADE;   // row stride of a wave's dq / dk staging
-  constexpr int STG_BYTES = 2 * NW * CH * LDQ * (int)sizeof(E);
+  constexpr int STG_BYTES = NW * CH * LDQ * (int)sizeof(E);
   constexpr int FIN_ALL = FIN_BYTES + STG_BYTES;
   constexpr int SMEM = RING_BYTES > FIN_ALL ? RING_BYTES : FIN_ALL;
+  static_assert(sizeof(E) == 4 || DK == 256 || SMEM + 7 * 1024 + 512 <= 80 * 1024,
+                "two bf16 workgroups must fit the CU's 160 KB of LDS at dk <= 128");
   __shared__ __align__(16) unsigned char smem[SMEM];
   __shared__ float sg[CH], sb[CH], seg[CH], sdec[CH];
   __shared__ float sdbA[CH], sxv[CH], sErow[2][CH], sEcol[2 * 4][CH];
@@ -68,12 +94,21 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
   E* sM1T = sM1 + CH * LD;               //         M1^T, A buffer
   E* sDA = sM1T + CH * LD;               //         D, A buffer
   E* sDT = sDA + CH * LD;                //         D^T, A buffer
-  E* sQst = (E*)(smem + FIN_BYTES) + (size_t)2 * wave_id() * CH * LDQ;  // this wave's dq rows
-  E* sKst = sQst + CH * LDQ;                                             //           dk rows
+  E* sSt = (E*)(smem + FIN_BYTES) + (size_t)wave_id() * CH * LDQ;  // this wave's dq, then dk rows
 
-  const int c = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, l = lane_id(), g4 = l >> 4;
+  // Workgroup -> (chunk-head, half).  The two halves of a chunk-head are 8
+  // workgroups apart: workgroup i runs on XCD i % 8, so both land on one XCD,
+  // are dispatched together, and the second finds the dv-side operands in L2.
+  int unit = blockIdx.x, half = 0;
+  if constexpr (HV == 2) {
+    half = (blockIdx.x >> 3) & 1;
+    unit = (blockIdx.x >> 4) * 8 + (blockIdx.x & 7);
+  }
+  if (unit >= a.NC * a.H) return;  // the last group of 8 may be partial
+  const int H = a.H, h = unit / a.NC, c = unit - h * a.NC;
+  const int tid = threadIdx.x, l = lane_id(), g4 = l >> 4;
   const int w = __builtin_amdgcn_readfirstlane(wave_id());
-  const int H = a.H;
+  const int dt0 = half * NDH;  // first dk column tile of this workgroup
   const int4 ci = chunk_info(a, c);
   const int start = ci.y, len = ci.z;
   const size_t ch = (size_t)c * H + h;
@@ -100,7 +135,8 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
   // a ring of R k-steps, each wave copying PF of a k-step's F fragments:
   //   f in [0, 12): dO, dX, V' rows of t-tile f % 4 (A operands of all waves)
   //   f in [12, 16): V rows of t-tile f - 12 (dX . V)
-  //   f in [16, F): S, then dS, columns of d-tile (B operands of their wave)
+  //   f in [16, F): S, then dS, columns of the workgroup's d-tiles (B
+  //   operands of their wave)
   // Rows past the chunk's end read a valid row instead: every product they
   // enter is multiplied by a zero row of dX, V', P, Q or beta, or lands in a
   // row that is masked out.  Slot it % R holds logical k-step it (clamped to
@@ -121,7 +157,7 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
       } else if (f < 12) {
         src = (f < 8 ? dXp : Vpp) + ((size_t)((f & 3) * NKS + ksd) * 64 + l) * M::KPL;
       } else {
-        const int j = f - 16, mat = j / NDTOT, dt = j - mat * NDTOT;
+        const int j = f - 16, mat = j / NDH, dt = dt0 + j - mat * NDH;
         src = (mat ? dSp : Sp) + ((size_t)(dt * NKS + ksd) * 64 + l) * M::KPL;
       }
       dma_frag<E>(src, slot + f * FR);
@@ -146,7 +182,7 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
 #pragma unroll
     for (int n = 0; n < NDT; ++n) {
       bS[n] = M::load(slot + (16 + w * NDT + n) * FR + lo);
-      bD[n] = M::load(slot + (16 + NDTOT + w * NDT + n) * FR + lo);
+      bD[n] = M::load(slot + (16 + NDH + w * NDT + n) * FR + lo);
     }
 #pragma unroll
     for (int s2 = 0; s2 < NPR; ++s2) {
@@ -189,9 +225,8 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
   };
 
   // Copies run NPRO k-steps ahead.  The last NPRO steps issue none; before
-  // them each wave loads the finish phase's global operands into registers
-  // (the P / Ak tiles of its [dO; dX] V'^T tiles, its K^T and Q^T
-  // fragments), so their latency hides behind those steps.
+  // them each wave loads the P / Ak tiles of its [dO; dX] V'^T tiles into
+  // registers, so their latency hides behind those steps.
   constexpr int NPRO = R - 1 < NKS ? R - 1 : NKS;
 #pragma unroll
   for (int it = 0; it < NPRO; ++it) issue(it);
@@ -202,7 +237,6 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
     step(it);
   }
   f32x4 side[PAT];
-  frag fkp[NDT][NKC], fqp[NDT][NKC];
   {
     const float* gP = a.Pm + ch * CH * CH;
     const float* gA = a.Ak + ch * CH * CH;
@@ -211,24 +245,29 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
       const int q = w * PAT + p, m = q >> 4, rt = (q >> 2) & 3, ct = q & 3;
       side[p] = *reinterpret_cast<const f32x4*>((m ? gA : gP) + cfrag_index(rt, ct, CH));
     }
-    const E* KTp = (const E*)a.KTf + ch * DK * CH;
-    const E* QTp = (const E*)a.QTf + ch * DK * CH;
-#pragma unroll
-    for (int n = 0; n < NDT; ++n)
-#pragma unroll
-      for (int kt = 0; kt < NKC; ++kt) {
-        const int dt = w * NDT + n;
-        fkp[n][kt] = M::load(KTp + (size_t)(dt * NKC + kt) * FR + l * M::KPL);
-        fqp[n][kt] = M::load(QTp + (size_t)(dt * NKC + kt) * FR + l * M::KPL);
-      }
   }
-  constexpr int NP = PAT + 2 * NDT * NKC;  // loads issued after the last copies
+  constexpr int NP = PAT;  // loads issued after the last copies
   static_for<0, NPRO>([&](auto tt) {
     wait_vmcnt<(NPRO - 1 - decltype(tt)::value) * PF + NP>();
     lds_barrier();
     step(NKS - NPRO + decltype(tt)::value);
   });
   lds_barrier();  // every wave is done with the ring before its LDS is reused
+
+  // the wave's K^T and Q^T fragments, first needed after step (1)
+  frag fkp[NDT][NKC], fqp[NDT][NKC];
+  {
+    const E* KTp = (const E*)a.KTf + ch * DK * CH;
+    const E* QTp = (const E*)a.QTf + ch * DK * CH;
+#pragma unroll
+    for (int n = 0; n < NDT; ++n)
+#pragma unroll
+      for (int kt = 0; kt < NKC; ++kt) {
+        const int dt = dt0 + w * NDT + n;
+        fkp[n][kt] = M::load(KTp + (size_t)(dt * NKC + kt) * FR + l * M::KPL);
+        fqp[n][kt] = M::load(QTp + (size_t)(dt * NKC + kt) * FR + l * M::KPL);
+      }
+  }
 
   // ---- finish phase (the staging ring is dead; its LDS is reused)
   // (1) the [dO; dX] V'^T tiles: M1, D, and the parts of E and dbeta.  A
@@ -346,57 +385,62 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
           srow[w][2][r] = a2;
         }
       }
+    // dq = diag(e^g) Gq + M1 K and dk = diag(e^{g_n - g}) Gs - diag(b e^g) Gk
+    // + M1^T Q + (D + D^T) K, formed in place of Gq and Gs; each A fragment
+    // of M1, M1^T, D, D^T is read from LDS once for all the wave's columns
 #pragma unroll
-    for (int n = 0; n < NDT; ++n) {
-      const frag(&fk)[NKC] = fkp[n];
-      const frag(&fq)[NKC] = fqp[n];
+    for (int i = 0; i < 4; ++i) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        f32x4 dq = Gq[i][n], dk;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int r = i * 16 + acc_row(e);
-          dq[e] *= seg[r];
-          dk[e] = sdec[r] * Gs[i][n][e] - sb[r] * seg[r] * Gk[i][n][e];
-        }
-#pragma unroll
-        for (int kt = 0; kt < NKC; ++kt) {
-          const int fo = ((i * NKC + kt) * 64 + l) * M::KPL;
-          const frag am = M::load(sM1 + fo), amt = M::load(sM1T + fo);
-          const frag ad = M::load(sDA + fo), adt = M::load(sDT + fo);
-          dq = M::mma(am, fk[kt], dq);
-          dk = M::mma(amt, fq[kt], dk);
-          dk = M::mma(ad, fk[kt], dk);
-          dk = M::mma(adt, fk[kt], dk);
-        }
+      for (int n = 0; n < NDT; ++n)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int r = i * 16 + acc_row(e);
-          sQst[r * LDQ + n * 16 + acc_col()] = to_e<E>(dq[e]);
-          sKst[r * LDQ + n * 16 + acc_col()] = to_e<E>(dk[e]);
+          Gq[i][n][e] *= seg[r];
+          Gs[i][n][e] = sdec[r] * Gs[i][n][e] - sb[r] * seg[r] * Gk[i][n][e];
+        }
+#pragma unroll
+      for (int kt = 0; kt < NKC; ++kt) {
+        const int fo = ((i * NKC + kt) * 64 + l) * M::KPL;
+        const frag am = M::load(sM1 + fo), amt = M::load(sM1T + fo);
+        const frag ad = M::load(sDA + fo), adt = M::load(sDT + fo);
+#pragma unroll
+        for (int n = 0; n < NDT; ++n) {
+          Gq[i][n] = M::mma(am, fkp[n][kt], Gq[i][n]);
+          Gs[i][n] = M::mma(amt, fqp[n][kt], Gs[i][n]);
+          Gs[i][n] = M::mma(ad, fkp[n][kt], Gs[i][n]);
+          Gs[i][n] = M::mma(adt, fkp[n][kt], Gs[i][n]);
         }
       }
     }
-    // the wave's dq and dk columns, row by row, 16 bytes per lane and store
+    // the wave's dq, then dk, columns through its staging rows (a wave's LDS
+    // operations complete in order), 16 bytes per lane and store
     constexpr int EPV = 16 / sizeof(E), VPR = NDT * 16 / EPV, PCS = CH * VPR / 64;
-    E* gq = (E*)a.dq + row0 * DK + w * NDT * 16;
-    E* gk = (E*)a.dk + row0 * DK + w * NDT * 16;
+    const int col0 = (dt0 + w * NDT) * 16;
 #pragma unroll
-    for (int x = 0; x < PCS; ++x) {
-      const int idx = l + 64 * x, r = idx / VPR, cv = idx - r * VPR;
-      const uint4 vq = *reinterpret_cast<const uint4*>(sQst + r * LDQ + cv * EPV);
-      const uint4 vk = *reinterpret_cast<const uint4*>(sKst + r * LDQ + cv * EPV);
-      if (r < len) {
-        store_stream(gq + (size_t)r * H * DK + cv * EPV, vq);
-        store_stream(gk + (size_t)r * H * DK + cv * EPV, vk);
+    for (int mat = 0; mat < 2; ++mat) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int n = 0; n < NDT; ++n)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            sSt[(i * 16 + acc_row(e)) * LDQ + n * 16 + acc_col()] =
+                to_e<E>(mat ? Gs[i][n][e] : Gq[i][n][e]);
+      E* gout = (E*)(mat ? a.dk : a.dq) + row0 * DK + col0;
+#pragma unroll
+      for (int x = 0; x < PCS; ++x) {
+        const int idx = l + 64 * x, r = idx / VPR, cv = idx - r * VPR;
+        const uint4 v = *reinterpret_cast<const uint4*>(sSt + r * LDQ + cv * EPV);
+        if (r < len) store_stream(gout + (size_t)r * H * DK + cv * EPV, v);
       }
     }
   }
   lds_barrier();
 
-  // (3) dbeta, dg, dlog_alpha (one wave, one lane per chunk position)
+  // (3) the partial sums of the gate gradients (one wave, one lane per row)
   if (w == 0) {
     const int r = l;
+    float* gp = a.gpart + ch * GP_FLOATS;
     float pq = 0.f, pk = 0.f, ps = 0.f, s_dot = 0.f;
 #pragma unroll
     for (int x = 0; x < NW; ++x) {
@@ -405,33 +449,78 @@ __global__ __launch_bounds__(512) void k_grad(Args a) {
       ps += srow[x][2][r];
       s_dot += sred[x];
     }
-    float ecol = 0.f;
+    gp[(3 * half + 0) * CH + r] = pq;
+    gp[(3 * half + 1) * CH + r] = pk;
+    gp[(3 * half + 2) * CH + r] = ps;
+    if (r == 0) gp[11 * CH + half] = s_dot;
+    if (half == 0) {
+      float ecol = 0.f;
 #pragma unroll
-    for (int x = 0; x < 8; ++x) ecol += sEcol[x][r];
-    const bool valid = r < len;
-    const float gn = sg[CH - 1];
-    const float eg = __expf(sg[r]), b = sb[r], dec = __expf(gn - sg[r]);
-    const float db = sdbA[r] + sxv[r] - eg * pk;
-    if (valid) a.dbeta[row0 + (size_t)r * H] = db;
-    if (a.dlog_alpha) {  // the gate gradient is optional
-      float dg = eg * pq - b * eg * pk - dec * ps + sErow[0][r] + sErow[1][r] - ecol;
-      float tail = valid ? dec * ps : 0.f;
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) tail += __shfl_xor(tail, off, 64);
-      if (r == len - 1) dg += tail + __expf(gn) * s_dot;
-      if (!valid) dg = 0.f;
-      // reverse inclusive scan: lane r receives sum_{r' >= r} dg_r'
-      const float rev = __shfl(dg, 63 - r, 64);
-      const float sc = wave_incl_scan(rev);
-      const float dla = __shfl(sc, 63 - r, 64);
-      if (valid) a.dlog_alpha[row0 + (size_t)r * H] = dla;
+      for (int x = 0; x < 8; ++x) ecol += sEcol[x][r];
+      gp[6 * CH + r] = sErow[0][r];
+      gp[7 * CH + r] = sErow[1][r];
+      gp[8 * CH + r] = ecol;
+      gp[9 * CH + r] = sdbA[r];
+      gp[10 * CH + r] = sxv[r];
     }
+  }
+}
+
+// Gate gradients from the gradient kernel's partial sums, one wave per
+// chunk-head and one lane per row:
+//   dbeta_r = sum_i dA_ri Ak_ri + dX_r . V_r - e^{g_r} k_r . Gk_r
+//   dg_r    = e^{g_r} q_r.Gq_r - b_r e^{g_r} k_r.Gk_r - e^{g_n-g_r} k_r.Gs_r
+//             + sum_i E_ri - sum_j E_jr
+//             (+ sum_r e^{g_n-g_r} k_r.Gs_r + e^{g_n} <dS, S> on the last token)
+//   dlog_alpha = reverse cumulative sum of dg inside the chunk.
+template <int HV>
+__global__ __launch_bounds__(256) void k_grad_gates(Args a) {
+  const int ch = blockIdx.x * 4 + wave_id();
+  if (ch >= a.NC * a.H) return;  // whole waves
+  const int H = a.H, c = ch / H, h = ch - c * H, r = lane_id();
+  const int4 ci = chunk_info(a, c);
+  const int len = ci.z;
+  const size_t row0 = (size_t)ci.y * H + h;
+  const float* gp = a.gpart + (size_t)ch * GP_FLOATS;
+  float pq = gp[r], pk = gp[CH + r], ps = gp[2 * CH + r], s_dot = gp[11 * CH];
+  if constexpr (HV == 2) {
+    pq += gp[3 * CH + r];
+    pk += gp[4 * CH + r];
+    ps += gp[5 * CH + r];
+    s_dot += gp[11 * CH + 1];
+  }
+  const bool valid = r < len;
+  // alpha == 1: g = 0 and every factor below is exp(0) = 1 exactly
+  const float g = a.gated ? a.g[(size_t)ch * CH + r] : 0.f;
+  const float gn = __shfl(g, CH - 1, 64);
+  const float b = valid ? a.beta[row0 + (size_t)r * H] : 0.f;
+  const float eg = __expf(g), dec = __expf(gn - g);
+  const float db = gp[9 * CH + r] + gp[10 * CH + r] - eg * pk;
+  if (valid) a.dbeta[row0 + (size_t)r * H] = db;
+  if (a.dlog_alpha) {  // the gate gradient is optional
+    float dg = eg * pq - b * eg * pk - dec * ps + gp[6 * CH + r] + gp[7 * CH + r] - gp[8 * CH + r];
+    float tail = valid ? dec * ps : 0.f;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) tail += __shfl_xor(tail, off, 64);
+    if (r == len - 1) dg += tail + __expf(gn) * s_dot;
+    if (!valid) dg = 0.f;
+    // reverse inclusive scan: lane r receives sum_{r' >= r} dg_r'
+    const float rev = __shfl(dg, 63 - r, 64);
+    const float sc = wave_incl_scan(rev);
+    const float dla = __shfl(sc, 63 - r, 64);
+    if (valid) a.dlog_alpha[row0 + (size_t)r * H] = dla;
   }
 }
 
 hipError_t launch_grad(Dt dt, int dk, int dv, const Args& a, hipStream_t s) {
   auto f = [&]<class E, int DK, int DV>() {
-    hipLaunchKernelGGL((k_grad<E, DK, DV>), dim3(a.NC, a.H), dim3(GradCfg<E, DK>::NTH), 0, s, a);
+    using C = GradCfg<E, DK>;
+    const long units = (long)a.NC * a.H;
+    const long wgs = C::HV == 1 ? units : (units + 7) / 8 * 16;
+    hipLaunchKernelGGL((k_grad<E, DK, DV>), dim3(wgs), dim3(C::NTH), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((k_grad_gates<C::HV>), dim3((units + 3) / 4), dim3(256), 0, s, a);
     return hipGetLastError();
   };
   GDN_DISPATCH(dt, dk, dv, f);

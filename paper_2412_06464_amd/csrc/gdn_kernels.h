@@ -48,7 +48,12 @@ struct Args {
   void* Vp;   // [ch] V' = U~ - W~ S              64 x dv
   void* dSc;  // [ch] gradient of each chunk's exit state  dk x dv
   void* dXb;  // [ch] dX = T^T dV'                64 x dv
+  // workspace: the gradient kernel's partial row sums for the gate gradients
+  float* gpart;  // [ch][GRAD_PART_FLOATS]
 };
+
+// Floats per chunk-head of Args::gpart (twelve blocks of one chunk, 64).
+constexpr int GRAD_PART_FLOATS = 12 * 64;
 
 enum class Dt { F32, BF16 };
 
