@@ -79,13 +79,14 @@ void k_grad(Args a) {
   constexpr int FIN_BYTES = 4 * CH * LD * (int)sizeof(E);
   constexpr int LDQ = NDT * 16 + PADE;   // row stride of a wave's dq / dk staging
   constexpr int STG_BYTES = NW * CH * LDQ * (int)sizeof(E);
-  constexpr int FIN_ALL = FIN_BYTES + STG_BYTES;
+  constexpr int ECP_BYTES = 4 * NW * CH * (int)sizeof(float);  // partial column sums of E
+  constexpr int FIN_ALL = FIN_BYTES + STG_BYTES + ECP_BYTES;
   constexpr int SMEM = RING_BYTES > FIN_ALL ? RING_BYTES : FIN_ALL;
-  static_assert(sizeof(E) == 4 || DK == 256 || SMEM + 7 * 1024 + 512 <= 80 * 1024,
+  static_assert(sizeof(E) == 4 || DK == 256 || SMEM + 5 * 1024 + 512 <= 80 * 1024,
                 "two bf16 workgroups must fit the CU's 160 KB of LDS at dk <= 128");
   __shared__ __align__(16) unsigned char smem[SMEM];
   __shared__ float sg[CH], sb[CH], seg[CH], sdec[CH];
-  __shared__ float sdbA[CH], sxv[CH], sErow[2][CH], sEcol[2 * 4][CH];
+  __shared__ float sdbA[CH], sxv[CH], sErow[2][CH];
   __shared__ float srow[NW][3][CH];
   __shared__ float sred[NW];
 
@@ -95,6 +96,7 @@ void k_grad(Args a) {
   E* sDA = sM1T + CH * LD;               //         D, A buffer
   E* sDT = sDA + CH * LD;                //         D^T, A buffer
   E* sSt = (E*)(smem + FIN_BYTES) + (size_t)wave_id() * CH * LDQ;  // this wave's dq, then dk rows
+  float* sEcp = (float*)(smem + FIN_BYTES + STG_BYTES);              // [4 NW][CH]
 
   // Workgroup -> (chunk-head, half).  The two halves of a chunk-head are 8
   // workgroups apart: workgroup i runs on XCD i % 8, so both land on one XCD,
@@ -272,48 +274,51 @@ void k_grad(Args a) {
   // ---- finish phase (the staging ring is dead; its LDS is reused)
   // (1) the [dO; dX] V'^T tiles: M1, D, and the parts of E and dbeta.  A
   // wave's tiles come in runs of 4 that cover one (m, rt) row block, so its
-  // row sums stay in registers over the run and are reduced once.
+  // row sums stay in registers over the run and are reduced once; column
+  // sums stay per lane (over the lane's 4 rows of each tile) and go to LDS
+  // as 4 NW partials per column.
   {
     static_assert(PAT % 4 == 0, "a wave's tiles must cover whole row blocks");
-    float racc[4], dacc[4], sgr[4];
+    float racc[4], dacc[4], sgr[4], sbr[4], ccol[4], sgc[4];
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) {
+      ccol[ct] = 0.f;
+      sgc[ct] = sg[ct * 16 + acc_col()];
+    }
 #pragma unroll
     for (int p = 0; p < PAT; ++p) {
-      const int q = w * PAT + p, m = q >> 4, rt = (q >> 2) & 3, ct = q & 3;
+      // ct = p & 3 at compile time (PAT is a multiple of 4)
+      const int q = w * PAT + p, m = q >> 4, rt = (q >> 2) & 3, ct = p & 3;
       if ((p & 3) == 0) {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           racc[e] = dacc[e] = 0.f;
           sgr[e] = sg[rt * 16 + acc_row(e)];
+          sbr[e] = sb[rt * 16 + acc_row(e)];
         }
       }
-      const float sgi = sg[ct * 16 + acc_col()];
-      float csum = 0.f;
+      E* dst = m ? sDA : sM1;
+      E* dstT = m ? sDT : sM1T;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int r = rt * 16 + acc_row(e), i = ct * 16 + acc_col();
-        const float gam = (i <= r) ? __expf(sgr[e] - sgi) : 0.f;
-        float ev;
+        const float gam = (i <= r) ? __expf(sgr[e] - sgc[ct]) : 0.f;
+        float ev, x;
         if (m == 0) {
           const float dp = (i <= r) ? PA[p][e] : 0.f;
-          const float m1 = dp * gam;
-          sM1[afrag_pos64<E>(r, i)] = to_e<E>(m1);
-          sM1T[afrag_pos64<E>(i, r)] = to_e<E>(m1);
+          x = dp * gam;
           ev = dp * side[p][e];
         } else {
           const float da = (i < r) ? -PA[p][e] : 0.f;
-          const float dd = sb[r] * da * gam;
-          sDA[afrag_pos64<E>(r, i)] = to_e<E>(dd);
-          sDT[afrag_pos64<E>(i, r)] = to_e<E>(dd);
-          ev = da * sb[r] * side[p][e];
+          x = sbr[e] * da * gam;
+          ev = da * sbr[e] * side[p][e];
           dacc[e] += da * side[p][e];
         }
+        dst[afrag_pos64<E>(r, i)] = to_e<E>(x);
+        dstT[afrag_pos64<E>(i, r)] = to_e<E>(x);
         racc[e] += ev;
-        csum += ev;
+        ccol[ct] += ev;
       }
-      // column sums over the tile's 16 rows
-      csum += __shfl_xor(csum, 16, 64);
-      csum += __shfl_xor(csum, 32, 64);
-      if (l < 16) sEcol[m * 4 + rt][ct * 16 + l] = csum;
       // row sums over the run's 64 columns
       if ((p & 3) == 3) {
 #pragma unroll
@@ -328,6 +333,8 @@ void k_grad(Args a) {
         }
       }
     }
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) sEcp[(w * 4 + g4) * CH + ct * 16 + acc_col()] = ccol[ct];
   }
   // partial row dots over this wave's columns, and <dS, S>
   {
@@ -456,7 +463,7 @@ void k_grad(Args a) {
     if (half == 0) {
       float ecol = 0.f;
 #pragma unroll
-      for (int x = 0; x < 8; ++x) ecol += sEcol[x][r];
+      for (int x = 0; x < 4 * NW; ++x) ecol += sEcp[x * CH + r];
       gp[6 * CH + r] = sErow[0][r];
       gp[7 * CH + r] = sErow[1][r];
       gp[8 * CH + r] = ecol;
