@@ -272,69 +272,73 @@ void k_grad(Args a) {
   }
 
   // ---- finish phase (the staging ring is dead; its LDS is reused)
-  // (1) the [dO; dX] V'^T tiles: M1, D, and the parts of E and dbeta.  A
-  // wave's tiles come in runs of 4 that cover one (m, rt) row block, so its
-  // row sums stay in registers over the run and are reduced once; column
-  // sums stay per lane (over the lane's 4 rows of each tile) and go to LDS
-  // as 4 NW partials per column.
+  // (1) the [dO; dX] V'^T tiles: M1, D, and the parts of E and dbeta.  All
+  // of a wave's tiles lie in one of dP (m = 0) and dA (m = 1), so m selects
+  // one of two unrolled loops; the tiles come in runs of 4 that cover one row
+  // block, so row sums stay in registers over the run and are reduced once;
+  // column sums stay per lane (over the lane's 4 rows of each tile) and go
+  // to LDS as 4 NW partials per column.
   {
-    static_assert(PAT % 4 == 0, "a wave's tiles must cover whole row blocks");
-    float racc[4], dacc[4], sgr[4], sbr[4], ccol[4], sgc[4];
+    static_assert(PAT % 4 == 0 && 16 % PAT == 0, "a wave's tiles must be whole row blocks of one matrix");
+    float sgc[4];
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct) {
-      ccol[ct] = 0.f;
-      sgc[ct] = sg[ct * 16 + acc_col()];
-    }
+    for (int ct = 0; ct < 4; ++ct) sgc[ct] = sg[ct * 16 + acc_col()];
+    auto tiles = [&](auto mc) {
+      constexpr int MM = decltype(mc)::value;
+      E* dst = MM ? sDA : sM1;
+      E* dstT = MM ? sDT : sM1T;
+      float ccol[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int p = 0; p < PAT; ++p) {
-      // ct = p & 3 at compile time (PAT is a multiple of 4)
-      const int q = w * PAT + p, m = q >> 4, rt = (q >> 2) & 3, ct = p & 3;
-      if ((p & 3) == 0) {
+      for (int p0 = 0; p0 < PAT; p0 += 4) {
+        const int rt = ((w * PAT + p0) >> 2) & 3;
+        float racc[4], dacc[4], sgr[4], sbr[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           racc[e] = dacc[e] = 0.f;
           sgr[e] = sg[rt * 16 + acc_row(e)];
           sbr[e] = sb[rt * 16 + acc_row(e)];
         }
-      }
-      E* dst = m ? sDA : sM1;
-      E* dstT = m ? sDT : sM1T;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int r = rt * 16 + acc_row(e), i = ct * 16 + acc_col();
-        const float gam = (i <= r) ? __expf(sgr[e] - sgc[ct]) : 0.f;
-        float ev, x;
-        if (m == 0) {
-          const float dp = (i <= r) ? PA[p][e] : 0.f;
-          x = dp * gam;
-          ev = dp * side[p][e];
-        } else {
-          const float da = (i < r) ? -PA[p][e] : 0.f;
-          x = sbr[e] * da * gam;
-          ev = da * sbr[e] * side[p][e];
-          dacc[e] += da * side[p][e];
+        for (int ct = 0; ct < 4; ++ct) {
+          const int p = p0 + ct;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int r = rt * 16 + acc_row(e), i = ct * 16 + acc_col();
+            const float gam = (i <= r) ? __expf(sgr[e] - sgc[ct]) : 0.f;
+            float ev, x;
+            if constexpr (MM == 0) {
+              const float dp = (i <= r) ? PA[p][e] : 0.f;
+              x = dp * gam;
+              ev = dp * side[p][e];
+            } else {
+              const float da = (i < r) ? -PA[p][e] : 0.f;
+              x = sbr[e] * da * gam;
+              ev = da * sbr[e] * side[p][e];
+              dacc[e] += da * side[p][e];
+            }
+            dst[afrag_pos64<E>(r, i)] = to_e<E>(x);
+            dstT[afrag_pos64<E>(i, r)] = to_e<E>(x);
+            racc[e] += ev;
+            ccol[ct] += ev;
+          }
         }
-        dst[afrag_pos64<E>(r, i)] = to_e<E>(x);
-        dstT[afrag_pos64<E>(i, r)] = to_e<E>(x);
-        racc[e] += ev;
-        ccol[ct] += ev;
-      }
-      // row sums over the run's 64 columns
-      if ((p & 3) == 3) {
+        // row sums over the run's 64 columns
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const float rs = reduce16(racc[e]);
-          const float db = m ? reduce16(dacc[e]) : 0.f;
+          const float db = MM ? reduce16(dacc[e]) : 0.f;
           if (acc_col() == 0) {
             const int r = rt * 16 + acc_row(e);
-            sErow[m][r] = rs;
-            if (m) sdbA[r] = db;
+            sErow[MM][r] = rs;
+            if (MM) sdbA[r] = db;
           }
         }
       }
-    }
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct) sEcp[(w * 4 + g4) * CH + ct * 16 + acc_col()] = ccol[ct];
+      for (int ct = 0; ct < 4; ++ct) sEcp[(w * 4 + g4) * CH + ct * 16 + acc_col()] = ccol[ct];
+    };
+    if ((w * PAT) >> 4) tiles(std::integral_constant<int, 1>{});
+    else tiles(std::integral_constant<int, 0>{});
   }
   // partial row dots over this wave's columns, and <dS, S>
   {
