@@ -87,12 +87,12 @@ def kernel_models(w, n_chunks_heads):
         # q, k, v, gates in; g, W~, Kbar^T, U~, P out; Gram, inverse, W~, U~
         "fwd:k_prep": (2 * kside + vside + gates + C * f32 + 2 * kside + vside + cc,
                        3 * prod_dk + prod_dv + C ** 3 / 3),
-        # as forward, plus P^T, T^T, -W~^T, (e^g Q)^T, and P, Ak in fp32
-        "bwd:k_prep": (2 * kside + vside + gates + C * f32 + 4 * kside + vside + 2 * cc
-                       + 2 * C * C * f32, 4 * prod_dk + prod_dv + C ** 3 / 3),
+        # as forward, plus P^T, T^T, -W~^T, (e^g Q)^T, and Ak^T
+        "bwd:k_prep": (2 * kside + vside + gates + C * f32 + 4 * kside + vside + 3 * cc,
+                       4 * prod_dk + prod_dv + C ** 3 / 3),
         # both of the above (P and P^T)
-        "fwd:k_prep_save": (2 * kside + vside + gates + C * f32 + 4 * kside + vside + 3 * cc
-                            + 2 * C * C * f32, 4 * prod_dk + prod_dv + C ** 3 / 3),
+        "fwd:k_prep_save": (2 * kside + vside + gates + C * f32 + 4 * kside + vside + 4 * cc,
+                            4 * prod_dk + prod_dv + C ** 3 / 3),
         # W~, q, Kbar^T, P, U~, g in; o out
         "k_fwd_seq": (3 * kside + cc + vside + C * f32 + vside, 3 * prod_s + prod_dv),
         # as k_fwd_seq, plus chunk states and V' out
@@ -103,8 +103,8 @@ def kernel_models(w, n_chunks_heads):
         # k, (e^g Q)^T, -W~^T, P^T, T^T, dO, g, beta in; dS, dX, dv out
         "k_bwd_seq": (3 * kside + 2 * cc + vside + gates + st + 2 * vside,
                       3 * prod_s + 2 * prod_dv),
-        # S, dS, q, k, v, dO, V', dX, P, Ak, gates in; dq, dk, dbeta, dlog_alpha out
-        "k_grad": (2 * st + 2 * kside + 4 * vside + 2 * C * C * f32 + 2 * gates
+        # S, dS, q, k, v, dO, V', dX, P^T, Ak^T, gates in; dq, dk, dbeta, dlog_alpha out
+        "k_grad": (2 * st + 2 * kside + 4 * vside + 2 * cc + 2 * gates
                    + 2 * kside + gates, 3 * prod_s + 2 * prod_dv + 3 * prod_dk),
         "k_chunk_table": (0, 0),
     }

@@ -81,13 +81,12 @@ struct Carver {
 };
 
 struct Sizes {
-  size_t kside, vside, cc, cf, st;
+  size_t kside, vside, cc, st;
   Sizes(const gdn_problem* p, const Shape& s) {
     const size_t NC = (size_t)s.NC, H = (size_t)p->H;
     kside = NC * H * CH * (size_t)p->dk * s.esz;        // 64 x dk per chunk
     vside = NC * H * CH * (size_t)p->dv * s.esz;        // 64 x dv per chunk
     cc = NC * H * CH * CH * s.esz;                      // 64 x 64 per chunk
-    cf = NC * H * CH * CH * sizeof(float);              // 64 x 64 fp32 per chunk
     st = NC * H * (size_t)p->dk * p->dv * s.esz;        // dk x dv per chunk
   }
 };
@@ -106,8 +105,7 @@ void carve_saved(const gdn_problem* p, const Shape& s, Carver& c, Args* a) {
   unsigned char* QgT = c.take(z.kside);
   unsigned char* KTf = c.take(z.kside);
   unsigned char* QTf = c.take(z.kside);
-  unsigned char* Pm = c.take(z.cf);
-  unsigned char* Ak = c.take(z.cf);
+  unsigned char* Ak = c.take(z.cc);
   unsigned char* Sc = c.take(z.st);
   unsigned char* Vp = c.take(z.vside);
   if (a) {
@@ -119,8 +117,7 @@ void carve_saved(const gdn_problem* p, const Shape& s, Carver& c, Args* a) {
     a->QgT = QgT;
     a->KTf = KTf;
     a->QTf = QTf;
-    a->Pm = (float*)Pm;
-    a->Ak = (float*)Ak;
+    a->Ak = Ak;
     a->Sc = Sc;
     a->Vp = Vp;
   }

@@ -256,6 +256,22 @@ template <> __device__ inline void afrag_put_T<float>(float* dst, int KD, int mt
   for (int e = 0; e < 4; ++e) dst[((size_t)mt * (KD / 4) + 4 * i16 + e) * 64 + lane_id()] = v[e];
 }
 
+// The inverse read: the accumulator tile (rows 16 i16 + 4 g + e, column
+// 16 mt + l % 16, as f32) of a 64 x 64 matrix M^T held as the A buffer of M,
+// one 8-byte load per lane for bf16.
+template <class E> __device__ inline f32x4 afrag_get_T(const E* src, int mt, int i16);
+template <> __device__ inline f32x4 afrag_get_T<bf16>(const bf16* src, int mt, int i16) {
+  typedef bf16 bf16x4 __attribute__((ext_vector_type(4)));
+  const bf16x4 x = *reinterpret_cast<const bf16x4*>(src + frag_slot_bf16((size_t)mt * 2 + (i16 >> 1), i16));
+  return f32x4{(float)x[0], (float)x[1], (float)x[2], (float)x[3]};
+}
+template <> __device__ inline f32x4 afrag_get_T<float>(const float* src, int mt, int i16) {
+  f32x4 v;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) v[e] = src[((size_t)mt * 16 + 4 * i16 + e) * 64 + lane_id()];
+  return v;
+}
+
 // A operand, permuted order, read straight from a row-major row of a global
 // matrix (`row` points at the row, k-step kt); zero when !valid.
 template <class E>
@@ -383,8 +399,10 @@ template <> __device__ inline void frag_to_lds_async<float>(const float* src_lan
 // lds_frag + l * KPL.  `lds_frag` must be the same for the whole wave.  It is
 // issued from inline assembly so that the compiler does not wait on it: the
 // caller owns the vmcnt bookkeeping (s_waitcnt before reading the LDS, and
-// vmcnt(0) before the LDS is reused for anything else) and must issue no
-// other vector-memory loads whose waits it relies on in between.
+// vmcnt(0) before the LDS is reused for anything else).  Copies are taken
+// to complete in issue order among themselves, but an ordinary load issued
+// after a copy may return before it: a partial vmcnt wait is sound only
+// while no ordinary load issued after the awaited copies is in flight.
 template <class E> __device__ inline void dma_frag(const E* src_lane, E* lds_frag);
 template <> __device__ inline void dma_frag<bf16>(const bf16* src_lane, bf16* lds_frag) {
   const unsigned lds = (unsigned)(uintptr_t)lds_frag;

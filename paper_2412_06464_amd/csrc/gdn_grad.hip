@@ -226,9 +226,11 @@ void k_grad(Args a) {
     }
   };
 
-  // Copies run NPRO k-steps ahead.  The last NPRO steps issue none; before
-  // them each wave loads the P / Ak tiles of its [dO; dX] V'^T tiles into
-  // registers, so their latency hides behind those steps.
+  // Copies run NPRO k-steps ahead.  The last NPRO steps issue none.  The
+  // waits count only direct copies, which complete in issue order: the P or
+  // Ak tiles of the wave's [dO; dX] V'^T tiles (ordinary loads, which may
+  // return before earlier copies) are issued only after the wait for every
+  // copy, before the last step, whose products hide their latency.
   constexpr int NPRO = R - 1 < NKS ? R - 1 : NKS;
 #pragma unroll
   for (int it = 0; it < NPRO; ++it) issue(it);
@@ -239,20 +241,20 @@ void k_grad(Args a) {
     step(it);
   }
   f32x4 side[PAT];
-  {
-    const float* gP = a.Pm + ch * CH * CH;
-    const float* gA = a.Ak + ch * CH * CH;
-#pragma unroll
-    for (int p = 0; p < PAT; ++p) {
-      const int q = w * PAT + p, m = q >> 4, rt = (q >> 2) & 3, ct = q & 3;
-      side[p] = *reinterpret_cast<const f32x4*>((m ? gA : gP) + cfrag_index(rt, ct, CH));
-    }
-  }
-  constexpr int NP = PAT;  // loads issued after the last copies
   static_for<0, NPRO>([&](auto tt) {
-    wait_vmcnt<(NPRO - 1 - decltype(tt)::value) * PF + NP>();
+    constexpr int T = decltype(tt)::value;
+    wait_vmcnt<(NPRO - 1 - T) * PF>();
     lds_barrier();
-    step(NKS - NPRO + decltype(tt)::value);
+    if constexpr (T == NPRO - 1) {
+      // P (m = 0) or Ak (m = 1) at the tile's positions, from their transposes
+      const E* src = (const E*)(((w * PAT) >> 4) ? a.Ak : a.PTf) + ch * CH * CH;
+#pragma unroll
+      for (int p = 0; p < PAT; ++p) {
+        const int q = w * PAT + p, rt = (q >> 2) & 3, ct = q & 3;
+        side[p] = afrag_get_T<E>(src, ct, rt);
+      }
+    }
+    step(NKS - NPRO + T);
   });
   lds_barrier();  // every wave is done with the ring before its LDS is reused
 

@@ -37,11 +37,12 @@ struct Args {
   void* TTf;  // T^T                       rows t', k = t    64 x 64  (backward)
   void* nWT;  // -W~^T                     rows d, k = t     dk x 64  (backward)
   void* QgT;  // (diag(e^g) Q)^T           rows d, k = t     dk x 64  (backward)
-  // workspace: backward intermediates for the gradient kernel
+  // workspace: backward intermediates for the gradient kernel (which also
+  // reads P^T)
   void* KTf;  // K^T                       rows d, k = t     dk x 64  (backward)
   void* QTf;  // Q^T                       rows d, k = t     dk x 64  (backward)
-  float* Pm;  // [ch] P, fp32, accumulator layout of a 64 x 64 matrix
-  float* Ak;  // [ch] strictLower(Gamma * K K^T), fp32, accumulator layout
+  void* Ak;   // Ak^T, Ak = strictLower(Gamma K K^T)
+              //                           rows t', k = t    64 x 64  (backward)
   // per-chunk matrices over dv, B operands of the gradient kernel in
   // fragment order over dv (fragment (16-row tile, k-step) of 64 lanes)
   void* Sc;   // [ch] chunk entry states          dk x dv

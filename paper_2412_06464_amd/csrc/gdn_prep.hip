@@ -22,7 +22,7 @@
 //                  LDS in 64-wide slices of dk and dv.  Forward: W~, Kbar^T, U~,
 //                  P, diag(e^g) Q.  Backward (recompute): W~, Kbar^T, U~, and
 //                  for the reverse pass K, P^T, T^T, -W~^T, (e^g Q)^T, plus
-//                  K^T, Q^T, and P and strictLower(Gamma K K^T) in fp32 for
+//                  K^T, Q^T and strictLower(Gamma K K^T)^T for
 //                  the gradient kernel.  Forward with save: both sets.
 #include "gdn_device.h"
 #include "gdn_kernels.h"
@@ -84,7 +84,7 @@ template <class E, int DK, int DV, int MODE>
 __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
   using M = Mfma<E>;
   // operands of the forward pass (diag(e^g) Q, P), of the reverse pass and
-  // gradient kernel (K, P^T, T^T, -W~^T, (e^g Q)^T, K^T, Q^T, P, Ak), or both
+  // gradient kernel (K, P^T, T^T, -W~^T, (e^g Q)^T, K^T, Q^T, Ak^T), or both
   constexpr bool FOUT = MODE != PREP_BWD, BOUT = MODE != PREP_FWD;
   constexpr int PADE = 16 / sizeof(E);
   constexpr int LD = CH + PADE;  // rows of 64 elements
@@ -217,12 +217,9 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
       qk[0][j][e] = p;
     }
   if (BOUT) {
-    // P and strictLower(Gamma K K^T) in fp32, accumulator layout
+    // strictLower(Gamma K K^T) as the A buffer of its transpose, like P^T
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      *reinterpret_cast<f32x4*>(a.Ak + ch * CH * CH + cfrag_index(w, j, CH)) = kk[0][j];
-      *reinterpret_cast<f32x4*>(a.Pm + ch * CH * CH + cfrag_index(w, j, CH)) = qk[0][j];
-    }
+    for (int j = 0; j < 4; ++j) afrag_put_T<E>((E*)a.Ak + ch * CH * CH, CH, j, w, kk[0][j]);
   }
   lds_barrier();
 

@@ -62,8 +62,8 @@ def test_workspace_sizes(lib):
     # forward: W~, Kbar^T (64 x dk), U~ (64 x dv), P (64 x 64) per chunk-head
     assert f >= NCH * (2 * 64 * 64 * e + 64 * 64 * e + 64 * 64 * e)
     # backward adds entry states and exit-state gradients (dk x dv), V' and dX
-    # (64 x dv), and P, strictLower(Gamma K K^T) in fp32
-    assert b - f >= NCH * (2 * 64 * 64 * e + 2 * 64 * 64 * e + 2 * 64 * 64 * 4)
+    # (64 x dv), and P^T, strictLower(Gamma K K^T)^T (64 x 64)
+    assert b - f >= NCH * (2 * 64 * 64 * e + 2 * 64 * 64 * e + 2 * 64 * 64 * e)
     bad, _ = problem(dk=96)
     assert gdn.gdn_chunk_fwd_workspace_size(bad) == 0
 
