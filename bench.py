@@ -444,7 +444,7 @@ def main():
     def step_saved(timers=None):
         gdn.gdn_chunk_fwd_save(d["q"], d["k"], d["v"], d["beta"], la, saved=saved,
                                workspace=ws_fs, timer=timers[0] if timers else None, **fwd_kw)
-        gdn.gdn_chunk_bwd_saved(d["q"], d["v"], d["beta"], d["dO"], saved, dht=d["dht"],
+        gdn.gdn_chunk_bwd_saved(d["q"], d["k"], d["v"], d["beta"], d["dO"], saved, dht=d["dht"],
                                 cu_seqlens=cu, cu_seqlens_host=cu_host, workspace=ws_bs,
                                 out=out_b, timer=timers[1] if timers else None)
 

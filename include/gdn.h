@@ -138,13 +138,14 @@ gdn_status gdn_chunk_fwd_save(const gdn_problem *p, const void *q,
 
 /* Backward from a saving forward's buffer: the same gradients as
  * gdn_chunk_bwd for the inputs gdn_chunk_fwd_save was called with, without
- * rebuilding the chunk operands or recomputing the chunk states.  Reads v
- * and beta (the delta-rule terms of dbeta), dO, dht (or NULL) and `saved`,
- * which it leaves unchanged; q, k, log_alpha and h0 enter through `saved`.
- * Same outputs as gdn_chunk_bwd.  `workspace` holds
+ * rebuilding the chunk operands or recomputing the chunk states.  Reads q,
+ * k, v and beta (the same tensors the saving forward read), dO, dht (or
+ * NULL) and `saved`, which it leaves unchanged; log_alpha and h0 enter
+ * through `saved`.  Same outputs as gdn_chunk_bwd.  `workspace` holds
  * gdn_chunk_bwd_saved_workspace_size bytes. */
 size_t gdn_chunk_bwd_saved_workspace_size(const gdn_problem *p);
-gdn_status gdn_chunk_bwd_saved(const gdn_problem *p, const void *v,
+gdn_status gdn_chunk_bwd_saved(const gdn_problem *p, const void *q,
+                               const void *k, const void *v,
                                const float *beta, const void *dO,
                                const float *dht, const void *saved,
                                size_t saved_bytes, void *dq, void *dk,
@@ -245,7 +246,8 @@ gdn_status gdn_chunk_fwd_save_timed(const gdn_problem *p, const void *q,
                                     void *saved, size_t saved_bytes,
                                     void *workspace, size_t workspace_bytes,
                                     void *stream, gdn_timing *timing);
-gdn_status gdn_chunk_bwd_saved_timed(const gdn_problem *p, const void *v,
+gdn_status gdn_chunk_bwd_saved_timed(const gdn_problem *p, const void *q,
+                                     const void *k, const void *v,
                                      const float *beta, const void *dO,
                                      const float *dht, const void *saved,
                                      size_t saved_bytes, void *dq, void *dk,

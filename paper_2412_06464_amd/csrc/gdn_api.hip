@@ -103,8 +103,6 @@ void carve_saved(const gdn_problem* p, const Shape& s, Carver& c, Args* a) {
   unsigned char* TTf = c.take(z.cc);
   unsigned char* nWT = c.take(z.kside);
   unsigned char* QgT = c.take(z.kside);
-  unsigned char* KTf = c.take(z.kside);
-  unsigned char* QTf = c.take(z.kside);
   unsigned char* Ak = c.take(z.cc);
   unsigned char* Sc = c.take(z.st);
   unsigned char* Vp = c.take(z.vside);
@@ -115,8 +113,6 @@ void carve_saved(const gdn_problem* p, const Shape& s, Carver& c, Args* a) {
     a->TTf = TTf;
     a->nWT = nWT;
     a->QgT = QgT;
-    a->KTf = KTf;
-    a->QTf = QTf;
     a->Ak = Ak;
     a->Sc = Sc;
     a->Vp = Vp;
@@ -406,7 +402,8 @@ gdn_status gdn_chunk_fwd_save(const gdn_problem* p, const void* q, const void* k
                                   workspace, workspace_bytes, stream, nullptr);
 }
 
-gdn_status gdn_chunk_bwd_saved_timed(const gdn_problem* p, const void* v, const float* beta,
+gdn_status gdn_chunk_bwd_saved_timed(const gdn_problem* p, const void* q, const void* k,
+                                     const void* v, const float* beta,
                                      const void* dO, const float* dht, const void* saved,
                                      size_t saved_bytes_, void* dq, void* dk, void* dv,
                                      float* dbeta, float* dlog_alpha, float* dh0,
@@ -415,8 +412,8 @@ gdn_status gdn_chunk_bwd_saved_timed(const gdn_problem* p, const void* v, const 
   Shape s;
   gdn_status st = check_problem(p, &s);
   if (st != GDN_OK) return st;
-  if (!v || !beta || !dO || !dq || !dk || !dv || !dbeta) return GDN_ERR_NULL;
-  const void* ptrs[] = {v, beta, dO, dht, saved, dq, dk, dv, dbeta, dlog_alpha, dh0, workspace};
+  if (!q || !k || !v || !beta || !dO || !dq || !dk || !dv || !dbeta) return GDN_ERR_NULL;
+  const void* ptrs[] = {q, k, v, beta, dO, dht, saved, dq, dk, dv, dbeta, dlog_alpha, dh0, workspace};
   for (const void* x : ptrs)
     if (x && !aligned16(x)) return GDN_ERR_ALIGN;
   if (!saved || saved_bytes_ < saved_bytes(p, s)) return GDN_ERR_SAVED;
@@ -428,6 +425,8 @@ gdn_status gdn_chunk_bwd_saved_timed(const gdn_problem* p, const void* v, const 
   carve(p, s, Use::BwdSaved, (unsigned char*)workspace, &a);
   Carver c{(unsigned char*)const_cast<void*>(saved)};
   carve_saved(p, s, c, &a);
+  a.q = q;
+  a.k = k;
   a.v = v;
   a.beta = beta;
   a.dO = dO;
@@ -444,12 +443,12 @@ gdn_status gdn_chunk_bwd_saved_timed(const gdn_problem* p, const void* v, const 
   return e == hipSuccess ? GDN_OK : GDN_ERR_HIP;
 }
 
-gdn_status gdn_chunk_bwd_saved(const gdn_problem* p, const void* v, const float* beta,
-                               const void* dO, const float* dht, const void* saved,
-                               size_t saved_bytes_, void* dq, void* dk, void* dv, float* dbeta,
-                               float* dlog_alpha, float* dh0, void* workspace,
-                               size_t workspace_bytes, void* stream) {
-  return gdn_chunk_bwd_saved_timed(p, v, beta, dO, dht, saved, saved_bytes_, dq, dk, dv, dbeta,
+gdn_status gdn_chunk_bwd_saved(const gdn_problem* p, const void* q, const void* k, const void* v,
+                               const float* beta, const void* dO, const float* dht,
+                               const void* saved, size_t saved_bytes_, void* dq, void* dk,
+                               void* dv, float* dbeta, float* dlog_alpha, float* dh0,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+  return gdn_chunk_bwd_saved_timed(p, q, k, v, beta, dO, dht, saved, saved_bytes_, dq, dk, dv, dbeta,
                                    dlog_alpha, dh0, workspace, workspace_bytes, stream, nullptr);
 }
 

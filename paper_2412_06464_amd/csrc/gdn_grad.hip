@@ -21,11 +21,11 @@
 // fragments of the workgroup's dk columns, the bulk of the bytes) is copied
 // HBM -> LDS by direct-to-LDS loads into a ring of k-steps; each wave then
 // owns a set of dk columns (B operands) and reads the shared A operands.
-// Finish phase: the 64 x 64 intra-chunk matrices go through LDS, and K^T /
-// Q^T come as ready-made fragments from the prep kernel.  At dk <= 128 a
-// bf16 workgroup needs under 80 KB of LDS and 256 registers per lane, so two
-// share a CU and one's finish phase (no HBM reads) overlaps the other's
-// streaming.  The halves of a split chunk-head both form the dv-side
+// Finish phase: the 64 x 64 intra-chunk matrices go through LDS, and the K
+// and Q operands are gathered from the chunk's k and q rows staged in LDS.
+// At dk <= 128 a bf16 workgroup needs under 80 KB of LDS and 256 registers
+// per lane, so two share a CU and one's finish phase (no HBM reads) overlaps
+// the other's streaming.  The halves of a split chunk-head both form the dv-side
 // products ([dO; dX] V'^T, dX . V) in full.  The row sums over dk and
 // <dS, S> are written as partial sums per workgroup, which k_grad_gates adds
 // in a fixed order before the gate-gradient scan.
@@ -37,7 +37,7 @@ namespace gdn {
 // Workgroups per (chunk, head): two at dk = 128, where the finish phase is a
 // large share of a workgroup's time and overlapping it with the other
 // workgroup's streaming pays for the second read of the dv-side operands
-// (packed dk = dv = 128: 1.08 against 1.20 ms); one at dk = 256, where the
+// (packed dk = dv = 128: 0.92 against 1.03 ms); one at dk = 256, where the
 // two measured the same, and at dk = 64.
 template <class E, int DK>
 struct GradCfg {
@@ -79,8 +79,12 @@ void k_grad(Args a) {
   constexpr int FIN_BYTES = 4 * CH * LD * (int)sizeof(E);
   constexpr int LDQ = NDT * 16 + PADE;   // row stride of a wave's dq / dk staging
   constexpr int STG_BYTES = NW * CH * LDQ * (int)sizeof(E);
+  constexpr int DKW = NDH * 16;          // dk columns of this workgroup
+  constexpr int LDK = DKW + PADE;        // row stride of the K / Q row staging
+  constexpr int KQ_BYTES = 2 * CH * LDK * (int)sizeof(E);
+  constexpr int MID_BYTES = STG_BYTES > KQ_BYTES ? STG_BYTES : KQ_BYTES;
   constexpr int ECP_BYTES = 4 * NW * CH * (int)sizeof(float);  // partial column sums of E
-  constexpr int FIN_ALL = FIN_BYTES + STG_BYTES + ECP_BYTES;
+  constexpr int FIN_ALL = FIN_BYTES + MID_BYTES + ECP_BYTES;
   constexpr int SMEM = RING_BYTES > FIN_ALL ? RING_BYTES : FIN_ALL;
   static_assert(sizeof(E) == 4 || DK == 256 || SMEM + 5 * 1024 + 512 <= 80 * 1024,
                 "two bf16 workgroups must fit the CU's 160 KB of LDS at dk <= 128");
@@ -96,7 +100,9 @@ void k_grad(Args a) {
   E* sDA = sM1T + CH * LD;               //         D, A buffer
   E* sDT = sDA + CH * LD;                //         D^T, A buffer
   E* sSt = (E*)(smem + FIN_BYTES) + (size_t)wave_id() * CH * LDQ;  // this wave's dq, then dk rows
-  float* sEcp = (float*)(smem + FIN_BYTES + STG_BYTES);              // [4 NW][CH]
+  E* sKr = (E*)(smem + FIN_BYTES);       // K rows (then Q rows) of the dk columns, before sSt
+  E* sQr = sKr + CH * LDK;
+  float* sEcp = (float*)(smem + FIN_BYTES + MID_BYTES);              // [4 NW][CH]
 
   // Workgroup -> (chunk-head, half).  The two halves of a chunk-head are 8
   // workgroups apart: workgroup i runs on XCD i % 8, so both land on one XCD,
@@ -258,19 +264,17 @@ void k_grad(Args a) {
   });
   lds_barrier();  // every wave is done with the ring before its LDS is reused
 
-  // the wave's K^T and Q^T fragments, first needed after step (1)
-  frag fkp[NDT][NKC], fqp[NDT][NKC];
-  {
-    const E* KTp = (const E*)a.KTf + ch * DK * CH;
-    const E* QTp = (const E*)a.QTf + ch * DK * CH;
+  // the chunk's k and q rows over this workgroup's dk columns (zero past
+  // the chunk's end), 16 bytes per load, first needed after step (1)
+  constexpr int EPV = 16 / sizeof(E), VPRW = DKW / EPV, KQV = CH * VPRW / (64 * NW);
+  static_assert(KQV * 64 * NW == CH * VPRW, "k / q rows do not divide over the threads");
+  uint4 kr[KQV], qr[KQV];
 #pragma unroll
-    for (int n = 0; n < NDT; ++n)
-#pragma unroll
-      for (int kt = 0; kt < NKC; ++kt) {
-        const int dt = dt0 + w * NDT + n;
-        fkp[n][kt] = M::load(KTp + (size_t)(dt * NKC + kt) * FR + l * M::KPL);
-        fqp[n][kt] = M::load(QTp + (size_t)(dt * NKC + kt) * FR + l * M::KPL);
-      }
+  for (int x = 0; x < KQV; ++x) {
+    const int v = tid + 64 * NW * x, t = v / VPRW, cv = v - t * VPRW;
+    const size_t off = (row0 + (size_t)t * H) * DK + dt0 * 16 + cv * EPV;
+    kr[x] = t < len ? *reinterpret_cast<const uint4*>((const E*)a.k + off) : uint4{0u, 0u, 0u, 0u};
+    qr[x] = t < len ? *reinterpret_cast<const uint4*>((const E*)a.q + off) : uint4{0u, 0u, 0u, 0u};
   }
 
   // ---- finish phase (the staging ring is dead; its LDS is reused)
@@ -355,13 +359,42 @@ void k_grad(Args a) {
       if (l < 16) sxv[w * 16 + l] = x;
     }
   }
+#pragma unroll
+  for (int x = 0; x < KQV; ++x) {
+    const int v = tid + 64 * NW * x, t = v / VPRW, cv = v - t * VPRW;
+    *reinterpret_cast<uint4*>(sKr + t * LDK + cv * EPV) = kr[x];
+    *reinterpret_cast<uint4*>(sQr + t * LDK + cv * EPV) = qr[x];
+  }
+  lds_barrier();
+
+  // K and Q as B operands (column d, k = t in permuted order) of the wave's
+  // dk columns, gathered from the staged rows; then the staging is free
+  frag fkp[NDT][NKC], fqp[NDT][NKC];
+#pragma unroll
+  for (int n = 0; n < NDT; ++n)
+#pragma unroll
+    for (int kt = 0; kt < NKC; ++kt) {
+      const int d = (w * NDT + n) * 16 + (l & 15);
+      union {
+        frag f;
+        E e[M::KPL];
+      } uk, uq;
+#pragma unroll
+      for (int j = 0; j < M::KPL; ++j) {
+        const int t = kperm<E>(kt, g4, j);
+        uk.e[j] = sKr[t * LDK + d];
+        uq.e[j] = sQr[t * LDK + d];
+      }
+      fkp[n][kt] = uk.f;
+      fqp[n][kt] = uq.f;
+    }
   lds_barrier();
 
   // (2) dQ and dK for this wave's dk columns
   {
     // row dots over the wave's dk columns: element e of row tile i pairs
     // with slot (i & 1) * 4 + e of k-step i >> 1 (bf16) or k-step 4 i + e
-    // (fp32) of the K^T / Q^T fragments; summed over the wave's tiles, then
+    // (fp32) of the K / Q fragments; summed over the wave's tiles, then
     // over each tile's 16 columns
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -427,7 +460,7 @@ void k_grad(Args a) {
     }
     // the wave's dq, then dk, columns through its staging rows (a wave's LDS
     // operations complete in order), 16 bytes per lane and store
-    constexpr int EPV = 16 / sizeof(E), VPR = NDT * 16 / EPV, PCS = CH * VPR / 64;
+    constexpr int VPR = NDT * 16 / EPV, PCS = CH * VPR / 64;
     const int col0 = (dt0 + w * NDT) * 16;
 #pragma unroll
     for (int mat = 0; mat < 2; ++mat) {
@@ -526,6 +559,7 @@ __global__ __launch_bounds__(256) void k_grad_gates(Args a) {
 }
 
 hipError_t launch_grad(Dt dt, int dk, int dv, const Args& a, hipStream_t s) {
+  if (!a.q || !a.k) return hipErrorInvalidValue;  // the kernel reads the chunk's q and k rows
   auto f = [&]<class E, int DK, int DV>() {
     using C = GradCfg<E, DK>;
     const long units = (long)a.NC * a.H;

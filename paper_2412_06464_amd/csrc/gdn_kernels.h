@@ -37,10 +37,8 @@ struct Args {
   void* TTf;  // T^T                       rows t', k = t    64 x 64  (backward)
   void* nWT;  // -W~^T                     rows d, k = t     dk x 64  (backward)
   void* QgT;  // (diag(e^g) Q)^T           rows d, k = t     dk x 64  (backward)
-  // workspace: backward intermediates for the gradient kernel (which also
+  // workspace: backward intermediate for the gradient kernel (which also
   // reads P^T)
-  void* KTf;  // K^T                       rows d, k = t     dk x 64  (backward)
-  void* QTf;  // Q^T                       rows d, k = t     dk x 64  (backward)
   void* Ak;   // Ak^T, Ak = strictLower(Gamma K K^T)
               //                           rows t', k = t    64 x 64  (backward)
   // per-chunk matrices over dv, B operands of the gradient kernel in

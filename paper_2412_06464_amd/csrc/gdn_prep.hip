@@ -22,8 +22,8 @@
 //                  LDS in 64-wide slices of dk and dv.  Forward: W~, Kbar^T, U~,
 //                  P, diag(e^g) Q.  Backward (recompute): W~, Kbar^T, U~, and
 //                  for the reverse pass K, P^T, T^T, -W~^T, (e^g Q)^T, plus
-//                  K^T, Q^T and strictLower(Gamma K K^T)^T for
-//                  the gradient kernel.  Forward with save: both sets.
+//                  strictLower(Gamma K K^T)^T for the gradient kernel.
+//                  Forward with save: both sets.
 #include "gdn_device.h"
 #include "gdn_kernels.h"
 
@@ -84,7 +84,7 @@ template <class E, int DK, int DV, int MODE>
 __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
   using M = Mfma<E>;
   // operands of the forward pass (diag(e^g) Q, P), of the reverse pass and
-  // gradient kernel (K, P^T, T^T, -W~^T, (e^g Q)^T, K^T, Q^T, Ak^T), or both
+  // gradient kernel (K, P^T, T^T, -W~^T, (e^g Q)^T, Ak^T), or both
   constexpr bool FOUT = MODE != PREP_BWD, BOUT = MODE != PREP_FWD;
   constexpr int PADE = 16 / sizeof(E);
   constexpr int LD = CH + PADE;  // rows of 64 elements
@@ -322,9 +322,9 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
     // W~ as A operands (rows t', k = d) for the state passes
 #pragma unroll
     for (int n = 0; n < 4; ++n) afrag_put_T<E>((E*)a.Wf + ch * CH * DK, DK, n, 4 * s + w, Wt[n]);
-    // Kbar^T as A operands (rows d, k = t), with raw K^T for the gradient kernel
-    export_afrag_perm_pair<E, 256>(BOUT ? (E*)a.KTf + ch * DK * CH + (size_t)64 * s * CH : nullptr,
-                                   (E*)a.KbT + ch * DK * CH + (size_t)64 * s * CH, sX, LD, sdec);
+    // Kbar^T as A operands (rows d, k = t)
+    export_afrag_perm_pair<E, 256>(nullptr, (E*)a.KbT + ch * DK * CH + (size_t)64 * s * CH, sX, LD,
+                                   sdec);
     if (BOUT) {
       // W~ (rows t' of this wave, columns d):  sum_t T[t'][t] (b e^g K)[t][d]
       f32x4 W[4];
@@ -345,9 +345,9 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
       // -W~^T as A operands (rows d, k = t')
 #pragma unroll
       for (int n = 0; n < 4; ++n) afrag_put_T<E>((E*)a.nWT + ch * DK * CH, CH, 4 * s + n, w, -W[n]);
-      // (e^g Q)^T as A operands (rows d, k = t), with raw Q^T for the gradient kernel
-      export_afrag_perm_pair<E, 256>((E*)a.QTf + ch * DK * CH + (size_t)64 * s * CH,
-                                     (E*)a.QgT + ch * DK * CH + (size_t)64 * s * CH, sY, LD, seg);
+      // (e^g Q)^T as A operands (rows d, k = t)
+      export_afrag_perm_pair<E, 256>(nullptr, (E*)a.QgT + ch * DK * CH + (size_t)64 * s * CH, sY,
+                                     LD, seg);
     }
     lds_barrier();
   });

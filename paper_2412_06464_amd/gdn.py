@@ -117,9 +117,9 @@ def load_library():
         lib.gdn_chunk_fwd_save.restype = ctypes.c_int
         lib.gdn_chunk_fwd_save_timed.argtypes = [pp] + [P] * 8 + [P, S, P, S, P, pt]
         lib.gdn_chunk_fwd_save_timed.restype = ctypes.c_int
-        lib.gdn_chunk_bwd_saved.argtypes = [pp] + [P] * 5 + [S] + [P] * 6 + [P, S, P]
+        lib.gdn_chunk_bwd_saved.argtypes = [pp] + [P] * 7 + [S] + [P] * 6 + [P, S, P]
         lib.gdn_chunk_bwd_saved.restype = ctypes.c_int
-        lib.gdn_chunk_bwd_saved_timed.argtypes = [pp] + [P] * 5 + [S] + [P] * 6 + [P, S, P, pt]
+        lib.gdn_chunk_bwd_saved_timed.argtypes = [pp] + [P] * 7 + [S] + [P] * 6 + [P, S, P, pt]
         lib.gdn_chunk_bwd_saved_timed.restype = ctypes.c_int
         lib.gdn_recurrent_fwd.argtypes = [pp] + [P] * 8 + [P]
         lib.gdn_recurrent_fwd.restype = ctypes.c_int
@@ -310,15 +310,15 @@ def gdn_chunk_fwd_save(q, k, v, beta, log_alpha, h0=None, cu_seqlens=None, cu_se
     return o, ht, saved
 
 
-def gdn_chunk_bwd_saved(q, v, beta, dO, saved, dht=None, cu_seqlens=None, cu_seqlens_host=None,
-                        need_dh0=True, need_dlog_alpha=True, workspace=None, out=None,
-                        timer=None):
+def gdn_chunk_bwd_saved(q, k, v, beta, dO, saved, dht=None, cu_seqlens=None,
+                        cu_seqlens_host=None, need_dh0=True, need_dlog_alpha=True,
+                        workspace=None, out=None, timer=None):
     """Backward from gdn_chunk_fwd_save's buffer: dict dq, dk, dv, dbeta, dlog_alpha, dh0.
 
-    ``q`` only gives the problem's shape and dtype (its values enter through
-    ``saved``); ``v`` and ``beta`` are read.  ``need_dlog_alpha`` False skips
-    the gate gradient.  ``timer`` routes the call
-    through gdn_chunk_bwd_saved_timed.
+    ``q``, ``k``, ``v`` and ``beta`` are the tensors the saving forward read;
+    the gates and h0 enter through ``saved``.  ``need_dlog_alpha`` False
+    skips the gate gradient.  ``timer`` routes the call through
+    gdn_chunk_bwd_saved_timed.
     """
     lib = load_library()
     p, keep = make_problem(q, v, cu_seqlens, cu_seqlens_host)
@@ -332,11 +332,12 @@ def gdn_chunk_bwd_saved(q, v, beta, dO, saved, dht=None, cu_seqlens=None, cu_seq
                                    device=q.device) if need_dh0 else None)
     need = lib.gdn_chunk_bwd_saved_workspace_size(ctypes.byref(p))
     if need == 0:
-        _check(lib.gdn_chunk_bwd_saved(ctypes.byref(p), *[None] * 5, 0, *[None] * 6, None, 0,
+        _check(lib.gdn_chunk_bwd_saved(ctypes.byref(p), *[None] * 7, 0, *[None] * 6, None, 0,
                                        None))
     if workspace is None or workspace.numel() < need:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
-    args = (ctypes.byref(p), _ptr(v), _ptr(beta), _ptr(dO), _ptr(dht), _ptr(saved),
+    args = (ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(beta), _ptr(dO), _ptr(dht),
+            _ptr(saved),
             saved.numel(), _ptr(out["dq"]), _ptr(out["dk"]), _ptr(out["dv"]), _ptr(out["dbeta"]),
             _ptr(out["dlog_alpha"]), _ptr(out["dh0"]), _ptr(workspace), workspace.numel(),
             _stream(q.device))

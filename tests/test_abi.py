@@ -158,14 +158,17 @@ def test_saved_path_rejects_bad_arguments(lib):
     assert lib.gdn_chunk_fwd_save(ctypes.byref(p), *fargs, odd, ns, fake, fw, None) == 7
     assert lib.gdn_chunk_fwd_save(ctypes.byref(p), None, *fargs[1:], fake, ns, fake, fw,
                                   None) == 1
-    # v, beta, dO, dht, saved, saved_bytes, dq, dk, dv, dbeta, dlog_alpha, dh0
-    bargs = [fake, fake, fake, None, fake, ns, fake, fake, fake, fake, fake, None]
+    # q, k, v, beta, dO, dht, saved, saved_bytes, dq, dk, dv, dbeta, dlog_alpha, dh0
+    bargs = [fake, fake, fake, fake, fake, None, fake, ns, fake, fake, fake, fake, fake, None]
     assert lib.gdn_chunk_bwd_saved(ctypes.byref(p), *bargs, fake, bw - 1, None) == 5
-    bargs[5] = ns - 1
+    bargs[7] = ns - 1
     assert lib.gdn_chunk_bwd_saved(ctypes.byref(p), *bargs, fake, bw, None) == 8
-    bargs[5] = ns
-    bargs[2] = None  # dO
-    assert lib.gdn_chunk_bwd_saved(ctypes.byref(p), *bargs, fake, bw, None) == 1
+    bargs[7] = ns
+    for i in (0, 1, 4):  # q, k, dO
+        nulled = list(bargs)
+        nulled[i] = None
+        assert lib.gdn_chunk_bwd_saved(ctypes.byref(p), *nulled, fake, bw, None) == 1
+    bargs[4] = None
     bad, _ = problem(dk=96)
     assert lib.gdn_chunk_bwd_saved(ctypes.byref(bad), *bargs, fake, bw, None) == 3
 

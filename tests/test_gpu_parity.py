@@ -216,7 +216,7 @@ def run_saved(G, d):
                                         h0=d.get("h0"), cu_seqlens=d.get("cu_seqlens"))
     torch.cuda.synchronize()
     snap = saved.clone()
-    r = G.gdn_chunk_bwd_saved(d["q"], d["v"], d["beta"], d["dO"], saved, dht=d.get("dht"),
+    r = G.gdn_chunk_bwd_saved(d["q"], d["k"], d["v"], d["beta"], d["dO"], saved, dht=d.get("dht"),
                               cu_seqlens=d.get("cu_seqlens"))
     torch.cuda.synchronize()
     assert torch.equal(saved, snap), "the saved backward wrote to the saved buffer"
@@ -358,7 +358,7 @@ def test_ungated_equals_zero_gates(G, dtype, dk, dv):
     r2 = G.gdn_chunk_bwd(d["q"], d["k"], d["v"], d["beta"], None, d["dO"], h0=d["h0"],
                          dht=d["dht"])
     o3, ht3, saved = G.gdn_chunk_fwd_save(d["q"], d["k"], d["v"], d["beta"], None, h0=d["h0"])
-    r3 = G.gdn_chunk_bwd_saved(d["q"], d["v"], d["beta"], d["dO"], saved, dht=d["dht"])
+    r3 = G.gdn_chunk_bwd_saved(d["q"], d["k"], d["v"], d["beta"], d["dO"], saved, dht=d["dht"])
     torch.cuda.synchronize()
     for x, y, z, name in ((o, o2, o3, "o"), (ht, ht2, ht3, "ht")):
         assert torch.equal(x, y) and torch.equal(x, z), name
