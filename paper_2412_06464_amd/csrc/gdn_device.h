@@ -272,55 +272,6 @@ template <> __device__ inline f32x4 afrag_get_T<float>(const float* src, int mt,
   return v;
 }
 
-// A operand, permuted order, read straight from a row-major row of a global
-// matrix (`row` points at the row, k-step kt); zero when !valid.
-template <class E>
-__device__ inline typename Mfma<E>::frag load_row_perm(const E* row, int kt, bool valid);
-template <>
-__device__ inline bf16x8 load_row_perm<bf16>(const bf16* row, int kt, bool valid) {
-  typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
-  union {
-    bf16x8 f;
-    u32x2 h[2];
-  } x;
-  x.h[0] = u32x2{0u, 0u};
-  x.h[1] = u32x2{0u, 0u};
-  if (valid) {
-    const int g = lane_id() >> 4;
-    x.h[0] = *reinterpret_cast<const u32x2*>(row + 32 * kt + 4 * g);
-    x.h[1] = *reinterpret_cast<const u32x2*>(row + 32 * kt + 16 + 4 * g);
-  }
-  return x.f;
-}
-template <>
-__device__ inline float load_row_perm<float>(const float* row, int kt, bool valid) {
-  return valid ? row[kperm<float>(kt, lane_id() >> 4, 0)] : 0.f;
-}
-
-// Same, with `p` already pointing at the lane's first element of k-step 0
-// (row + 4 g for bf16, row + 4 g for fp32).
-template <class E>
-__device__ inline typename Mfma<E>::frag load_row_perm_at(const E* p, int kt, bool valid);
-template <>
-__device__ inline bf16x8 load_row_perm_at<bf16>(const bf16* p, int kt, bool valid) {
-  typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
-  union {
-    bf16x8 f;
-    u32x2 h[2];
-  } x;
-  x.h[0] = u32x2{0u, 0u};
-  x.h[1] = u32x2{0u, 0u};
-  if (valid) {
-    x.h[0] = *reinterpret_cast<const u32x2*>(p + 32 * kt);
-    x.h[1] = *reinterpret_cast<const u32x2*>(p + 32 * kt + 16);
-  }
-  return x.f;
-}
-template <>
-__device__ inline float load_row_perm_at<float>(const float* p, int kt, bool valid) {
-  return valid ? p[16 * (kt >> 2) + (kt & 3)] : 0.f;
-}
-
 // Write the A buffer (permuted order) of an R x KD matrix whose elements are
 // val(r, k).
 template <class E, int R, int KD, int NTH, class F>
@@ -377,21 +328,6 @@ __device__ inline typename Mfma<E>::frag load_frag_scaled(const E* row, int kt, 
 #pragma unroll
   for (int j = 0; j < M::KPL; ++j) x.e[j] = to_e<E>(to_f(x.e[j]) * sc[k0 + j]);
   return x.f;
-}
-
-// Asynchronous copy of one fragment per lane from global memory straight
-// into LDS (gfx950 global_load_lds): lane l's KPL elements land at
-// lds_frag + l * KPL.  `lds_frag` must be the same for the whole wave.  The
-// copy is tracked by vmcnt; a wave may read back its own fragment once the
-// compiler-inserted wait for it has passed.
-template <class E> __device__ inline void frag_to_lds_async(const E* src_lane, E* lds_frag);
-template <> __device__ inline void frag_to_lds_async<bf16>(const bf16* src_lane, bf16* lds_frag) {
-  __builtin_amdgcn_global_load_lds((const void*)src_lane,
-                                   (__attribute__((address_space(3))) void*)lds_frag, 16, 0, 0);
-}
-template <> __device__ inline void frag_to_lds_async<float>(const float* src_lane, float* lds_frag) {
-  __builtin_amdgcn_global_load_lds((const void*)src_lane,
-                                   (__attribute__((address_space(3))) void*)lds_frag, 4, 0, 0);
 }
 
 // Copy one MFMA fragment (KPL elements per lane, lane-contiguous) from global
