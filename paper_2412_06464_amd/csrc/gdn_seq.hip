@@ -49,13 +49,39 @@ inline int unit_tile_grid(int ntiles, int nunits) { return (nunits + 7) / 8 * 8 
 #ifndef GDN_SAVE_MINB
 #define GDN_SAVE_MINB GDN_SEQ_MINB
 #endif
+// L2 warm-up distance in chunks (0: none) of the saving forward and of the
+// reverse pass: where it measured faster (saving forward at dk 256: 629 ->
+// 598 us; reverse pass at dk 128: 736 -> 709 us).  Elsewhere its registers
+// spilled (reverse pass at dk 256) or its lines crowded L2 (forward at dk
+// 128).
 template <class E, int DK, int DV>
 struct SeqCfg {
   static constexpr int BV = 32;
   static constexpr int FWD_BV = DK == 256 ? GDN_FWD_BV256 : 32;
   static constexpr int SAVE_BV = DK == 256 ? GDN_SAVE_BV256 : 32;
   static constexpr int MINB = GDN_SEQ_MINB;
+  static constexpr int WARM_SAVE = sizeof(E) == 2 && DK == 256 ? 3 : 0;
+  static constexpr int WARM_BWD = sizeof(E) == 2 && DK == 128 ? 3 : 0;
 };
+
+// L2 warm-up of a later chunk: the state passes read each chunk's dk-side
+// operands when they reach it, and their latency from HBM is most of a
+// chunk's time.  The dv slices of a unit share those operands through L2;
+// here wave 0 of slice `slice` (of `nslices`) loads one dword of each of its
+// 128-byte lines (lines slice, slice + nslices, ...) of each buffer, so that
+// the slices' own loads, a few chunks later, find them in L2.  The values
+// are kept (tv) until the next call, which hands them to an empty asm
+// statement: the loads stay live, and their wait falls a chunk later.
+template <int NB>
+__device__ inline void warm_l2(const unsigned char* const (&base)[NB], const int (&lines)[NB],
+                               int slice, int nslices, float (&tv)[NB]) {
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    asm volatile("" ::"v"(tv[b]));
+    const int idx = slice + nslices * lane_id();
+    tv[b] = idx < lines[b] ? *reinterpret_cast<const float*>(base[b] + (size_t)idx * 128) : 0.f;
+  }
+}
 
 // ------------------------------------------------------------------ forward / recompute
 // SEQ_FWD  : forward, writes O and ht.
@@ -187,6 +213,8 @@ __global__ __launch_bounds__(256, (MODE == SEQ_SAVE ? GDN_SAVE_MINB : GDN_SEQ_MI
   };
   (void)PO;
 
+  constexpr int WARM = MODE == SEQ_SAVE ? SeqCfg<E, DK, DV>::WARM_SAVE : 0;
+  float tv[4] = {0.f, 0.f, 0.f, 0.f};  // warm-up loads in flight
   if (nch > 0) {
     load_wq(0);
     load_u(0);
@@ -283,6 +311,20 @@ __global__ __launch_bounds__(256, (MODE == SEQ_SAVE ? GDN_SAVE_MINB : GDN_SEQ_MI
         if (OUT) Qs[jj] = M::mma(fPc[kt], b, Qs[jj]);
       }
     load_kp(min(j + 1, nch - 1));
+    if constexpr (WARM > 0) {
+      const int jt = j + WARM;
+      if (w == 0 && jt < nch) {
+        const size_t cht = (size_t)(c0 + jt) * H + h;
+        constexpr int LK = CH * DK * (int)sizeof(E) / 128, LP = CH * CH * (int)sizeof(E) / 128;
+        const unsigned char* const base[4] = {
+            (const unsigned char*)((const E*)a.Wf + cht * CH * DK),
+            (const unsigned char*)((const E*)a.KbT + cht * DK * CH),
+            (const unsigned char*)((const E*)a.Qf + cht * CH * DK),
+            (const unsigned char*)((const E*)a.Pf + cht * CH * CH)};
+        const int lines[4] = {LK, LK, LK, LP};
+        warm_l2<4>(base, lines, tile, DV / BV, tv);
+      }
+    }
     if constexpr (STORE && !SPREAD)
       copy_out_frags<E, CH, BV, LDV, 256, true>((E*)a.Vp + ch * CH * DV, DV / M::K, v0,
                                                 sOut + (j & 1) * CH * LDV);
@@ -468,6 +510,8 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
     load_first(nch - 1);
     load_second(nch - 1);
   }
+  constexpr int WARM = SeqCfg<E, DK, DV>::WARM_BWD;
+  float tv[5] = {0.f, 0.f, 0.f, 0.f, 0.f};  // warm-up loads in flight
   size_t prev_ch = 0;  // chunk whose dX rows wait in sOut
   for (int j = nch - 1; j >= 0; --j) {
     const int start = s0 + j * CH, len = min(CH, L - j * CH);
@@ -579,6 +623,21 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
                                 w, len);
     }
     prev_ch = ch;
+    if constexpr (WARM > 0) {
+      const int jt = j - WARM;
+      if (w == 0 && jt >= 0) {
+        const size_t cht = (size_t)(c0 + jt) * H + h;
+        constexpr int LK = CH * DK * (int)sizeof(E) / 128, LC = CH * CH * (int)sizeof(E) / 128;
+        const unsigned char* const base[5] = {
+            (const unsigned char*)((const E*)a.Kf + cht * CH * DK),
+            (const unsigned char*)((const E*)a.QgT + cht * DK * CH),
+            (const unsigned char*)((const E*)a.nWT + cht * DK * CH),
+            (const unsigned char*)((const E*)a.PTf + cht * CH * CH),
+            (const unsigned char*)((const E*)a.TTf + cht * CH * CH)};
+        const int lines[5] = {LK, LK, LK, LC, LC};
+        warm_l2<5>(base, lines, tile, DV / BV, tv);
+      }
+    }
   }
   if (nch > 0) {
     lds_barrier();
