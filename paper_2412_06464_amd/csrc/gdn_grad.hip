@@ -100,8 +100,8 @@ void k_grad(Args a) {
   E* sDA = sM1T + CH * LD;               //         D, A buffer
   E* sDT = sDA + CH * LD;                //         D^T, A buffer
   E* sSt = (E*)(smem + FIN_BYTES) + (size_t)wave_id() * CH * LDQ;  // this wave's dq, then dk rows
-  E* sKr = (E*)(smem + FIN_BYTES);       // K rows (then Q rows) of the dk columns, before sSt
-  E* sQr = sKr + CH * LDK;
+  E* sKr = (E*)(smem + FIN_BYTES);       // the chunk's k rows over the dk columns (under sSt)
+  E* sQr = sKr + CH * LDK;               // and its q rows
   float* sEcp = (float*)(smem + FIN_BYTES + MID_BYTES);              // [4 NW][CH]
 
   // Workgroup -> (chunk-head, half).  The two halves of a chunk-head are 8
