@@ -181,6 +181,7 @@ def test_bwd_ragged(G, oracle_mod, dtype, dk, dv, B, T, H):
     ("alpha_one", dict(log_alpha_value=0.0)),
     ("beta_0_2", dict(beta_scale=2.0, log_alpha_scale=0.1)),
     ("beta_zero", dict(beta_value=0.0, log_alpha_scale=0.05)),
+    ("strong_decay", dict(log_alpha_scale=8.0)),  # in-chunk log gates to about -350
 ])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_bwd_stress(G, oracle_mod, label, kw, dtype):
@@ -252,10 +253,19 @@ def test_saved_ragged(G, oracle_mod, dtype, dk, dv, B, T, H):
 @pytest.mark.parametrize("label,kw", [
     ("alpha_one", dict(log_alpha_value=0.0)),
     ("beta_0_2", dict(beta_scale=2.0, log_alpha_scale=0.1)),
+    ("strong_decay", dict(log_alpha_scale=8.0)),
 ])
 def test_saved_stress(G, oracle_mod, label, kw):
     inp = make_inputs(1, 200, 2, 64, 64, "f32", seed=12, h0_std=0.05, backward=True, **kw)
     check_saved(G, oracle_mod, inp, TOL["f32"], "saved_stress_" + label)
+
+
+def test_saved_strong_decay_bf16_256_512(G, oracle_mod):
+    """The bench shape's saved path when every decay factor past a few tokens
+    underflows fp32 (per-token log gates of about -5.5)."""
+    inp = make_inputs(1, 200, 2, 256, 512, "bf16", seed=8, h0_std=0.05, backward=True,
+                      log_alpha_scale=8.0)
+    check_saved(G, oracle_mod, inp, TOL["bf16"], "saved_strong_bf16_256")
 
 
 @pytest.mark.parametrize("dtype,dk,dv", [("f32", 64, 64), ("bf16", 256, 512)])
