@@ -62,6 +62,8 @@ struct SeqCfg {
   static constexpr int MINB = GDN_SEQ_MINB;
   static constexpr int WARM_SAVE = sizeof(E) == 2 && DK == 256 ? 3 : 0;
   static constexpr int WARM_BWD = sizeof(E) == 2 && DK == 128 ? 3 : 0;
+  // the reverse pass at dk 256 warms through LDS (its registers are all in use)
+  static constexpr int WARM_BWD_LDS = sizeof(E) == 2 && DK == 256 ? 3 : 0;
 };
 
 // L2 warm-up of a later chunk: the state passes read each chunk's dk-side
@@ -81,6 +83,25 @@ __device__ inline void warm_l2(const unsigned char* const (&base)[NB], const int
     const int idx = slice + nslices * lane_id();
     tv[b] = idx < lines[b] ? *reinterpret_cast<const float*>(base[b] + (size_t)idx * 128) : 0.f;
   }
+}
+
+// The same warm-up with the loads landing in LDS (global_load_lds_dword into
+// `sink`, 256 bytes that nothing reads) instead of registers, for a kernel
+// with no register to spare: no VGPR stays live.  The compiler does not see
+// these loads, so its own vmcnt waits only get stricter, never looser; the
+// caller waits for them (vmcnt(0)) before the workgroup ends.
+template <int NB>
+__device__ inline void warm_l2_lds(const unsigned char* const (&base)[NB], const int (&lines)[NB],
+                                   int slice, int nslices, float* sink) {
+  const unsigned lds = (unsigned)(uintptr_t)sink;
+  const int idx = slice + nslices * lane_id();
+  const unsigned off = (unsigned)idx * 128u;  // lane offset (the bases are uniform, in SGPRs)
+#pragma unroll
+  for (int b = 0; b < NB; ++b)
+    if (idx < lines[b])
+      asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, %2" ::"s"(lds), "v"(off),
+                   "s"(base[b])
+                   : "memory");
 }
 
 // ------------------------------------------------------------------ forward / recompute
@@ -390,6 +411,8 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
   __shared__ __align__(16) E sSs[DK * LDV];     // dS rows for the store
   __shared__ __align__(16) E sOut[CH * LDV];    // dX rows for the store
   __shared__ __align__(16) E sDv[CH * LDV];     // dv rows for the store (per wave)
+  constexpr int WARM_LDS = SeqCfg<E, DK, DV>::WARM_BWD_LDS;
+  __shared__ __align__(16) float sSink[WARM_LDS > 0 ? 64 : 1];  // warm-up loads land here
 
   int unit, tile;
   if (!map_unit_tile(DV / BV, a.N * a.H, unit, tile)) return;
@@ -638,7 +661,23 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
         warm_l2<5>(base, lines, tile, DV / BV, tv);
       }
     }
+    if constexpr (WARM_LDS > 0) {
+      const int jt = j - WARM_LDS;
+      if (w == 0 && jt >= 0) {
+        const size_t cht = (size_t)(c0 + jt) * H + h;
+        constexpr int LK = CH * DK * (int)sizeof(E) / 128, LC = CH * CH * (int)sizeof(E) / 128;
+        const unsigned char* const base[5] = {
+            (const unsigned char*)((const E*)a.Kf + cht * CH * DK),
+            (const unsigned char*)((const E*)a.QgT + cht * DK * CH),
+            (const unsigned char*)((const E*)a.nWT + cht * DK * CH),
+            (const unsigned char*)((const E*)a.PTf + cht * CH * CH),
+            (const unsigned char*)((const E*)a.TTf + cht * CH * CH)};
+        const int lines[5] = {LK, LK, LK, LC, LC};
+        warm_l2_lds<5>(base, lines, tile, DV / BV, sSink);
+      }
+    }
   }
+  if constexpr (WARM_LDS > 0) wait_vmcnt<0>();  // no LDS write in flight past the end
   if (nch > 0) {
     lds_barrier();
     copy_out_frags<E, CH, BV, LDV, 256, true>((E*)a.dXb + prev_ch * CH * DV, DV / M::K, v0, sOut);
