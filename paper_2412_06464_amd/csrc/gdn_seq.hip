@@ -49,21 +49,46 @@ inline int unit_tile_grid(int ntiles, int nunits) { return (nunits + 7) / 8 * 8 
 #ifndef GDN_SAVE_MINB
 #define GDN_SAVE_MINB GDN_SEQ_MINB
 #endif
-// L2 warm-up distance in chunks (0: none) of the saving forward and of the
-// reverse pass: where it measured faster (saving forward at dk 256: 629 ->
-// 598 us; reverse pass at dk 128: 736 -> 709 us).  Elsewhere its registers
-// spilled (reverse pass at dk 256) or its lines crowded L2 (forward at dk
-// 128).
+// L2 warm-up distance in chunks (0: none) of each state pass, where it
+// measured faster.  The warm-up loads land in LDS; an earlier form that kept
+// them in registers was slower wherever both were measured (its results had
+// to stay live, and it spilled the reverse pass at dk 256).  At dk 256:
+// saving forward 629 -> 548 us (598 through registers; distances 3 to 6
+// within 4 us); reverse pass 645 -> 587 us (distance 2: 626, 3: 596, 5 and
+// 6: 592).  At dk 128: reverse pass 736 -> 684 us (709 through registers;
+// distance 4: 699); in the saving forward its lines crowd L2 (distance 1:
+// 605 -> 631 us, 3: 651 us).  The plain forward and the recompute pass at
+// dk 256 measured within 3% either way (none kept).
+#ifndef GDN_WARM_SAVE
+#define GDN_WARM_SAVE 4
+#endif
+#ifndef GDN_WARM_STORE
+#define GDN_WARM_STORE 0
+#endif
+#ifndef GDN_WARM_FWD
+#define GDN_WARM_FWD 0
+#endif
+#ifndef GDN_WARM_BWD256
+#define GDN_WARM_BWD256 4
+#endif
+#ifndef GDN_WARM_BWD128
+#define GDN_WARM_BWD128 3
+#endif
+#ifndef GDN_WARM_SAVE128
+#define GDN_WARM_SAVE128 0
+#endif
 template <class E, int DK, int DV>
 struct SeqCfg {
   static constexpr int BV = 32;
   static constexpr int FWD_BV = DK == 256 ? GDN_FWD_BV256 : 32;
   static constexpr int SAVE_BV = DK == 256 ? GDN_SAVE_BV256 : 32;
   static constexpr int MINB = GDN_SEQ_MINB;
-  static constexpr int WARM_SAVE = sizeof(E) == 2 && DK == 256 ? 3 : 0;
-  static constexpr int WARM_BWD = sizeof(E) == 2 && DK == 128 ? 3 : 0;
-  // the reverse pass at dk 256 warms through LDS (its registers are all in use)
-  static constexpr int WARM_BWD_LDS = sizeof(E) == 2 && DK == 256 ? 3 : 0;
+  static constexpr bool B256 = sizeof(E) == 2 && DK == 256;
+  static constexpr bool B128 = sizeof(E) == 2 && DK == 128;
+  static constexpr int WARM_SAVE = B256 ? GDN_WARM_SAVE : B128 ? GDN_WARM_SAVE128 : 0;
+  static constexpr int WARM_STORE = B256 ? GDN_WARM_STORE : 0;
+  static constexpr int WARM_FWD = B256 ? GDN_WARM_FWD : 0;
+  static constexpr int WARM_BWD = B256 ? GDN_WARM_BWD256 : B128 ? GDN_WARM_BWD128 : 0;
 };
 
 // L2 warm-up of a later chunk: the state passes read each chunk's dk-side
@@ -71,28 +96,14 @@ struct SeqCfg {
 // chunk's time.  The dv slices of a unit share those operands through L2;
 // here wave 0 of slice `slice` (of `nslices`) loads one dword of each of its
 // 128-byte lines (lines slice, slice + nslices, ...) of each buffer, so that
-// the slices' own loads, a few chunks later, find them in L2.  The values
-// are kept (tv) until the next call, which hands them to an empty asm
-// statement: the loads stay live, and their wait falls a chunk later.
-template <int NB>
-__device__ inline void warm_l2(const unsigned char* const (&base)[NB], const int (&lines)[NB],
-                               int slice, int nslices, float (&tv)[NB]) {
-#pragma unroll
-  for (int b = 0; b < NB; ++b) {
-    asm volatile("" ::"v"(tv[b]));
-    const int idx = slice + nslices * lane_id();
-    tv[b] = idx < lines[b] ? *reinterpret_cast<const float*>(base[b] + (size_t)idx * 128) : 0.f;
-  }
-}
-
-// The same warm-up with the loads landing in LDS (global_load_lds_dword into
-// `sink`, 256 bytes that nothing reads) instead of registers, for a kernel
-// with no register to spare: no VGPR stays live.  The compiler does not see
+// the slices' own loads, a few chunks later, find them in L2.  The loads
+// land in LDS (global_load_lds_dword into `sink`, 256 bytes that nothing
+// reads), so no register stays live for them.  The compiler does not see
 // these loads, so its own vmcnt waits only get stricter, never looser; the
 // caller waits for them (vmcnt(0)) before the workgroup ends.
 template <int NB>
-__device__ inline void warm_l2_lds(const unsigned char* const (&base)[NB], const int (&lines)[NB],
-                                   int slice, int nslices, float* sink) {
+__device__ inline void warm_l2(const unsigned char* const (&base)[NB], const int (&lines)[NB],
+                               int slice, int nslices, float* sink) {
   const unsigned lds = (unsigned)(uintptr_t)sink;
   const int idx = slice + nslices * lane_id();
   const unsigned off = (unsigned)idx * 128u;  // lane offset (the bases are uniform, in SGPRs)
@@ -134,6 +145,10 @@ __global__ __launch_bounds__(256, (MODE == SEQ_SAVE ? GDN_SAVE_MINB : GDN_SEQ_MI
   __shared__ __align__(16) E sSs[STORE ? 2 * DK * LDV : 1];  // state rows, by chunk parity
   __shared__ __align__(16) E sOut[STORE ? 2 * CH * LDV : 1];  // V' rows, by chunk parity
   __shared__ __align__(16) E sO[OUT ? CH * LDV : 1];      // O rows for the store
+  using SC = SeqCfg<E, DK, DV>;
+  constexpr int WARM = MODE == SEQ_SAVE ? SC::WARM_SAVE : MODE == SEQ_STORE ? SC::WARM_STORE
+                                                                           : SC::WARM_FWD;
+  __shared__ __align__(16) float sSink[WARM > 0 ? 64 : 1];  // warm-up loads land here
 
   int unit, tile;
   if (!map_unit_tile(DV / BV, a.N * a.H, unit, tile)) return;
@@ -234,8 +249,6 @@ __global__ __launch_bounds__(256, (MODE == SEQ_SAVE ? GDN_SAVE_MINB : GDN_SEQ_MI
   };
   (void)PO;
 
-  constexpr int WARM = MODE == SEQ_SAVE ? SeqCfg<E, DK, DV>::WARM_SAVE : 0;
-  float tv[4] = {0.f, 0.f, 0.f, 0.f};  // warm-up loads in flight
   if (nch > 0) {
     load_wq(0);
     load_u(0);
@@ -340,10 +353,10 @@ __global__ __launch_bounds__(256, (MODE == SEQ_SAVE ? GDN_SAVE_MINB : GDN_SEQ_MI
         const unsigned char* const base[4] = {
             (const unsigned char*)((const E*)a.Wf + cht * CH * DK),
             (const unsigned char*)((const E*)a.KbT + cht * DK * CH),
-            (const unsigned char*)((const E*)a.Qf + cht * CH * DK),
-            (const unsigned char*)((const E*)a.Pf + cht * CH * CH)};
-        const int lines[4] = {LK, LK, LK, LP};
-        warm_l2<4>(base, lines, tile, DV / BV, tv);
+            (const unsigned char*)(OUT ? (const E*)a.Qf + cht * CH * DK : (const E*)a.Wf),
+            (const unsigned char*)(OUT ? (const E*)a.Pf + cht * CH * CH : (const E*)a.Wf)};
+        const int lines[4] = {LK, LK, OUT ? LK : 0, OUT ? LP : 0};
+        warm_l2<4>(base, lines, tile, DV / BV, sSink);
       }
     }
     if constexpr (STORE && !SPREAD)
@@ -357,6 +370,7 @@ __global__ __launch_bounds__(256, (MODE == SEQ_SAVE ? GDN_SAVE_MINB : GDN_SEQ_MI
           sO[(w * 16 + acc_row(e)) * LDV + jj * 16 + acc_col()] = to_e<E>(Qs[jj][e]);
     }
   }
+  if constexpr (WARM > 0) wait_vmcnt<0>();  // no LDS write in flight past the end
   // what the last chunk leaves pending
   if (nch > 0) {
     const size_t chl = (size_t)(c0 + nch - 1) * H + h;
@@ -411,8 +425,8 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
   __shared__ __align__(16) E sSs[DK * LDV];     // dS rows for the store
   __shared__ __align__(16) E sOut[CH * LDV];    // dX rows for the store
   __shared__ __align__(16) E sDv[CH * LDV];     // dv rows for the store (per wave)
-  constexpr int WARM_LDS = SeqCfg<E, DK, DV>::WARM_BWD_LDS;
-  __shared__ __align__(16) float sSink[WARM_LDS > 0 ? 64 : 1];  // warm-up loads land here
+  constexpr int WARM = SeqCfg<E, DK, DV>::WARM_BWD;
+  __shared__ __align__(16) float sSink[WARM > 0 ? 64 : 1];  // warm-up loads land here
 
   int unit, tile;
   if (!map_unit_tile(DV / BV, a.N * a.H, unit, tile)) return;
@@ -533,8 +547,6 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
     load_first(nch - 1);
     load_second(nch - 1);
   }
-  constexpr int WARM = SeqCfg<E, DK, DV>::WARM_BWD;
-  float tv[5] = {0.f, 0.f, 0.f, 0.f, 0.f};  // warm-up loads in flight
   size_t prev_ch = 0;  // chunk whose dX rows wait in sOut
   for (int j = nch - 1; j >= 0; --j) {
     const int start = s0 + j * CH, len = min(CH, L - j * CH);
@@ -658,26 +670,11 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
             (const unsigned char*)((const E*)a.PTf + cht * CH * CH),
             (const unsigned char*)((const E*)a.TTf + cht * CH * CH)};
         const int lines[5] = {LK, LK, LK, LC, LC};
-        warm_l2<5>(base, lines, tile, DV / BV, tv);
-      }
-    }
-    if constexpr (WARM_LDS > 0) {
-      const int jt = j - WARM_LDS;
-      if (w == 0 && jt >= 0) {
-        const size_t cht = (size_t)(c0 + jt) * H + h;
-        constexpr int LK = CH * DK * (int)sizeof(E) / 128, LC = CH * CH * (int)sizeof(E) / 128;
-        const unsigned char* const base[5] = {
-            (const unsigned char*)((const E*)a.Kf + cht * CH * DK),
-            (const unsigned char*)((const E*)a.QgT + cht * DK * CH),
-            (const unsigned char*)((const E*)a.nWT + cht * DK * CH),
-            (const unsigned char*)((const E*)a.PTf + cht * CH * CH),
-            (const unsigned char*)((const E*)a.TTf + cht * CH * CH)};
-        const int lines[5] = {LK, LK, LK, LC, LC};
-        warm_l2_lds<5>(base, lines, tile, DV / BV, sSink);
+        warm_l2<5>(base, lines, tile, DV / BV, sSink);
       }
     }
   }
-  if constexpr (WARM_LDS > 0) wait_vmcnt<0>();  // no LDS write in flight past the end
+  if constexpr (WARM > 0) wait_vmcnt<0>();  // no LDS write in flight past the end
   if (nch > 0) {
     lds_barrier();
     copy_out_frags<E, CH, BV, LDV, 256, true>((E*)a.dXb + prev_ch * CH * DV, DV / M::K, v0, sOut);
