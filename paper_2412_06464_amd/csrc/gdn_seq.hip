@@ -54,11 +54,15 @@ inline int unit_tile_grid(int ntiles, int nunits) { return (nunits + 7) / 8 * 8 
 // them in registers was slower wherever both were measured (its results had
 // to stay live, and it spilled the reverse pass at dk 256).  At dk 256:
 // saving forward 629 -> 548 us (598 through registers; distances 3 to 6
-// within 4 us); reverse pass 645 -> 587 us (distance 2: 626, 3: 596, 5 and
-// 6: 592).  At dk 128: reverse pass 736 -> 684 us (709 through registers;
-// distance 4: 699); in the saving forward its lines crowd L2 (distance 1:
-// 605 -> 631 us, 3: 651 us).  The plain forward and the recompute pass at
-// dk 256 measured within 3% either way (none kept).
+// within 4 us), 524 us when each wave also warms its own U~ tiles; reverse
+// pass 645 -> 587 us (distance 2: 626, 3: 596, 5 and 6: 592).  At dk 128:
+// reverse pass 736 -> 684 us (709 through registers; distance 4: 699); in
+// the saving forward its lines crowd L2 (distance 1: 605 -> 631 us, 3:
+// 651 us).  Measured and not kept: the plain forward and the recompute pass
+// at dk 256 (within 3% either way); one load per 64 bytes instead of per
+// 128-byte line (slower in both passes: L2 fills whole lines); the reverse
+// pass warming its own dO rows (dk 256: within noise; dk 128: 682 -> 743
+// us); warming the gates and betas too (within noise).
 #ifndef GDN_WARM_SAVE
 #define GDN_WARM_SAVE 4
 #endif
@@ -102,14 +106,15 @@ struct SeqCfg {
 // these loads, so its own vmcnt waits only get stricter, never looser; the
 // caller waits for them (vmcnt(0)) before the workgroup ends.
 template <int NB>
-__device__ inline void warm_l2(const unsigned char* const (&base)[NB], const int (&lines)[NB],
+__device__ inline void warm_l2(const unsigned char* const (&base)[NB], const int (&bytes)[NB],
                                int slice, int nslices, float* sink) {
+  constexpr int WL = 128;  // L2 line
   const unsigned lds = (unsigned)(uintptr_t)sink;
   const int idx = slice + nslices * lane_id();
-  const unsigned off = (unsigned)idx * 128u;  // lane offset (the bases are uniform, in SGPRs)
+  const unsigned off = (unsigned)idx * WL;  // lane offset (the bases are uniform, in SGPRs)
 #pragma unroll
   for (int b = 0; b < NB; ++b)
-    if (idx < lines[b])
+    if (idx < bytes[b] / WL)
       asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, %2" ::"s"(lds), "v"(off),
                    "s"(base[b])
                    : "memory");
@@ -349,14 +354,21 @@ __global__ __launch_bounds__(256, (MODE == SEQ_SAVE ? GDN_SAVE_MINB : GDN_SEQ_MI
       const int jt = j + WARM;
       if (w == 0 && jt < nch) {
         const size_t cht = (size_t)(c0 + jt) * H + h;
-        constexpr int LK = CH * DK * (int)sizeof(E) / 128, LP = CH * CH * (int)sizeof(E) / 128;
+        constexpr int LK = CH * DK * (int)sizeof(E), LP = CH * CH * (int)sizeof(E);
         const unsigned char* const base[4] = {
             (const unsigned char*)((const E*)a.Wf + cht * CH * DK),
             (const unsigned char*)((const E*)a.KbT + cht * DK * CH),
             (const unsigned char*)(OUT ? (const E*)a.Qf + cht * CH * DK : (const E*)a.Wf),
             (const unsigned char*)(OUT ? (const E*)a.Pf + cht * CH * CH : (const E*)a.Wf)};
-        const int lines[4] = {LK, LK, OUT ? LK : 0, OUT ? LP : 0};
-        warm_l2<4>(base, lines, tile, DV / BV, sSink);
+        const int nbytes[4] = {LK, LK, OUT ? LK : 0, OUT ? LP : 0};
+        warm_l2<4>(base, nbytes, tile, DV / BV, sSink);
+      }
+      if (jt < nch) {  // this wave's U~ tiles (read by this slice only)
+        const unsigned char* const base[1] = {(const unsigned char*)(
+            (const E*)a.Uc + ((size_t)(c0 + jt) * H + h) * CH * DV +
+            ((size_t)w * (DV / 16) + v0 / 16) * 256)};
+        const int nb[1] = {NTV * 256 * (int)sizeof(E)};
+        warm_l2<1>(base, nb, 0, 1, sSink);
       }
     }
     if constexpr (STORE && !SPREAD)
@@ -662,15 +674,15 @@ __global__ __launch_bounds__(256, GDN_SEQ_MINB) void k_bwd_seq(Args a) {
       const int jt = j - WARM;
       if (w == 0 && jt >= 0) {
         const size_t cht = (size_t)(c0 + jt) * H + h;
-        constexpr int LK = CH * DK * (int)sizeof(E) / 128, LC = CH * CH * (int)sizeof(E) / 128;
+        constexpr int LK = CH * DK * (int)sizeof(E), LC = CH * CH * (int)sizeof(E);
         const unsigned char* const base[5] = {
             (const unsigned char*)((const E*)a.Kf + cht * CH * DK),
             (const unsigned char*)((const E*)a.QgT + cht * DK * CH),
             (const unsigned char*)((const E*)a.nWT + cht * DK * CH),
             (const unsigned char*)((const E*)a.PTf + cht * CH * CH),
             (const unsigned char*)((const E*)a.TTf + cht * CH * CH)};
-        const int lines[5] = {LK, LK, LK, LC, LC};
-        warm_l2<5>(base, lines, tile, DV / BV, sSink);
+        const int nbytes[5] = {LK, LK, LK, LC, LC};
+        warm_l2<5>(base, nbytes, tile, DV / BV, sSink);
       }
     }
   }
