@@ -58,8 +58,9 @@ inline int unit_tile_grid(int ntiles, int nunits) { return (nunits + 7) / 8 * 8 
 // pass 645 -> 587 us (distance 2: 626, 3: 596, 5 and 6: 592).  At dk 128:
 // reverse pass 736 -> 684 us (709 through registers; distance 4: 699); in
 // the saving forward its lines crowd L2 (distance 1: 605 -> 631 us, 3:
-// 651 us).  Measured and not kept: the plain forward and the recompute pass
-// at dk 256 (within 3% either way); one load per 64 bytes instead of per
+// 651 us).  Recompute pass at dk 256: 444 -> 411 us (distance 3: 423).
+// Measured and not kept: the plain forward at dk 256 (one round of 64-wide
+// slices; within 2% at distances 3 and 4); one load per 64 bytes instead of per
 // 128-byte line (slower in both passes: L2 fills whole lines); the reverse
 // pass warming its own dO rows (dk 256: within noise; dk 128: 682 -> 743
 // us); warming the gates and betas too (within noise).
@@ -67,7 +68,7 @@ inline int unit_tile_grid(int ntiles, int nunits) { return (nunits + 7) / 8 * 8 
 #define GDN_WARM_SAVE 4
 #endif
 #ifndef GDN_WARM_STORE
-#define GDN_WARM_STORE 0
+#define GDN_WARM_STORE 4
 #endif
 #ifndef GDN_WARM_FWD
 #define GDN_WARM_FWD 0
