@@ -29,23 +29,37 @@
 
 namespace gdn {
 
+// One workgroup of 256 threads.  Sequences are taken 256 at a time: thread
+// i reads the bounds of sequence base + i, an exclusive scan of the chunk
+// counts in LDS (plus the running total of the earlier groups) gives its
+// first chunk, and the thread writes that sequence's chunk entries.
 __global__ void k_chunk_table(const int32_t* cu, int N, int T, int4* info, int* seq_chunk0) {
-  if (threadIdx.x == 0) {
-    int acc = 0;
-    for (int n = 0; n < N; ++n) {
-      seq_chunk0[n] = acc;
-      const int L = cu ? cu[n + 1] - cu[n] : T;
-      acc += (L + CH - 1) / CH;
+  __shared__ int scan[2][256];
+  const int tid = threadIdx.x;
+  int carry = 0;  // chunks of the sequences before this group
+  for (int base = 0; base < N; base += 256) {
+    const int n = base + tid;
+    const int s = n < N ? (cu ? cu[n] : n * T) : 0;
+    const int L = n < N ? (cu ? cu[n + 1] - s : T) : 0;
+    const int c = (L + CH - 1) / CH;
+    // inclusive Hillis-Steele scan of c over the 256 threads
+    int p = 0;
+    scan[p][tid] = c;
+    __syncthreads();
+    for (int d = 1; d < 256; d <<= 1) {
+      scan[p ^ 1][tid] = scan[p][tid] + (tid >= d ? scan[p][tid - d] : 0);
+      p ^= 1;
+      __syncthreads();
     }
-    seq_chunk0[N] = acc;
+    const int c0 = carry + scan[p][tid] - c;
+    if (n < N) {
+      seq_chunk0[n] = c0;
+      for (int j = 0; j < c; ++j) info[c0 + j] = make_int4(n, s + j * CH, min(CH, L - j * CH), 0);
+    }
+    carry += scan[p][255];
+    __syncthreads();  // the scan buffers are reused by the next group
   }
-  __syncthreads();
-  for (int n = threadIdx.x; n < N; n += blockDim.x) {
-    const int s = cu ? cu[n] : n * T;
-    const int L = cu ? cu[n + 1] - cu[n] : T;
-    const int c0 = seq_chunk0[n];
-    for (int j = 0; j * CH < L; ++j) info[c0 + j] = make_int4(n, s + j * CH, min(CH, L - j * CH), 0);
-  }
+  if (tid == 0) seq_chunk0[N] = carry;
 }
 
 // ------------------------------------------------------------------ prep

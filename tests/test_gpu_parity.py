@@ -139,6 +139,19 @@ def test_fwd_packed(G, oracle_mod, dtype, dk, dv):
     check_fwd(G, oracle_mod, inp, TOL[dtype], "fwd_packed_%s_%d" % (dtype, dk))
 
 
+def test_packed_many_sequences(G, oracle_mod):
+    """More than 256 sequences (the chunk table scans them 256 at a time),
+    lengths 0 to 69, forward and stateless backward."""
+    rng = np.random.default_rng(11)
+    lens = rng.integers(0, 70, size=300)
+    lens[5] = 0
+    cu = torch.tensor(np.concatenate([[0], np.cumsum(lens)]), dtype=torch.int32)
+    inp = make_inputs(1, int(cu[-1]), 1, 64, 64, "f32", seed=12, h0_std=0.05, backward=True,
+                      cu_seqlens=cu)
+    check_fwd(G, oracle_mod, inp, TOL["f32"], "packed_many")
+    check_bwd(G, oracle_mod, inp, TOL["f32"], "packed_many")
+
+
 def test_fwd_split_carry(G):
     inp = to_dev(make_inputs(2, 300, 2, 128, 128, "bf16", seed=5, h0_std=0.05))
     o, ht = run_fwd(G, inp)
