@@ -63,7 +63,10 @@ inline int unit_tile_grid(int ntiles, int nunits) { return (nunits + 7) / 8 * 8 
 // slices; within 2% at distances 3 and 4); one load per 64 bytes instead of per
 // 128-byte line (slower in both passes: L2 fills whole lines); the reverse
 // pass warming its own dO rows (dk 256: within noise; dk 128: 682 -> 743
-// us); warming the gates and betas too (within noise).
+// us); warming the gates and betas too (within noise); warming the chunks
+// before the loop's first warm-up at the start of the workgroup (every
+// workgroup starts at once: reverse pass 587 -> 611 us, recompute pass 411
+// -> 504 us).
 #ifndef GDN_WARM_SAVE
 #define GDN_WARM_SAVE 4
 #endif
