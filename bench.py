@@ -8,14 +8,27 @@ For forward+backward workloads that is a training step: gdn_chunk_fwd_save
 (the forward, keeping what the backward needs) followed by
 gdn_chunk_bwd_saved; the stateless pair gdn_chunk_fwd + gdn_chunk_bwd (the
 backward recomputes the chunk states) is timed the same way afterwards and
-reported beside it.  Forward-only workloads run gdn_chunk_fwd.  Inputs,
-outputs, the saved buffer and the workspaces are resident in HBM before the
-timed region; the timed region is K steps between two device
-synchronisations.  Per-kernel durations come from HIP events that the
-library records around each of its launches on the same stream (the *_timed
-entry points), one event set per step.
+reported beside it.  Forward-only workloads run gdn_chunk_fwd.
 
-Prints one JSON line (rank 0; this build runs on one GPU only).
+Timing.  Inputs, outputs, the saved buffer and the workspaces are resident in
+HBM before anything is timed.  After W untimed warm-up steps, K steps are
+timed one by one with HIP events on the launch stream, each after a 512 MiB
+write to a scratch buffer that evicts the 256 MB last-level cache and the
+L2s ("cold"); the headline is the median cold step, with p10 and p90.  K
+more steps back to back without the write give the warm figures.  The
+library records events around each of its own launches on the same stream
+(the *_timed entry points), so every kernel's duration comes from the same
+timed steps.
+
+Roofline.  Each kernel is credited only with the algorithmic work of its step
+of the method: the FLOP of its products at full chunk size, and the bytes of
+the call's own tensors (inputs, outputs, initial and final states) that it
+reads or writes.  Intermediates the kernels hand each other (chunk states
+and their gradients, the chunk-local operands, V', dX) are design overhead
+and earn nothing; `traffic_ratio` = HBM bytes measured by counters / those
+algorithmic bytes.
+
+Prints one JSON line (this build runs on one GPU only).
 """
 import argparse
 import hashlib
@@ -38,13 +51,17 @@ PEAK_HBM = 8.0e12          # bytes/s, MI355X HBM3E
 PEAK_MFMA_BF16 = 2.5e15    # dense bf16 MFMA FLOP/s
 PEAK_MFMA_F32 = 157.3e12   # fp32 matrix FLOP/s
 PEAK_VALU_F32 = 157.3e12   # fp32 vector FLOP/s (256 CUs x 2.4 GHz, packed FMA)
+FLUSH_BYTES = 512 << 20    # scratch write before every cold step
 CH = 64
+TOL = {"f32": 1e-4, "bf16": 2e-2}
 
+
+# ------------------------------------------------------------------ algorithmic work
 
 def path_flops(w, tokens_heads):
     """Algorithmic FLOP of the path per step (full C x C products counted).
     Forward 6 dk dv + 6 C dk + 4 C dv + C^2/3 per token-head; backward
-    12 dk dv + 12 C dk + 8 C dv + 4 C^2 (the stateless recompute not credited)."""
+    12 dk dv + 12 C dk + 8 C dv + 4 C^2 (a stateless recompute not credited)."""
     dk, dv, C = w.dk, w.dv, CH
     f = 6 * dk * dv + 6 * C * dk + 4 * C * dv + C * C / 3
     if w.backward:
@@ -56,153 +73,69 @@ def path_bytes(w, tokens_heads, n_states, has_h0):
     """Algorithmic HBM bytes per step: every call reads its inputs and writes
     its outputs once.  Forward (2 dk + 2 dv) e + 8 per token-head (q, k, v, o,
     beta, log_alpha); backward (4 dk + 3 dv) e + 16 (q, k, v, dO in; dq, dk, dv
-    out; gates in, gate gradients out); plus the fp32 states (ht, h0 if
-    given, and dht, dh0 for the backward)."""
+    out; gates in, gate gradients out); plus the fp32 states of every
+    (sequence, head): ht, h0 if given, and dht, dh0 for the backward."""
     e = 4 if w.dtype == "f32" else 2
     dk, dv = w.dk, w.dv
-    st = n_states * dk * dv * 4
+    st = n_states * w.H * dk * dv * 4
     b = ((2 * dk + 2 * dv) * e + 8) * tokens_heads + st * (2 if has_h0 else 1)
     if w.backward:
         b += ((4 * dk + 3 * dv) * e + 16) * tokens_heads + st * (3 if has_h0 else 2)
     return b
 
 
-def kernel_models(w, n_chunks_heads):
-    """Algorithmic work of each kernel launch: {name: (bytes, flops)}.
+def kernel_models(w, tokens_heads, n_units, has_h0):
+    """Algorithmic work of each launch: {name: (bytes, flops)}.
 
-    Bytes: the operands the kernel's step of the path must read and write
-    once (inputs, outputs and the per-chunk intermediates it hands over), per
-    chunk-head x number of chunk-heads.  Flops: its matrix products counted at
-    full 64 x 64 chunk size (2 M N K each).  e = element bytes of q/k/v."""
+    FLOP per token-head of the method's step(s) the kernel performs (products
+    at full 64-token chunks): a1 + a2 (gate cumsum, Gram matrices, inverse,
+    W~, U~) 6 C dk + 2 C dv + C^2/3; a3 + a4 (state passing and output)
+    6 dk dv + 2 C dv; a5 (reverse state pass) 6 dk dv + 4 C dv; a6 + a7
+    (per-chunk gradients, gate scan) 6 dk dv + 12 C dk + 4 C dv + 4 C^2.  The
+    sum is the path's forward + backward FLOP.  The stateless backward's
+    recompute launches are credited with the recompute they perform.
+    Bytes: only the call's own tensors the kernel reads or writes (e = element
+    bytes; gates fp32; each state dk dv fp32 per (sequence, head))."""
     e = 4 if w.dtype == "f32" else 2
     dk, dv, C = w.dk, w.dv, CH
-    f32 = 4
-    kside, vside, st = C * dk * e, C * dv * e, dk * dv * e
-    cc = C * C * e                     # one 64 x 64 operand in the element type
-    gates = 2 * C * f32
-    prod_dk = 2 * C * C * dk           # 64 x 64 times 64 x dk
-    prod_dv = 2 * C * C * dv
-    prod_s = 2 * C * dk * dv           # chunk rows times a dk x dv state
+    st = w.dk * w.dv * 4 * n_units
+    a12 = 6 * C * dk + 2 * C * dv + C * C / 3
+    qkv_in = (2 * dk + dv) * e + 8                  # q, k, v, beta, log_alpha
     per = {
-        # q, k, v, gates in; g, W~, Kbar^T, U~, P out; Gram, inverse, W~, U~
-        "fwd:k_prep": (2 * kside + vside + gates + C * f32 + 2 * kside + vside + cc,
-                       3 * prod_dk + prod_dv + C ** 3 / 3),
-        # as forward, plus P^T, T^T, -W~^T, (e^g Q)^T, and Ak^T
-        "bwd:k_prep": (2 * kside + vside + gates + C * f32 + 4 * kside + vside + 3 * cc,
-                       4 * prod_dk + prod_dv + C ** 3 / 3),
-        # both of the above (P and P^T)
-        "fwd:k_prep_save": (2 * kside + vside + gates + C * f32 + 4 * kside + vside + 4 * cc,
-                            4 * prod_dk + prod_dv + C ** 3 / 3),
-        # W~, q, Kbar^T, P, U~, g in; o out
-        "k_fwd_seq": (3 * kside + cc + vside + C * f32 + vside, 3 * prod_s + prod_dv),
-        # as k_fwd_seq, plus chunk states and V' out
-        "k_fwd_seq_save": (3 * kside + cc + vside + C * f32 + vside + st + vside,
-                           3 * prod_s + prod_dv),
-        # W~, Kbar^T, U~ in; chunk states and V' out
-        "k_fwd_seq_store": (2 * kside + vside + C * f32 + st + vside, 2 * prod_s),
-        # k, (e^g Q)^T, -W~^T, P^T, T^T, dO, g, beta in; dS, dX, dv out
-        "k_bwd_seq": (3 * kside + 2 * cc + vside + gates + st + 2 * vside,
-                      3 * prod_s + 2 * prod_dv),
-        # S, dS, q, k, v, dO, V', dX, P^T, Ak^T, gates in; dq, dk, dbeta, dlog_alpha out
-        "k_grad": (2 * st + 2 * kside + 4 * vside + 2 * cc + 2 * gates
-                   + 2 * kside + gates, 3 * prod_s + 2 * prod_dv + 3 * prod_dk),
-        "k_chunk_table": (0, 0),
+        "k_prep": (qkv_in, a12, 0),
+        "k_prep_save": (qkv_in, a12, 0),
+        "k_fwd_seq": (dv * e, 6 * dk * dv + 2 * C * dv, st * (2 if has_h0 else 1)),
+        "k_fwd_seq_save": (dv * e, 6 * dk * dv + 2 * C * dv, st * (2 if has_h0 else 1)),
+        "k_fwd_seq_store": (0, 4 * dk * dv, st if has_h0 else 0),
+        # dO, beta in; dv out; dht in, dh0 out
+        "k_bwd_seq": (2 * dv * e + 4, 6 * dk * dv + 4 * C * dv, 2 * st),
+        # q, k, v, dO, beta in; dq, dk, dbeta, dlog_alpha out
+        "k_grad": ((4 * dk + 2 * dv) * e + 12, 6 * dk * dv + 12 * C * dk + 4 * C * dv + 4 * C * C,
+                   0),
+        "k_chunk_table": (0, 0, 0),
     }
-    return {k: (b * n_chunks_heads, f * n_chunks_heads) for k, (b, f) in per.items()}
+    return {k: (b * tokens_heads + s, f * tokens_heads) for k, (b, f, s) in per.items()}
 
 
 def recurrent_model(w, n_units):
     """Algorithmic work of one token-by-token launch: {name: (bytes, flops)}.
-    Bytes: the fp32 state slice in and out once per (sequence, head), plus
-    q, k, v, o and the two gates per token.  Flops: S^T k, S^T q and the
-    rank-one update, 6 dk dv per token (vector ALU, not MFMA)."""
+    Bytes: the fp32 state in and out once per (sequence, head), plus q, k, v,
+    o and the two gates per token.  Flops: S^T k, S^T q and the rank-one
+    update, 6 dk dv per token (vector ALU, not MFMA)."""
     e = 4 if w.dtype == "f32" else 2
     per_unit = 2 * w.dk * w.dv * 4
     per_tok = (2 * w.dk + 2 * w.dv) * e + 8
     tokens_heads = w.B * w.T * w.H
-    return {"fwd:k_recurrent": (per_unit * n_units + per_tok * tokens_heads,
-                                6 * w.dk * w.dv * tokens_heads)}
+    return {"k_recurrent": (per_unit * n_units + per_tok * tokens_heads,
+                            6 * w.dk * w.dv * tokens_heads)}
 
 
 def model_for(models, name):
     """Model of a timed launch named 'fwd:k' / 'bwd:k'."""
-    if name in models:
-        return models[name]
     return models.get(name.split(":", 1)[-1], (0, 0))
 
 
-def cpu_baseline(inp, w, budget_s=20.0):
-    """Time the oracle (fp64, all host cores) on a bounded sample of the same
-    workload: whole (sequence, head) units with their initial states, fwd
-    (+bwd).  The sample is run again until about half the budget has passed
-    (a decode step takes many passes), and the mean is taken."""
-    import torch
-
-    from oracle import oracle
-    threads = oracle.default_threads()
-    cu = inp.get("cu_seqlens")
-    N = w.B if cu is None else cu.numel() - 1
-    units = []
-    for n in range(N):
-        for h in range(w.H):
-            units.append((n, h))
-    # estimate: ~20 flop * dk * dv per token for fwd+bwd, ~6 for fwd, ~3 GFLOP/s a core
-    per_tok = (20 if w.backward else 6) * w.dk * w.dv
-    tok_per_unit = w.T if cu is None else w.T / N
-    per_unit_s = per_tok * tok_per_unit / 3e9
-    n_units = int(max(1, min(len(units), threads * max(1.0, budget_s / per_unit_s / 1.5))))
-    if tok_per_unit >= 64:  # long units: a few per thread are enough
-        n_units = min(n_units, max(threads, 1) * 4)
-    sel = units[:n_units]
-    sl = {}
-    # pack the selected units as independent sequences of one head each
-    qs, ks, vs, bs, las, dOs, dhts, h0s, cus = [], [], [], [], [], [], [], [], [0]
-    for n, h in sel:
-        if cu is None:
-            s = (slice(n, n + 1), slice(None), slice(h, h + 1))
-        else:
-            s = (slice(0, 1), slice(int(cu[n]), int(cu[n + 1])), slice(h, h + 1))
-        qs.append(inp["q"][s][0])
-        ks.append(inp["k"][s][0])
-        vs.append(inp["v"][s][0])
-        bs.append(inp["beta"][s][0])
-        las.append(inp["log_alpha"][s][0])
-        if w.backward:
-            dOs.append(inp["dO"][s][0])
-            dhts.append(inp["dht"][n:n + 1, h:h + 1, :, :][0])
-        if inp.get("h0") is not None:
-            h0s.append(inp["h0"][n:n + 1, h:h + 1, :, :][0])
-        cus.append(cus[-1] + qs[-1].shape[0])
-    cat = lambda xs: torch.cat(xs, 0).unsqueeze(0)
-    sl = dict(q=cat(qs), k=cat(ks), v=cat(vs), beta=cat(bs), log_alpha=cat(las))
-    cu_s = torch.tensor(cus, dtype=torch.int64)
-    tokens = int(cus[-1])
-    h0 = torch.stack(h0s, 0) if h0s else None
-
-    def one_pass():
-        if w.backward:
-            oracle.bwd(sl["q"], sl["k"], sl["v"], sl["beta"], sl["log_alpha"], cat(dOs), h0=h0,
-                       dht=torch.stack(dhts, 0), cu_seqlens=cu_s, nthreads=threads)
-        else:
-            oracle.fwd(sl["q"], sl["k"], sl["v"], sl["beta"], sl["log_alpha"], h0=h0,
-                       cu_seqlens=cu_s, nthreads=threads)
-
-    passes, t0 = 0, time.perf_counter()
-    while passes < 10000:
-        one_pass()
-        passes += 1
-        if time.perf_counter() - t0 >= budget_s / 2:
-            break
-    dt = (time.perf_counter() - t0) / passes
-    # each token of the workload carries H heads; the sample covers `tokens`
-    # token-heads, i.e. tokens / H workload tokens
-    value = (tokens / w.H) / dt
-    return {"value": value, "unit": "tokens/s", "cores": min(threads, len(sel)),
-            "kind": "oracle",
-            "sample": "%d of %d (sequence, head) units, %d token-heads, %s, %.2f s per pass, "
-                      "%d passes" % (len(sel), len(units), tokens,
-                                     "fwd+bwd" if w.backward else "fwd", dt, passes)}
-
+# ------------------------------------------------------------------ counters on record
 
 def kernel_source_digest():
     """sha256 over the HIP sources, to tell whether recorded counters are stale."""
@@ -215,51 +148,222 @@ def kernel_source_digest():
     return h.hexdigest()
 
 
-def traffic_from_profiles(kernel, workload):
-    """HBM bytes per launch measured by rocprofv3 PMC (FETCH_SIZE + WRITE_SIZE,
-    scaled by a copy-kernel calibration), if recorded for the current kernel
-    source; otherwise None."""
+def traffic_record(workload):
+    """{launch name: HBM bytes per launch} measured by rocprofv3 PMC
+    (FETCH_SIZE + WRITE_SIZE, scaled by a copy-kernel calibration) for the
+    current kernel sources, or {} if none is on record."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
-        return None
+        return {}
     try:
         rec = json.load(open(path))
     except ValueError:
-        return None
+        return {}
     digest = kernel_source_digest()
-    ent = rec.get(workload, {}).get(kernel)
-    if not ent or ent.get("kernel_source_sha256") != digest:
-        return None
-    return ent.get("bytes_per_launch")
+    return {k: e["bytes_per_launch"] for k, e in rec.get(workload, {}).items()
+            if e.get("kernel_source_sha256") == digest}
 
+
+# ------------------------------------------------------------------ timing
+
+def percentiles(xs):
+    import numpy as np
+    a = np.asarray(xs, dtype=np.float64)
+    return {"median": float(np.median(a)), "p10": float(np.percentile(a, 10)),
+            "p90": float(np.percentile(a, 90)), "mean": float(a.mean()), "n": int(a.size)}
+
+
+class StepTimer:
+    """Times steps one by one with events on `stream`, optionally after a
+    cache-evicting write; collects the library's per-launch event timings."""
+
+    def __init__(self, torch, stream, device):
+        self.torch = torch
+        self.stream = stream
+        self.flush_buf = torch.empty(FLUSH_BYTES // 4, dtype=torch.int32, device=device)
+
+    def run(self, step, k, cold, n_calls, gdn):
+        torch = self.torch
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(k)]
+        timers = [[gdn.LaunchTimer(8) for _ in range(n_calls)] for _ in range(k)]
+        torch.cuda.synchronize()
+        for i in range(k):
+            if cold:
+                self.flush_buf.fill_(i + 1)
+            evs[i][0].record(self.stream)
+            step(timers[i])
+            evs[i][1].record(self.stream)
+        torch.cuda.synchronize()
+        step_ms = [a.elapsed_time(b) for a, b in evs]
+        per_kernel = {}
+        for tl in timers:
+            for call, t in zip(("fwd", "bwd"), tl):
+                for name, kms in t.durations_ms().items():
+                    per_kernel.setdefault(call + ":" + name, []).append(kms)
+                t.close()
+        return step_ms, per_kernel
+
+
+# ------------------------------------------------------------------ CPU baseline and parity sample
+
+def cpu_model():
+    """The host CPU's model name (from /proc/cpuinfo) and the threads this
+    process may run on."""
+    name = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                name = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        threads = len(os.sched_getaffinity(0))
+    except AttributeError:
+        threads = os.cpu_count() or 1
+    return name, threads
+
+
+def sample_units(inp, w, units):
+    """Pack the listed (sequence, head) units of the workload as independent
+    one-head sequences: (inputs, [(unit, first row, length)])."""
+    import torch
+    cu = inp.get("cu_seqlens")
+    keys = ["q", "k", "v", "beta", "log_alpha"] + (["dO"] if w.backward else [])
+    parts = {k: [] for k in keys}
+    h0s, dhts, spans, at = [], [], [], 0
+    for n, h in units:
+        for key in keys:
+            x = inp[key]
+            parts[key].append(x[n, :, h:h + 1] if cu is None else
+                              x[0, int(cu[n]):int(cu[n + 1]), h:h + 1])
+        if inp.get("h0") is not None:
+            h0s.append(inp["h0"][n:n + 1, h:h + 1])
+        if w.backward:
+            dhts.append(inp["dht"][n:n + 1, h:h + 1])
+        L = parts["q"][-1].shape[0]
+        spans.append(((n, h), at, L))
+        at += L
+    s = {k: torch.cat(v, 0).unsqueeze(0) for k, v in parts.items()}
+    s["cu_seqlens"] = torch.tensor([0] + [a + L for _, a, L in spans], dtype=torch.int64)
+    s["h0"] = torch.cat(h0s, 0) if h0s else None
+    s["dht"] = torch.cat(dhts, 0) if dhts else None
+    return s, spans
+
+
+def oracle_pass(oracle, s, w, threads):
+    if w.backward:
+        return oracle.bwd(s["q"], s["k"], s["v"], s["beta"], s["log_alpha"], s["dO"], h0=s["h0"],
+                          dht=s["dht"], cu_seqlens=s["cu_seqlens"], nthreads=threads)
+    o, ht = oracle.fwd(s["q"], s["k"], s["v"], s["beta"], s["log_alpha"], h0=s["h0"],
+                       cu_seqlens=s["cu_seqlens"], nthreads=threads)
+    return {"o": o, "ht": ht}
+
+
+def cpu_baseline(inp, w, budget_s=20.0):
+    """Time the oracle (fp64) on a bounded sample of the same workload: whole
+    (sequence, head) units with their initial states, fwd (+bwd), on every
+    host thread, repeated until about half the budget has passed; then once
+    more on one thread over a smaller sample.  Returns (record, sampled units,
+    spans, oracle results of the multi-thread pass)."""
+    from oracle import oracle
+    model, threads = cpu_model()
+    cu = inp.get("cu_seqlens")
+    N = w.B if cu is None else cu.numel() - 1
+    units = [(n, h) for n in range(N) for h in range(w.H)]
+    # estimate: ~20 flop * dk * dv per token for fwd+bwd, ~6 for fwd, ~3 GFLOP/s a core
+    per_tok = (20 if w.backward else 6) * w.dk * w.dv
+    tok_per_unit = w.T if cu is None else w.T / N
+    per_unit_s = per_tok * tok_per_unit / 3e9
+    n_units = int(max(1, min(len(units), threads * max(1.0, budget_s / per_unit_s / 1.5))))
+    if tok_per_unit >= 64:  # long units: a few per thread are enough
+        n_units = min(n_units, max(threads, 1) * 4)
+    # the first sequences with all their heads, and the last unit
+    sel = sorted(set(units[:n_units]) | {(N - 1, w.H - 1)})
+    s, spans = sample_units(inp, w, sel)
+    tokens = int(spans[-1][1] + spans[-1][2])
+
+    passes, t0, ref = 0, time.perf_counter(), None
+    while passes < 10000:
+        ref = oracle_pass(oracle, s, w, threads)
+        passes += 1
+        if time.perf_counter() - t0 >= budget_s / 2:
+            break
+    dt = (time.perf_counter() - t0) / passes
+    # single thread: the first units of the sample, about budget / 4 of work
+    n1 = max(1, min(len(sel), int(budget_s / 4 / max(per_unit_s, 1e-9))))
+    s1, spans1 = sample_units(inp, w, sel[:n1])
+    tok1 = int(spans1[-1][1] + spans1[-1][2])
+    t1 = time.perf_counter()
+    oracle_pass(oracle, s1, w, 1)
+    dt1 = time.perf_counter() - t1
+    # each token of the workload carries H heads; a sample of `tokens`
+    # token-heads is tokens / H workload tokens
+    rec = {"value": (tokens / w.H) / dt, "unit": "tokens/s", "cores": min(threads, len(sel)),
+           "kind": "oracle", "cpu": model,
+           "sample": "%d of %d (sequence, head) units, %d token-heads, %s, %.2f s per pass, "
+                     "%d passes, %d threads" % (len(sel), len(units), tokens,
+                                                "fwd+bwd" if w.backward else "fwd", dt, passes,
+                                                threads),
+           "single_thread": {"value": (tok1 / w.H) / dt1, "unit": "tokens/s",
+                             "sample": "%d units, %d token-heads, %.2f s" % (n1, tok1, dt1)}}
+    return rec, sel, spans, ref
+
+
+def parity_sample(got, ref, spans, w, cu):
+    """max |x - ref| / max |ref| per output tensor over the sampled units."""
+    import numpy as np
+    import torch
+    errs = {}
+    for i, ((n, h), at, L) in enumerate(spans):
+        for key, x in got.items():
+            if x is None:
+                continue
+            if key in ("ht", "dh0"):
+                a, b = x[n, h], ref[key][i, 0]
+            else:
+                rows = x[n, :, h] if cu is None else x[0, int(cu[n]):int(cu[n + 1]), h]
+                a, b = rows, ref[key][at:at + L, 0]
+            a = a.detach().to("cpu", torch.float64).numpy().reshape(b.shape)
+            num, den = float(np.abs(a - b).max(initial=0.0)), float(np.abs(b).max(initial=0.0))
+            e = errs.setdefault(key, [0.0, 0.0])
+            e[0], e[1] = max(e[0], num), max(e[1], den)
+    out = {k: v[0] / max(v[1], 1e-30) for k, v in errs.items()}
+    return {"units": len(spans), "tol": TOL[w.dtype], "err": out,
+            "ok": all(v <= TOL[w.dtype] for v in out.values())}
+
+
+# ------------------------------------------------------------------ block prologue / epilogue
 
 def bench_block(args):
     """One step = the block's prologue and epilogue, forward and backward:
     conv+SiLU+L2 of q and k, conv+SiLU of v, RMS norm x gate of the output,
-    then the backward of each.  Every call is timed with events on the
-    stream the library launches on; the roofline is the slowest call's
+    then the backward of each.  Steps are timed as in the main path (cold
+    median after a cache-evicting write); the roofline is the slowest call's
     algorithmic bytes (its inputs and outputs once) over its mean time."""
+    import ctypes
+
     import torch
 
     from paper_2412_06464_amd import gdn
     from paper_2412_06464_amd.inputs import make_block_inputs
 
     B, T, H, dk, dv, W = BLOCK_WORKLOADS[args.workload]
-    gdn.load_library()
+    lib = gdn.load_library()
     inp = make_block_inputs(B, T, H, dk, dv, "bf16", seed=0, width=W)
     d = {k: v.cuda() for k, v in inp.items()}
     out = {k: torch.empty_like(d[k]) for k in ("xq", "xk", "xv", "o")}
     grads = {k: torch.empty_like(d[k]) for k in ("xq", "xk", "xv", "o", "g")}
     dws = {k: torch.empty_like(d[k]) for k in ("wq", "wk", "wv", "wo")}
     pq, _ = gdn.block_problem(d["xq"])
-    ws = torch.empty(max(gdn.load_library().gdn_conv_silu_workspace_size(pq, dv, W),
-                         gdn.load_library().gdn_norm_gate_workspace_size(pq)), dtype=torch.uint8,
+    ws = torch.empty(max(lib.gdn_conv_silu_workspace_size(pq, dv, W),
+                         lib.gdn_norm_gate_workspace_size(pq)), dtype=torch.uint8,
                      device="cuda")
     # C arguments prepared once: a step is eight library calls and nothing else
-    import ctypes
-    lib = gdn.load_library()
     P = lambda t: ctypes.c_void_p(t.data_ptr())
-    st = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    stream = torch.cuda.current_stream()
+    st = ctypes.c_void_p(stream.cuda_stream)
     probs = {}
     for key in ("xq", "xv"):
         probs[key], _ = gdn.block_problem(d[key])
@@ -268,13 +372,13 @@ def bench_block(args):
     eps_l2, eps_n = ctypes.c_float(1e-6), ctypes.c_float(1e-5)
 
     def conv_fwd(pp, dim, l2, x, w, y):
-        args = (pp, dim, W, l2, eps_l2, P(d[x]), P(d[w]), P(out[y]), wsp, wsn, st)
-        return lambda: lib.gdn_conv_silu_fwd(*args)
+        a = (pp, dim, W, l2, eps_l2, P(d[x]), P(d[w]), P(out[y]), wsp, wsn, st)
+        return lambda: lib.gdn_conv_silu_fwd(*a)
 
     def conv_bwd(pp, dim, l2, x, w, dy):
-        args = (pp, dim, W, l2, eps_l2, P(d[x]), P(d[w]), P(d[dy]), P(grads[x]), P(dws[w]),
-                wsp, wsn, st)
-        return lambda: lib.gdn_conv_silu_bwd(*args)
+        a = (pp, dim, W, l2, eps_l2, P(d[x]), P(d[w]), P(d[dy]), P(grads[x]), P(dws[w]),
+             wsp, wsn, st)
+        return lambda: lib.gdn_conv_silu_bwd(*a)
 
     nf = (pv, eps_n, P(d["o"]), P(d["g"]), P(d["wo"]), P(out["o"]), st)
     nb = (pv, eps_n, P(d["o"]), P(d["g"]), P(d["wo"]), P(d["dy"]), P(grads["o"]), P(grads["g"]),
@@ -293,37 +397,45 @@ def bench_block(args):
         rc = f()
         if rc != 0:
             raise gdn.GdnError(rc)
-    stream = torch.cuda.current_stream()
+    flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.int32, device="cuda")
 
-    def step(evs=None):
-        for i, (_, f, _) in enumerate(calls):
-            if evs:
-                evs[i][0].record(stream)
-            f()
-            if evs:
-                evs[i][1].record(stream)
+    def run(k, cold):
+        evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                for _ in calls] for _ in range(k)]
+        se = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(k)]
+        torch.cuda.synchronize()
+        for i in range(k):
+            if cold:
+                flush.fill_(i + 1)
+            se[i][0].record(stream)
+            for j, (_, f, _) in enumerate(calls):
+                evs[i][j][0].record(stream)
+                f()
+                evs[i][j][1].record(stream)
+            se[i][1].record(stream)
+        torch.cuda.synchronize()
+        steps = [a.elapsed_time(b) for a, b in se]
+        per = {name: [evs[i][j][0].elapsed_time(evs[i][j][1]) for i in range(k)]
+               for j, (name, _, _) in enumerate(calls)}
+        return steps, per
 
     for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-            for _ in calls] for _ in range(args.steps)]
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    start.record(stream)
-    for k in range(args.steps):
-        step(evs[k])
-    end.record(stream)
-    torch.cuda.synchronize()
-    ms = start.elapsed_time(end) / args.steps
-    call_ms = {name: sum(evs[k][i][0].elapsed_time(evs[k][i][1]) for k in range(args.steps))
-               / args.steps for i, (name, _, _) in enumerate(calls)}
+        for _, f, _ in calls:
+            f()
+    cold, per = run(args.steps, True)
+    warm, _ = run(args.steps, False)
+    tc, tw = percentiles(cold), percentiles(warm)
+    ms = tc["median"]
+    call_ms = {name: sum(v) / len(v) for name, v in per.items()}
     th = B * T * H
-    nbytes = {name: per * 2 * th for name, _, per in calls}  # bf16 elements per token-head
+    nbytes = {name: n * 2 * th for name, _, n in calls}  # bf16 elements per token-head
     dom = max(call_ms, key=lambda k: call_ms[k])
     ach = nbytes[dom] / (call_ms[dom] / 1e3)
+    traffic = traffic_record(args.workload).get(dom)
     roof = {"bound": "hbm", "achieved": ach / 1e9, "peak": PEAK_HBM / 1e9, "unit": "GB/s",
-            "frac": ach / PEAK_HBM, "traffic": traffic_from_profiles(dom, args.workload),
+            "frac": ach / PEAK_HBM, "traffic": traffic,
+            "traffic_ratio": traffic / nbytes[dom] if traffic else None,
             "kernel": dom, "kernel_ms": call_ms[dom]}
     total_bytes = sum(nbytes.values())
     res = {
@@ -332,11 +444,13 @@ def bench_block(args):
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": args.workload, "B": B, "T": T, "H": H, "dk": dk, "dv": dv,
                    "conv_width": W},
+        "timing": {"cold_ms": tc, "warm_ms": tw, "flush_bytes": FLUSH_BYTES},
         "hbm_frac": total_bytes / (ms / 1e3) / PEAK_HBM, "path_gbytes": total_bytes / 1e9,
         "calls_ms": call_ms, "roofline": roof,
     }
     if not args.no_cpu_baseline:
         from oracle import block
+        model, _ = cpu_model()
         t0 = time.perf_counter()
         n = 0
         while time.perf_counter() - t0 < 10.0 and n < B:
@@ -352,11 +466,13 @@ def bench_block(args):
             n += 1
         dt = time.perf_counter() - t0
         res["cpu_baseline"] = {"value": n * T / dt, "unit": "tokens/s", "cores": 1,
-                               "kind": "oracle",
+                               "kind": "oracle", "cpu": model,
                                "sample": "%d of %d sequences, all heads, fwd+bwd, %.1f s" % (
                                    n, B, dt)}
     print(json.dumps(res), flush=True)
 
+
+# ------------------------------------------------------------------ main path
 
 def main():
     ap = argparse.ArgumentParser()
@@ -365,6 +481,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-path", action="store_true",
+                    help="time only the headline path of a fwd+bwd workload")
     ap.add_argument("--path", choices=("saved", "stateless"), default="saved",
                     help="backward path of the headline step (the other is timed beside it)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -423,11 +541,14 @@ def main():
     la = d["log_alpha"] if w.gated else None  # None: alpha == 1, no gate arithmetic
 
     state = torch.zeros((n_states, w.H, w.dk, w.dv), dtype=torch.float32, device=dev)
-    if d.get("h0") is not None:
-        state.copy_(d["h0"])
+    h0_dev = d.get("h0")
+
+    if h0_dev is not None:
+        state.copy_(h0_dev)
 
     def step_recurrent(timers=None):
-        # one decode step per sequence, the state updated in place
+        # one decode step per sequence, the state updated in place (every
+        # step continues from the state the previous one left)
         gdn.gdn_recurrent_fwd(d["q"], d["k"], d["v"], d["beta"], la, h0=state, ht=state,
                               cu_seqlens=cu, cu_seqlens_host=cu_host, o=o,
                               timer=timers[0] if timers else None)
@@ -449,52 +570,45 @@ def main():
                                 out=out_b, timer=timers[1] if timers else None)
 
     stream = torch.cuda.current_stream(dev)
+    timer = StepTimer(torch, stream, dev)
+    n_calls = 2 if w.backward else 1
 
-    def timed_run(step):
-        """Warm up, then time K steps; returns (ms per step, {kernel: mean ms})."""
+    def measure(step):
+        """W warm-up steps, K cold steps, K warm steps."""
         for _ in range(args.warmup):
             step()
         torch.cuda.synchronize()
-        timers = [(gdn.LaunchTimer(8), gdn.LaunchTimer(8) if w.backward else None)
-                  for _ in range(args.steps)]
-        start = torch.cuda.Event(enable_timing=True)
-        end = torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        start.record(stream)
-        for i in range(args.steps):
-            step(timers[i])
-        end.record(stream)
-        torch.cuda.synchronize()
-        per_kernel = {}
-        for tf, tb in timers:
-            for call, t in (("fwd", tf), ("bwd", tb)):
-                if t is None:
-                    continue
-                for name, kms in t.durations_ms().items():
-                    per_kernel.setdefault(call + ":" + name, []).append(kms)
-            tf.close()
-            if tb is not None:
-                tb.close()
-        return (start.elapsed_time(end) / args.steps,
-                {k: sum(v) / len(v) for k, v in per_kernel.items()})
+        cold, kern = timer.run(step, args.steps, True, n_calls, gdn)
+        warm, _ = timer.run(step, args.steps, False, n_calls, gdn)
+        return percentiles(cold), percentiles(warm), {k: sum(v) / len(v) for k, v in kern.items()}
 
     path = args.path if w.backward else ("recurrent" if w.recurrent else "stateless")
     steps = {"saved": step_saved, "stateless": step_stateless, "recurrent": step_recurrent}
-    ms, kern_ms = timed_run(steps[path])
-    other = None
+    tc, tw, kern_ms = measure(steps[path])
+    ms = tc["median"]
+    # outputs of the headline path, for the parity sample (a decode step
+    # restarts from the prefill state)
+    if w.recurrent and h0_dev is not None:
+        state.copy_(h0_dev)
+    steps[path]()
+    torch.cuda.synchronize()
+    got = {"o": o, "ht": state if w.recurrent else ht}
     if w.backward:
+        got.update(out_b)
+    got = {k: v.detach().to("cpu") for k, v in got.items()}
+    other = None
+    if w.backward and not args.no_other_path:
         oname = "stateless" if path == "saved" else "saved"
-        oms, okern = timed_run(steps[oname])
-        other = {"path": oname, "ms_per_step": oms, "value": w.B * w.T / (oms / 1e3),
+        oc, ow, okern = measure(steps[oname])
+        other = {"path": oname, "ms_per_step": oc["median"],
+                 "value": w.B * w.T / (oc["median"] / 1e3), "warm_ms": ow["median"],
                  "kernels_ms": okern}
 
     tokens = w.B * w.T
     tokens_heads = tokens * w.H
-    n_chunks = (w.B * ((w.T + CH - 1) // CH) if cu_host is None else
-                int(sum((int(cu_host[i + 1]) - int(cu_host[i]) + CH - 1) // CH
-                        for i in range(n_states))))
+    has_h0 = d.get("h0") is not None
     models = (recurrent_model(w, n_states * w.H) if w.recurrent else
-              kernel_models(w, n_chunks * w.H))
+              kernel_models(w, tokens_heads, n_states * w.H, has_h0))
     dom = max(kern_ms, key=lambda k: kern_ms[k])
     kb, kf = model_for(models, dom)
     peak_mfma = PEAK_MFMA_F32 if w.dtype == "f32" else PEAK_MFMA_BF16
@@ -508,15 +622,20 @@ def main():
         roof = {"bound": cbound, "achieved": kf / t_dom / 1e12, "peak": peak_c / 1e12,
                 "unit": "TFLOP/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = traffic_from_profiles(dom, args.workload)
-    roof["kernel"] = dom
-    roof["kernel_ms"] = kern_ms[dom]
+    counters = traffic_record(args.workload)
+    roof["traffic"] = counters.get(dom)
+    roof["traffic_ratio"] = counters[dom] / kb if counters.get(dom) and kb else None
+    roof.update(kernel=dom, kernel_ms=kern_ms[dom], algorithmic_gbytes=kb / 1e9,
+                algorithmic_gflop=kf / 1e9)
 
     if w.recurrent:
-        nbytes, flops = models["fwd:k_recurrent"]
+        nbytes, flops = models["k_recurrent"]
     else:
         flops = path_flops(w, tokens_heads)
-        nbytes = path_bytes(w, tokens_heads, n_states, d.get("h0") is not None)
+        nbytes = path_bytes(w, tokens_heads, n_states, has_h0)
+    step_counter = None
+    if counters and all(k in counters for k in kern_ms):
+        step_counter = sum(counters[k] for k in kern_ms)
     res = {
         "metric": METRIC if w.backward else (METRIC_RECURRENT if w.recurrent else METRIC_FWD),
         "value": tokens / (ms / 1e3),
@@ -533,17 +652,23 @@ def main():
         "config": {"workload": args.workload, "B": w.B, "T": w.T, "H": w.H, "dk": w.dk,
                    "dv": w.dv, "chunk": CH, "backward": w.backward,
                    "num_seqs": n_states, "path": path},
+        "timing": {"cold_ms": tc, "warm_ms": tw, "flush_bytes": FLUSH_BYTES,
+                   "warm_value": tokens / (tw["median"] / 1e3)},
         "mfma_frac": None if w.recurrent else flops / (ms / 1e3) / peak_mfma,
         "hbm_frac": nbytes / (ms / 1e3) / PEAK_HBM,
         "path_gflop": flops / 1e9,
         "path_gbytes": nbytes / 1e9,
+        "step_traffic_gbytes": step_counter / 1e9 if step_counter else None,
+        "step_traffic_ratio": step_counter / nbytes if step_counter else None,
         "kernels_ms": kern_ms,
         "roofline": roof,
     }
     if other is not None:
         res["other_path"] = other
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(inp, w)
+        rec, sel, spans, ref = cpu_baseline(inp, w)
+        res["cpu_baseline"] = rec
+        res["parity"] = parity_sample(got, ref, spans, w, cu_host)
     print(json.dumps(res), flush=True)
 
 

@@ -343,12 +343,12 @@ template <class E> __device__ inline void dma_frag(const E* src_lane, E* lds_fra
 template <> __device__ inline void dma_frag<bf16>(const bf16* src_lane, bf16* lds_frag) {
   const unsigned lds = (unsigned)(uintptr_t)lds_frag;
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(src_lane)
-               : "memory");
+               : "memory", "m0");
 }
 template <> __device__ inline void dma_frag<float>(const float* src_lane, float* lds_frag) {
   const unsigned lds = (unsigned)(uintptr_t)lds_frag;
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off" ::"s"(lds), "v"(src_lane)
-               : "memory");
+               : "memory", "m0");
 }
 // Wait until at most N vector-memory operations of this wave are in flight.
 template <int N> __device__ inline void wait_vmcnt() {

@@ -121,7 +121,7 @@ __device__ inline void warm_l2(const unsigned char* const (&base)[NB], const int
     if (idx < bytes[b] / WL)
       asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, %2" ::"s"(lds), "v"(off),
                    "s"(base[b])
-                   : "memory");
+                   : "memory", "m0");
 }
 
 // ------------------------------------------------------------------ forward / recompute

@@ -148,8 +148,40 @@ def _ptr(t: Optional[torch.Tensor]):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
+def _cu_pair(cu_seqlens, cu_seqlens_host, device, keep):
+    """Device and host int32 copies of packed sequence boundaries.
+
+    The kernels read the device copy as contiguous int32 on the device of the
+    data; an int64 tensor (what ``torch.tensor`` and ``cumsum`` give) is
+    converted here, and the converted copy is kept alive in ``keep`` until the
+    call returns.  Without a host copy it is read back from the device (a
+    synchronisation)."""
+    if not isinstance(cu_seqlens, torch.Tensor) or cu_seqlens.dim() != 1:
+        raise TypeError("cu_seqlens must be a 1-d tensor")
+    if cu_seqlens.device != device:
+        raise ValueError("cu_seqlens is on %s, the data on %s" % (cu_seqlens.device, device))
+    if cu_seqlens.dtype not in (torch.int32, torch.int64):
+        raise TypeError("cu_seqlens must be int32 (or int64, converted)")
+    dev = cu_seqlens
+    if dev.dtype != torch.int32 or not dev.is_contiguous():
+        dev = dev.to(torch.int32).contiguous()
+        keep.append(dev)
+    if cu_seqlens_host is None:
+        cu_seqlens_host = dev.to("cpu")
+    if not isinstance(cu_seqlens_host, torch.Tensor) or cu_seqlens_host.device.type != "cpu":
+        raise TypeError("cu_seqlens_host must be a CPU tensor")
+    host = cu_seqlens_host.to(torch.int32).contiguous()
+    if host.numel() != dev.numel():
+        raise ValueError("cu_seqlens (%d values) and cu_seqlens_host (%d values) differ"
+                         % (dev.numel(), host.numel()))
+    keep.append(host)
+    return dev, host
+
+
 def make_problem(q: torch.Tensor, v: torch.Tensor, cu_seqlens=None, cu_seqlens_host=None):
     """Build the gdn_problem for q [B,T,H,dk], v [B,T,H,dv].  Returns (problem, keepalive)."""
+    if q.dim() != 4 or v.dim() != 4 or q.shape[:3] != v.shape[:3]:
+        raise ValueError("q must be [B,T,H,dk] and v [B,T,H,dv] over the same B, T, H")
     B, T, H, dk = q.shape
     dv = v.shape[-1]
     dt = {torch.float32: GDN_F32, torch.bfloat16: GDN_BF16}.get(q.dtype)
@@ -158,14 +190,37 @@ def make_problem(q: torch.Tensor, v: torch.Tensor, cu_seqlens=None, cu_seqlens_h
     keep = []
     p = Problem(B, T, H, dk, dv, 0, None, None, dt)
     if cu_seqlens is not None:
-        if cu_seqlens_host is None:
-            cu_seqlens_host = cu_seqlens.to("cpu")
-        host = cu_seqlens_host.to(torch.int32).contiguous()
-        keep.append(host)
+        dev, host = _cu_pair(cu_seqlens, cu_seqlens_host, q.device, keep)
         p.num_seqs = host.numel() - 1
-        p.cu_seqlens = cu_seqlens.data_ptr()
+        p.cu_seqlens = dev.data_ptr()
         p.cu_seqlens_host = host.data_ptr()
     return p, keep
+
+
+def _check_tensors(q, rows=(), gates=(), states=(), nstate=None):
+    """Argument checks before a call: every tensor on q's device and
+    contiguous; ``rows`` [B,T,H,*] in q's dtype; ``gates`` [B,T,H] float32;
+    ``states`` [Nseq,H,dk,dv] float32.  None entries are skipped."""
+    B, T, H, dk = q.shape
+    named = (("q", q),) + tuple(rows) + tuple(gates) + tuple((n, t) for n, t, _ in states)
+    for name, t in named:
+        if t is None:
+            continue
+        if not isinstance(t, torch.Tensor):
+            raise TypeError("%s must be a tensor" % name)
+        if t.device != q.device:
+            raise ValueError("%s is on %s, q on %s" % (name, t.device, q.device))
+        if not t.is_contiguous():
+            raise ValueError("%s must be contiguous" % name)
+    for name, t in rows:
+        if t is not None and (t.dtype != q.dtype or t.dim() != 4 or t.shape[:3] != q.shape[:3]):
+            raise ValueError("%s must be [B,T,H,*] in q's dtype %s" % (name, q.dtype))
+    for name, t in gates:
+        if t is not None and (t.dtype != torch.float32 or tuple(t.shape) != (B, T, H)):
+            raise ValueError("%s must be float32 [B,T,H]" % name)
+    for name, t, d2 in states:
+        if t is not None and (t.dtype != torch.float32 or tuple(t.shape) != (nstate, H, dk, d2)):
+            raise ValueError("%s must be float32 [%d,%d,%d,%d]" % (name, nstate, H, dk, d2))
 
 
 def gdn_chunk_fwd_workspace_size(p: Problem) -> int:
@@ -224,6 +279,11 @@ def gdn_chunk_fwd(q, k, v, beta, log_alpha, h0=None, cu_seqlens=None, cu_seqlens
     if ht is None and output_final_state:
         ht = torch.empty((_nstate(q, cu_seqlens), H, dk, dv), dtype=torch.float32,
                          device=q.device)
+    _check_tensors(q, rows=(("k", k), ("v", v), ("o", o)), gates=(("beta", beta),
+                   ("log_alpha", log_alpha)), states=(("h0", h0, dv), ("ht", ht, dv)),
+                   nstate=_nstate(q, cu_seqlens))
+    if k.shape != q.shape or o.shape != v.shape:
+        raise ValueError("k must match q, and o must match v")
     need = lib.gdn_chunk_fwd_workspace_size(ctypes.byref(p))
     if need == 0:
         _check(lib.gdn_chunk_fwd(ctypes.byref(p), *[None] * 8, None, 0, None))
@@ -256,6 +316,14 @@ def gdn_chunk_bwd(q, k, v, beta, log_alpha, dO, h0=None, dht=None, cu_seqlens=No
                    dlog_alpha=torch.empty_like(beta) if need_dlog_alpha else None,
                    dh0=torch.empty((_nstate(q, cu_seqlens), H, dk, dv), dtype=torch.float32,
                                    device=q.device) if need_dh0 else None)
+    _check_tensors(q, rows=(("k", k), ("v", v), ("dO", dO), ("dq", out["dq"]), ("dk", out["dk"]),
+                            ("dv", out["dv"])),
+                   gates=(("beta", beta), ("log_alpha", log_alpha), ("dbeta", out["dbeta"]),
+                          ("dlog_alpha", out["dlog_alpha"])),
+                   states=(("h0", h0, dv), ("dht", dht, dv), ("dh0", out["dh0"], dv)),
+                   nstate=_nstate(q, cu_seqlens))
+    if k.shape != q.shape or dO.shape != v.shape:
+        raise ValueError("k must match q, and dO must match v")
     need = lib.gdn_chunk_bwd_workspace_size(ctypes.byref(p))
     if need == 0:
         _check(lib.gdn_chunk_bwd(ctypes.byref(p), *[None] * 14, None, 0, None))
@@ -291,6 +359,11 @@ def gdn_chunk_fwd_save(q, k, v, beta, log_alpha, h0=None, cu_seqlens=None, cu_se
     if ht is None and output_final_state:
         ht = torch.empty((_nstate(q, cu_seqlens), H, dk, dv), dtype=torch.float32,
                          device=q.device)
+    _check_tensors(q, rows=(("k", k), ("v", v), ("o", o)), gates=(("beta", beta),
+                   ("log_alpha", log_alpha)), states=(("h0", h0, dv), ("ht", ht, dv)),
+                   nstate=_nstate(q, cu_seqlens))
+    if k.shape != q.shape or o.shape != v.shape:
+        raise ValueError("k must match q, and o must match v")
     need = lib.gdn_chunk_fwd_save_workspace_size(ctypes.byref(p))
     if need == 0:
         _check(lib.gdn_chunk_fwd_save(ctypes.byref(p), *[None] * 8, None, 0, None, 0, None))
@@ -330,6 +403,16 @@ def gdn_chunk_bwd_saved(q, k, v, beta, dO, saved, dht=None, cu_seqlens=None,
                    dlog_alpha=torch.empty_like(beta) if need_dlog_alpha else None,
                    dh0=torch.empty((_nstate(q, cu_seqlens), H, dk, dv), dtype=torch.float32,
                                    device=q.device) if need_dh0 else None)
+    _check_tensors(q, rows=(("k", k), ("v", v), ("dO", dO), ("dq", out["dq"]), ("dk", out["dk"]),
+                            ("dv", out["dv"])),
+                   gates=(("beta", beta), ("dbeta", out["dbeta"]),
+                          ("dlog_alpha", out["dlog_alpha"])),
+                   states=(("dht", dht, dv), ("dh0", out["dh0"], dv)),
+                   nstate=_nstate(q, cu_seqlens))
+    if k.shape != q.shape or dO.shape != v.shape:
+        raise ValueError("k must match q, and dO must match v")
+    if saved.device != q.device or saved.dtype != torch.uint8 or not saved.is_contiguous():
+        raise ValueError("saved must be a contiguous uint8 tensor on q's device")
     need = lib.gdn_chunk_bwd_saved_workspace_size(ctypes.byref(p))
     if need == 0:
         _check(lib.gdn_chunk_bwd_saved(ctypes.byref(p), *[None] * 7, 0, *[None] * 6, None, 0,
@@ -366,6 +449,11 @@ def gdn_recurrent_fwd(q, k, v, beta, log_alpha, h0=None, cu_seqlens=None, cu_seq
     if ht is None and output_final_state:
         ht = torch.empty((_nstate(q, cu_seqlens), H, dk, dv), dtype=torch.float32,
                          device=q.device)
+    _check_tensors(q, rows=(("k", k), ("v", v), ("o", o)), gates=(("beta", beta),
+                   ("log_alpha", log_alpha)), states=(("h0", h0, dv), ("ht", ht, dv)),
+                   nstate=_nstate(q, cu_seqlens))
+    if k.shape != q.shape or o.shape != v.shape:
+        raise ValueError("k must match q, and o must match v")
     args = (ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(beta), _ptr(log_alpha), _ptr(h0),
             _ptr(o), _ptr(ht), _stream(q.device))
     if timer is None:
@@ -403,12 +491,9 @@ def make_problem_meta(q, v, cu_seqlens=None, cu_seqlens_host=None):
     keep = []
     p = Problem(B, T, H, dk, dv, 0, None, None, dt)
     if cu_seqlens is not None:
-        if cu_seqlens_host is None:
-            cu_seqlens_host = cu_seqlens.to("cpu")
-        host = cu_seqlens_host.to(torch.int32).contiguous()
-        keep.append(host)
+        dev, host = _cu_pair(cu_seqlens, cu_seqlens_host, cu_seqlens.device, keep)
         p.num_seqs = host.numel() - 1
-        p.cu_seqlens = cu_seqlens.data_ptr()
+        p.cu_seqlens = dev.data_ptr()
         p.cu_seqlens_host = host.data_ptr()
     return p, keep
 

@@ -224,3 +224,43 @@ def test_block_ops_reject_bad_arguments(lib):
     assert lib.gdn_norm_gate_fwd(ctypes.byref(p), 1e-5, fake, None, fake, fake, None) == 1
     assert lib.gdn_norm_gate_bwd(ctypes.byref(p), 1e-5, fake, fake, fake, fake, fake, fake, fake,
                                  fake, nw - 1, None) == 5
+
+
+def test_binding_converts_int64_cu_seqlens():
+    """torch.tensor and cumsum give int64; the kernels read int32.  The binding
+    hands the library an int32 copy (kept alive for the call) and checks that
+    the host and device copies describe the same number of sequences."""
+    import torch
+    q = torch.zeros((1, 10, 2, 64), dtype=torch.bfloat16)
+    v = torch.zeros((1, 10, 2, 64), dtype=torch.bfloat16)
+    cu = torch.tensor([0, 3, 3, 10])  # int64
+    p, keep = gdn.make_problem(q, v, cu)
+    assert p.num_seqs == 3
+    dev = ctypes.cast(p.cu_seqlens, ctypes.POINTER(ctypes.c_int32))
+    host = ctypes.cast(p.cu_seqlens_host, ctypes.POINTER(ctypes.c_int32))
+    assert [dev[i] for i in range(4)] == [0, 3, 3, 10]
+    assert [host[i] for i in range(4)] == [0, 3, 3, 10]
+    assert any(t.data_ptr() == p.cu_seqlens for t in keep)
+    with pytest.raises(ValueError):
+        gdn.make_problem(q, v, cu, torch.tensor([0, 10], dtype=torch.int32))
+    with pytest.raises(TypeError):
+        gdn.make_problem(q, v, cu.to(torch.float32))
+
+
+def test_binding_rejects_mismatched_tensors():
+    import torch
+    q = torch.zeros((1, 10, 2, 64), dtype=torch.bfloat16)
+    good = dict(rows=(("k", q.clone()),), gates=(("beta", torch.zeros(1, 10, 2)),),
+                states=(("h0", torch.zeros(1, 2, 64, 64), 64),), nstate=1)
+    gdn._check_tensors(q, **good)
+    bad_cases = [
+        dict(good, rows=(("k", q.to(torch.float32)),)),                  # dtype
+        dict(good, rows=(("k", q.transpose(1, 2).contiguous().transpose(1, 2)),)),  # strides
+        dict(good, gates=(("beta", torch.zeros(1, 10, 2, dtype=torch.float64)),)),
+        dict(good, gates=(("beta", torch.zeros(1, 10, 3)),)),           # shape
+        dict(good, states=(("h0", torch.zeros(2, 2, 64, 64), 64),)),    # sequences
+        dict(good, states=(("h0", torch.zeros(1, 2, 64, 64).to(torch.bfloat16), 64),)),
+    ]
+    for kw in bad_cases:
+        with pytest.raises(ValueError):
+            gdn._check_tensors(q, **kw)

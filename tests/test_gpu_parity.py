@@ -273,6 +273,29 @@ def test_saved_stress(G, oracle_mod, label, kw):
     check_saved(G, oracle_mod, inp, TOL["f32"], "saved_stress_" + label)
 
 
+@pytest.mark.parametrize("label,kw", [
+    ("weak_decay", dict(log_alpha_scale=0.01)),
+    ("mid_decay", dict(log_alpha_scale=0.05)),
+    ("beta_0_2", dict(beta_scale=2.0, log_alpha_scale=0.1)),
+])
+@pytest.mark.parametrize("dk,dv", [(128, 128), (256, 512)])
+@pytest.mark.parametrize("path", ["fwd", "bwd", "saved"])
+def test_stress_wide_heads(G, oracle_mod, path, dk, dv, label, kw):
+    """Weak and intermediate decay and beta in (0, 2) at the wide head dims,
+    whose kernels are separate instantiations: with e^{g_n} near 1 the
+    carried state e^{g_n} S, its gradient and the <dS, S> gate term weigh as
+    much as the in-chunk terms.  Four chunks, the last one ragged."""
+    inp = make_inputs(1, 200, 2, dk, dv, "bf16", seed=21, h0_std=0.05, backward=path != "fwd",
+                      **kw)
+    name = "stress_%s_%d_%d_%s" % (path, dk, dv, label)
+    if path == "fwd":
+        check_fwd(G, oracle_mod, inp, TOL["bf16"], name)
+    elif path == "bwd":
+        check_bwd(G, oracle_mod, inp, TOL["bf16"], name)
+    else:
+        check_saved(G, oracle_mod, inp, TOL["bf16"], name)
+
+
 def test_saved_strong_decay_bf16_256_512(G, oracle_mod):
     """The bench shape's saved path when every decay factor past a few tokens
     underflows fp32 (per-token log gates of about -5.5)."""
@@ -473,24 +496,46 @@ def test_decode_continues_prefill(G, oracle_mod, dtype, dk, dv):
 
 
 def sample_units(inp, units):
-    """Slice inputs to the listed (sequence, head) units, each as its own dense call."""
+    """The listed (sequence, head) units as independent one-head sequences of
+    one packed problem: (inputs, [(unit, start, length)])."""
     cu = inp.get("cu_seqlens")
-    out = []
+    parts = {k: [] for k in ("q", "k", "v", "beta", "log_alpha", "dO")}
+    h0s, dhts, spans, at = [], [], [], 0
     for n, h in units:
         if cu is None:
-            sl = lambda x: x[n:n + 1, :, h:h + 1]
-            st = lambda x: None if x is None else x[n:n + 1, h:h + 1]
+            sl = lambda x: x[n, :, h:h + 1]
         else:
-            s, e = int(cu[n]), int(cu[n + 1])
-            sl = lambda x, s=s, e=e: x[:, s:e, h:h + 1]
-            st = lambda x: None if x is None else x[n:n + 1, h:h + 1]
-        d = {k: sl(inp[k]) for k in ("q", "k", "v", "beta", "log_alpha")}
-        d["h0"] = st(inp.get("h0"))
-        if "dO" in inp:
-            d["dO"] = sl(inp["dO"])
-            d["dht"] = st(inp.get("dht"))
-        out.append(((n, h), d))
-    return out
+            s_, e_ = int(cu[n]), int(cu[n + 1])
+            sl = lambda x, s_=s_, e_=e_: x[0, s_:e_, h:h + 1]
+        for key in parts:
+            if key in inp:
+                parts[key].append(sl(inp[key]))
+        if inp.get("h0") is not None:
+            h0s.append(inp["h0"][n:n + 1, h:h + 1])
+        if inp.get("dht") is not None:
+            dhts.append(inp["dht"][n:n + 1, h:h + 1])
+        L = parts["q"][-1].shape[0]
+        spans.append(((n, h), at, L))
+        at += L
+    out = {k: torch.cat(v, 0).unsqueeze(0) for k, v in parts.items() if v}
+    out["cu_seqlens"] = torch.tensor([0] + [a + L for _, a, L in spans], dtype=torch.int64)
+    out["h0"] = torch.cat(h0s, 0) if h0s else None
+    out["dht"] = torch.cat(dhts, 0) if dhts else None
+    return out, spans
+
+
+def full_size_units(w, cu):
+    """Every head index at least once, and the first and the last sequence
+    (and, packed, the longest) at least once each."""
+    N = w.B if cu is None else cu.numel() - 1
+    seqs = [0, N - 1]
+    if cu is not None:
+        seqs.append(int((cu[1:] - cu[:-1]).argmax()))
+    rng = np.random.default_rng(0)
+    seqs += [int(x) for x in rng.integers(0, N, size=max(0, w.H - len(seqs)))]
+    units = {(seqs[h % len(seqs)], h) for h in range(w.H)}
+    units |= {(n, int(rng.integers(w.H))) for n in seqs[:3]}
+    return sorted(units)
 
 
 FULL_CASES = [(name, "stateless") for name in WORKLOADS] + \
@@ -499,6 +544,9 @@ FULL_CASES = [(name, "stateless") for name in WORKLOADS] + \
 
 @pytest.mark.parametrize("name,path", FULL_CASES)
 def test_full_workload_sampled(G, oracle_mod, name, path):
+    """The whole workload on the GPU as the benchmark launches it; the oracle
+    recomputes a sample of (sequence, head) units that covers every head and
+    the first, last and longest sequences.  Prints the per-tensor margin."""
     w = WORKLOADS[name]
     inp = workload_inputs(name)
     say(name, path, "full-size run")
@@ -514,39 +562,86 @@ def test_full_workload_sampled(G, oracle_mod, name, path):
     del d
     tol = TOL[w.dtype]
     cu = inp.get("cu_seqlens")
-    N = w.B if cu is None else cu.numel() - 1
-    rng = np.random.default_rng(0)
-    units = [(int(rng.integers(N)), int(rng.integers(w.H))) for _ in range(2)]
-    if cu is not None:  # include the longest sequence
-        lens = (cu[1:] - cu[:-1]).numpy()
-        units[0] = (int(lens.argmax()), units[0][1])
-    for (n, h), s in sample_units(inp, units):
-        say(name, "oracle unit", (n, h))
-        if w.backward:
-            ref = oracle_mod.bwd(s["q"], s["k"], s["v"], s["beta"], s["log_alpha"], s["dO"],
-                                 h0=s["h0"], dht=s["dht"])
-        else:
-            ro, rh = oracle_mod.fwd(s["q"], s["k"], s["v"], s["beta"], s["log_alpha"],
-                                    h0=s["h0"])
-            ref = dict(o=ro, ht=rh)
+    units = full_size_units(w, cu)
+    s, spans = sample_units(inp, units)
+    say(name, "oracle units", units)
+    if w.backward:
+        ref = oracle_mod.bwd(s["q"], s["k"], s["v"], s["beta"], s["log_alpha"], s["dO"],
+                             h0=s["h0"], dht=s["dht"], cu_seqlens=s["cu_seqlens"])
+    else:
+        ro, rh = oracle_mod.fwd(s["q"], s["k"], s["v"], s["beta"], s["log_alpha"], h0=s["h0"],
+                                cu_seqlens=s["cu_seqlens"])
+        ref = dict(o=ro, ht=rh)
+    worst = {}
+    for i, ((n, h), at, L) in enumerate(spans):
         if cu is None:
-            got = dict(o=o[n:n + 1, :, h:h + 1], ht=ht[n:n + 1, h:h + 1])
-            if r is not None:
-                got.update(dq=r["dq"][n:n + 1, :, h:h + 1], dk=r["dk"][n:n + 1, :, h:h + 1],
-                           dv=r["dv"][n:n + 1, :, h:h + 1],
-                           dbeta=r["dbeta"][n:n + 1, :, h:h + 1],
-                           dlog_alpha=r["dlog_alpha"][n:n + 1, :, h:h + 1],
-                           dh0=r["dh0"][n:n + 1, h:h + 1])
+            rows = lambda x: x[n, :, h]
         else:
             s_, e_ = int(cu[n]), int(cu[n + 1])
-            got = dict(o=o[:, s_:e_, h:h + 1], ht=ht[n:n + 1, h:h + 1])
-            if r is not None:
-                got.update(dq=r["dq"][:, s_:e_, h:h + 1], dk=r["dk"][:, s_:e_, h:h + 1],
-                           dv=r["dv"][:, s_:e_, h:h + 1],
-                           dbeta=r["dbeta"][:, s_:e_, h:h + 1],
-                           dlog_alpha=r["dlog_alpha"][:, s_:e_, h:h + 1],
-                           dh0=r["dh0"][n:n + 1, h:h + 1])
-        errs = {k: rel_err(f64(v).reshape(ref[k].shape), ref[k]) for k, v in got.items()}
-        say(name, (n, h), {k: "%.3g" % v for k, v in errs.items()})
+            rows = lambda x, s_=s_, e_=e_: x[0, s_:e_, h]
+        got = dict(o=rows(o), ht=ht[n, h])
+        want = dict(o=ref["o"][at:at + L, 0], ht=ref["ht"][i, 0])
+        if r is not None:
+            for key in ("dq", "dk", "dv", "dbeta", "dlog_alpha"):
+                got[key] = rows(r[key])
+                want[key] = ref[key][at:at + L, 0]
+            got["dh0"] = r["dh0"][n, h]
+            want["dh0"] = ref["dh0"][i, 0]
+        errs = {k: rel_err(f64(v).reshape(want[k].shape), want[k]) for k, v in got.items()}
+        for k, e in errs.items():
+            worst[k] = max(worst.get(k, 0.0), e)
+        say(name, path, (n, h), {k: "%.3g" % v for k, v in errs.items()})
         bad = {k: v for k, v in errs.items() if not v <= tol}
-        assert not bad, bad
+        assert not bad, ((n, h), bad)
+    say("margin", name, path, "units=%d" % len(units), "tol=%g" % tol,
+        {k: "%.3g (%.0f%% of tol)" % (v, 100 * v / tol) for k, v in worst.items()})
+
+
+# ------------------------------------------------------------------ NaN isolation
+
+
+@pytest.mark.parametrize("where", ["q", "k", "v", "beta", "log_alpha", "dO"])
+@pytest.mark.parametrize("dtype,dk,dv", [("f32", 64, 64), ("bf16", 128, 128),
+                                         ("bf16", 256, 512)])
+def test_nan_stays_in_its_unit(G, dtype, dk, dv, where):
+    """A NaN planted in one (sequence, head) unit's input leaves every other
+    unit bit-identical on every path (forward, stateless backward, saving
+    forward + saved backward); packed input, so chunks of several sequences
+    share the launches.  No unit's work mixes with another's."""
+    cu = torch.tensor([0, 70, 70, 200, 261], dtype=torch.int32)
+    inp = make_inputs(1, 261, 3, dk, dv, dtype, seed=32, h0_std=0.05, backward=True,
+                      cu_seqlens=cu)
+    n0, h0, t0 = 2, 1, 150
+    say("nan_isolation", dtype, dk, dv, where)
+    clean = to_dev(inp)
+    bad = {k: (v.clone() if isinstance(v, torch.Tensor) else v) for k, v in clean.items()}
+    bad[where][0, t0, h0] = float("nan")
+
+    def run_all(d):
+        o, ht = run_fwd(G, d)
+        r = run_bwd(G, d)
+        o2, ht2, r2 = run_saved(G, d)
+        out = dict(o=o, o2=o2, ht=ht, ht2=ht2)
+        out.update({k: v for k, v in r.items()})
+        out.update({k + "_s": v for k, v in r2.items()})
+        return out
+
+    a, b = run_all(clean), run_all(bad)
+    s0, e0 = int(cu[n0]), int(cu[n0 + 1])
+    hit = False
+    for name in a:
+        x, y = a[name].clone(), b[name].clone()
+        if x.dim() == 4 and x.shape[0] == 1 and x.shape[1] == 261:  # token rows
+            hit |= bool(torch.isnan(y[0, s0:e0, h0]).any())
+            x[0, s0:e0, h0] = 0
+            y[0, s0:e0, h0] = 0
+        elif x.dim() == 3:  # [1, T, H] gates
+            hit |= bool(torch.isnan(y[0, s0:e0, h0]).any())
+            x[0, s0:e0, h0] = 0
+            y[0, s0:e0, h0] = 0
+        else:  # states [N, H, dk, dv]
+            hit |= bool(torch.isnan(y[n0, h0]).any())
+            x[n0, h0] = 0
+            y[n0, h0] = 0
+        assert torch.equal(x, y), name
+    assert hit

@@ -19,6 +19,8 @@ import numpy as np
 import pytest
 import torch
 
+from paper_2412_06464_amd.inputs import make_inputs
+
 # ---------------------------------------------------------------- helpers
 
 
@@ -347,3 +349,36 @@ def test_gradients_by_central_differences(oracle_mod, seed, beta_scale):
             fd = (loss(plus) - loss(minus)) / (2 * h)
             an = (r[gname] * d).sum()
             assert abs(fd - an) <= 1e-7 * max(1.0, abs(an)), (name, fd, an)
+
+
+@pytest.mark.parametrize("where", ["q", "k", "v", "beta", "log_alpha", "dO"])
+def test_nan_stays_in_its_unit(oracle_mod, where):
+    """Every (sequence, head) pair is an independent recurrence: a NaN planted
+    in one input of one unit leaves every other unit's outputs and gradients
+    bit-identical, and does reach the unit it was planted in."""
+    cu = torch.tensor([0, 70, 70, 200], dtype=torch.int32)
+    inp = make_inputs(1, 200, 3, 8, 6, "f32", seed=31, h0_std=0.05, backward=True,
+                      cu_seqlens=cu)
+    n0, h0, t0 = 2, 1, 150  # token 150 lies in sequence 2 (tokens 70..199)
+    bad = {k: (v.clone() if isinstance(v, torch.Tensor) else v) for k, v in inp.items()}
+    bad[where][0, t0, h0] = float("nan")
+
+    def run(x):
+        return oracle_mod.bwd(x["q"], x["k"], x["v"], x["beta"], x["log_alpha"], x["dO"],
+                              h0=x["h0"], dht=x["dht"], cu_seqlens=cu)
+
+    a, b = run(inp), run(bad)
+    s0, e0 = int(cu[n0]), int(cu[n0 + 1])
+    hit = False  # some output of the planted unit is NaN (not every one: o
+    # does not depend on dO, nor dq on q, nor dv on v)
+    for name in ("o", "dq", "dk", "dv", "dbeta", "dlog_alpha"):
+        x, y = a[name].copy(), b[name].copy()
+        hit |= bool(np.isnan(y[s0:e0, h0]).any())
+        x[s0:e0, h0] = y[s0:e0, h0] = 0.0  # every other unit is bit-identical
+        assert np.array_equal(x, y), name
+    for name in ("ht", "dh0"):
+        x, y = a[name].copy(), b[name].copy()
+        hit |= bool(np.isnan(y[n0, h0]).any())
+        x[n0, h0] = y[n0, h0] = 0.0
+        assert np.array_equal(x, y), name
+    assert hit
