@@ -39,7 +39,8 @@
  *  - Pointers must be 16-byte aligned.
  *  - The library never allocates, frees or synchronises and keeps no state
  *    between calls: the caller owns every buffer, including the workspace,
- *    whose size the *_workspace_size queries return.  All work is enqueued on
+ *    whose size the *_workspace_size queries return.  (One exception:
+ *    gdn_chunk_fwd_noalloc uses a static device array of the library.)  All work is enqueued on
  *    `stream` (a hipStream_t; NULL = the default stream); outputs are valid
  *    when the stream reaches them.  Calls on different streams with distinct
  *    workspaces are independent.
@@ -102,6 +103,27 @@ gdn_status gdn_chunk_fwd(const gdn_problem *p, const void *q, const void *k,
                          const float *log_alpha, const float *h0, void *o,
                          float *ht, void *workspace, size_t workspace_bytes,
                          void *stream);
+
+/* Forward without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same operation, arguments (minus the workspace),
+ * outputs, checks and statuses as gdn_chunk_fwd, and the same kernels.  The
+ * workspace is a static device array of GDN_NOALLOC_SCRATCH_BYTES bytes inside
+ * the library, one per GPU, held until the process ends; the call allocates
+ * nothing.  Problems whose gdn_chunk_fwd_workspace_size exceeds it return
+ * GDN_ERR_WORKSPACE before any HIP call (about 390 chunk-heads at
+ * dk = 256, dv = 512; 900 at dk = dv = 128).  The array belongs to the
+ * calling thread's current device (hipGetDevice), which must be the device of
+ * the pointers and of `stream`.  All calls on one GPU share the array:
+ * calls that overlap in time on that GPU (other streams, other threads) race
+ * and give wrong results; serialise them.  Nothing in the array needs to
+ * start at zero. */
+#define GDN_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+gdn_status gdn_chunk_fwd_noalloc(const gdn_problem *p, const void *q,
+                                 const void *k, const void *v,
+                                 const float *beta, const float *log_alpha,
+                                 const float *h0, void *o, float *ht,
+                                 void *stream);
 
 /* Backward (stateless: recomputes the forward's chunk states itself).
  *   in : the forward's inputs; dO = gradient of o; dht = gradient of the

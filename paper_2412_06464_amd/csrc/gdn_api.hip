@@ -6,6 +6,7 @@
 
 #include <math.h>
 
+#include <mutex>
 #include <new>
 
 #include "../../include/gdn.h"
@@ -235,6 +236,37 @@ void fill_common(const gdn_problem* p, const Shape& s, Args* a) {
   a->cu = p->cu_seqlens;
 }
 
+constexpr size_t NOALLOC_BYTES = GDN_NOALLOC_SCRATCH_BYTES;
+constexpr int MAX_DEVICES = 64;
+static_assert(NOALLOC_BYTES % ALIGN == 0, "scratch size must keep the carve-up aligned");
+
+}  // namespace
+
+// Workspace of gdn_chunk_fwd_noalloc: a file-scope device array, one copy on
+// every GPU the library runs on, held until the process ends.  In host code
+// `scratch` is only the registration handle of that array, not a device
+// address: the device address of each GPU's copy is looked up once per
+// device (hipGetSymbolAddress with that device current) and kept below.
+static __device__ __align__(256) unsigned char scratch[GDN_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+std::mutex scratch_mu;
+void* scratch_ptr[MAX_DEVICES];  // device address of `scratch` per device, once looked up
+
+// The current device's copy of the scratch array, or nullptr on failure.
+void* scratch_for_current_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEVICES) return nullptr;
+  std::lock_guard<std::mutex> lk(scratch_mu);
+  if (!scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+    scratch_ptr[dev] = ptr;
+  }
+  return scratch_ptr[dev];
+}
+
 }  // namespace
 
 extern "C" {
@@ -288,6 +320,23 @@ gdn_status gdn_chunk_fwd(const gdn_problem* p, const void* q, const void* k, con
                          float* ht, void* workspace, size_t workspace_bytes, void* stream) {
   return gdn_chunk_fwd_timed(p, q, k, v, beta, log_alpha, h0, o, ht, workspace, workspace_bytes,
                              stream, nullptr);
+}
+
+gdn_status gdn_chunk_fwd_noalloc(const gdn_problem* p, const void* q, const void* k,
+                                 const void* v, const float* beta, const float* log_alpha,
+                                 const float* h0, void* o, float* ht, void* stream) {
+  Shape s;
+  const gdn_status st = check_problem(p, &s);
+  if (st != GDN_OK) return st;
+  if (!q || !k || !v || !beta || !o) return GDN_ERR_NULL;
+  // the size check runs before any HIP call
+  if (carve(p, s, Use::Fwd, nullptr, nullptr) > NOALLOC_BYTES) return GDN_ERR_WORKSPACE;
+  void* ws = scratch_for_current_device();
+  if (!ws) return GDN_ERR_HIP;
+  // every byte of the forward's workspace that a kernel reads is written by
+  // an earlier kernel of the same call: nothing needs clearing
+  return gdn_chunk_fwd_timed(p, q, k, v, beta, log_alpha, h0, o, ht, ws, NOALLOC_BYTES, stream,
+                             nullptr);
 }
 
 gdn_status gdn_chunk_bwd_timed(const gdn_problem* p, const void* q, const void* k,

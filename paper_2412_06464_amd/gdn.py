@@ -26,7 +26,9 @@ EXPORTS = ("gdn_chunk_fwd", "gdn_chunk_bwd", "gdn_chunk_fwd_workspace_size",
            "gdn_chunk_fwd_save_timed", "gdn_chunk_bwd_saved_timed", "gdn_recurrent_fwd",
            "gdn_recurrent_fwd_timed", "gdn_conv_silu_workspace_size", "gdn_conv_silu_fwd",
            "gdn_conv_silu_bwd", "gdn_norm_gate_workspace_size", "gdn_norm_gate_fwd",
-           "gdn_norm_gate_bwd", "gdn_status_string")
+           "gdn_norm_gate_bwd", "gdn_status_string", "gdn_chunk_fwd_noalloc")
+# bytes of the library's static workspace behind gdn_chunk_fwd_noalloc
+NOALLOC_SCRATCH_BYTES = 64 << 20
 
 
 class Problem(ctypes.Structure):
@@ -102,6 +104,8 @@ def load_library():
         lib.gdn_chunk_bwd_workspace_size.restype = S
         lib.gdn_chunk_fwd.argtypes = [pp] + [P] * 8 + [P, S, P]
         lib.gdn_chunk_fwd.restype = ctypes.c_int
+        lib.gdn_chunk_fwd_noalloc.argtypes = [pp] + [P] * 8 + [P]
+        lib.gdn_chunk_fwd_noalloc.restype = ctypes.c_int
         lib.gdn_chunk_bwd.argtypes = [pp] + [P] * 14 + [P, S, P]
         lib.gdn_chunk_bwd.restype = ctypes.c_int
         pt = ctypes.POINTER(Timing)
@@ -295,6 +299,30 @@ def gdn_chunk_fwd(q, k, v, beta, log_alpha, h0=None, cu_seqlens=None, cu_seqlens
         _check(lib.gdn_chunk_fwd(*args))
     else:
         _check(lib.gdn_chunk_fwd_timed(*args, ctypes.byref(timer.timing)))
+    del keep
+    return o, ht
+
+
+def gdn_chunk_fwd_noalloc(q, k, v, beta, log_alpha, h0=None, cu_seqlens=None,
+                          cu_seqlens_host=None, o=None, ht=None):
+    """gdn_chunk_fwd on the library's static workspace (no allocation in the
+    library; pass ``o`` and ``ht`` to allocate nothing here either).  Raises
+    GdnError(GDN_ERR_WORKSPACE) for problems whose workspace exceeds
+    NOALLOC_SCRATCH_BYTES.  Calls on one GPU must not overlap in time."""
+    lib = load_library()
+    p, keep = make_problem(q, v, cu_seqlens, cu_seqlens_host)
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    if o is None:
+        o = torch.empty((B, T, H, dv), dtype=q.dtype, device=q.device)
+    _check_tensors(q, rows=(("k", k), ("v", v), ("o", o)), gates=(("beta", beta),
+                   ("log_alpha", log_alpha)), states=(("h0", h0, dv), ("ht", ht, dv)),
+                   nstate=_nstate(q, cu_seqlens))
+    if k.shape != q.shape or o.shape != v.shape:
+        raise ValueError("k must match q, and o must match v")
+    _check(lib.gdn_chunk_fwd_noalloc(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(beta),
+                                     _ptr(log_alpha), _ptr(h0), _ptr(o), _ptr(ht),
+                                     _stream(q.device)))
     del keep
     return o, ht
 

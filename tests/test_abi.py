@@ -264,3 +264,26 @@ def test_binding_rejects_mismatched_tensors():
     for kw in bad_cases:
         with pytest.raises(ValueError):
             gdn._check_tensors(q, **kw)
+
+
+def test_noalloc_forward_checks_before_any_hip_call(lib):
+    """The no-allocation forward rejects bad arguments and problems whose
+    workspace exceeds the static array with a status, before it touches the
+    GPU (this runs on a host without one)."""
+    assert gdn.NOALLOC_SCRATCH_BYTES == 64 << 20
+    fake = ctypes.c_void_p(0x10000)
+    # 8 x 4096 tokens x 6 heads at 256/512: 3072 chunk-heads, ~517 MB of workspace
+    big, _ = problem(B=8, T=4096, H=6, dk=256, dv=512)
+    assert gdn.gdn_chunk_fwd_workspace_size(big) > gdn.NOALLOC_SCRATCH_BYTES
+    rc = lib.gdn_chunk_fwd_noalloc(ctypes.byref(big), fake, fake, fake, fake, fake, None, fake,
+                                   None, None)
+    assert rc == 5  # GDN_ERR_WORKSPACE
+    small, _ = problem(B=1, T=64, H=1)
+    assert gdn.gdn_chunk_fwd_workspace_size(small) <= gdn.NOALLOC_SCRATCH_BYTES
+    rc = lib.gdn_chunk_fwd_noalloc(ctypes.byref(small), None, fake, fake, fake, fake, None, fake,
+                                   None, None)
+    assert rc == 1  # GDN_ERR_NULL
+    bad, _ = problem(dk=96)
+    rc = lib.gdn_chunk_fwd_noalloc(ctypes.byref(bad), fake, fake, fake, fake, fake, None, fake,
+                                   None, None)
+    assert rc == 3  # GDN_ERR_UNSUPPORTED
