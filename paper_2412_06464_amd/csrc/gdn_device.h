@@ -339,16 +339,21 @@ __device__ inline typename Mfma<E>::frag load_frag_scaled(const E* row, int kt, 
 // to complete in issue order among themselves, but an ordinary load issued
 // after a copy may return before it: a partial vmcnt wait is sound only
 // while no ordinary load issued after the awaited copies is in flight.
+// The statement sets m0 (the LDS base of the copy).  The compiler treats m0
+// as reserved and does not honour it as an asm clobber; these kernels rely
+// on the compiler never holding a value in m0 itself, which
+// tests/test_m0_use.py checks on the built code object: every write of m0 is
+// one of these statements, directly followed by its copy.
 template <class E> __device__ inline void dma_frag(const E* src_lane, E* lds_frag);
 template <> __device__ inline void dma_frag<bf16>(const bf16* src_lane, bf16* lds_frag) {
   const unsigned lds = (unsigned)(uintptr_t)lds_frag;
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(src_lane)
-               : "memory", "m0");
+               : "memory");
 }
 template <> __device__ inline void dma_frag<float>(const float* src_lane, float* lds_frag) {
   const unsigned lds = (unsigned)(uintptr_t)lds_frag;
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off" ::"s"(lds), "v"(src_lane)
-               : "memory", "m0");
+               : "memory");
 }
 // Wait until at most N vector-memory operations of this wave are in flight.
 template <int N> __device__ inline void wait_vmcnt() {
