@@ -232,6 +232,73 @@ gdn_status gdn_norm_gate_bwd(const gdn_problem *p, float eps, const void *o,
                              void *dout, void *dg, float *dw, void *workspace,
                              size_t workspace_bytes, void *stream);
 
+/* Fused block: the prologue above run inside the chunked rule's own kernels
+ * (Sec. 3.4 and the block-design figure: the projections of q, k and v pass
+ * through the short convolution and SiLU, q and k through the L2
+ * normalisation, before the gated delta rule).  The result is that of
+ * gdn_conv_silu_fwd (l2norm 1 for q and k, 0 for v) followed by the chunked
+ * rule on its outputs, up to rounding, without the rule's q, k and v making
+ * a round trip through memory: the prep kernel forms them from the
+ * projections as it loads its chunk's rows, and in the backward the
+ * gradient kernel recomputes q and k from their projections and applies the
+ * prologue's backward to its own dq and dk before anything is stored.
+ * bf16 problems only (GDN_ERR_UNSUPPORTED otherwise), any dk, dv the rule
+ * supports; dense or packed sequences as for the rule.
+ *
+ * The prologue is described by gdn_block_prologue: width 1..4 and eps >= 0
+ * (finite) as for gdn_conv_silu_fwd (GDN_ERR_VALUE otherwise), the
+ * projections xq, xk [B, T, H, dk] and xv [B, T, H, dv] (bf16, the
+ * problem's layout and sequences), and the fp32 weights wq, wk [H * dk][width]
+ * and wv [H * dv][width] (tap width-1 multiplies the current token).  All six
+ * pointers are required and 16-byte aligned. */
+typedef struct {
+  int32_t width;            /* convolution taps, 1..4             */
+  float eps;                /* L2 epsilon of q and k              */
+  const void *xq, *xk, *xv; /* projections, bf16                  */
+  const float *wq, *wk, *wv;/* convolution weights, fp32          */
+} gdn_block_prologue;
+
+/* Forward of the fused block: o and ht as gdn_chunk_fwd computes them from
+ * the rule's q, k, v; beta, log_alpha, h0, o, ht and the workspace
+ * (gdn_chunk_fwd_workspace_size bytes) as there.  q, k, v (optional, NULL
+ * to skip) receive the rule's inputs the prologue formed, [B, T, H, d]
+ * bf16. */
+gdn_status gdn_block_fwd(const gdn_problem *p, const gdn_block_prologue *pro,
+                         const float *beta, const float *log_alpha,
+                         const float *h0, void *o, float *ht, void *q, void *k,
+                         void *v, void *workspace, size_t workspace_bytes,
+                         void *stream);
+
+/* Saving forward of the fused block (training): as gdn_block_fwd, and fills
+ * `saved` (gdn_chunk_saved_size bytes) as gdn_chunk_fwd_save does, with
+ * gdn_chunk_fwd_save_workspace_size bytes of workspace.  v is required
+ * here: the backward reads the rule's v. */
+gdn_status gdn_block_fwd_save(const gdn_problem *p,
+                              const gdn_block_prologue *pro, const float *beta,
+                              const float *log_alpha, const float *h0, void *o,
+                              float *ht, void *q, void *k, void *v, void *saved,
+                              size_t saved_bytes, void *workspace,
+                              size_t workspace_bytes, void *stream);
+
+/* Backward of the fused block from a saving fused forward: the gradients
+ * with respect to the block's inputs, dxq, dxk [B, T, H, dk] and dxv
+ * [B, T, H, dv] (bf16), dwq, dwk, dwv (fp32, shaped as the weights, summed
+ * over all tokens in a fixed order: deterministic), and dbeta, dlog_alpha
+ * (optional), dh0 (optional) as gdn_chunk_bwd_saved returns them.  Reads
+ * the same prologue, the rule's v that gdn_block_fwd_save wrote, beta, dO,
+ * dht (or NULL) and `saved` (unchanged).  `workspace` holds
+ * gdn_block_bwd_saved_workspace_size(p, width) bytes. */
+size_t gdn_block_bwd_saved_workspace_size(const gdn_problem *p, int width);
+gdn_status gdn_block_bwd_saved(const gdn_problem *p,
+                               const gdn_block_prologue *pro, const void *v,
+                               const float *beta, const void *dO,
+                               const float *dht, const void *saved,
+                               size_t saved_bytes, void *dxq, void *dxk,
+                               void *dxv, float *dwq, float *dwk, float *dwv,
+                               float *dbeta, float *dlog_alpha, float *dh0,
+                               void *workspace, size_t workspace_bytes,
+                               void *stream);
+
 /* Optional launch timing, for benchmarks and profilers.  The caller creates
  * and owns the events (hipEvent_t handles, e.g. from hipEventCreate).  A
  * *_timed call records events[2i] just before and events[2i+1] just after
@@ -277,6 +344,27 @@ gdn_status gdn_chunk_bwd_saved_timed(const gdn_problem *p, const void *q,
                                      float *dh0, void *workspace,
                                      size_t workspace_bytes, void *stream,
                                      gdn_timing *timing);
+
+gdn_status gdn_block_fwd_timed(const gdn_problem *p,
+                               const gdn_block_prologue *pro, const float *beta,
+                               const float *log_alpha, const float *h0, void *o,
+                               float *ht, void *q, void *k, void *v,
+                               void *workspace, size_t workspace_bytes,
+                               void *stream, gdn_timing *timing);
+gdn_status gdn_block_fwd_save_timed(const gdn_problem *p,
+                                    const gdn_block_prologue *pro,
+                                    const float *beta, const float *log_alpha,
+                                    const float *h0, void *o, float *ht, void *q,
+                                    void *k, void *v, void *saved,
+                                    size_t saved_bytes, void *workspace,
+                                    size_t workspace_bytes, void *stream,
+                                    gdn_timing *timing);
+gdn_status gdn_block_bwd_saved_timed(
+    const gdn_problem *p, const gdn_block_prologue *pro, const void *v,
+    const float *beta, const void *dO, const float *dht, const void *saved,
+    size_t saved_bytes, void *dxq, void *dxk, void *dxv, float *dwq, float *dwk,
+    float *dwv, float *dbeta, float *dlog_alpha, float *dh0, void *workspace,
+    size_t workspace_bytes, void *stream, gdn_timing *timing);
 
 gdn_status gdn_recurrent_fwd_timed(const gdn_problem *p, const void *q,
                                    const void *k, const void *v,

@@ -227,6 +227,62 @@ size_t carve_conv(const gdn_problem* p, const Shape& s, int dim, int width, unsi
   return c.off;
 }
 
+// Fused block (prologue + rule): checks of the prologue description.
+gdn_status check_block(const gdn_problem* p, const gdn_block_prologue* b, Shape* s) {
+  const gdn_status st = check_problem(p, s);
+  if (st != GDN_OK) return st;
+  if (!b) return GDN_ERR_NULL;
+  if (p->dtype != GDN_BF16) return GDN_ERR_UNSUPPORTED;
+  if (b->width < 1 || b->width > 4 || !(b->eps >= 0.f) || !isfinite(b->eps)) return GDN_ERR_VALUE;
+  const void* ptrs[] = {b->xq, b->xk, b->xv, b->wq, b->wk, b->wv};
+  for (const void* x : ptrs)
+    if (!x) return GDN_ERR_NULL;
+  for (const void* x : ptrs)
+    if (!aligned16(x)) return GDN_ERR_ALIGN;
+  return GDN_OK;
+}
+
+void fill_prologue(const gdn_block_prologue* b, Args* a) {
+  a->q = b->xq;
+  a->k = b->xk;
+  a->v = b->xv;
+  a->cwq = b->wq;
+  a->cwk = b->wk;
+  a->cwv = b->wv;
+  a->cw = b->width;
+  a->ceps = b->eps;
+}
+
+// Workspace of the fused block's backward: the rule's backward workspace,
+// then the rule's dv (the v prologue's input gradient), the q and k
+// prologue's side buffers and per-chunk weight gradients, and the v
+// prologue's per-chunk weight gradients.
+size_t carve_block_bwd(const gdn_problem* p, const Shape& s, int width, unsigned char* base,
+                       Args* a, gdn::ConvArgs* cv) {
+  Carver c{base, carve(p, s, Use::BwdSaved, base, a)};
+  const size_t NCH = (size_t)s.NC * p->H, NS = (size_t)((s.NC + 255) / 256);
+  unsigned char* dyv = c.take((size_t)s.Ttot * p->H * p->dv * s.esz);
+  unsigned char* head = c.take(2 * NCH * 3 * p->dk * sizeof(float));
+  unsigned char* tail = c.take(2 * NCH * 3 * p->dk * sizeof(float));
+  unsigned char* part = c.take(2 * NCH * p->dk * width * sizeof(float));
+  unsigned char* tmp = c.take(NS * p->H * p->dk * width * sizeof(float));
+  unsigned char* vpart = c.take(NCH * p->dv * width * sizeof(float));
+  unsigned char* vtmp = c.take(NS * p->H * p->dv * width * sizeof(float));
+  if (a) {
+    a->dv = dyv;
+    a->bhead = (float*)head;
+    a->btail = (float*)tail;
+    a->bpart = (float*)part;
+    a->btmp = (float*)tmp;
+  }
+  if (cv) {
+    cv->dy = dyv;
+    cv->part = (float*)vpart;
+    cv->tmp = (float*)vtmp;
+  }
+  return c.off;
+}
+
 void fill_common(const gdn_problem* p, const Shape& s, Args* a) {
   a->gated = 1;
   a->H = p->H;
@@ -534,6 +590,169 @@ gdn_status gdn_recurrent_fwd(const gdn_problem* p, const void* q, const void* k,
                              const float* beta, const float* log_alpha, const float* h0, void* o,
                              float* ht, void* stream) {
   return gdn_recurrent_fwd_timed(p, q, k, v, beta, log_alpha, h0, o, ht, stream, nullptr);
+}
+
+gdn_status gdn_block_fwd_timed(const gdn_problem* p, const gdn_block_prologue* pro,
+                               const float* beta, const float* log_alpha, const float* h0,
+                               void* o, float* ht, void* q, void* k, void* v, void* workspace,
+                               size_t workspace_bytes, void* stream, gdn_timing* timing) {
+  Shape s;
+  gdn_status st = check_block(p, pro, &s);
+  if (st != GDN_OK) return st;
+  if (!beta || !o) return GDN_ERR_NULL;
+  const void* ptrs[] = {beta, log_alpha, h0, o, ht, q, k, v, workspace};
+  for (const void* x : ptrs)
+    if (x && !aligned16(x)) return GDN_ERR_ALIGN;
+  if (!workspace || workspace_bytes < carve(p, s, Use::Fwd, nullptr, nullptr))
+    return GDN_ERR_WORKSPACE;
+  Args a;
+  memset(&a, 0, sizeof a);
+  fill_common(p, s, &a);
+  carve(p, s, Use::Fwd, (unsigned char*)workspace, &a);
+  fill_prologue(pro, &a);
+  a.yq = q;
+  a.yk = k;
+  a.yv = v;
+  a.beta = beta;
+  a.log_alpha = log_alpha;
+  a.gated = log_alpha != nullptr;
+  a.h0 = h0;
+  a.o = o;
+  a.ht = ht;
+  TimingGuard tg(timing);
+  const hipError_t e =
+      gdn::launch_fwd(Dt::BF16, p->dk, p->dv, a, (hipStream_t)stream, tg.get(), true);
+  return e == hipSuccess ? GDN_OK : GDN_ERR_HIP;
+}
+
+gdn_status gdn_block_fwd(const gdn_problem* p, const gdn_block_prologue* pro, const float* beta,
+                         const float* log_alpha, const float* h0, void* o, float* ht, void* q,
+                         void* k, void* v, void* workspace, size_t workspace_bytes,
+                         void* stream) {
+  return gdn_block_fwd_timed(p, pro, beta, log_alpha, h0, o, ht, q, k, v, workspace,
+                             workspace_bytes, stream, nullptr);
+}
+
+gdn_status gdn_block_fwd_save_timed(const gdn_problem* p, const gdn_block_prologue* pro,
+                                    const float* beta, const float* log_alpha, const float* h0,
+                                    void* o, float* ht, void* q, void* k, void* v, void* saved,
+                                    size_t saved_bytes_, void* workspace,
+                                    size_t workspace_bytes, void* stream, gdn_timing* timing) {
+  Shape s;
+  gdn_status st = check_block(p, pro, &s);
+  if (st != GDN_OK) return st;
+  if (!beta || !o || !v) return GDN_ERR_NULL;
+  const void* ptrs[] = {beta, log_alpha, h0, o, ht, q, k, v, saved, workspace};
+  for (const void* x : ptrs)
+    if (x && !aligned16(x)) return GDN_ERR_ALIGN;
+  if (!saved || saved_bytes_ < saved_bytes(p, s)) return GDN_ERR_SAVED;
+  if (!workspace || workspace_bytes < carve(p, s, Use::FwdSave, nullptr, nullptr))
+    return GDN_ERR_WORKSPACE;
+  Args a;
+  memset(&a, 0, sizeof a);
+  fill_common(p, s, &a);
+  carve(p, s, Use::FwdSave, (unsigned char*)workspace, &a);
+  Carver c{(unsigned char*)saved};
+  carve_saved(p, s, c, &a);
+  fill_prologue(pro, &a);
+  a.yq = q;
+  a.yk = k;
+  a.yv = v;
+  a.beta = beta;
+  a.log_alpha = log_alpha;
+  a.gated = log_alpha != nullptr;
+  a.h0 = h0;
+  a.o = o;
+  a.ht = ht;
+  TimingGuard tg(timing);
+  const hipError_t e =
+      gdn::launch_fwd_save(Dt::BF16, p->dk, p->dv, a, (hipStream_t)stream, tg.get(), true);
+  return e == hipSuccess ? GDN_OK : GDN_ERR_HIP;
+}
+
+gdn_status gdn_block_fwd_save(const gdn_problem* p, const gdn_block_prologue* pro,
+                              const float* beta, const float* log_alpha, const float* h0,
+                              void* o, float* ht, void* q, void* k, void* v, void* saved,
+                              size_t saved_bytes_, void* workspace, size_t workspace_bytes,
+                              void* stream) {
+  return gdn_block_fwd_save_timed(p, pro, beta, log_alpha, h0, o, ht, q, k, v, saved,
+                                  saved_bytes_, workspace, workspace_bytes, stream, nullptr);
+}
+
+size_t gdn_block_bwd_saved_workspace_size(const gdn_problem* p, int width) {
+  Shape s;
+  if (check_problem(p, &s) != GDN_OK || width < 1 || width > 4) return 0;
+  return carve_block_bwd(p, s, width, nullptr, nullptr, nullptr);
+}
+
+gdn_status gdn_block_bwd_saved_timed(const gdn_problem* p, const gdn_block_prologue* pro,
+                                     const void* v, const float* beta, const void* dO,
+                                     const float* dht, const void* saved, size_t saved_bytes_,
+                                     void* dxq, void* dxk, void* dxv, float* dwq, float* dwk,
+                                     float* dwv, float* dbeta, float* dlog_alpha, float* dh0,
+                                     void* workspace, size_t workspace_bytes, void* stream,
+                                     gdn_timing* timing) {
+  Shape s;
+  gdn_status st = check_block(p, pro, &s);
+  if (st != GDN_OK) return st;
+  if (!v || !beta || !dO || !dxq || !dxk || !dxv || !dwq || !dwk || !dwv || !dbeta)
+    return GDN_ERR_NULL;
+  const void* ptrs[] = {v,   beta, dO,   dht,   saved,      dxq, dxk,      dxv,
+                        dwq, dwk,  dwv,  dbeta, dlog_alpha, dh0, workspace};
+  for (const void* x : ptrs)
+    if (x && !aligned16(x)) return GDN_ERR_ALIGN;
+  if (!saved || saved_bytes_ < saved_bytes(p, s)) return GDN_ERR_SAVED;
+  if (!workspace ||
+      workspace_bytes < carve_block_bwd(p, s, pro->width, nullptr, nullptr, nullptr))
+    return GDN_ERR_WORKSPACE;
+  Args a;
+  memset(&a, 0, sizeof a);
+  gdn::ConvArgs cv;
+  memset(&cv, 0, sizeof cv);
+  fill_common(p, s, &a);
+  carve_block_bwd(p, s, pro->width, (unsigned char*)workspace, &a, &cv);
+  Carver c{(unsigned char*)const_cast<void*>(saved)};
+  carve_saved(p, s, c, &a);
+  fill_prologue(pro, &a);
+  a.v = v;  // the rule's v (the forward's output): the gradient kernel reads it
+  a.beta = beta;
+  a.dO = dO;
+  a.dht = dht;
+  a.dq = dxq;
+  a.dk = dxk;
+  a.dwq = dwq;
+  a.dwk = dwk;
+  a.dbeta = dbeta;
+  a.dlog_alpha = dlog_alpha;
+  a.dh0 = dh0;
+  cv.H = p->H;
+  cv.N = s.N;
+  cv.NC = (int)s.NC;
+  cv.T = a.T;
+  cv.W = pro->width;
+  cv.l2 = 0;
+  cv.eps = pro->eps;
+  cv.cu = p->cu_seqlens;
+  cv.info = a.info;
+  cv.x = pro->xv;
+  cv.w = pro->wv;
+  cv.dx = dxv;
+  cv.dw = dwv;
+  TimingGuard tg(timing);
+  const hipError_t e =
+      gdn::launch_block_bwd_saved(p->dk, p->dv, a, cv, (hipStream_t)stream, tg.get());
+  return e == hipSuccess ? GDN_OK : GDN_ERR_HIP;
+}
+
+gdn_status gdn_block_bwd_saved(const gdn_problem* p, const gdn_block_prologue* pro,
+                               const void* v, const float* beta, const void* dO,
+                               const float* dht, const void* saved, size_t saved_bytes_,
+                               void* dxq, void* dxk, void* dxv, float* dwq, float* dwk,
+                               float* dwv, float* dbeta, float* dlog_alpha, float* dh0,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+  return gdn_block_bwd_saved_timed(p, pro, v, beta, dO, dht, saved, saved_bytes_, dxq, dxk, dxv,
+                                   dwq, dwk, dwv, dbeta, dlog_alpha, dh0, workspace,
+                                   workspace_bytes, stream, nullptr);
 }
 
 size_t gdn_conv_silu_workspace_size(const gdn_problem* p, int dim, int width) {

@@ -86,10 +86,6 @@ __device__ inline float wave_sum(float x) {
   return x;
 }
 
-// 1 / (1 + e^-x) with the hardware reciprocal (1 ulp) instead of a full
-// IEEE division sequence
-__device__ inline float sigmoidf(float x) { return __builtin_amdgcn_rcpf(1.f + __expf(-x)); }
-
 }  // namespace
 
 // ------------------------------------------------------------------ prologue

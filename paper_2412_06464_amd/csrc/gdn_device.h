@@ -428,6 +428,10 @@ __device__ inline void wave_rows_out(E* g, size_t rs, const E* lds, int w, int n
   }
 }
 
+// 1 / (1 + e^-x) with the hardware reciprocal (1 ulp) instead of a full
+// IEEE division sequence (the block prologue's and epilogue's SiLU)
+__device__ inline float sigmoidf(float x) { return __builtin_amdgcn_rcpf(1.f + __expf(-x)); }
+
 // Inclusive prefix sum across the 64 lanes of a wave.
 __device__ inline float wave_incl_scan(float x) {
   const int l = lane_id();

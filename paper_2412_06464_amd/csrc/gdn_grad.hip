@@ -31,6 +31,7 @@
 // in a fixed order before the gate-gradient scan.
 #include "gdn_device.h"
 #include "gdn_kernels.h"
+#include "gdn_prologue.h"
 
 namespace gdn {
 
@@ -39,9 +40,11 @@ namespace gdn {
 // workgroup's streaming pays for the second read of the dv-side operands
 // (packed dk = dv = 128: 0.92 against 1.03 ms); one at dk = 256, where the
 // two measured the same, and at dk = 64.
-template <class E, int DK>
+// With the fused block prologue (BLK) a workgroup needs whole rows of q and
+// k for their L2 norms, so it owns every dk column.
+template <class E, int DK, bool BLK = false>
 struct GradCfg {
-  static constexpr int HV = DK == 128 ? 2 : 1;
+  static constexpr int HV = (DK == 128 && !BLK) ? 2 : 1;
   static constexpr int NW = (HV == 1 && DK > 64) ? 8 : 4;  // waves
   static constexpr int NTH = 64 * NW;
   static constexpr int NDH = DK / HV / 16;  // dk column tiles of a workgroup
@@ -58,14 +61,15 @@ struct GradCfg {
 constexpr int GP_FLOATS = GRAD_PART_FLOATS;
 static_assert(GP_FLOATS == 12 * CH, "partial-sum blocks");
 
-template <class E, int DK, int DV>
-__global__ __attribute__((amdgpu_flat_work_group_size(1, GradCfg<E, DK>::NTH),
+template <class E, int DK, int DV, bool BLK = false>
+__global__ __attribute__((amdgpu_flat_work_group_size(1, GradCfg<E, DK, BLK>::NTH),
                           amdgpu_waves_per_eu(sizeof(E) == 2 ? 2 : 1)))
 void k_grad(Args a) {
   using M = Mfma<E>;
   using frag = typename M::frag;
-  using C = GradCfg<E, DK>;
+  using C = GradCfg<E, DK, BLK>;
   constexpr int NW = C::NW, NDT = C::NDT, PAT = C::PAT, HV = C::HV, NDH = C::NDH;
+  constexpr int NTH_ = C::NTH;
   constexpr int NKS = DV / M::K;         // MFMA k-steps over dv
   constexpr int F = 16 + 2 * NDH;        // fragments per k-step: dO, dX, V' (4 each), V (4), S, dS
   constexpr int PF = F / NW;             // fragments each wave copies per k-step
@@ -85,8 +89,19 @@ void k_grad(Args a) {
   constexpr int MID_BYTES = STG_BYTES > KQ_BYTES ? STG_BYTES : KQ_BYTES;
   constexpr int ECP_BYTES = 4 * NW * CH * (int)sizeof(float);  // partial column sums of E
   constexpr int FIN_ALL = FIN_BYTES + MID_BYTES + ECP_BYTES;
-  constexpr int SMEM = RING_BYTES > FIN_ALL ? RING_BYTES : FIN_ALL;
-  static_assert(sizeof(E) == 4 || DK == 256 || SMEM + 5 * 1024 + 512 <= 80 * 1024,
+  // block prologue (BLK): forming the q and k rows, beside the finish
+  // buffers (one 64-wide slice of x, the row sums, the weights by lag) ...
+  using PS = ProStage<E, 64, NTH_>;
+  constexpr int PRO_FWD = BLK ? up16(PS::BYTES) + NW * CH * 4 + 2 * DK * 16 : 0;
+  // ... and its backward after step (2), from the start of the LDS: dy,
+  // then du, in fp32; x over all dk columns; two row sums; the weights
+  using PB = ProStage<E, DK, NTH_>;
+  constexpr int LDY = DK + 4;
+  constexpr int PRO_BWD = BLK ? CH * LDY * 4 + up16(PB::BYTES) + 2 * NW * CH * 4 + DK * 16 : 0;
+  constexpr int FIN_PRO = FIN_ALL + PRO_FWD > PRO_BWD ? FIN_ALL + PRO_FWD : PRO_BWD;
+  constexpr int SMEM = RING_BYTES > FIN_PRO ? RING_BYTES : FIN_PRO;
+  static_assert(SMEM + 6 * 1024 <= 160 * 1024, "LDS of one workgroup");
+  static_assert(sizeof(E) == 4 || NW == 8 || SMEM + 5 * 1024 + 512 <= 80 * 1024,
                 "two bf16 workgroups must fit the CU's 160 KB of LDS at dk <= 128");
   __shared__ __align__(16) unsigned char smem[SMEM];
   __shared__ float sg[CH], sb[CH], seg[CH], sdec[CH];
@@ -269,14 +284,15 @@ void k_grad(Args a) {
   constexpr int EPV = 16 / sizeof(E), VPRW = DKW / EPV, KQV = CH * VPRW / (64 * NW);
   static_assert(KQV * 64 * NW == CH * VPRW, "k / q rows do not divide over the threads");
   uint4 kr[KQV], qr[KQV];
+  if constexpr (!BLK) {
 #pragma unroll
-  for (int x = 0; x < KQV; ++x) {
-    const int v = tid + 64 * NW * x, t = v / VPRW, cv = v - t * VPRW;
-    const size_t off = (row0 + (size_t)t * H) * DK + dt0 * 16 + cv * EPV;
-    kr[x] = t < len ? *reinterpret_cast<const uint4*>((const E*)a.k + off) : uint4{0u, 0u, 0u, 0u};
-    qr[x] = t < len ? *reinterpret_cast<const uint4*>((const E*)a.q + off) : uint4{0u, 0u, 0u, 0u};
+    for (int x = 0; x < KQV; ++x) {
+      const int v = tid + 64 * NW * x, t = v / VPRW, cv = v - t * VPRW;
+      const size_t off = (row0 + (size_t)t * H) * DK + dt0 * 16 + cv * EPV;
+      kr[x] = t < len ? *reinterpret_cast<const uint4*>((const E*)a.k + off) : uint4{0u, 0u, 0u, 0u};
+      qr[x] = t < len ? *reinterpret_cast<const uint4*>((const E*)a.q + off) : uint4{0u, 0u, 0u, 0u};
+    }
   }
-
   // ---- finish phase (the staging ring is dead; its LDS is reused)
   // (1) the [dO; dX] V'^T tiles: M1, D, and the parts of E and dbeta.  All
   // of a wave's tiles lie in one of dP (m = 0) and dA (m = 1), so m selects
@@ -359,12 +375,72 @@ void k_grad(Args a) {
       if (l < 16) sxv[w * 16 + l] = x;
     }
   }
+  if constexpr (!BLK) {
 #pragma unroll
-  for (int x = 0; x < KQV; ++x) {
-    const int v = tid + 64 * NW * x, t = v / VPRW, cv = v - t * VPRW;
-    *reinterpret_cast<uint4*>(sKr + t * LDK + cv * EPV) = kr[x];
-    *reinterpret_cast<uint4*>(sQr + t * LDK + cv * EPV) = qr[x];
+    for (int x = 0; x < KQV; ++x) {
+      const int v = tid + 64 * NW * x, t = v / VPRW, cv = v - t * VPRW;
+      *reinterpret_cast<uint4*>(sKr + t * LDK + cv * EPV) = kr[x];
+      *reinterpret_cast<uint4*>(sQr + t * LDK + cv * EPV) = qr[x];
+    }
   }
+  // block prologue: a.q and a.k are the projections; the rule's q and k rows
+  // are formed from them as in the prep and go straight to their staging
+  // (after step (1), when its products are in LDS and fewer registers live)
+  if constexpr (BLK) {
+    static_assert(sizeof(E) == 2 && HV == 1, "the fused block prologue: bf16, whole rows");
+    const int nprev = start > pro_seq_start(a, ci) ? 3 : 0;  // chunks start 64-aligned
+    constexpr int NG = 64 / EPV / NW, KS = DK / 64;  // groups of a lane per slice; slices
+    E* sXs = (E*)(smem + FIN_ALL);
+    float* sNrm = (float*)(smem + FIN_ALL + up16(PS::BYTES));  // [NW][CH]
+    float4* sWl = (float4*)(sNrm + NW * CH);                   // [2 DK]: q, then k
+    pro_weights(sWl, a.cwq + (size_t)h * DK * a.cw, a.cw, DK, tid, NTH_);
+    pro_weights(sWl + DK, a.cwk + (size_t)h * DK * a.cw, a.cw, DK, tid, NTH_);
+    PS st;
+    const int t = l;
+#pragma unroll
+    for (int mat = 0; mat < 2; ++mat) {  // q into sQr, then k into sKr
+      const E* X = (const E*)(mat ? a.k : a.q);
+      E* dst = mat ? sKr : sQr;
+      float z[KS][NG][EPV], ss = 0.f;
+      st.fetch(X, DK, H, h, start, len, nprev, 0, tid);
+#pragma unroll
+      for (int sl = 0; sl < KS; ++sl) {
+        lds_barrier();  // the previous slice's taps (and the row sums) are read
+        st.store(sXs, tid);
+        if (sl + 1 < KS) st.fetch(X, DK, H, h, start, len, nprev, 64 * (sl + 1), tid);
+        lds_barrier();
+#pragma unroll
+        for (int i = 0; i < NG; ++i) {
+          const int cg = (w + NW * i) * EPV;
+          PS::u_of(sXs, sWl + mat * DK + 64 * sl + cg, t, cg, z[sl][i]);
+#pragma unroll
+          for (int q = 0; q < EPV; ++q) {
+            z[sl][i][q] *= sigmoidf(z[sl][i][q]);
+            ss += z[sl][i][q] * z[sl][i][q];
+          }
+        }
+      }
+      sNrm[w * CH + t] = ss;
+      lds_barrier();
+      float tot = 0.f;
+#pragma unroll
+      for (int x = 0; x < NW; ++x) tot += sNrm[x * CH + t];
+      const float sc = rsqrtf(tot + a.ceps);
+#pragma unroll
+      for (int sl = 0; sl < KS; ++sl)
+#pragma unroll
+        for (int i = 0; i < NG; ++i) {
+          union {
+            uint4 u;
+            E e[EPV];
+          } y;
+#pragma unroll
+          for (int q = 0; q < EPV; ++q) y.e[q] = to_e<E>(t < len ? z[sl][i][q] * sc : 0.f);
+          *reinterpret_cast<uint4*>(dst + t * LDK + 64 * sl + (w + NW * i) * EPV) = y.u;
+        }
+    }
+  }
+
   lds_barrier();
 
   // K and Q as B operands (column d, k = t in permuted order) of the wave's
@@ -389,6 +465,149 @@ void k_grad(Args a) {
       fqp[n][kt] = uq.f;
     }
   lds_barrier();
+
+  // Backward of the block prologue (BLK), for q (dy = the rule's dq) and
+  // then k (dy = dk), from dy in accumulator layout.  Per row t:
+  //   dz = (dy - y (y . dy)) / sqrt(|z|^2 + eps),  du = dz s (1 + u (1 - s)),
+  //   s = sigmoid(u), du = 0 past the chunk's end; then per channel
+  //   dx_t = sum_j wl_j du_{t+j},   dw_j = sum_t du_t x_{t-j}.
+  // dx of the last three rows also takes du of the next chunk's first rows:
+  // a chunk followed by another of its sequence writes those rows as fp32
+  // partial sums (btail), every chunk after the first of its sequence writes
+  // its first three rows of du (bhead), and k_block_fixup adds them.  dw goes
+  // out per chunk (bpart), in the weights' tap order.
+  auto block_bwd = [&](auto mc, const f32x4 (&G)[4][NDT]) {
+    if constexpr (BLK) {
+      constexpr int MAT = decltype(mc)::value;
+      constexpr int NGR = DK / EPV / NW;  // groups of EPV columns of a lane
+      float* sDy = (float*)smem;                                    // [CH][LDY]
+      E* sXf = (E*)(smem + CH * LDY * 4);                           // x over all dk columns
+      float* sR = (float*)(smem + CH * LDY * 4 + up16(PB::BYTES));  // [2][NW][CH] row sums
+      float4* sWb = (float4*)(sR + 2 * NW * CH);                    // [DK] weights by lag
+      const int t = l;
+      const int s0 = pro_seq_start(a, ci);
+      const bool succ = start + CH < pro_seq_end(a, ci);  // a next chunk in the sequence
+      const size_t NCH = (size_t)a.NC * H;
+      PB xs;
+      xs.fetch((const E*)(MAT ? a.k : a.q), DK, H, h, start, len, start > s0 ? 3 : 0, 0, tid);
+      if (MAT) lds_barrier();  // q's du, x and weights are read
+      pro_weights(sWb, (MAT ? a.cwk : a.cwq) + (size_t)h * DK * a.cw, a.cw, DK, tid, NTH_);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int n = 0; n < NDT; ++n)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            sDy[(i * 16 + acc_row(e)) * LDY + (w * NDT + n) * 16 + acc_col()] = G[i][n][e];
+      xs.store(sXf, tid);
+      lds_barrier();
+      auto ld8 = [&](const float* src, float (&d)[EPV]) {
+        const float4 d0 = *reinterpret_cast<const float4*>(src);
+        const float4 d1 = *reinterpret_cast<const float4*>(src + 4);
+        d[0] = d0.x; d[1] = d0.y; d[2] = d0.z; d[3] = d0.w;
+        d[4] = d1.x; d[5] = d1.y; d[6] = d1.z; d[7] = d1.w;
+      };
+      static_assert(EPV == 8, "bf16 groups of eight channels");
+      float u[NGR][EPV], ss = 0.f, zd = 0.f;
+#pragma unroll
+      for (int gi = 0; gi < NGR; ++gi) {
+        const int cg = (w + NW * gi) * EPV;
+        PB::u_of(sXf, sWb + cg, t, cg, u[gi]);
+        float dy[EPV];
+        ld8(sDy + t * LDY + cg, dy);
+#pragma unroll
+        for (int q = 0; q < EPV; ++q) {
+          const float z = u[gi][q] * sigmoidf(u[gi][q]);
+          ss += z * z;
+          zd += z * dy[q];
+        }
+      }
+      sR[w * CH + t] = ss;
+      sR[(NW + w) * CH + t] = zd;
+      lds_barrier();
+      float SS = 0.f, ZD = 0.f;
+#pragma unroll
+      for (int x = 0; x < NW; ++x) {
+        SS += sR[x * CH + t];
+        ZD += sR[(NW + x) * CH + t];
+      }
+      const float sc = rsqrtf(SS + a.ceps), yg = ZD * sc;  // 1 / |z|',  y . dy
+#pragma unroll
+      for (int gi = 0; gi < NGR; ++gi) {
+        const int cg = (w + NW * gi) * EPV;
+        float dy[EPV];
+        ld8(sDy + t * LDY + cg, dy);
+#pragma unroll
+        for (int q = 0; q < EPV; ++q) {
+          const float sg = sigmoidf(u[gi][q]), z = u[gi][q] * sg;
+          const float dz = (dy[q] - z * sc * yg) * sc;
+          dy[q] = t < len ? dz * sg * (1.f + u[gi][q] * (1.f - sg)) : 0.f;
+        }
+        *reinterpret_cast<float4*>(sDy + t * LDY + cg) = make_float4(dy[0], dy[1], dy[2], dy[3]);
+        *reinterpret_cast<float4*>(sDy + t * LDY + cg + 4) = make_float4(dy[4], dy[5], dy[6], dy[7]);
+      }
+      lds_barrier();
+      // dx of row t
+      E* DX = (E*)(MAT ? a.dk : a.dq);
+      float* tail = a.btail + ((size_t)MAT * NCH + ch) * 3 * DK;
+#pragma unroll
+      for (int gi = 0; gi < NGR; ++gi) {
+        const int cg = (w + NW * gi) * EPV;
+        float dx[EPV];
+#pragma unroll
+        for (int q = 0; q < EPV; ++q) dx[q] = 0.f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (t + j < CH) {
+            float du[EPV];
+            ld8(sDy + (t + j) * LDY + cg, du);
+#pragma unroll
+            for (int q = 0; q < EPV; ++q)
+              dx[q] += reinterpret_cast<const float*>(sWb + cg + q)[j] * du[q];
+          }
+        if (succ && t >= CH - 3) {
+          float* dst = tail + (t - (CH - 3)) * DK + cg;
+          *reinterpret_cast<float4*>(dst) = make_float4(dx[0], dx[1], dx[2], dx[3]);
+          *reinterpret_cast<float4*>(dst + 4) = make_float4(dx[4], dx[5], dx[6], dx[7]);
+        } else if (t < len) {
+          union {
+            uint4 u;
+            E e[EPV];
+          } y;
+#pragma unroll
+          for (int q = 0; q < EPV; ++q) y.e[q] = to_e<E>(dx[q]);
+          *reinterpret_cast<uint4*>(DX + (row0 + (size_t)t * H) * DK + cg) = y.u;
+        }
+      }
+      // du of the first three rows, for the previous chunk's dx
+      if (start > s0) {
+        float* head = a.bhead + ((size_t)MAT * NCH + ch) * 3 * DK;
+        for (int idx = tid; idx < 3 * DK; idx += NTH_) {
+          const int r = idx / DK, cc = idx - r * DK;
+          head[idx] = sDy[r * LDY + cc];
+        }
+      }
+      // dw partials: thread (column cc, lags jg, jg + TPC, ...)
+      constexpr int TPC = NTH_ / DK, LPT = 4 / TPC;
+      static_assert(TPC * LPT == 4, "threads per column must divide the four lags");
+      const int cc = tid % DK, jg = tid / DK;
+      float acc[LPT];
+#pragma unroll
+      for (int m = 0; m < LPT; ++m) acc[m] = 0.f;
+      for (int tt = 0; tt < len; ++tt) {
+        const float d = sDy[tt * LDY + cc];
+#pragma unroll
+        for (int m = 0; m < LPT; ++m)
+          acc[m] += d * to_f(sXf[(tt + 3 - (jg + TPC * m)) * PB::LD + cc]);
+      }
+      float* part = a.bpart + (((size_t)MAT * NCH + ch) * DK + cc) * a.cw;
+#pragma unroll
+      for (int m = 0; m < LPT; ++m) {
+        const int j = jg + TPC * m;
+        if (j < a.cw) part[a.cw - 1 - j] = acc[m];
+      }
+    }
+  };
 
   // (2) dQ and dK for this wave's dk columns
   {
@@ -459,11 +678,12 @@ void k_grad(Args a) {
       }
     }
     // the wave's dq, then dk, columns through its staging rows (a wave's LDS
-    // operations complete in order), 16 bytes per lane and store
+    // operations complete in order), 16 bytes per lane and store (with the
+    // block prologue, its backward (4) takes them instead)
     constexpr int VPR = NDT * 16 / EPV, PCS = CH * VPR / 64;
     const int col0 = (dt0 + w * NDT) * 16;
 #pragma unroll
-    for (int mat = 0; mat < 2; ++mat) {
+    for (int mat = 0; mat < 2 && !BLK; ++mat) {
 #pragma unroll
       for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -509,6 +729,13 @@ void k_grad(Args a) {
       gp[9 * CH + r] = sdbA[r];
       gp[10 * CH + r] = sxv[r];
     }
+  }
+  // (4) block prologue: the backward of q's and k's, on dq and dk in
+  // registers; its LDS covers the finish buffers and sEcp
+  if constexpr (BLK) {
+    lds_barrier();
+    block_bwd(std::integral_constant<int, 0>{}, Gq);
+    block_bwd(std::integral_constant<int, 1>{}, Gs);
   }
 }
 
@@ -558,9 +785,67 @@ __global__ __launch_bounds__(256) void k_grad_gates(Args a) {
   }
 }
 
-hipError_t launch_grad(Dt dt, int dk, int dv, const Args& a, hipStream_t s) {
+// Finishes dx of the last three rows of every chunk that another chunk of
+// its sequence follows: their partial sums (btail) plus sum_j wl_j du of
+// the next chunk's first rows (bhead).  Grid (NC, H, 2: q, k), DK threads.
+template <class E, int DK>
+__global__ __launch_bounds__(256) void k_block_fixup(Args a) {
+  const int c = blockIdx.x, h = blockIdx.y, mat = blockIdx.z, cc = threadIdx.x;
+  const int4 ci = chunk_info(a, c);
+  if (ci.y == pro_seq_start(a, ci)) return;  // the first chunk of its sequence
+  const int H = a.H;
+  const size_t NCH = (size_t)a.NC * H;
+  const float* head = a.bhead + ((size_t)mat * NCH + (size_t)c * H + h) * 3 * DK;
+  const float* tail = a.btail + ((size_t)mat * NCH + (size_t)(c - 1) * H + h) * 3 * DK;
+  const float* wrow = (mat ? a.cwk : a.cwq) + ((size_t)h * DK + cc) * a.cw;
+  float wl[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) wl[j] = j < a.cw ? wrow[a.cw - 1 - j] : 0.f;
+  E* DX = (E*)(mat ? a.dk : a.dq);
+  const int r0 = ci.y - 3;  // token of the previous chunk's row CH - 3
+#pragma unroll
+  for (int r = 0; r < 3; ++r) {  // lags j >= 3 - r reach the next chunk's row r + j - 3
+    float x = tail[r * DK + cc];
+#pragma unroll
+    for (int j = 3 - r; j < 4; ++j) x += wl[j] * head[(r + j - 3) * DK + cc];
+    DX[((size_t)(r0 + r) * H + h) * DK + cc] = to_e<E>(x);
+  }
+}
+
+// The fix-up and the deterministic sums of the per-chunk weight gradients.
+hipError_t launch_block_fixup(int dk, const Args& a, hipStream_t s) {
+  auto run = [&]<int DK>() {
+    hipLaunchKernelGGL((k_block_fixup<bf16, DK>), dim3(a.NC, a.H, 2), dim3(DK), 0, s, a);
+    hipError_t e = hipGetLastError();
+    const int M = a.H * DK * a.cw;
+    const size_t per = (size_t)a.NC * M;
+    if (e == hipSuccess) e = launch_sum_rows(a.bpart, a.NC, M, a.btmp, a.dwq, s);
+    if (e == hipSuccess) e = launch_sum_rows(a.bpart + per, a.NC, M, a.btmp, a.dwk, s);
+    return e;
+  };
+  if (dk == 64) return run.template operator()<64>();
+  if (dk == 128) return run.template operator()<128>();
+  if (dk == 256) return run.template operator()<256>();
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_grad(Dt dt, int dk, int dv, const Args& a, hipStream_t s, bool block) {
   if (!a.q || !a.k) return hipErrorInvalidValue;  // the kernel reads the chunk's q and k rows
+  if (block && (dt != Dt::BF16 || !a.cwq || !a.cwk || a.cw < 1 || a.cw > 4 || !a.bhead ||
+                !a.btail || !a.bpart))
+    return hipErrorInvalidValue;
   auto f = [&]<class E, int DK, int DV>() {
+    if constexpr (sizeof(E) == 2) {
+      if (block) {
+        const long units = (long)a.NC * a.H;
+        hipLaunchKernelGGL((k_grad<E, DK, DV, true>), dim3(units),
+                           dim3(GradCfg<E, DK, true>::NTH), 0, s, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL((k_grad_gates<1>), dim3((units + 3) / 4), dim3(256), 0, s, a);
+        return hipGetLastError();
+      }
+    }
     using C = GradCfg<E, DK>;
     const long units = (long)a.NC * a.H;
     const long wgs = C::HV == 1 ? units : (units + 7) / 8 * 16;

@@ -49,6 +49,18 @@ struct Args {
   void* dXb;  // [ch] dX = T^T dV'                64 x dv
   // workspace: the gradient kernel's partial row sums for the gate gradients
   float* gpart;  // [ch][GRAD_PART_FLOATS]
+  // fused block prologue (q, k, v point at the projections xq, xk, xv):
+  // causal depthwise convolution of width cw, SiLU, and L2 (eps ceps) for q, k
+  const float *cwq, *cwk, *cwv;  // weights [H * d][cw]
+  int cw;
+  float ceps;
+  void *yq, *yk, *yv;            // the prologue's outputs: the rule's q, k, v
+  // its backward in the gradient kernel (dq, dk are then dxq, dxk), for q
+  // and then k: [2][NC * H][3][dk] du of each chunk's first three rows and
+  // partial dx of its last three, [2][NC * H][dk][cw] per-chunk partial weight
+  // gradients, their slice sums, and the weight gradients [H * dk][cw]
+  float *bhead, *btail, *bpart, *btmp;
+  float *dwq, *dwk;
 };
 
 // Floats per chunk-head of Args::gpart (twelve blocks of one chunk, 64).
@@ -104,10 +116,13 @@ struct Timing {
 
 // Individual launches (each returns the launch status).
 hipError_t launch_chunk_table(const Args& a, hipStream_t s);
-hipError_t launch_prep(Dt dt, int dk, int dv, int mode, const Args& a, hipStream_t s);
+hipError_t launch_prep(Dt dt, int dk, int dv, int mode, const Args& a, hipStream_t s,
+                       bool block = false);
 hipError_t launch_fwd_seq(Dt dt, int dk, int dv, int mode, const Args& a, hipStream_t s);
 hipError_t launch_bwd_seq(Dt dt, int dk, int dv, const Args& a, hipStream_t s);
-hipError_t launch_grad(Dt dt, int dk, int dv, const Args& a, hipStream_t s);
+hipError_t launch_grad(Dt dt, int dk, int dv, const Args& a, hipStream_t s, bool block = false);
+hipError_t launch_block_fixup(int dk, const Args& a, hipStream_t s);
+hipError_t launch_sum_rows(const float* part, int N, int M, float* tmp, float* out, hipStream_t s);
 hipError_t launch_recurrent(Dt dt, int dk, int dv, const Args& a, hipStream_t s);
 hipError_t launch_conv_fwd(Dt dt, int d, const ConvArgs& a, hipStream_t s);
 hipError_t launch_conv_bwd(Dt dt, int d, const ConvArgs& a, hipStream_t s);
@@ -115,10 +130,17 @@ hipError_t launch_norm_gate_fwd(Dt dt, int dv, const NormArgs& a, hipStream_t s)
 hipError_t launch_norm_gate_bwd(Dt dt, int dv, const NormArgs& a, hipStream_t s);
 
 // The forward / backward sequences, with optional timing.
-hipError_t launch_fwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t);
+hipError_t launch_fwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t,
+                      bool block = false);
 hipError_t launch_bwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t);
-hipError_t launch_fwd_save(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t);
+hipError_t launch_fwd_save(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t,
+                           bool block = false);
 hipError_t launch_bwd_saved(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t);
+// Backward of prologue + rule from a saving fused forward: the rule's
+// backward with the q and k prologue folded into the gradient kernel, then
+// the v prologue's backward (cv, on the rule's dv).
+hipError_t launch_block_bwd_saved(int dk, int dv, const Args& a, const ConvArgs& cv,
+                                  hipStream_t s, Timing* t);
 hipError_t launch_recurrent_fwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t);
 
 // Call a lambda templated on (element type, dk, dv) for the supported

@@ -26,6 +26,7 @@
 //                  Forward with save: both sets.
 #include "gdn_device.h"
 #include "gdn_kernels.h"
+#include "gdn_prologue.h"
 
 namespace gdn {
 
@@ -94,7 +95,11 @@ __device__ inline void export_afrag_perm_pair(E* dst_raw, E* dst_scaled, const E
 // Grid (NC, H), 256 threads (4 waves).  LDS stays below 80 KB for bf16 so
 // that two workgroups share a CU: one streams while the other solves.
 
-template <class E, int DK, int DV, int MODE>
+// BLK: the block prologue (Sec. 3.4: short causal convolution, SiLU, and L2
+// normalisation of q and k) runs on the rows as they are loaded: a.q, a.k,
+// a.v point at the projections, and the rule's q, k and v are formed here in
+// registers (and written to a.yq, a.yk, a.yv when those are set).
+template <class E, int DK, int DV, int MODE, bool BLK = false>
 __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
   using M = Mfma<E>;
   // operands of the forward pass (diag(e^g) Q, P), of the reverse pass and
@@ -129,7 +134,7 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
   constexpr int EPV = 16 / sizeof(E), NI = 64 / EPV / 4;
   constexpr int KS = DK / 64, VS = DV / 64;
   uint4 rk[KS][NI], rq[KS][NI], rv[VS][NI];
-  {
+  if constexpr (!BLK) {
     const int t = lane_id();
     const bool tv = t < len;
     const size_t ko = (size_t)(tv ? t : 0) * H * DK, vo = (size_t)(tv ? t : 0) * H * DV;
@@ -149,6 +154,101 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
         rv[sl][i] = tv ? *reinterpret_cast<const uint4*>(V + vo + c) : uint4{0u, 0u, 0u, 0u};
       }
   }
+  if constexpr (BLK) {
+    // ---- block prologue, instead of the row loads: each 64-wide slice of
+    // x (the chunk's rows and the three before them) is staged in LDS; lane
+    // t forms row t from its four taps there and keeps the fp32 z of the
+    // tensor in progress until its row norm is known, then packs y into the
+    // registers the prep works on (rq, rk, rv)
+    using S = ProStage<E, 64, 256>;
+    static_assert(sizeof(E) == 2, "the fused block prologue is built for bf16");
+    static_assert((S::BYTES + 15) / 16 * 16 + 4 * CH * sizeof(float) <= CH * LDA * sizeof(float),
+                  "staging and row sums must fit in A");
+    E* sXs = reinterpret_cast<E*>(sA);                    // staged slice (A is not formed yet)
+    float* sNrm = sA + (S::BYTES + 15) / 16 * 4;          // [4 waves][CH] row sums
+    // weights by lag of the q | k | v channels, in the fp32 T buffer, which
+    // the inverse does not use yet
+    constexpr int RW = 2 * DK + DV;
+    float4* sWl = reinterpret_cast<float4*>(sTf);
+    static_assert(RW * sizeof(float4) <= CH * LDA * sizeof(float), "weights must fit in T");
+    pro_weights(sWl, a.cwq + (size_t)h * DK * a.cw, a.cw, DK, tid, 256);
+    pro_weights(sWl + DK, a.cwk + (size_t)h * DK * a.cw, a.cw, DK, tid, 256);
+    pro_weights(sWl + 2 * DK, a.cwv + (size_t)h * DV * a.cw, a.cw, DV, tid, 256);
+    const int nprev = start > pro_seq_start(a, ci) ? 3 : 0;  // chunks start 64-aligned in a sequence
+    const int t = lane_id();
+    S st;
+    auto pack = [&](const float (&y)[EPV]) {
+      union {
+        uint4 u;
+        E e[EPV];
+      } x;
+#pragma unroll
+      for (int q = 0; q < EPV; ++q) x.e[q] = to_e<E>(t < len ? y[q] : 0.f);
+      return x.u;
+    };
+    // one slice's z for this lane's groups of channels (chan0: the slice's
+    // first channel among q | k | v); the slice is staged first
+    auto slice_z = [&](const E* X, int D, int sl, int nsl, int chan0, float (&z)[NI][EPV]) {
+      lds_barrier();  // the previous slice's taps are read
+      st.store(sXs, tid);
+      if (sl + 1 < nsl) st.fetch(X, D, H, h, start, len, nprev, 64 * (sl + 1), tid);
+      lds_barrier();
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const int cg = (w + 4 * i) * EPV;
+        S::u_of(sXs, sWl + chan0 + cg, t, cg, z[i]);
+#pragma unroll
+        for (int q = 0; q < EPV; ++q) z[i][q] *= sigmoidf(z[i][q]);
+      }
+    };
+    // one tensor with a row norm (q or k): out[sl][i] = y
+    auto prologue_l2 = [&](const E* X, int po, uint4 (&out)[KS][NI], void* yout) {
+      float z[KS][NI][EPV], ss = 0.f;  // (slice_z's first barrier also orders sNrm's reuse)
+      st.fetch(X, DK, H, h, start, len, nprev, 0, tid);
+#pragma unroll
+      for (int sl = 0; sl < KS; ++sl) {
+        slice_z(X, DK, sl, KS, po + 64 * sl, z[sl]);
+#pragma unroll
+        for (int i = 0; i < NI; ++i)
+#pragma unroll
+          for (int q = 0; q < EPV; ++q) ss += z[sl][i][q] * z[sl][i][q];
+      }
+      sNrm[w * CH + t] = ss;
+      lds_barrier();
+      const float sc = rsqrtf(sNrm[t] + sNrm[CH + t] + sNrm[2 * CH + t] + sNrm[3 * CH + t] + a.ceps);
+#pragma unroll
+      for (int sl = 0; sl < KS; ++sl)
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+#pragma unroll
+          for (int q = 0; q < EPV; ++q) z[sl][i][q] *= sc;
+          out[sl][i] = pack(z[sl][i]);
+          if (yout && t < len)
+            *reinterpret_cast<uint4*>((E*)yout + (row0 + (size_t)t * H) * DK + 64 * sl +
+                                      (w + 4 * i) * EPV) = out[sl][i];
+        }
+    };
+    prologue_l2((const E*)a.q, 0, rq, a.yq);
+    prologue_l2((const E*)a.k, DK, rk, a.yk);
+    {  // v: no norm
+      const E* X = (const E*)a.v;
+      st.fetch(X, DV, H, h, start, len, nprev, 0, tid);
+#pragma unroll
+      for (int sl = 0; sl < VS; ++sl) {
+        float z[NI][EPV];
+        slice_z(X, DV, sl, VS, 2 * DK + 64 * sl, z);
+#pragma unroll
+        for (int i = 0; i < NI; ++i) {
+          rv[sl][i] = pack(z[i]);
+          if (a.yv && t < len)
+            *reinterpret_cast<uint4*>((E*)a.yv + (row0 + (size_t)t * H) * DV + 64 * sl +
+                                      (w + 4 * i) * EPV) = rv[sl][i];
+        }
+      }
+    }
+    lds_barrier();  // A and T are formed below
+  }
+
   // a slice of raw rows into LDS, row-major (dst[t][c]) or transposed
   // (dst[c][t], element scaled by scale)
   auto put_rows = [&](E* dst, const uint4 (&r)[NI]) {
@@ -390,8 +490,21 @@ hipError_t launch_chunk_table(const Args& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_prep(Dt dt, int dk, int dv, int mode, const Args& a, hipStream_t s) {
+hipError_t launch_prep(Dt dt, int dk, int dv, int mode, const Args& a, hipStream_t s,
+                       bool block) {
   auto f = [&]<class E, int DK, int DV>() {
+    if (block) {  // fused block prologue (bf16): forward and saving forward only
+      if constexpr (sizeof(E) != 2) return hipErrorInvalidValue;
+      else if (mode == PREP_SAVE)
+        hipLaunchKernelGGL((k_prep<E, DK, DV, PREP_SAVE, true>), dim3(a.NC, a.H), dim3(256), 0, s,
+                           a);
+      else if (mode == PREP_FWD)
+        hipLaunchKernelGGL((k_prep<E, DK, DV, PREP_FWD, true>), dim3(a.NC, a.H), dim3(256), 0, s,
+                           a);
+      else
+        return hipErrorInvalidValue;
+      return hipGetLastError();
+    }
     if (mode == PREP_BWD)
       hipLaunchKernelGGL((k_prep<E, DK, DV, PREP_BWD>), dim3(a.NC, a.H), dim3(256), 0, s, a);
     else if (mode == PREP_SAVE)

@@ -26,7 +26,10 @@ EXPORTS = ("gdn_chunk_fwd", "gdn_chunk_bwd", "gdn_chunk_fwd_workspace_size",
            "gdn_chunk_fwd_save_timed", "gdn_chunk_bwd_saved_timed", "gdn_recurrent_fwd",
            "gdn_recurrent_fwd_timed", "gdn_conv_silu_workspace_size", "gdn_conv_silu_fwd",
            "gdn_conv_silu_bwd", "gdn_norm_gate_workspace_size", "gdn_norm_gate_fwd",
-           "gdn_norm_gate_bwd", "gdn_status_string", "gdn_chunk_fwd_noalloc")
+           "gdn_norm_gate_bwd", "gdn_status_string", "gdn_chunk_fwd_noalloc",
+           "gdn_block_fwd", "gdn_block_fwd_save", "gdn_block_bwd_saved",
+           "gdn_block_bwd_saved_workspace_size", "gdn_block_fwd_timed",
+           "gdn_block_fwd_save_timed", "gdn_block_bwd_saved_timed")
 # bytes of the library's static workspace behind gdn_chunk_fwd_noalloc
 NOALLOC_SCRATCH_BYTES = 64 << 20
 
@@ -36,6 +39,12 @@ class Problem(ctypes.Structure):
                 ("dk", ctypes.c_int32), ("dv", ctypes.c_int32), ("num_seqs", ctypes.c_int32),
                 ("cu_seqlens", ctypes.c_void_p), ("cu_seqlens_host", ctypes.c_void_p),
                 ("dtype", ctypes.c_int)]
+
+
+class BlockPrologue(ctypes.Structure):
+    _fields_ = [("width", ctypes.c_int32), ("eps", ctypes.c_float),
+                ("xq", ctypes.c_void_p), ("xk", ctypes.c_void_p), ("xv", ctypes.c_void_p),
+                ("wq", ctypes.c_void_p), ("wk", ctypes.c_void_p), ("wv", ctypes.c_void_p)]
 
 
 class Timing(ctypes.Structure):
@@ -142,6 +151,22 @@ def load_library():
         lib.gdn_norm_gate_fwd.restype = ctypes.c_int
         lib.gdn_norm_gate_bwd.argtypes = [pp, F, P, P, P, P, P, P, P, P, S, P]
         lib.gdn_norm_gate_bwd.restype = ctypes.c_int
+        pb = ctypes.POINTER(BlockPrologue)
+        lib.gdn_block_fwd.argtypes = [pp, pb] + [P] * 8 + [P, S, P]
+        lib.gdn_block_fwd.restype = ctypes.c_int
+        lib.gdn_block_fwd_timed.argtypes = [pp, pb] + [P] * 8 + [P, S, P, pt]
+        lib.gdn_block_fwd_timed.restype = ctypes.c_int
+        lib.gdn_block_fwd_save.argtypes = [pp, pb] + [P] * 8 + [P, S, P, S, P]
+        lib.gdn_block_fwd_save.restype = ctypes.c_int
+        lib.gdn_block_fwd_save_timed.argtypes = [pp, pb] + [P] * 8 + [P, S, P, S, P, pt]
+        lib.gdn_block_fwd_save_timed.restype = ctypes.c_int
+        lib.gdn_block_bwd_saved_workspace_size.argtypes = [pp, I]
+        lib.gdn_block_bwd_saved_workspace_size.restype = S
+        lib.gdn_block_bwd_saved.argtypes = [pp, pb] + [P] * 5 + [S] + [P] * 9 + [P, S, P]
+        lib.gdn_block_bwd_saved.restype = ctypes.c_int
+        lib.gdn_block_bwd_saved_timed.argtypes = [pp, pb] + [P] * 5 + [S] + [P] * 9 + [P, S, P,
+                                                                                     pt]
+        lib.gdn_block_bwd_saved_timed.restype = ctypes.c_int
         lib.gdn_status_string.argtypes = [ctypes.c_int]
         lib.gdn_status_string.restype = ctypes.c_char_p
         _lib = lib
@@ -593,3 +618,128 @@ def gdn_norm_gate_bwd(o, g, w, dy, eps=1e-5, dout=None, dg=None, dw=None, worksp
                                  workspace.numel(), _stream(o.device)))
     del keep
     return dout, dg, dw
+
+
+# ------------------------------------------------------------ fused block
+
+
+def _prologue(xq, xk, xv, wq, wk, wv, eps):
+    """BlockPrologue for the projections and fp32 weights [H * d, W]."""
+    B, T, H, dk = xq.shape
+    dv = xv.shape[-1]
+    W = wq.shape[1] if wq.dim() == 2 else -1
+    _check_tensors(xq, rows=(("xk", xk), ("xv", xv)))
+    if xk.shape != xq.shape:
+        raise ValueError("xk must match xq")
+    for name, w, d in (("wq", wq, dk), ("wk", wk, dk), ("wv", wv, dv)):
+        if (not isinstance(w, torch.Tensor) or w.device != xq.device or w.dtype != torch.float32
+                or not w.is_contiguous() or tuple(w.shape) != (H * d, W)):
+            raise ValueError("%s must be contiguous float32 [%d, width] on %s"
+                             % (name, H * d, xq.device))
+    return BlockPrologue(W, eps, xq.data_ptr(), xk.data_ptr(), xv.data_ptr(), wq.data_ptr(),
+                         wk.data_ptr(), wv.data_ptr())
+
+
+def gdn_block_fwd(xq, xk, xv, wq, wk, wv, beta, log_alpha, h0=None, eps=1e-6, cu_seqlens=None,
+                  cu_seqlens_host=None, output_final_state=True, want_qkv=False, save=False,
+                  o=None, ht=None, saved=None, workspace=None, timer=None):
+    """Fused block forward: the prologue (short convolution, SiLU, L2 of q
+    and k) inside the chunked rule's kernels.  Returns a dict with o, ht, the
+    rule's v (always when ``save``) and q, k (with ``want_qkv``), and saved
+    (with ``save``: gdn_block_fwd_save, for gdn_block_bwd_saved)."""
+    lib = load_library()
+    p, keep = make_problem(xq, xv, cu_seqlens, cu_seqlens_host)
+    pro = _prologue(xq, xk, xv, wq, wk, wv, eps)
+    B, T, H, dk = xq.shape
+    dv = xv.shape[-1]
+    ns = _nstate(xq, cu_seqlens)
+    if o is None:
+        o = torch.empty((B, T, H, dv), dtype=xq.dtype, device=xq.device)
+    if ht is None and output_final_state:
+        ht = torch.empty((ns, H, dk, dv), dtype=torch.float32, device=xq.device)
+    q = torch.empty_like(xq) if want_qkv else None
+    k = torch.empty_like(xk) if want_qkv else None
+    v = torch.empty_like(xv) if (want_qkv or save) else None
+    _check_tensors(xq, rows=(("o", o),), gates=(("beta", beta), ("log_alpha", log_alpha)),
+                   states=(("h0", h0, dv), ("ht", ht, dv)), nstate=ns)
+    if o.shape != xv.shape:
+        raise ValueError("o must match xv")
+    need = (lib.gdn_chunk_fwd_save_workspace_size if save
+            else lib.gdn_chunk_fwd_workspace_size)(ctypes.byref(p))
+    if need == 0:  # the problem is invalid: let the library name the error
+        _check(lib.gdn_block_fwd(ctypes.byref(p), ctypes.byref(pro), *[None] * 8, None, 0, None))
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=xq.device)
+    head = (ctypes.byref(p), ctypes.byref(pro), _ptr(beta), _ptr(log_alpha), _ptr(h0), _ptr(o),
+            _ptr(ht), _ptr(q), _ptr(k), _ptr(v))
+    tail = (_ptr(workspace), workspace.numel(), _stream(xq.device))
+    if save:
+        nsave = lib.gdn_chunk_saved_size(ctypes.byref(p))
+        if saved is None or saved.numel() < nsave:
+            saved = torch.empty(nsave, dtype=torch.uint8, device=xq.device)
+        args = head + (_ptr(saved), saved.numel()) + tail
+        if timer is None:
+            _check(lib.gdn_block_fwd_save(*args))
+        else:
+            _check(lib.gdn_block_fwd_save_timed(*args, ctypes.byref(timer.timing)))
+    else:
+        args = head + tail
+        if timer is None:
+            _check(lib.gdn_block_fwd(*args))
+        else:
+            _check(lib.gdn_block_fwd_timed(*args, ctypes.byref(timer.timing)))
+    del keep
+    return dict(o=o, ht=ht, q=q, k=k, v=v, saved=saved if save else None)
+
+
+def gdn_block_bwd_saved(xq, xk, xv, wq, wk, wv, v, beta, dO, saved, dht=None, eps=1e-6,
+                        cu_seqlens=None, cu_seqlens_host=None, need_dh0=True,
+                        need_dlog_alpha=True, workspace=None, out=None, timer=None):
+    """Fused block backward from gdn_block_fwd(save=True): dict dxq, dxk,
+    dxv, dwq, dwk, dwv, dbeta, dlog_alpha, dh0.  ``v`` is the rule's v the
+    saving forward returned."""
+    lib = load_library()
+    p, keep = make_problem(xq, xv, cu_seqlens, cu_seqlens_host)
+    pro = _prologue(xq, xk, xv, wq, wk, wv, eps)
+    B, T, H, dk = xq.shape
+    dv = xv.shape[-1]
+    ns = _nstate(xq, cu_seqlens)
+    if out is None:
+        out = dict(dxq=torch.empty_like(xq), dxk=torch.empty_like(xk), dxv=torch.empty_like(xv),
+                   dwq=torch.empty_like(wq), dwk=torch.empty_like(wk), dwv=torch.empty_like(wv),
+                   dbeta=torch.empty_like(beta),
+                   dlog_alpha=torch.empty_like(beta) if need_dlog_alpha else None,
+                   dh0=torch.empty((ns, H, dk, dv), dtype=torch.float32,
+                                   device=xq.device) if need_dh0 else None)
+    _check_tensors(xq, rows=(("v", v), ("dO", dO), ("dxq", out["dxq"]), ("dxk", out["dxk"]),
+                             ("dxv", out["dxv"])),
+                   gates=(("beta", beta), ("dbeta", out["dbeta"]),
+                          ("dlog_alpha", out["dlog_alpha"])),
+                   states=(("dht", dht, dv), ("dh0", out["dh0"], dv)), nstate=ns)
+    if v.shape != xv.shape or dO.shape != xv.shape:
+        raise ValueError("v and dO must match xv")
+    for name in ("dwq", "dwk", "dwv"):
+        w = {"dwq": wq, "dwk": wk, "dwv": wv}[name]
+        t = out[name]
+        if t.dtype != torch.float32 or t.shape != w.shape or not t.is_contiguous() \
+                or t.device != xq.device:
+            raise ValueError("%s must be contiguous float32 shaped as its weight" % name)
+    if saved.device != xq.device or saved.dtype != torch.uint8 or not saved.is_contiguous():
+        raise ValueError("saved must be a contiguous uint8 tensor on xq's device")
+    need = lib.gdn_block_bwd_saved_workspace_size(ctypes.byref(p), pro.width)
+    if need == 0:
+        _check(lib.gdn_block_bwd_saved(ctypes.byref(p), ctypes.byref(pro), *[None] * 5, 0,
+                                       *[None] * 9, None, 0, None))
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=xq.device)
+    args = (ctypes.byref(p), ctypes.byref(pro), _ptr(v), _ptr(beta), _ptr(dO), _ptr(dht),
+            _ptr(saved), saved.numel(), _ptr(out["dxq"]), _ptr(out["dxk"]), _ptr(out["dxv"]),
+            _ptr(out["dwq"]), _ptr(out["dwk"]), _ptr(out["dwv"]), _ptr(out["dbeta"]),
+            _ptr(out["dlog_alpha"]), _ptr(out["dh0"]), _ptr(workspace), workspace.numel(),
+            _stream(xq.device))
+    if timer is None:
+        _check(lib.gdn_block_bwd_saved(*args))
+    else:
+        _check(lib.gdn_block_bwd_saved_timed(*args, ctypes.byref(timer.timing)))
+    del keep
+    return out

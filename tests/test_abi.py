@@ -287,3 +287,58 @@ def test_noalloc_forward_checks_before_any_hip_call(lib):
     rc = lib.gdn_chunk_fwd_noalloc(ctypes.byref(bad), fake, fake, fake, fake, fake, None, fake,
                                    None, None)
     assert rc == 3  # GDN_ERR_UNSUPPORTED
+
+
+def test_fused_block_checks_before_any_launch(lib):
+    """The fused block's entry points check the prologue description, the
+    pointers and the workspace on the host, and return a status before any
+    launch (this runs on a host without a GPU)."""
+    fake = ctypes.c_void_p(0x10000)
+    odd = 0x10008
+    p, _ = problem(dk=256, dv=512)
+    ws = gdn.gdn_chunk_fwd_workspace_size(p)
+
+    def pro(width=4, eps=1e-6, **kw):
+        ptrs = dict(xq=0x10000, xk=0x10000, xv=0x10000, wq=0x10000, wk=0x10000, wv=0x10000)
+        ptrs.update(kw)
+        return gdn.BlockPrologue(width, eps, *[ptrs[n] for n in ("xq", "xk", "xv", "wq", "wk",
+                                                                 "wv")])
+
+    def fwd(pr, prob=p, o=fake, n=ws):
+        return lib.gdn_block_fwd(ctypes.byref(prob), None if pr is None else ctypes.byref(pr),
+                                 fake, fake, None, o, None, None, None, None, fake, n, None)
+
+    assert fwd(None) == 1                      # GDN_ERR_NULL
+    assert fwd(pro(width=0)) == 9              # GDN_ERR_VALUE
+    assert fwd(pro(width=5)) == 9
+    assert fwd(pro(eps=-1.0)) == 9
+    assert fwd(pro(eps=float("inf"))) == 9
+    assert fwd(pro(xk=None)) == 1
+    assert fwd(pro(wv=None)) == 1
+    assert fwd(pro(xv=odd)) == 7               # GDN_ERR_ALIGN
+    assert fwd(pro(), o=None) == 1
+    assert fwd(pro(), n=ws - 1) == 5           # GDN_ERR_WORKSPACE
+    f32, _ = problem(dk=64, dv=64, dtype=gdn.GDN_F32)
+    assert fwd(pro(), prob=f32, n=1 << 30) == 3  # GDN_ERR_UNSUPPORTED: bf16 only
+    # the saving forward needs the rule's v and a large enough saved buffer
+    nsave = gdn.gdn_chunk_saved_size(p)
+    wss = gdn.gdn_chunk_fwd_save_workspace_size(p)
+    fs = lambda v, n: lib.gdn_block_fwd_save(ctypes.byref(p), ctypes.byref(pro()), fake, fake,
+                                             None, fake, None, None, None, v, fake, n, fake, wss,
+                                             None)
+    assert fs(None, nsave) == 1
+    assert fs(fake, nsave - 1) == 8            # GDN_ERR_SAVED
+    # backward: workspace of the rule's backward plus the prologue's buffers
+    wb = lib.gdn_block_bwd_saved_workspace_size(ctypes.byref(p), 4)
+    assert wb > gdn.gdn_chunk_bwd_saved_workspace_size(p)
+    assert lib.gdn_block_bwd_saved_workspace_size(ctypes.byref(p), 5) == 0
+    assert lib.gdn_block_bwd_saved_workspace_size(ctypes.byref(p), 1) < wb
+
+    def bwd(pr, n=wb, dxv=fake):
+        return lib.gdn_block_bwd_saved(ctypes.byref(p), ctypes.byref(pr), fake, fake, fake, None,
+                                       fake, nsave, fake, fake, dxv, fake, fake, fake, fake,
+                                       None, None, fake, n, None)
+
+    assert bwd(pro(), dxv=None) == 1
+    assert bwd(pro(width=7)) == 9
+    assert bwd(pro(), n=wb - 1) == 5
