@@ -45,8 +45,13 @@ METRIC = "tokens/sec gated-delta chunk fwd+bwd (1 GPU); % bf16 MFMA peak"
 METRIC_FWD = "tokens/sec gated-delta chunk fwd (1 GPU); % bf16 MFMA peak"
 METRIC_RECURRENT = "tokens/sec gated-delta recurrent step (1 GPU); % HBM peak"
 METRIC_BLOCK = "tokens/sec gated-delta block prologue+epilogue fwd+bwd (1 GPU); % HBM peak"
+METRIC_FUSED = "tokens/sec gated-delta block (prologue + chunk rule) fwd+bwd (1 GPU); % bf16 MFMA peak"
 # block prologue / epilogue workloads: (B, T, H, dk, dv, conv width)
 BLOCK_WORKLOADS = {"block_bf16_b8_t4096_h6_dk256_dv512": (8, 4096, 6, 256, 512, 4)}
+# the fused block (prologue inside the rule's kernels), fwd+bwd: the rule's
+# training workload of the same name without the prefix, plus its prologue
+FUSED_WORKLOADS = {"fusedblock_fwdbwd_bf16_b8_t4096_h6_dk256_dv512":
+                   ("fwdbwd_bf16_b8_t4096_h6_dk256_dv512", 4)}
 PEAK_HBM = 8.0e12          # bytes/s, MI355X HBM3E
 PEAK_MFMA_BF16 = 2.5e15    # dense bf16 MFMA FLOP/s
 PEAK_MFMA_F32 = 157.3e12   # fp32 matrix FLOP/s
@@ -137,31 +142,22 @@ def model_for(models, name):
 
 # ------------------------------------------------------------------ counters on record
 
-def kernel_source_digest():
-    """sha256 over the HIP sources, to tell whether recorded counters are stale."""
-    h = hashlib.sha256()
-    csrc = os.path.join(ROOT, "paper_2412_06464_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
-        if name.endswith((".hip", ".h")):
-            h.update(name.encode())
-            h.update(open(os.path.join(csrc, name), "rb").read())
-    return h.hexdigest()
-
-
 def traffic_record(workload):
-    """{launch name: HBM bytes per launch} measured by rocprofv3 PMC
-    (FETCH_SIZE + WRITE_SIZE, scaled by a copy-kernel calibration) for the
-    current kernel sources, or {} if none is on record."""
-    path = os.path.join(ROOT, "profiles", "traffic.json")
-    if not os.path.exists(path):
-        return {}
+    """({kernel key: HBM bytes per launch}, HBM bytes per step) measured by
+    rocprofv3 PMC (FETCH_SIZE + WRITE_SIZE, scaled by a copy-kernel
+    calibration; paper_2412_06464_amd.profiling) on the current kernel
+    sources, or ({}, None) if none is on record."""
+    from paper_2412_06464_amd.profiling import TRAFFIC, kernel_source_digest
+    if not os.path.exists(TRAFFIC):
+        return {}, None
     try:
-        rec = json.load(open(path))
+        rec = json.load(open(TRAFFIC)).get(workload)
     except ValueError:
-        return {}
-    digest = kernel_source_digest()
-    return {k: e["bytes_per_launch"] for k, e in rec.get(workload, {}).items()
-            if e.get("kernel_source_sha256") == digest}
+        return {}, None
+    if not rec or rec.get("kernel_source_sha256") != kernel_source_digest():
+        return {}, None
+    return ({k: e["bytes_per_launch"] for k, e in rec.get("kernels", {}).items()},
+            rec.get("step_bytes"))
 
 
 # ------------------------------------------------------------------ timing
@@ -432,7 +428,8 @@ def bench_block(args):
     nbytes = {name: n * 2 * th for name, _, n in calls}  # bf16 elements per token-head
     dom = max(call_ms, key=lambda k: call_ms[k])
     ach = nbytes[dom] / (call_ms[dom] / 1e3)
-    traffic = traffic_record(args.workload).get(dom)
+    from paper_2412_06464_amd.profiling import block_kernel_key
+    traffic = traffic_record(args.workload)[0].get(block_kernel_key(dom, dk, dv))
     roof = {"bound": "hbm", "achieved": ach / 1e9, "peak": PEAK_HBM / 1e9, "unit": "GB/s",
             "frac": ach / PEAK_HBM, "traffic": traffic,
             "traffic_ratio": traffic / nbytes[dom] if traffic else None,
@@ -472,6 +469,196 @@ def bench_block(args):
     print(json.dumps(res), flush=True)
 
 
+def fused_models(w, tokens_heads, n_units, has_h0):
+    """kernel_models for the fused block's launches: the prologue's
+    projections replace the rule's q, k, v as the prep's and the gradient
+    kernel's inputs (same sizes), the gradient kernel writes dx instead of
+    the rule's dq, dk, and the v prologue's backward reads xv and writes dxv
+    (the rule's dv it reads is an intermediate).  The fix-up, which finishes
+    three rows per chunk from partial sums, is credited with nothing."""
+    m = kernel_models(w, tokens_heads, n_units, has_h0)
+    m["k_prep_save_block"] = m["k_prep_save"]
+    m["k_prep_block"] = m["k_prep"]
+    m["k_grad_block"] = m["k_grad"]
+    m["k_block_fixup"] = (0, 0)
+    m["k_conv_bwd"] = (2 * w.dv * 2 * tokens_heads, 0)
+    return m
+
+
+def fused_step_bytes(w, tokens_heads, n_states, has_h0):
+    """(algorithmic bytes of the block step, bytes the fusion keeps off HBM).
+    The block's own tensors: the projections xq, xk, xv read by the forward
+    and again by the backward, beta, log_alpha, o, dO, the states, and the
+    gradients dxq, dxk, dxv, dbeta, dlog_alpha (= the rule's path bytes, with
+    the projections for q, k, v; the weights are a few kB).  Kept off HBM
+    against the unfused composition, per token-head (e = 2): the rule's q and
+    k written by the prologue and read by the prep (4 dk e) and v read by it
+    (dv e; v is still written once, for the backward); in the backward the
+    rule's dq and dk written and read back (4 dk e), and q and k read by the
+    gradient kernel beside the projections the prologue's backward reads
+    (2 dk e)."""
+    e = 2
+    return (path_bytes(w, tokens_heads, n_states, has_h0),
+            (10 * w.dk + w.dv) * e * tokens_heads)
+
+
+def bench_fused_block(args):
+    """One step = the block's prologue and the chunked rule, forward and
+    backward: gdn_block_fwd_save + gdn_block_bwd_saved.  The unfused
+    composition on the same inputs (gdn_conv_silu_fwd for q, k, v, the
+    rule's saving forward and saved backward, gdn_conv_silu_bwd for q, k, v)
+    is timed the same way and reported beside it."""
+    import ctypes
+
+    import torch
+
+    from paper_2412_06464_amd import gdn
+    from paper_2412_06464_amd.inputs import WORKLOADS, make_block_inputs, workload_inputs
+
+    rule_name, W = FUSED_WORKLOADS[args.workload]
+    w = WORKLOADS[rule_name]
+    lib = gdn.load_library()
+    rule = workload_inputs(rule_name, seed=0)
+    blk = make_block_inputs(w.B, w.T, w.H, w.dk, w.dv, "bf16", seed=1000, width=W)
+    dev = torch.device("cuda", 0)
+    d = {k: blk[k].to(dev) for k in ("xq", "xk", "xv", "wq", "wk", "wv")}
+    d.update({k: rule[k].to(dev) for k in ("beta", "log_alpha", "dO", "dht")})
+    B, T, H, dk, dv = w.B, w.T, w.H, w.dk, w.dv
+    eps = 1e-6
+    # everything allocated before the timed region
+    xs = (d["xq"], d["xk"], d["xv"], d["wq"], d["wk"], d["wv"])
+    f0 = gdn.gdn_block_fwd(*xs, d["beta"], d["log_alpha"], eps=eps, save=True)
+    g0 = gdn.gdn_block_bwd_saved(*xs, f0["q"], f0["k"], f0["v"], d["beta"], d["dO"],
+                                 f0["saved"], dht=d["dht"], eps=eps)
+    p, _ = gdn.make_problem(d["xq"], d["xv"])
+    ws_f = torch.empty(gdn.gdn_chunk_fwd_save_workspace_size(p), dtype=torch.uint8, device=dev)
+    ws_b = torch.empty(lib.gdn_block_bwd_saved_workspace_size(ctypes.byref(p), W),
+                       dtype=torch.uint8, device=dev)
+    y = {k: torch.empty_like(d["x" + k]) for k in ("q", "k", "v")}
+    pk, _ = gdn.block_problem(d["xq"])
+    ws_c = torch.empty(lib.gdn_conv_silu_workspace_size(ctypes.byref(pk), dv, W),
+                       dtype=torch.uint8, device=dev)
+    saved_u = torch.empty(gdn.gdn_chunk_saved_size(p), dtype=torch.uint8, device=dev)
+    ws_bs = torch.empty(gdn.gdn_chunk_bwd_saved_workspace_size(p), dtype=torch.uint8,
+                        device=dev)
+    o_u = torch.empty_like(d["xv"])
+    ht_u = torch.empty_like(f0["ht"])
+    out_u = dict(dq=torch.empty_like(d["xq"]), dk=torch.empty_like(d["xk"]),
+                 dv=torch.empty_like(d["xv"]), dbeta=torch.empty_like(d["beta"]),
+                 dlog_alpha=torch.empty_like(d["beta"]), dh0=torch.empty_like(f0["ht"]))
+    dx_u = {k: torch.empty_like(d["x" + k]) for k in ("q", "k", "v")}
+    dw_u = {k: torch.empty_like(d["w" + k]) for k in ("q", "k", "v")}
+
+    def step_fused(timers):
+        gdn.gdn_block_fwd(*xs, d["beta"], d["log_alpha"], eps=eps, save=True, o=f0["o"],
+                          ht=f0["ht"], q=f0["q"], k=f0["k"], v=f0["v"],
+                          saved=f0["saved"], workspace=ws_f,
+                          timer=timers[0])
+        gdn.gdn_block_bwd_saved(*xs, f0["q"], f0["k"], f0["v"], d["beta"], d["dO"],
+                                f0["saved"], dht=d["dht"], eps=eps, workspace=ws_b, out=g0,
+                                timer=timers[1])
+
+    def step_unfused(timers):
+        for k in ("q", "k", "v"):
+            gdn.gdn_conv_silu_fwd(d["x" + k], d["w" + k], l2norm=k != "v", eps=eps, y=y[k],
+                                  workspace=ws_c)
+        gdn.gdn_chunk_fwd_save(y["q"], y["k"], y["v"], d["beta"], d["log_alpha"], o=o_u,
+                               ht=ht_u, saved=saved_u, workspace=ws_f, timer=timers[0])
+        gdn.gdn_chunk_bwd_saved(y["q"], y["k"], y["v"], d["beta"], d["dO"], saved_u,
+                                dht=d["dht"], workspace=ws_bs, out=out_u, timer=timers[1])
+        for k in ("q", "k", "v"):
+            gdn.gdn_conv_silu_bwd(d["x" + k], d["w" + k], out_u["d" + k], l2norm=k != "v",
+                                  eps=eps, dx=dx_u[k], dw=dw_u[k], workspace=ws_c)
+
+    stream = torch.cuda.current_stream(dev)
+    timer = StepTimer(torch, stream, dev)
+
+    def measure(step):
+        for _ in range(args.warmup):
+            step([None, None])
+        torch.cuda.synchronize()
+        cold, kern = timer.run(step, args.steps, True, 2, gdn)
+        warm, _ = timer.run(step, args.steps, False, 2, gdn)
+        return percentiles(cold), percentiles(warm), {k: sum(v) / len(v) for k, v in kern.items()}
+
+    tc, tw, kern_ms = measure(step_fused)
+    unfused = agree = None
+    if not args.no_other_path:
+        uc, uw, ukern = measure(step_unfused)
+        unfused = {"ms_per_step": uc["median"], "value": B * T / (uc["median"] / 1e3),
+                   "warm_ms": uw["median"], "rule_kernels_ms": ukern}
+        # the two compositions agree (same inputs; the fused backward's dx
+        # against the unfused one's)
+        step_fused([None, None])
+        step_unfused([None, None])
+        torch.cuda.synchronize()
+
+        def rel(a, b):
+            a, b = a.double(), b.double()
+            return float((a - b).abs().max() / b.abs().max().clamp_min(1e-30))
+
+        agree = {"o": rel(f0["o"], o_u), "dxq": rel(g0["dxq"], dx_u["q"]),
+                 "dxk": rel(g0["dxk"], dx_u["k"]), "dxv": rel(g0["dxv"], dx_u["v"]),
+                 "dwq": rel(g0["dwq"], dw_u["q"]),
+                 "dbeta": rel(g0["dbeta"], out_u["dbeta"])}
+
+    tokens = B * T
+    tokens_heads = tokens * H
+    n_states = B
+    models = fused_models(w, tokens_heads, n_states * H, False)
+    dom = max(kern_ms, key=lambda k: kern_ms[k])
+    kb, kf = model_for(models, dom)
+    t_dom = kern_ms[dom] / 1e3
+    if kb / PEAK_HBM >= kf / PEAK_MFMA_BF16:
+        roof = {"bound": "hbm", "achieved": kb / t_dom / 1e9, "peak": PEAK_HBM / 1e9,
+                "unit": "GB/s"}
+    else:
+        roof = {"bound": "mfma", "achieved": kf / t_dom / 1e12, "peak": PEAK_MFMA_BF16 / 1e12,
+                "unit": "TFLOP/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    from paper_2412_06464_amd.profiling import block_kernel_key, kernel_key
+    counters, step_counter = traffic_record(args.workload)
+    tr = counters.get(kernel_key(dom, "bf16", dk, dv))
+    roof["traffic"] = tr
+    roof["traffic_ratio"] = tr / kb if tr and kb else None
+    roof.update(kernel=dom, kernel_ms=kern_ms[dom], algorithmic_gbytes=kb / 1e9,
+                algorithmic_gflop=kf / 1e9)
+    nbytes, saved_model = fused_step_bytes(w, tokens_heads, n_states, False)
+    flops = path_flops(w, tokens_heads)
+    ms = tc["median"]
+    # the unfused composition's counters: the rule's saving training step and
+    # the standalone prologue kernels (q and k each one dk-wide call), as
+    # measured on their own workloads (the slice sums of dw left out)
+    _, rule_step = traffic_record(rule_name)
+    bc, _ = traffic_record("block_bf16_b8_t4096_h6_dk256_dv512")
+    conv = [(block_kernel_key(c, dk, dv), n) for c, n in (("conv_fwd_q", 2), ("conv_fwd_v", 1),
+                                                          ("conv_bwd_q", 2), ("conv_bwd_v", 1))]
+    unfused_counter = None
+    if rule_step and all(k in bc for k, _ in conv):
+        unfused_counter = rule_step + sum(bc[k] * n for k, n in conv)
+    res = {
+        "metric": METRIC_FUSED, "value": tokens / (ms / 1e3), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "B": B, "T": T, "H": H, "dk": dk, "dv": dv,
+                   "chunk": CH, "conv_width": W, "backward": True, "path": "fused"},
+        "timing": {"cold_ms": tc, "warm_ms": tw, "flush_bytes": FLUSH_BYTES,
+                   "warm_value": tokens / (tw["median"] / 1e3)},
+        "mfma_frac": flops / (ms / 1e3) / PEAK_MFMA_BF16,
+        "hbm_frac": nbytes / (ms / 1e3) / PEAK_HBM,
+        "path_gflop": flops / 1e9, "path_gbytes": nbytes / 1e9,
+        "fusion_saved_gbytes_model": saved_model / 1e9,
+        "step_traffic_gbytes": step_counter / 1e9 if step_counter else None,
+        "unfused_traffic_gbytes": unfused_counter / 1e9 if unfused_counter else None,
+        "fusion_saved_gbytes_counters": ((unfused_counter - step_counter) / 1e9
+                                         if unfused_counter and step_counter else None),
+        "kernels_ms": kern_ms, "roofline": roof,
+        "unfused": unfused, "fused_vs_unfused_rel": agree,
+    }
+    print(json.dumps(res), flush=True)
+
+
 # ------------------------------------------------------------------ main path
 
 def main():
@@ -500,6 +687,9 @@ def main():
 
     if args.workload in BLOCK_WORKLOADS:
         bench_block(args)
+        return
+    if args.workload in FUSED_WORKLOADS:
+        bench_fused_block(args)
         return
     if args.copy_calibration:
         x = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
@@ -622,9 +812,13 @@ def main():
         roof = {"bound": cbound, "achieved": kf / t_dom / 1e12, "peak": peak_c / 1e12,
                 "unit": "TFLOP/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    counters = traffic_record(args.workload)
-    roof["traffic"] = counters.get(dom)
-    roof["traffic_ratio"] = counters[dom] / kb if counters.get(dom) and kb else None
+    from paper_2412_06464_amd.profiling import kernel_key
+    counters, step_counter = traffic_record(args.workload)
+    if path != ("saved" if w.backward else path):
+        step_counter = None  # the counters are taken on the headline path
+    tr = counters.get(kernel_key(dom, w.dtype, w.dk, w.dv))
+    roof["traffic"] = tr
+    roof["traffic_ratio"] = tr / kb if tr and kb else None
     roof.update(kernel=dom, kernel_ms=kern_ms[dom], algorithmic_gbytes=kb / 1e9,
                 algorithmic_gflop=kf / 1e9)
 
@@ -633,9 +827,6 @@ def main():
     else:
         flops = path_flops(w, tokens_heads)
         nbytes = path_bytes(w, tokens_heads, n_states, has_h0)
-    step_counter = None
-    if counters and all(k in counters for k in kern_ms):
-        step_counter = sum(counters[k] for k in kern_ms)
     res = {
         "metric": METRIC if w.backward else (METRIC_RECURRENT if w.recurrent else METRIC_FWD),
         "value": tokens / (ms / 1e3),

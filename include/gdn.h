@@ -238,10 +238,11 @@ gdn_status gdn_norm_gate_bwd(const gdn_problem *p, float eps, const void *o,
  * normalisation, before the gated delta rule).  The result is that of
  * gdn_conv_silu_fwd (l2norm 1 for q and k, 0 for v) followed by the chunked
  * rule on its outputs, up to rounding, without the rule's q, k and v making
- * a round trip through memory: the prep kernel forms them from the
- * projections as it loads its chunk's rows, and in the backward the
- * gradient kernel recomputes q and k from their projections and applies the
- * prologue's backward to its own dq and dk before anything is stored.
+ * a round trip through memory between the prologue and the rule: the prep
+ * kernel forms them from the projections as it loads its chunk's rows, and
+ * in the backward the gradient kernel applies the prologue's backward to its
+ * own dq and dk (recomputing the convolution from the projections) before
+ * anything is stored.
  * bf16 problems only (GDN_ERR_UNSUPPORTED otherwise), any dk, dv the rule
  * supports; dense or packed sequences as for the rule.
  *
@@ -271,8 +272,8 @@ gdn_status gdn_block_fwd(const gdn_problem *p, const gdn_block_prologue *pro,
 
 /* Saving forward of the fused block (training): as gdn_block_fwd, and fills
  * `saved` (gdn_chunk_saved_size bytes) as gdn_chunk_fwd_save does, with
- * gdn_chunk_fwd_save_workspace_size bytes of workspace.  v is required
- * here: the backward reads the rule's v. */
+ * gdn_chunk_fwd_save_workspace_size bytes of workspace.  q, k and v are
+ * required here: the backward reads the rule's q, k, v. */
 gdn_status gdn_block_fwd_save(const gdn_problem *p,
                               const gdn_block_prologue *pro, const float *beta,
                               const float *log_alpha, const float *h0, void *o,
@@ -285,12 +286,13 @@ gdn_status gdn_block_fwd_save(const gdn_problem *p,
  * [B, T, H, dv] (bf16), dwq, dwk, dwv (fp32, shaped as the weights, summed
  * over all tokens in a fixed order: deterministic), and dbeta, dlog_alpha
  * (optional), dh0 (optional) as gdn_chunk_bwd_saved returns them.  Reads
- * the same prologue, the rule's v that gdn_block_fwd_save wrote, beta, dO,
- * dht (or NULL) and `saved` (unchanged).  `workspace` holds
+ * the same prologue, the rule's q, k, v that gdn_block_fwd_save wrote, beta,
+ * dO, dht (or NULL) and `saved` (unchanged).  `workspace` holds
  * gdn_block_bwd_saved_workspace_size(p, width) bytes. */
 size_t gdn_block_bwd_saved_workspace_size(const gdn_problem *p, int width);
 gdn_status gdn_block_bwd_saved(const gdn_problem *p,
-                               const gdn_block_prologue *pro, const void *v,
+                               const gdn_block_prologue *pro, const void *q,
+                               const void *k, const void *v,
                                const float *beta, const void *dO,
                                const float *dht, const void *saved,
                                size_t saved_bytes, void *dxq, void *dxk,
@@ -360,8 +362,8 @@ gdn_status gdn_block_fwd_save_timed(const gdn_problem *p,
                                     size_t workspace_bytes, void *stream,
                                     gdn_timing *timing);
 gdn_status gdn_block_bwd_saved_timed(
-    const gdn_problem *p, const gdn_block_prologue *pro, const void *v,
-    const float *beta, const void *dO, const float *dht, const void *saved,
+    const gdn_problem *p, const gdn_block_prologue *pro, const void *q,
+    const void *k, const void *v, const float *beta, const void *dO, const float *dht, const void *saved,
     size_t saved_bytes, void *dxq, void *dxk, void *dxv, float *dwq, float *dwk,
     float *dwv, float *dbeta, float *dlog_alpha, float *dh0, void *workspace,
     size_t workspace_bytes, void *stream, gdn_timing *timing);

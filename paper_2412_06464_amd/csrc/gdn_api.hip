@@ -243,9 +243,9 @@ gdn_status check_block(const gdn_problem* p, const gdn_block_prologue* b, Shape*
 }
 
 void fill_prologue(const gdn_block_prologue* b, Args* a) {
-  a->q = b->xq;
-  a->k = b->xk;
-  a->v = b->xv;
+  a->xq = b->xq;
+  a->xk = b->xk;
+  a->xv = b->xv;
   a->cwq = b->wq;
   a->cwk = b->wk;
   a->cwv = b->wv;
@@ -641,7 +641,7 @@ gdn_status gdn_block_fwd_save_timed(const gdn_problem* p, const gdn_block_prolog
   Shape s;
   gdn_status st = check_block(p, pro, &s);
   if (st != GDN_OK) return st;
-  if (!beta || !o || !v) return GDN_ERR_NULL;
+  if (!beta || !o || !q || !k || !v) return GDN_ERR_NULL;
   const void* ptrs[] = {beta, log_alpha, h0, o, ht, q, k, v, saved, workspace};
   for (const void* x : ptrs)
     if (x && !aligned16(x)) return GDN_ERR_ALIGN;
@@ -686,7 +686,8 @@ size_t gdn_block_bwd_saved_workspace_size(const gdn_problem* p, int width) {
 }
 
 gdn_status gdn_block_bwd_saved_timed(const gdn_problem* p, const gdn_block_prologue* pro,
-                                     const void* v, const float* beta, const void* dO,
+                                     const void* q, const void* k, const void* v,
+                                     const float* beta, const void* dO,
                                      const float* dht, const void* saved, size_t saved_bytes_,
                                      void* dxq, void* dxk, void* dxv, float* dwq, float* dwk,
                                      float* dwv, float* dbeta, float* dlog_alpha, float* dh0,
@@ -695,10 +696,10 @@ gdn_status gdn_block_bwd_saved_timed(const gdn_problem* p, const gdn_block_prolo
   Shape s;
   gdn_status st = check_block(p, pro, &s);
   if (st != GDN_OK) return st;
-  if (!v || !beta || !dO || !dxq || !dxk || !dxv || !dwq || !dwk || !dwv || !dbeta)
+  if (!q || !k || !v || !beta || !dO || !dxq || !dxk || !dxv || !dwq || !dwk || !dwv || !dbeta)
     return GDN_ERR_NULL;
-  const void* ptrs[] = {v,   beta, dO,   dht,   saved,      dxq, dxk,      dxv,
-                        dwq, dwk,  dwv,  dbeta, dlog_alpha, dh0, workspace};
+  const void* ptrs[] = {q,   k,   v,     beta,  dO,         dht, saved,    dxq,
+                        dxk, dxv, dwq,   dwk,   dwv,        dbeta, dlog_alpha, dh0, workspace};
   for (const void* x : ptrs)
     if (x && !aligned16(x)) return GDN_ERR_ALIGN;
   if (!saved || saved_bytes_ < saved_bytes(p, s)) return GDN_ERR_SAVED;
@@ -714,7 +715,9 @@ gdn_status gdn_block_bwd_saved_timed(const gdn_problem* p, const gdn_block_prolo
   Carver c{(unsigned char*)const_cast<void*>(saved)};
   carve_saved(p, s, c, &a);
   fill_prologue(pro, &a);
-  a.v = v;  // the rule's v (the forward's output): the gradient kernel reads it
+  a.q = q;  // the rule's q, k, v (the saving forward's outputs)
+  a.k = k;
+  a.v = v;
   a.beta = beta;
   a.dO = dO;
   a.dht = dht;
@@ -745,12 +748,13 @@ gdn_status gdn_block_bwd_saved_timed(const gdn_problem* p, const gdn_block_prolo
 }
 
 gdn_status gdn_block_bwd_saved(const gdn_problem* p, const gdn_block_prologue* pro,
-                               const void* v, const float* beta, const void* dO,
-                               const float* dht, const void* saved, size_t saved_bytes_,
-                               void* dxq, void* dxk, void* dxv, float* dwq, float* dwk,
-                               float* dwv, float* dbeta, float* dlog_alpha, float* dh0,
-                               void* workspace, size_t workspace_bytes, void* stream) {
-  return gdn_block_bwd_saved_timed(p, pro, v, beta, dO, dht, saved, saved_bytes_, dxq, dxk, dxv,
+                               const void* q, const void* k, const void* v, const float* beta,
+                               const void* dO, const float* dht, const void* saved,
+                               size_t saved_bytes_, void* dxq, void* dxk, void* dxv, float* dwq,
+                               float* dwk, float* dwv, float* dbeta, float* dlog_alpha,
+                               float* dh0, void* workspace, size_t workspace_bytes,
+                               void* stream) {
+  return gdn_block_bwd_saved_timed(p, pro, q, k, v, beta, dO, dht, saved, saved_bytes_, dxq, dxk, dxv,
                                    dwq, dwk, dwv, dbeta, dlog_alpha, dh0, workspace,
                                    workspace_bytes, stream, nullptr);
 }

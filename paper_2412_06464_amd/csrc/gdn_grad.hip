@@ -89,16 +89,14 @@ void k_grad(Args a) {
   constexpr int MID_BYTES = STG_BYTES > KQ_BYTES ? STG_BYTES : KQ_BYTES;
   constexpr int ECP_BYTES = 4 * NW * CH * (int)sizeof(float);  // partial column sums of E
   constexpr int FIN_ALL = FIN_BYTES + MID_BYTES + ECP_BYTES;
-  // block prologue (BLK): forming the q and k rows, beside the finish
-  // buffers (one 64-wide slice of x, the row sums, the weights by lag) ...
-  using PS = ProStage<E, 64, NTH_>;
-  constexpr int PRO_FWD = BLK ? up16(PS::BYTES) + NW * CH * 4 + 2 * DK * 16 : 0;
-  // ... and its backward after step (2), from the start of the LDS: dy,
-  // then du, in fp32; x over all dk columns; two row sums; the weights
+  // block prologue's backward (BLK), after step (3), from the start of the
+  // LDS: dy, then du, in fp32; x over all dk columns; two row sums; the
+  // weights by lag; the dw sums of the row blocks
   using PB = ProStage<E, DK, NTH_>;
   constexpr int LDY = DK + 4;
-  constexpr int PRO_BWD = BLK ? CH * LDY * 4 + up16(PB::BYTES) + 2 * NW * CH * 4 + DK * 16 : 0;
-  constexpr int FIN_PRO = FIN_ALL + PRO_FWD > PRO_BWD ? FIN_ALL + PRO_FWD : PRO_BWD;
+  constexpr int PRO_BWD =
+      BLK ? CH * LDY * 4 + up16(PB::BYTES) + 2 * NW * CH * 4 + DK * 16 + NTH_ * 16 : 0;
+  constexpr int FIN_PRO = FIN_ALL > PRO_BWD ? FIN_ALL : PRO_BWD;
   constexpr int SMEM = RING_BYTES > FIN_PRO ? RING_BYTES : FIN_PRO;
   static_assert(SMEM + 6 * 1024 <= 160 * 1024, "LDS of one workgroup");
   static_assert(sizeof(E) == 4 || NW == 8 || SMEM + 5 * 1024 + 512 <= 80 * 1024,
@@ -284,14 +282,12 @@ void k_grad(Args a) {
   constexpr int EPV = 16 / sizeof(E), VPRW = DKW / EPV, KQV = CH * VPRW / (64 * NW);
   static_assert(KQV * 64 * NW == CH * VPRW, "k / q rows do not divide over the threads");
   uint4 kr[KQV], qr[KQV];
-  if constexpr (!BLK) {
 #pragma unroll
-    for (int x = 0; x < KQV; ++x) {
-      const int v = tid + 64 * NW * x, t = v / VPRW, cv = v - t * VPRW;
-      const size_t off = (row0 + (size_t)t * H) * DK + dt0 * 16 + cv * EPV;
-      kr[x] = t < len ? *reinterpret_cast<const uint4*>((const E*)a.k + off) : uint4{0u, 0u, 0u, 0u};
-      qr[x] = t < len ? *reinterpret_cast<const uint4*>((const E*)a.q + off) : uint4{0u, 0u, 0u, 0u};
-    }
+  for (int x = 0; x < KQV; ++x) {
+    const int v = tid + 64 * NW * x, t = v / VPRW, cv = v - t * VPRW;
+    const size_t off = (row0 + (size_t)t * H) * DK + dt0 * 16 + cv * EPV;
+    kr[x] = t < len ? *reinterpret_cast<const uint4*>((const E*)a.k + off) : uint4{0u, 0u, 0u, 0u};
+    qr[x] = t < len ? *reinterpret_cast<const uint4*>((const E*)a.q + off) : uint4{0u, 0u, 0u, 0u};
   }
   // ---- finish phase (the staging ring is dead; its LDS is reused)
   // (1) the [dO; dX] V'^T tiles: M1, D, and the parts of E and dbeta.  All
@@ -375,72 +371,12 @@ void k_grad(Args a) {
       if (l < 16) sxv[w * 16 + l] = x;
     }
   }
-  if constexpr (!BLK) {
 #pragma unroll
-    for (int x = 0; x < KQV; ++x) {
-      const int v = tid + 64 * NW * x, t = v / VPRW, cv = v - t * VPRW;
-      *reinterpret_cast<uint4*>(sKr + t * LDK + cv * EPV) = kr[x];
-      *reinterpret_cast<uint4*>(sQr + t * LDK + cv * EPV) = qr[x];
-    }
+  for (int x = 0; x < KQV; ++x) {
+    const int v = tid + 64 * NW * x, t = v / VPRW, cv = v - t * VPRW;
+    *reinterpret_cast<uint4*>(sKr + t * LDK + cv * EPV) = kr[x];
+    *reinterpret_cast<uint4*>(sQr + t * LDK + cv * EPV) = qr[x];
   }
-  // block prologue: a.q and a.k are the projections; the rule's q and k rows
-  // are formed from them as in the prep and go straight to their staging
-  // (after step (1), when its products are in LDS and fewer registers live)
-  if constexpr (BLK) {
-    static_assert(sizeof(E) == 2 && HV == 1, "the fused block prologue: bf16, whole rows");
-    const int nprev = start > pro_seq_start(a, ci) ? 3 : 0;  // chunks start 64-aligned
-    constexpr int NG = 64 / EPV / NW, KS = DK / 64;  // groups of a lane per slice; slices
-    E* sXs = (E*)(smem + FIN_ALL);
-    float* sNrm = (float*)(smem + FIN_ALL + up16(PS::BYTES));  // [NW][CH]
-    float4* sWl = (float4*)(sNrm + NW * CH);                   // [2 DK]: q, then k
-    pro_weights(sWl, a.cwq + (size_t)h * DK * a.cw, a.cw, DK, tid, NTH_);
-    pro_weights(sWl + DK, a.cwk + (size_t)h * DK * a.cw, a.cw, DK, tid, NTH_);
-    PS st;
-    const int t = l;
-#pragma unroll
-    for (int mat = 0; mat < 2; ++mat) {  // q into sQr, then k into sKr
-      const E* X = (const E*)(mat ? a.k : a.q);
-      E* dst = mat ? sKr : sQr;
-      float z[KS][NG][EPV], ss = 0.f;
-      st.fetch(X, DK, H, h, start, len, nprev, 0, tid);
-#pragma unroll
-      for (int sl = 0; sl < KS; ++sl) {
-        lds_barrier();  // the previous slice's taps (and the row sums) are read
-        st.store(sXs, tid);
-        if (sl + 1 < KS) st.fetch(X, DK, H, h, start, len, nprev, 64 * (sl + 1), tid);
-        lds_barrier();
-#pragma unroll
-        for (int i = 0; i < NG; ++i) {
-          const int cg = (w + NW * i) * EPV;
-          PS::u_of(sXs, sWl + mat * DK + 64 * sl + cg, t, cg, z[sl][i]);
-#pragma unroll
-          for (int q = 0; q < EPV; ++q) {
-            z[sl][i][q] *= sigmoidf(z[sl][i][q]);
-            ss += z[sl][i][q] * z[sl][i][q];
-          }
-        }
-      }
-      sNrm[w * CH + t] = ss;
-      lds_barrier();
-      float tot = 0.f;
-#pragma unroll
-      for (int x = 0; x < NW; ++x) tot += sNrm[x * CH + t];
-      const float sc = rsqrtf(tot + a.ceps);
-#pragma unroll
-      for (int sl = 0; sl < KS; ++sl)
-#pragma unroll
-        for (int i = 0; i < NG; ++i) {
-          union {
-            uint4 u;
-            E e[EPV];
-          } y;
-#pragma unroll
-          for (int q = 0; q < EPV; ++q) y.e[q] = to_e<E>(t < len ? z[sl][i][q] * sc : 0.f);
-          *reinterpret_cast<uint4*>(dst + t * LDK + 64 * sl + (w + NW * i) * EPV) = y.u;
-        }
-    }
-  }
-
   lds_barrier();
 
   // K and Q as B operands (column d, k = t in permuted order) of the wave's
@@ -489,7 +425,7 @@ void k_grad(Args a) {
       const bool succ = start + CH < pro_seq_end(a, ci);  // a next chunk in the sequence
       const size_t NCH = (size_t)a.NC * H;
       PB xs;
-      xs.fetch((const E*)(MAT ? a.k : a.q), DK, H, h, start, len, start > s0 ? 3 : 0, 0, tid);
+      xs.fetch((const E*)(MAT ? a.xk : a.xq), DK, H, h, start, len, start > s0 ? 3 : 0, 0, tid);
       if (MAT) lds_barrier();  // q's du, x and weights are read
       pro_weights(sWb, (MAT ? a.cwk : a.cwq) + (size_t)h * DK * a.cw, a.cw, DK, tid, NTH_);
 #pragma unroll
@@ -547,64 +483,60 @@ void k_grad(Args a) {
         *reinterpret_cast<float4*>(sDy + t * LDY + cg + 4) = make_float4(dy[4], dy[5], dy[6], dy[7]);
       }
       lds_barrier();
-      // dx of row t
+      // dx and dw: thread (column cc, row block rb) walks rows r0 .. r0 + RPB - 1
+      // with its column's weights in registers and sliding windows of du and
+      // x:  dx_s = sum_j wl_j du_{s+j} (du past the chunk's last row is the
+      // next chunk's: those rows go out as partial sums),  dw_j = sum_s du_s x_{s-j}
+      constexpr int TPC = NTH_ / DK, RPB = CH / TPC;
+      static_assert(TPC * DK == NTH_ && RPB * TPC == CH, "whole row blocks per column");
       E* DX = (E*)(MAT ? a.dk : a.dq);
       float* tail = a.btail + ((size_t)MAT * NCH + ch) * 3 * DK;
-#pragma unroll
-      for (int gi = 0; gi < NGR; ++gi) {
-        const int cg = (w + NW * gi) * EPV;
-        float dx[EPV];
-#pragma unroll
-        for (int q = 0; q < EPV; ++q) dx[q] = 0.f;
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          if (t + j < CH) {
-            float du[EPV];
-            ld8(sDy + (t + j) * LDY + cg, du);
-#pragma unroll
-            for (int q = 0; q < EPV; ++q)
-              dx[q] += reinterpret_cast<const float*>(sWb + cg + q)[j] * du[q];
-          }
-        if (succ && t >= CH - 3) {
-          float* dst = tail + (t - (CH - 3)) * DK + cg;
-          *reinterpret_cast<float4*>(dst) = make_float4(dx[0], dx[1], dx[2], dx[3]);
-          *reinterpret_cast<float4*>(dst + 4) = make_float4(dx[4], dx[5], dx[6], dx[7]);
-        } else if (t < len) {
-          union {
-            uint4 u;
-            E e[EPV];
-          } y;
-#pragma unroll
-          for (int q = 0; q < EPV; ++q) y.e[q] = to_e<E>(dx[q]);
-          *reinterpret_cast<uint4*>(DX + (row0 + (size_t)t * H) * DK + cg) = y.u;
-        }
+      const int cc = tid % DK, rb = tid / DK, r0 = rb * RPB;
+      const float4 wl = sWb[cc];
+      auto du_at = [&](int r) { return r < CH ? sDy[r * LDY + cc] : 0.f; };
+      auto x_at = [&](int r) { return to_f(sXf[(r + 3) * PB::LD + cc]); };  // chunk row r >= -3
+      float d1 = du_at(r0), d2 = du_at(r0 + 1), d3 = du_at(r0 + 2);
+      float x1 = x_at(r0 - 1), x2 = x_at(r0 - 2), x3 = x_at(r0 - 3);
+      float dw0 = 0.f, dw1 = 0.f, dw2 = 0.f, dw3 = 0.f;
+#pragma unroll 4
+      for (int r = r0; r < r0 + RPB; ++r) {
+        const float d0 = d1;  // du_r .. du_{r+3}
+        d1 = d2;
+        d2 = d3;
+        d3 = du_at(r + 3);
+        const float dx = wl.x * d0 + wl.y * d1 + wl.z * d2 + wl.w * d3;
+        const float x0 = x_at(r);
+        dw0 += d0 * x0;
+        dw1 += d0 * x1;
+        dw2 += d0 * x2;
+        dw3 += d0 * x3;
+        x3 = x2;
+        x2 = x1;
+        x1 = x0;
+        if (succ && r >= CH - 3)
+          tail[(r - (CH - 3)) * DK + cc] = dx;
+        else if (r < len)
+          DX[(row0 + (size_t)r * H) * DK + cc] = to_e<E>(dx);
       }
       // du of the first three rows, for the previous chunk's dx
       if (start > s0) {
         float* head = a.bhead + ((size_t)MAT * NCH + ch) * 3 * DK;
         for (int idx = tid; idx < 3 * DK; idx += NTH_) {
-          const int r = idx / DK, cc = idx - r * DK;
-          head[idx] = sDy[r * LDY + cc];
+          const int r = idx / DK;
+          head[idx] = sDy[r * LDY + idx - r * DK];
         }
       }
-      // dw partials: thread (column cc, lags jg, jg + TPC, ...)
-      constexpr int TPC = NTH_ / DK, LPT = 4 / TPC;
-      static_assert(TPC * LPT == 4, "threads per column must divide the four lags");
-      const int cc = tid % DK, jg = tid / DK;
-      float acc[LPT];
+      // dw partials of the chunk: the row blocks' sums added in order
+      float* sDw = (float*)(sWb + DK);  // [TPC][DK] weights-by-lag sums
+      *reinterpret_cast<float4*>(sDw + ((size_t)rb * DK + cc) * 4) = make_float4(dw0, dw1, dw2, dw3);
+      lds_barrier();
+      float* part = a.bpart + ((size_t)MAT * NCH + ch) * DK * a.cw;
+      for (int idx = tid; idx < DK * a.cw; idx += NTH_) {
+        const int c2 = idx / a.cw, j = a.cw - 1 - (idx - c2 * a.cw);  // tap -> lag
+        float sum = 0.f;
 #pragma unroll
-      for (int m = 0; m < LPT; ++m) acc[m] = 0.f;
-      for (int tt = 0; tt < len; ++tt) {
-        const float d = sDy[tt * LDY + cc];
-#pragma unroll
-        for (int m = 0; m < LPT; ++m)
-          acc[m] += d * to_f(sXf[(tt + 3 - (jg + TPC * m)) * PB::LD + cc]);
-      }
-      float* part = a.bpart + (((size_t)MAT * NCH + ch) * DK + cc) * a.cw;
-#pragma unroll
-      for (int m = 0; m < LPT; ++m) {
-        const int j = jg + TPC * m;
-        if (j < a.cw) part[a.cw - 1 - j] = acc[m];
+        for (int b = 0; b < TPC; ++b) sum += sDw[((size_t)b * DK + c2) * 4 + j];
+        part[idx] = sum;
       }
     }
   };
@@ -731,7 +663,7 @@ void k_grad(Args a) {
     }
   }
   // (4) block prologue: the backward of q's and k's, on dq and dk in
-  // registers; its LDS covers the finish buffers and sEcp
+  // registers; its LDS covers the finish buffers and sEcp, which (3) has read
   if constexpr (BLK) {
     lds_barrier();
     block_bwd(std::integral_constant<int, 0>{}, Gq);
@@ -831,8 +763,8 @@ hipError_t launch_block_fixup(int dk, const Args& a, hipStream_t s) {
 
 hipError_t launch_grad(Dt dt, int dk, int dv, const Args& a, hipStream_t s, bool block) {
   if (!a.q || !a.k) return hipErrorInvalidValue;  // the kernel reads the chunk's q and k rows
-  if (block && (dt != Dt::BF16 || !a.cwq || !a.cwk || a.cw < 1 || a.cw > 4 || !a.bhead ||
-                !a.btail || !a.bpart))
+  if (block && (dt != Dt::BF16 || !a.xq || !a.xk || !a.cwq || !a.cwk || a.cw < 1 || a.cw > 4 ||
+                !a.bhead || !a.btail || !a.bpart))
     return hipErrorInvalidValue;
   auto f = [&]<class E, int DK, int DV>() {
     if constexpr (sizeof(E) == 2) {

@@ -49,16 +49,18 @@ struct Args {
   void* dXb;  // [ch] dX = T^T dV'                64 x dv
   // workspace: the gradient kernel's partial row sums for the gate gradients
   float* gpart;  // [ch][GRAD_PART_FLOATS]
-  // fused block prologue (q, k, v point at the projections xq, xk, xv):
-  // causal depthwise convolution of width cw, SiLU, and L2 (eps ceps) for q, k
+  // fused block prologue: causal depthwise convolution of width cw, SiLU,
+  // and L2 (eps ceps) for q and k, of the projections xq, xk, xv
+  const void *xq, *xk, *xv;      // [*, T, H, d]
   const float *cwq, *cwk, *cwv;  // weights [H * d][cw]
   int cw;
   float ceps;
-  void *yq, *yk, *yv;            // the prologue's outputs: the rule's q, k, v
-  // its backward in the gradient kernel (dq, dk are then dxq, dxk), for q
-  // and then k: [2][NC * H][3][dk] du of each chunk's first three rows and
-  // partial dx of its last three, [2][NC * H][dk][cw] per-chunk partial weight
-  // gradients, their slice sums, and the weight gradients [H * dk][cw]
+  void *yq, *yk, *yv;            // the forward's outputs: the rule's q, k, v
+  // its backward in the gradient kernel (which reads the rule's q, k, v
+  // through q, k, v; dq, dk are then dxq, dxk), for q and then k:
+  // [2][NC * H][3][dk] du of each chunk's first three rows and partial dx of
+  // its last three, [2][NC * H][dk][cw] per-chunk partial weight gradients,
+  // their slice sums, and the weight gradients [H * dk][cw]
   float *bhead, *btail, *bpart, *btmp;
   float *dwq, *dwk;
 };

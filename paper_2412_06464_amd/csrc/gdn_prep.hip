@@ -96,9 +96,9 @@ __device__ inline void export_afrag_perm_pair(E* dst_raw, E* dst_scaled, const E
 // that two workgroups share a CU: one streams while the other solves.
 
 // BLK: the block prologue (Sec. 3.4: short causal convolution, SiLU, and L2
-// normalisation of q and k) runs on the rows as they are loaded: a.q, a.k,
-// a.v point at the projections, and the rule's q, k and v are formed here in
-// registers (and written to a.yq, a.yk, a.yv when those are set).
+// normalisation of q and k) runs in place of the row loads: the rule's q, k
+// and v are formed in registers from the projections a.xq, a.xk, a.xv (and
+// written to a.yq, a.yk, a.yv where those are set).
 template <class E, int DK, int DV, int MODE, bool BLK = false>
 __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
   using M = Mfma<E>;
@@ -118,7 +118,8 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
   __shared__ float sYb[32 * 33];         // products of the block recursion
   __shared__ float sg[CH], sb[CH], seg[CH], sdec[CH], sbeg[CH];
 
-  const int c = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, w = wave_id();
+  const int c = blockIdx.x, h = blockIdx.y, tid = threadIdx.x;
+  const int w = __builtin_amdgcn_readfirstlane(wave_id());
   const int H = a.H;
   const int4 ci = chunk_info(a, c);
   const int start = ci.y, len = ci.z;
@@ -168,9 +169,9 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
     float* sNrm = sA + (S::BYTES + 15) / 16 * 4;          // [4 waves][CH] row sums
     // weights by lag of the q | k | v channels, in the fp32 T buffer, which
     // the inverse does not use yet
-    constexpr int RW = 2 * DK + DV;
     float4* sWl = reinterpret_cast<float4*>(sTf);
-    static_assert(RW * sizeof(float4) <= CH * LDA * sizeof(float), "weights must fit in T");
+    static_assert((2 * DK + DV) * sizeof(float4) <= CH * LDA * sizeof(float),
+                  "weights must fit in T");
     pro_weights(sWl, a.cwq + (size_t)h * DK * a.cw, a.cw, DK, tid, 256);
     pro_weights(sWl + DK, a.cwk + (size_t)h * DK * a.cw, a.cw, DK, tid, 256);
     pro_weights(sWl + 2 * DK, a.cwv + (size_t)h * DV * a.cw, a.cw, DV, tid, 256);
@@ -186,28 +187,28 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
       for (int q = 0; q < EPV; ++q) x.e[q] = to_e<E>(t < len ? y[q] : 0.f);
       return x.u;
     };
-    // one slice's z for this lane's groups of channels (chan0: the slice's
-    // first channel among q | k | v); the slice is staged first
-    auto slice_z = [&](const E* X, int D, int sl, int nsl, int chan0, float (&z)[NI][EPV]) {
-      lds_barrier();  // the previous slice's taps are read
+    // one slice's z for this lane's groups of channels (wt: the weights by
+    // lag of the tensor's channels); the slice is staged first
+    auto slice_z = [&](const E* X, int D, const float4* wt, int sl, int nsl, float (&z)[NI][EPV]) {
+      lds_barrier();  // the previous slice's taps (and the row sums) are read
       st.store(sXs, tid);
       if (sl + 1 < nsl) st.fetch(X, D, H, h, start, len, nprev, 64 * (sl + 1), tid);
       lds_barrier();
 #pragma unroll
       for (int i = 0; i < NI; ++i) {
         const int cg = (w + 4 * i) * EPV;
-        S::u_of(sXs, sWl + chan0 + cg, t, cg, z[i]);
+        S::u_of(sXs, wt + 64 * sl + cg, t, cg, z[i]);
 #pragma unroll
         for (int q = 0; q < EPV; ++q) z[i][q] *= sigmoidf(z[i][q]);
       }
     };
     // one tensor with a row norm (q or k): out[sl][i] = y
-    auto prologue_l2 = [&](const E* X, int po, uint4 (&out)[KS][NI], void* yout) {
-      float z[KS][NI][EPV], ss = 0.f;  // (slice_z's first barrier also orders sNrm's reuse)
+    auto prologue_l2 = [&](const E* X, const float4* wt, uint4 (&out)[KS][NI], void* yout) {
+      float z[KS][NI][EPV], ss = 0.f;
       st.fetch(X, DK, H, h, start, len, nprev, 0, tid);
 #pragma unroll
       for (int sl = 0; sl < KS; ++sl) {
-        slice_z(X, DK, sl, KS, po + 64 * sl, z[sl]);
+        slice_z(X, DK, wt, sl, KS, z[sl]);
 #pragma unroll
         for (int i = 0; i < NI; ++i)
 #pragma unroll
@@ -228,15 +229,16 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
                                       (w + 4 * i) * EPV) = out[sl][i];
         }
     };
-    prologue_l2((const E*)a.q, 0, rq, a.yq);
-    prologue_l2((const E*)a.k, DK, rk, a.yk);
+    prologue_l2((const E*)a.xq, sWl, rq, a.yq);
+    prologue_l2((const E*)a.xk, sWl + DK, rk, a.yk);
     {  // v: no norm
-      const E* X = (const E*)a.v;
+      const E* X = (const E*)a.xv;
+      const float4* wt = sWl + 2 * DK;
       st.fetch(X, DV, H, h, start, len, nprev, 0, tid);
 #pragma unroll
       for (int sl = 0; sl < VS; ++sl) {
         float z[NI][EPV];
-        slice_z(X, DV, sl, VS, 2 * DK + 64 * sl, z);
+        slice_z(X, DV, wt, sl, VS, z);
 #pragma unroll
         for (int i = 0; i < NI; ++i) {
           rv[sl][i] = pack(z[i]);
@@ -492,6 +494,10 @@ hipError_t launch_chunk_table(const Args& a, hipStream_t s) {
 
 hipError_t launch_prep(Dt dt, int dk, int dv, int mode, const Args& a, hipStream_t s,
                        bool block) {
+  if (block && (!a.xq || !a.xk || !a.xv || !a.cwq || !a.cwk || !a.cwv || a.cw < 1 || a.cw > 4))
+    return hipErrorInvalidValue;
+  if (block && mode == PREP_SAVE && (!a.yq || !a.yk || !a.yv))
+    return hipErrorInvalidValue;  // the backward reads the rule's q, k, v
   auto f = [&]<class E, int DK, int DV>() {
     if (block) {  // fused block prologue (bf16): forward and saving forward only
       if constexpr (sizeof(E) != 2) return hipErrorInvalidValue;

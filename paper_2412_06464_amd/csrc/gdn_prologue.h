@@ -30,6 +30,19 @@ template <> __device__ inline float elem_f<float>(const uint4& r, int q) {
   return __uint_as_float(q == 0 ? r.x : q == 1 ? r.y : q == 2 ? r.z : r.w);
 }
 
+// A wave-uniform float in a scalar register (the bits, moved as an int: the
+// builtin converts a float argument to int).
+__device__ inline float uniform_f(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(__builtin_bit_cast(int, x)));
+}
+// A wave-uniform float4 (weights by lag of one channel) in scalar registers:
+// read from LDS by every lane at the same address, then kept once per wave.
+// (As vector registers, the weights of all of a lane's channels spill; read
+// through the scalar cache, their waits serialise with the LDS reads.)
+__device__ inline float4 uniform_weights(const float4 v) {
+  return make_float4(uniform_f(v.x), uniform_f(v.y), uniform_f(v.z), uniform_f(v.w));
+}
+
 // Staging of NCOL columns of the chunk's rows of x (and the three before).
 template <class E, int NCOL, int NTH>
 struct ProStage {
@@ -67,14 +80,15 @@ struct ProStage {
     }
   }
   // u of row t for the EPV channels at staged column cg, with the weights
-  // by lag of those channels at wl[0 .. EPV)
+  // by lag of those channels at wl[0 .. EPV) (LDS); cg and wl are the same
+  // for every lane of the wave
   __device__ static void u_of(const E* s, const float4* wl, int t, int cg, float (&u)[EPV]) {
     uint4 tap[4];  // x_{t-j}: staged row t + 3 - j
 #pragma unroll
     for (int j = 0; j < 4; ++j) tap[j] = *reinterpret_cast<const uint4*>(s + (t + 3 - j) * LD + cg);
 #pragma unroll
     for (int q = 0; q < EPV; ++q) {
-      const float4 w = wl[q];
+      const float4 w = uniform_weights(wl[q]);
       u[q] = w.x * elem_f<E>(tap[0], q) + w.y * elem_f<E>(tap[1], q) +
              w.z * elem_f<E>(tap[2], q) + w.w * elem_f<E>(tap[3], q);
     }

@@ -162,9 +162,9 @@ def load_library():
         lib.gdn_block_fwd_save_timed.restype = ctypes.c_int
         lib.gdn_block_bwd_saved_workspace_size.argtypes = [pp, I]
         lib.gdn_block_bwd_saved_workspace_size.restype = S
-        lib.gdn_block_bwd_saved.argtypes = [pp, pb] + [P] * 5 + [S] + [P] * 9 + [P, S, P]
+        lib.gdn_block_bwd_saved.argtypes = [pp, pb] + [P] * 7 + [S] + [P] * 9 + [P, S, P]
         lib.gdn_block_bwd_saved.restype = ctypes.c_int
-        lib.gdn_block_bwd_saved_timed.argtypes = [pp, pb] + [P] * 5 + [S] + [P] * 9 + [P, S, P,
+        lib.gdn_block_bwd_saved_timed.argtypes = [pp, pb] + [P] * 7 + [S] + [P] * 9 + [P, S, P,
                                                                                      pt]
         lib.gdn_block_bwd_saved_timed.restype = ctypes.c_int
         lib.gdn_status_string.argtypes = [ctypes.c_int]
@@ -642,11 +642,13 @@ def _prologue(xq, xk, xv, wq, wk, wv, eps):
 
 def gdn_block_fwd(xq, xk, xv, wq, wk, wv, beta, log_alpha, h0=None, eps=1e-6, cu_seqlens=None,
                   cu_seqlens_host=None, output_final_state=True, want_qkv=False, save=False,
-                  o=None, ht=None, saved=None, workspace=None, timer=None):
+                  o=None, ht=None, q=None, k=None, v=None, saved=None, workspace=None,
+                  timer=None):
     """Fused block forward: the prologue (short convolution, SiLU, L2 of q
     and k) inside the chunked rule's kernels.  Returns a dict with o, ht, the
-    rule's v (always when ``save``) and q, k (with ``want_qkv``), and saved
-    (with ``save``: gdn_block_fwd_save, for gdn_block_bwd_saved)."""
+    rule's q, k, v (with ``want_qkv``, and always with ``save``), and saved
+    (with ``save``: gdn_block_fwd_save, for gdn_block_bwd_saved).  Output
+    tensors passed in (o, ht, q, k, v, saved) are written in place."""
     lib = load_library()
     p, keep = make_problem(xq, xv, cu_seqlens, cu_seqlens_host)
     pro = _prologue(xq, xk, xv, wq, wk, wv, eps)
@@ -657,13 +659,19 @@ def gdn_block_fwd(xq, xk, xv, wq, wk, wv, beta, log_alpha, h0=None, eps=1e-6, cu
         o = torch.empty((B, T, H, dv), dtype=xq.dtype, device=xq.device)
     if ht is None and output_final_state:
         ht = torch.empty((ns, H, dk, dv), dtype=torch.float32, device=xq.device)
-    q = torch.empty_like(xq) if want_qkv else None
-    k = torch.empty_like(xk) if want_qkv else None
-    v = torch.empty_like(xv) if (want_qkv or save) else None
-    _check_tensors(xq, rows=(("o", o),), gates=(("beta", beta), ("log_alpha", log_alpha)),
+    want_qkv = want_qkv or save
+    if q is None and want_qkv:
+        q = torch.empty_like(xq)
+    if k is None and want_qkv:
+        k = torch.empty_like(xk)
+    if v is None and want_qkv:
+        v = torch.empty_like(xv)
+    _check_tensors(xq, rows=(("o", o), ("q", q), ("k", k), ("v", v)),
+                   gates=(("beta", beta), ("log_alpha", log_alpha)),
                    states=(("h0", h0, dv), ("ht", ht, dv)), nstate=ns)
-    if o.shape != xv.shape:
-        raise ValueError("o must match xv")
+    if o.shape != xv.shape or (v is not None and v.shape != xv.shape) or any(
+            t is not None and t.shape != xq.shape for t in (q, k)):
+        raise ValueError("o and v must match xv, q and k must match xq")
     need = (lib.gdn_chunk_fwd_save_workspace_size if save
             else lib.gdn_chunk_fwd_workspace_size)(ctypes.byref(p))
     if need == 0:  # the problem is invalid: let the library name the error
@@ -692,12 +700,12 @@ def gdn_block_fwd(xq, xk, xv, wq, wk, wv, beta, log_alpha, h0=None, eps=1e-6, cu
     return dict(o=o, ht=ht, q=q, k=k, v=v, saved=saved if save else None)
 
 
-def gdn_block_bwd_saved(xq, xk, xv, wq, wk, wv, v, beta, dO, saved, dht=None, eps=1e-6,
+def gdn_block_bwd_saved(xq, xk, xv, wq, wk, wv, q, k, v, beta, dO, saved, dht=None, eps=1e-6,
                         cu_seqlens=None, cu_seqlens_host=None, need_dh0=True,
                         need_dlog_alpha=True, workspace=None, out=None, timer=None):
     """Fused block backward from gdn_block_fwd(save=True): dict dxq, dxk,
-    dxv, dwq, dwk, dwv, dbeta, dlog_alpha, dh0.  ``v`` is the rule's v the
-    saving forward returned."""
+    dxv, dwq, dwk, dwv, dbeta, dlog_alpha, dh0.  ``q``, ``k``, ``v`` are the
+    rule's inputs the saving forward returned."""
     lib = load_library()
     p, keep = make_problem(xq, xv, cu_seqlens, cu_seqlens_host)
     pro = _prologue(xq, xk, xv, wq, wk, wv, eps)
@@ -711,13 +719,13 @@ def gdn_block_bwd_saved(xq, xk, xv, wq, wk, wv, v, beta, dO, saved, dht=None, ep
                    dlog_alpha=torch.empty_like(beta) if need_dlog_alpha else None,
                    dh0=torch.empty((ns, H, dk, dv), dtype=torch.float32,
                                    device=xq.device) if need_dh0 else None)
-    _check_tensors(xq, rows=(("v", v), ("dO", dO), ("dxq", out["dxq"]), ("dxk", out["dxk"]),
-                             ("dxv", out["dxv"])),
+    _check_tensors(xq, rows=(("q", q), ("k", k), ("v", v), ("dO", dO), ("dxq", out["dxq"]),
+                             ("dxk", out["dxk"]), ("dxv", out["dxv"])),
                    gates=(("beta", beta), ("dbeta", out["dbeta"]),
                           ("dlog_alpha", out["dlog_alpha"])),
                    states=(("dht", dht, dv), ("dh0", out["dh0"], dv)), nstate=ns)
-    if v.shape != xv.shape or dO.shape != xv.shape:
-        raise ValueError("v and dO must match xv")
+    if v.shape != xv.shape or dO.shape != xv.shape or q.shape != xq.shape or k.shape != xq.shape:
+        raise ValueError("q and k must match xq, v and dO xv")
     for name in ("dwq", "dwk", "dwv"):
         w = {"dwq": wq, "dwk": wk, "dwv": wv}[name]
         t = out[name]
@@ -728,11 +736,12 @@ def gdn_block_bwd_saved(xq, xk, xv, wq, wk, wv, v, beta, dO, saved, dht=None, ep
         raise ValueError("saved must be a contiguous uint8 tensor on xq's device")
     need = lib.gdn_block_bwd_saved_workspace_size(ctypes.byref(p), pro.width)
     if need == 0:
-        _check(lib.gdn_block_bwd_saved(ctypes.byref(p), ctypes.byref(pro), *[None] * 5, 0,
+        _check(lib.gdn_block_bwd_saved(ctypes.byref(p), ctypes.byref(pro), *[None] * 7, 0,
                                        *[None] * 9, None, 0, None))
     if workspace is None or workspace.numel() < need:
         workspace = torch.empty(need, dtype=torch.uint8, device=xq.device)
-    args = (ctypes.byref(p), ctypes.byref(pro), _ptr(v), _ptr(beta), _ptr(dO), _ptr(dht),
+    args = (ctypes.byref(p), ctypes.byref(pro), _ptr(q), _ptr(k), _ptr(v), _ptr(beta), _ptr(dO),
+            _ptr(dht),
             _ptr(saved), saved.numel(), _ptr(out["dxq"]), _ptr(out["dxk"]), _ptr(out["dxv"]),
             _ptr(out["dwq"]), _ptr(out["dwk"]), _ptr(out["dwv"]), _ptr(out["dbeta"]),
             _ptr(out["dlog_alpha"]), _ptr(out["dh0"]), _ptr(workspace), workspace.numel(),

@@ -323,10 +323,10 @@ def test_fused_block_checks_before_any_launch(lib):
     # the saving forward needs the rule's v and a large enough saved buffer
     nsave = gdn.gdn_chunk_saved_size(p)
     wss = gdn.gdn_chunk_fwd_save_workspace_size(p)
-    fs = lambda v, n: lib.gdn_block_fwd_save(ctypes.byref(p), ctypes.byref(pro()), fake, fake,
-                                             None, fake, None, None, None, v, fake, n, fake, wss,
+    fs = lambda k, n: lib.gdn_block_fwd_save(ctypes.byref(p), ctypes.byref(pro()), fake, fake,
+                                             None, fake, None, fake, k, fake, fake, n, fake, wss,
                                              None)
-    assert fs(None, nsave) == 1
+    assert fs(None, nsave) == 1                # the rule's q, k, v are required here
     assert fs(fake, nsave - 1) == 8            # GDN_ERR_SAVED
     # backward: workspace of the rule's backward plus the prologue's buffers
     wb = lib.gdn_block_bwd_saved_workspace_size(ctypes.byref(p), 4)
@@ -334,11 +334,12 @@ def test_fused_block_checks_before_any_launch(lib):
     assert lib.gdn_block_bwd_saved_workspace_size(ctypes.byref(p), 5) == 0
     assert lib.gdn_block_bwd_saved_workspace_size(ctypes.byref(p), 1) < wb
 
-    def bwd(pr, n=wb, dxv=fake):
-        return lib.gdn_block_bwd_saved(ctypes.byref(p), ctypes.byref(pr), fake, fake, fake, None,
-                                       fake, nsave, fake, fake, dxv, fake, fake, fake, fake,
-                                       None, None, fake, n, None)
+    def bwd(pr, n=wb, dxv=fake, q=fake):
+        return lib.gdn_block_bwd_saved(ctypes.byref(p), ctypes.byref(pr), q, fake, fake, fake,
+                                       fake, None, fake, nsave, fake, fake, dxv, fake, fake, fake,
+                                       fake, None, None, fake, n, None)
 
     assert bwd(pro(), dxv=None) == 1
+    assert bwd(pro(), q=None) == 1
     assert bwd(pro(width=7)) == 9
     assert bwd(pro(), n=wb - 1) == 5

@@ -89,8 +89,8 @@ def run_fused(G, inp):
     args = [d[n] for n in ("xq", "xk", "xv", "wq", "wk", "wv")]
     f = G.gdn_block_fwd(*args, d["beta"], d["log_alpha"], h0=d.get("h0"), eps=EPS,
                         cu_seqlens=cu, cu_seqlens_host=cuh, want_qkv=True, save=True)
-    g = G.gdn_block_bwd_saved(*args, f["v"], d["beta"], d["dO"], f["saved"], dht=d.get("dht"),
-                              eps=EPS, cu_seqlens=cu, cu_seqlens_host=cuh)
+    g = G.gdn_block_bwd_saved(*args, f["q"], f["k"], f["v"], d["beta"], d["dO"], f["saved"],
+                              dht=d.get("dht"), eps=EPS, cu_seqlens=cu, cu_seqlens_host=cuh)
     plain = G.gdn_block_fwd(*args, d["beta"], d["log_alpha"], h0=d.get("h0"), eps=EPS,
                             cu_seqlens=cu, cu_seqlens_host=cuh)
     torch.cuda.synchronize()
