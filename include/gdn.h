@@ -374,6 +374,21 @@ gdn_status gdn_recurrent_fwd_timed(const gdn_problem *p, const void *q,
                                    const float *h0, void *o, float *ht,
                                    void *stream, gdn_timing *timing);
 
+/* Diagnostics, for tests of the library itself.  Before its first launch
+ * every call checks that each device pointer its kernels dereference is set
+ * (an internal consistency check behind the argument checks above; a failure
+ * is GDN_ERR_HIP).  gdn_debug_audit runs that check for launch sequence
+ * `sequence` (0 forward, 1 stateless backward, 2 saving forward, 3 saved
+ * backward, 4 token-by-token forward, 5 fused block forward, 6 its saving
+ * forward, 7 its saved backward) on a description in which exactly the
+ * pointer fields whose bit is set in `present` are non-null (field i is
+ * named by gdn_debug_audit_field(i), NULL past the last; the field log_alpha
+ * also switches the gate arithmetic on, cu the packed layout).  It returns
+ * the index of the first required field that is missing, -1 if none is, -2
+ * for an unknown sequence.  Nothing is launched or dereferenced. */
+int32_t gdn_debug_audit(int32_t sequence, uint64_t present);
+const char *gdn_debug_audit_field(int32_t index);
+
 /* Human-readable name of a status. */
 const char *gdn_status_string(gdn_status s);
 

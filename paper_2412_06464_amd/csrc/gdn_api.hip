@@ -899,4 +899,13 @@ const char* gdn_status_string(gdn_status s) {
   return "GDN: unknown status";
 }
 
+int gdn_debug_audit(int sequence, uint64_t present) {
+  if (sequence < 0 || sequence >= gdn::SEQ_COUNT) return -2;
+  return gdn::audit((gdn::Seq)sequence, gdn::audit_probe(present));
+}
+
+const char* gdn_debug_audit_field(int index) {
+  return index >= 0 && index < gdn::AUDIT_FIELDS ? gdn::audit_field_names[index] : nullptr;
+}
+
 }  // extern "C"

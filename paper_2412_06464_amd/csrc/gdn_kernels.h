@@ -116,6 +116,20 @@ struct Timing {
   const char** names;  // at least 8 entries
 };
 
+// The launch sequences, for the pointer audit.
+enum class Seq { Fwd, Bwd, FwdSave, BwdSaved, Recurrent, BlockFwd, BlockFwdSave, BlockBwdSaved };
+constexpr int SEQ_COUNT = 8;
+// The Args pointers the audit knows, by index (names for diagnostics).
+constexpr int AUDIT_FIELDS = 51;
+extern const char* const audit_field_names[AUDIT_FIELDS];
+// Index of the first pointer that sequence s dereferences and a lacks, or
+// -1.  (Whether log_alpha and the chunk table are needed follows a.gated and
+// a.cu.)  Every launch sequence below checks it before its first launch.
+int audit(Seq s, const Args& a);
+// An Args whose pointer fields are a dummy non-null address where bit i of
+// present is set (for tests of the audit only; never launched).
+Args audit_probe(uint64_t present);
+
 // Individual launches (each returns the launch status).
 hipError_t launch_chunk_table(const Args& a, hipStream_t s);
 hipError_t launch_prep(Dt dt, int dk, int dv, int mode, const Args& a, hipStream_t s,

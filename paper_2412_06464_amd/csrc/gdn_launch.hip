@@ -1,5 +1,7 @@
 // Launch sequences of the forward and backward calls, with optional event
 // recording around every launch.
+#include <string.h>
+
 #include "gdn_kernels.h"
 
 namespace gdn {
@@ -22,10 +24,97 @@ hipError_t timed(Timing* t, const char* name, hipStream_t s, F&& launch) {
   return hipSuccess;
 }
 
+// Pointer fields of Args, in audit order.
+#define GDN_AUDIT_FIELDS(X)                                                                    \
+  X(q) X(k) X(v) X(beta) X(log_alpha) X(h0) X(dO) X(dht) X(o) X(ht) X(dq) X(dk) X(dv) X(dbeta) \
+  X(dlog_alpha) X(dh0) X(cu) X(info) X(seq_chunk0) X(g) X(Wf) X(KbT) X(Uc) X(Pf) X(Qf) X(Kf)  \
+  X(PTf) X(TTf) X(nWT) X(QgT) X(Ak) X(Sc) X(Vp) X(dSc) X(dXb) X(gpart) X(xq) X(xk) X(xv)      \
+  X(cwq) X(cwk) X(cwv) X(yq) X(yk) X(yv) X(bhead) X(btail) X(bpart) X(btmp) X(dwq) X(dwk)
+
+enum Field : int {
+#define GDN_ENUM(f) F_##f,
+  GDN_AUDIT_FIELDS(GDN_ENUM)
+#undef GDN_ENUM
+  F_COUNT
+};
+static_assert(F_COUNT == AUDIT_FIELDS, "audit field count");
+
+constexpr uint64_t bit(Field f) { return 1ull << f; }
+template <class... F>
+constexpr uint64_t bits(F... f) {
+  return (bit(f) | ...);
+}
+
+// What each sequence reads or writes unconditionally.
+constexpr uint64_t FWD_OPS = bits(F_g, F_Wf, F_KbT, F_Uc, F_Pf, F_Qf);
+constexpr uint64_t SAVED = bits(F_g, F_Kf, F_PTf, F_TTf, F_nWT, F_QgT, F_Ak, F_Sc, F_Vp);
+constexpr uint64_t BWD_WS = bits(F_dSc, F_dXb, F_gpart);
+constexpr uint64_t BWD_IO = bits(F_beta, F_dO, F_dq, F_dk, F_dv, F_dbeta);
+constexpr uint64_t RULE_IN = bits(F_q, F_k, F_v, F_beta);
+constexpr uint64_t PRO_IN = bits(F_xq, F_xk, F_xv, F_cwq, F_cwk, F_cwv, F_beta);
+
+uint64_t required(Seq s) {
+  switch (s) {
+    case Seq::Fwd: return RULE_IN | bit(F_o) | FWD_OPS;
+    case Seq::Bwd: return RULE_IN | BWD_IO | bits(F_Wf, F_KbT, F_Uc) | SAVED | BWD_WS;
+    case Seq::FwdSave: return RULE_IN | bit(F_o) | FWD_OPS | SAVED;
+    case Seq::BwdSaved: return RULE_IN | BWD_IO | SAVED | BWD_WS;
+    case Seq::Recurrent: return RULE_IN | bit(F_o);
+    case Seq::BlockFwd: return PRO_IN | bit(F_o) | FWD_OPS;
+    case Seq::BlockFwdSave: return PRO_IN | bit(F_o) | FWD_OPS | SAVED | bits(F_yq, F_yk, F_yv);
+    case Seq::BlockBwdSaved:
+      return RULE_IN | BWD_IO | SAVED | BWD_WS | bits(F_xq, F_xk, F_cwq, F_cwk, F_info,
+                                                        F_seq_chunk0, F_bhead, F_btail, F_bpart,
+                                                        F_btmp, F_dwq, F_dwk);
+  }
+  return 0;
+}
+
+const void* field(const Args& a, int i) {
+  switch (i) {
+#define GDN_CASE(f) \
+  case F_##f:       \
+    return (const void*)a.f;
+    GDN_AUDIT_FIELDS(GDN_CASE)
+#undef GDN_CASE
+  }
+  return nullptr;
+}
+
 }  // namespace
+
+const char* const audit_field_names[AUDIT_FIELDS] = {
+#define GDN_NAME(f) #f,
+    GDN_AUDIT_FIELDS(GDN_NAME)
+#undef GDN_NAME
+};
+
+int audit(Seq s, const Args& a) {
+  uint64_t need = required(s);
+  // the gates are read unless alpha == 1 (the saved backward reads them from
+  // the saved buffer); packed input reads the chunk table
+  if (a.gated && s != Seq::BwdSaved && s != Seq::BlockBwdSaved) need |= bit(F_log_alpha);
+  if (a.cu && s != Seq::Recurrent) need |= bits(F_info, F_seq_chunk0);
+  for (int i = 0; i < F_COUNT; ++i)
+    if ((need >> i & 1) && !field(a, i)) return i;
+  return -1;
+}
+
+Args audit_probe(uint64_t present) {
+  Args a;
+  memset(&a, 0, sizeof a);
+  char* dummy = reinterpret_cast<char*>(0x1000);
+#define GDN_SET(f) \
+  if (present >> F_##f & 1) a.f = reinterpret_cast<decltype(a.f)>(dummy);
+  GDN_AUDIT_FIELDS(GDN_SET)
+#undef GDN_SET
+  a.gated = a.log_alpha != nullptr;
+  return a;
+}
 
 hipError_t launch_fwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t,
                       bool block) {
+  if (audit(block ? Seq::BlockFwd : Seq::Fwd, a) >= 0) return hipErrorInvalidValue;
   hipError_t e;
   // the chunk table serves packed input only; dense chunks are arithmetic
   if (a.cu && (e = timed(t, "k_chunk_table", s, [&] { return launch_chunk_table(a, s); })) !=
@@ -38,6 +127,7 @@ hipError_t launch_fwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timin
 }
 
 hipError_t launch_bwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t) {
+  if (audit(Seq::Bwd, a) >= 0) return hipErrorInvalidValue;
   hipError_t e;
   // the chunk table serves packed input only; dense chunks are arithmetic
   if (a.cu && (e = timed(t, "k_chunk_table", s, [&] { return launch_chunk_table(a, s); })) !=
@@ -59,6 +149,7 @@ hipError_t launch_bwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timin
 // sets and the state pass stores chunk states and V' beside O.
 hipError_t launch_fwd_save(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t,
                            bool block) {
+  if (audit(block ? Seq::BlockFwdSave : Seq::FwdSave, a) >= 0) return hipErrorInvalidValue;
   hipError_t e;
   // the chunk table serves packed input only; dense chunks are arithmetic
   if (a.cu && (e = timed(t, "k_chunk_table", s, [&] { return launch_chunk_table(a, s); })) !=
@@ -73,6 +164,7 @@ hipError_t launch_fwd_save(Dt dt, int dk, int dv, const Args& a, hipStream_t s, 
 
 // Backward from a saving forward's buffer: no prep, no recompute.
 hipError_t launch_bwd_saved(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t) {
+  if (audit(Seq::BwdSaved, a) >= 0) return hipErrorInvalidValue;
   hipError_t e;
   // the chunk table serves packed input only; dense chunks are arithmetic
   if (a.cu && (e = timed(t, "k_chunk_table", s, [&] { return launch_chunk_table(a, s); })) !=
@@ -92,6 +184,7 @@ hipError_t launch_bwd_saved(Dt dt, int dk, int dv, const Args& a, hipStream_t s,
 // on the rule's dv.
 hipError_t launch_block_bwd_saved(int dk, int dv, const Args& a, const ConvArgs& cv,
                                   hipStream_t s, Timing* t) {
+  if (audit(Seq::BlockBwdSaved, a) >= 0) return hipErrorInvalidValue;
   hipError_t e;
   if ((e = timed(t, "k_chunk_table", s, [&] { return launch_chunk_table(a, s); })) != hipSuccess)
     return e;
@@ -109,6 +202,7 @@ hipError_t launch_block_bwd_saved(int dk, int dv, const Args& a, const ConvArgs&
 
 // Token-by-token form: one launch, no workspace.
 hipError_t launch_recurrent_fwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t) {
+  if (audit(Seq::Recurrent, a) >= 0) return hipErrorInvalidValue;
   return timed(t, "k_recurrent", s, [&] { return launch_recurrent(dt, dk, dv, a, s); });
 }
 

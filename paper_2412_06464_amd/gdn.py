@@ -29,7 +29,8 @@ EXPORTS = ("gdn_chunk_fwd", "gdn_chunk_bwd", "gdn_chunk_fwd_workspace_size",
            "gdn_norm_gate_bwd", "gdn_status_string", "gdn_chunk_fwd_noalloc",
            "gdn_block_fwd", "gdn_block_fwd_save", "gdn_block_bwd_saved",
            "gdn_block_bwd_saved_workspace_size", "gdn_block_fwd_timed",
-           "gdn_block_fwd_save_timed", "gdn_block_bwd_saved_timed")
+           "gdn_block_fwd_save_timed", "gdn_block_bwd_saved_timed", "gdn_debug_audit",
+           "gdn_debug_audit_field")
 # bytes of the library's static workspace behind gdn_chunk_fwd_noalloc
 NOALLOC_SCRATCH_BYTES = 64 << 20
 
@@ -167,6 +168,10 @@ def load_library():
         lib.gdn_block_bwd_saved_timed.argtypes = [pp, pb] + [P] * 7 + [S] + [P] * 9 + [P, S, P,
                                                                                      pt]
         lib.gdn_block_bwd_saved_timed.restype = ctypes.c_int
+        lib.gdn_debug_audit.argtypes = [ctypes.c_int32, ctypes.c_uint64]
+        lib.gdn_debug_audit.restype = ctypes.c_int32
+        lib.gdn_debug_audit_field.argtypes = [ctypes.c_int32]
+        lib.gdn_debug_audit_field.restype = ctypes.c_char_p
         lib.gdn_status_string.argtypes = [ctypes.c_int]
         lib.gdn_status_string.restype = ctypes.c_char_p
         _lib = lib

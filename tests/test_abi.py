@@ -23,8 +23,8 @@ def lib():
 
 def declared_functions():
     text = open(HEADER).read()
-    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_]+\s*\*?\s*(gdn_[a-z_0-9]+)\s*\(",
-                                 text, re.M)))
+    return sorted(set(re.findall(
+        r"^\s*(?:const\s+)?[a-z_][a-z_0-9]*\s*\*?\s*(gdn_[a-z_0-9]+)\s*\(", text, re.M)))
 
 
 def test_header_declares_expected_entry_points():
@@ -343,3 +343,53 @@ def test_fused_block_checks_before_any_launch(lib):
     assert bwd(pro(), q=None) == 1
     assert bwd(pro(width=7)) == 9
     assert bwd(pro(), n=wb - 1) == 5
+
+
+# What every launch sequence dereferences, written from the kernels' reads
+# and writes: the prep's operands (W~, Kbar^T, U~ and the forward's P and
+# e^g Q), what a saving forward keeps (gates, the backward's operands, chunk
+# states, V'), the backward's own intermediates (dS, dX, gate partial sums).
+_SAVED = {"g", "Kf", "PTf", "TTf", "nWT", "QgT", "Ak", "Sc", "Vp"}
+_FWD = {"q", "k", "v", "beta", "o", "g", "Wf", "KbT", "Uc", "Pf", "Qf"}
+_BWD_SAVED = {"q", "k", "v", "beta", "dO", "dq", "dk", "dv", "dbeta", "dSc", "dXb",
+              "gpart"} | _SAVED
+_BLOCK_FWD = {"xq", "xk", "xv", "cwq", "cwk", "cwv", "beta", "o", "g", "Wf", "KbT", "Uc", "Pf",
+              "Qf"}
+AUDIT_EXPECT = {
+    0: _FWD,
+    1: _BWD_SAVED | {"Wf", "KbT", "Uc"},
+    2: _FWD | _SAVED,
+    3: _BWD_SAVED,
+    4: {"q", "k", "v", "beta", "o"},
+    5: _BLOCK_FWD,
+    6: _BLOCK_FWD | _SAVED | {"yq", "yk", "yv"},
+    7: _BWD_SAVED | {"xq", "xk", "cwq", "cwk", "info", "seq_chunk0", "bhead", "btail", "bpart",
+                     "btmp", "dwq", "dwk"},
+}
+
+
+def test_launch_sequences_audit_their_pointers(lib):
+    """Each launch sequence refuses a description that lacks a pointer its
+    kernels dereference, and only those: every required field, removed alone,
+    is reported; every other field may be missing.  Packed input adds the
+    chunk table (the token-by-token form reads the boundaries directly)."""
+    names = []
+    while lib.gdn_debug_audit_field(len(names)) is not None:
+        names.append(lib.gdn_debug_audit_field(len(names)).decode())
+    idx = {n: i for i, n in enumerate(names)}
+    everything = (1 << len(names)) - 1
+    assert lib.gdn_debug_audit(8, everything) == -2
+    for seq, need in AUDIT_EXPECT.items():
+        assert need <= set(names), need - set(names)
+        base = everything & ~(1 << idx["log_alpha"]) & ~(1 << idx["cu"])  # ungated, dense
+        assert lib.gdn_debug_audit(seq, base) == -1, seq
+        for n in names:
+            if n in ("log_alpha", "cu"):
+                continue
+            got = lib.gdn_debug_audit(seq, base & ~(1 << idx[n]))
+            assert got == (idx[n] if n in need else -1), (seq, n, got)
+        table = {"info", "seq_chunk0"} if seq != 4 else set()
+        packed = base | (1 << idx["cu"])
+        for n in ("info", "seq_chunk0"):
+            got = lib.gdn_debug_audit(seq, packed & ~(1 << idx[n]))
+            assert got == (idx[n] if (n in table or n in need) else -1), (seq, n, got)
