@@ -491,15 +491,13 @@ def fused_step_bytes(w, tokens_heads, n_states, has_h0):
     and again by the backward, beta, log_alpha, o, dO, the states, and the
     gradients dxq, dxk, dxv, dbeta, dlog_alpha (= the rule's path bytes, with
     the projections for q, k, v; the weights are a few kB).  Kept off HBM
-    against the unfused composition, per token-head (e = 2): the rule's q and
-    k written by the prologue and read by the prep (4 dk e) and v read by it
-    (dv e; v is still written once, for the backward); in the backward the
-    rule's dq and dk written and read back (4 dk e), and q and k read by the
-    gradient kernel beside the projections the prologue's backward reads
-    (2 dk e)."""
+    against the unfused composition, per token-head (e = 2): the read of the
+    rule's q, k, v by the prep (the prologue wrote them; the fused prep writes
+    them once, for the backward) (2 dk + dv) e, and in the backward the rule's
+    dq and dk written and read back 4 dk e."""
     e = 2
     return (path_bytes(w, tokens_heads, n_states, has_h0),
-            (10 * w.dk + w.dv) * e * tokens_heads)
+            (6 * w.dk + w.dv) * e * tokens_heads)
 
 
 def bench_fused_block(args):

@@ -55,6 +55,14 @@ def kernel_key_of(name: str) -> str:
         m2 = re.match(r"_ZN3gdn\d+(k_[a-z_0-9]+)Ev?", name)
         if m2:
             return m2.group(1)
+        # already demangled: [void ]gdn::k_name<float, 64, 64, 0, false>(...)
+        d = re.match(r"(?:void )?gdn::(k_[a-z_0-9]+)(?:<([^>]*)>)?", name)
+        if d:
+            if d.group(2) is None:
+                return d.group(1)
+            conv = {"float": "f32", "__bf16": "bf16", "false": "0", "true": "1"}
+            args = [conv.get(x.strip(), x.strip()) for x in d.group(2).split(",")]
+            return "%s<%s>" % (d.group(1), ",".join(args))
         return name.split("(")[0].replace("void ", "")
     base, tpl = m.group(1), m.group(3)
     if tpl is None:
@@ -186,6 +194,46 @@ def stats(workload, trace_dir, out, cmd):
     open(out, "w").write("\n".join(lines) + "\n")
 
 
+def summary(workload, out, bench_json=None, trace_dir=None, pmc=None, step_kernel=None,
+            commands=()):
+    """One summary per workload: the bench line, the kernel trace and the
+    counters (pmc = (fetch_dir, write_dir, cal_fetch_dir, cal_write_dir));
+    commands are the ones that produced them, listed first."""
+    lines = ["# %s" % workload, "",
+             "Commands (from the repository root, on one MI355X; rocprofv3 after "
+             "`cd /tmp && export TMPDIR=/tmp`; the last two build this file and "
+             "profiles/traffic.json from their output):", "", "```"]
+    lines += list(commands) + ["```", ""]
+    if bench_json:
+        j = json.loads(open(bench_json).read().strip().splitlines()[-1])
+        lines += ["## bench.py line", "", "```json", json.dumps(j, indent=1), "```", ""]
+    if trace_dir:
+        rows = _csv_rows(trace_dir, "kernel_stats.csv")
+        lines += ["## Kernel trace (rocprofv3 --kernel-trace --stats)", "",
+                  "| kernel | calls | avg µs | min µs | max µs | % of GPU time |",
+                  "|---|---|---|---|---|---|"]
+        for r in rows:
+            lines.append("| `%s` | %s | %.1f | %.1f | %.1f | %.1f |" % (
+                kernel_key_of(r["Name"]), r["Calls"], float(r["AverageNs"]) / 1e3,
+                float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3, float(r["Percentage"])))
+        lines.append("")
+    if pmc:
+        rec = traffic(workload, *pmc, step_kernel, "\n".join(commands))
+        cf, cw = rec["calibration"]["FETCH_SIZE"], rec["calibration"]["WRITE_SIZE"]
+        lines += ["## HBM traffic per launch (rocprofv3 --pmc FETCH_SIZE, WRITE_SIZE)", "",
+                  "Each counter scaled by what it reads for a 1 GiB device-to-device copy: "
+                  "x%.3f and x%.3f." % (cf, cw), "",
+                  "| kernel | launches | read MB | write MB | total MB per launch |",
+                  "|---|---|---|---|---|"]
+        for k, v in sorted(rec["kernels"].items(), key=lambda kv: -kv[1]["bytes_per_launch"]):
+            lines.append("| `%s` | %d | %.1f | %.1f | %.1f |" % (
+                k, v["launches"], v["read_bytes"] / 1e6, v["write_bytes"] / 1e6,
+                v["bytes_per_launch"] / 1e6))
+        lines += ["", "One step (%d steps counted by `%s`): %.3f GB." % (
+            rec["steps"], step_kernel, rec["step_bytes"] / 1e9), ""]
+    open(out, "w").write("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="what", required=True)
@@ -201,7 +249,18 @@ def main():
     t.add_argument("--step-kernel", required=True)
     t.add_argument("--cmd", required=True)
     t.add_argument("--md")
+    u = sub.add_parser("summary")
+    u.add_argument("workload")
+    u.add_argument("out")
+    u.add_argument("--bench")
+    u.add_argument("--trace")
+    u.add_argument("--pmc", nargs=4, metavar=("FETCH", "WRITE", "CAL_FETCH", "CAL_WRITE"))
+    u.add_argument("--step-kernel")
+    u.add_argument("--cmd", action="append", default=[])
     a = ap.parse_args()
+    if a.what == "summary":
+        summary(a.workload, a.out, a.bench, a.trace, a.pmc, a.step_kernel, a.cmd)
+        return
     if a.what == "stats":
         stats(a.workload, a.trace_dir, a.out, a.cmd)
     else:
