@@ -35,7 +35,8 @@ gdn_status check_problem(const gdn_problem* p, Shape* out) {
   if (!p) return GDN_ERR_NULL;
   if (p->dtype != GDN_F32 && p->dtype != GDN_BF16) return GDN_ERR_UNSUPPORTED;
   if (p->B < 1 || p->T < 1 || p->H < 1) return GDN_ERR_SHAPE;
-  const bool ok_dims = (p->dtype == GDN_F32 && p->dk == 64 && p->dv == 64) ||
+  const bool ok_dims = (p->dtype == GDN_F32 && ((p->dk == 64 && p->dv == 64) ||
+                                                (p->dk == 128 && p->dv == 128))) ||
                        (p->dtype == GDN_BF16 && ((p->dk == 64 && p->dv == 64) ||
                                                  (p->dk == 128 && p->dv == 128) ||
                                                  (p->dk == 256 && p->dv == 512)));

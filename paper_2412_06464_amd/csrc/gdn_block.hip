@@ -410,6 +410,7 @@ __global__ __launch_bounds__(256) void k_norm_gate_bwd(NormArgs a) {
 #define GDN_BLOCK_DISPATCH(dt, d, f)                                                       \
   do {                                                                                     \
     if ((dt) == Dt::F32 && (d) == 64) return (f).template operator()<float, 64>();         \
+    if ((dt) == Dt::F32 && (d) == 128) return (f).template operator()<float, 128>();       \
     if ((dt) == Dt::BF16 && (d) == 64) return (f).template operator()<__bf16, 64>();       \
     if ((dt) == Dt::BF16 && (d) == 128) return (f).template operator()<__bf16, 128>();     \
     if ((dt) == Dt::BF16 && (d) == 256) return (f).template operator()<__bf16, 256>();     \

@@ -64,6 +64,7 @@ def check_conv(G, blk, x, w, dy, l2norm, tol, label, cu=None):
 @pytest.mark.parametrize("dtype,d,B,T,H,W,l2", [
     ("f32", 64, 2, 150, 2, 4, True),
     ("f32", 64, 1, 70, 2, 1, False),
+    ("f32", 128, 1, 130, 2, 3, True),
     ("bf16", 128, 1, 200, 2, 3, True),
     ("bf16", 256, 1, 130, 2, 4, True),
     ("bf16", 256, 2, 64, 1, 2, True),

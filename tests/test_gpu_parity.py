@@ -107,6 +107,7 @@ def test_fwd_f32_workload(G, oracle_mod):
 
 @pytest.mark.parametrize("dtype,dk,dv,B,T,H", [
     ("f32", 64, 64, 2, 200, 3),
+    ("f32", 128, 128, 2, 150, 2),
     ("bf16", 64, 64, 2, 200, 3),
     ("bf16", 128, 128, 2, 130, 2),
     ("bf16", 256, 512, 1, 150, 2),
@@ -130,7 +131,7 @@ def test_fwd_stress(G, oracle_mod, label, kw, dtype):
     check_fwd(G, oracle_mod, inp, TOL[dtype], "fwd_stress_" + label)
 
 
-@pytest.mark.parametrize("dtype,dk,dv", [("f32", 64, 64), ("bf16", 128, 128),
+@pytest.mark.parametrize("dtype,dk,dv", [("f32", 64, 64), ("f32", 128, 128), ("bf16", 128, 128),
                                          ("bf16", 256, 512)])
 def test_fwd_packed(G, oracle_mod, dtype, dk, dv):
     lens = [1, 0, 64, 65, 130, 7, 128]
@@ -180,6 +181,7 @@ def test_fwd_deterministic(G):
 @pytest.mark.parametrize("dtype,dk,dv,B,T,H", [
     ("f32", 64, 64, 1, 256, 2),
     ("f32", 64, 64, 2, 150, 2),
+    ("f32", 128, 128, 1, 200, 2),
     ("bf16", 64, 64, 2, 150, 2),
     ("bf16", 128, 128, 1, 200, 2),
     ("bf16", 256, 512, 1, 130, 2),
@@ -202,7 +204,7 @@ def test_bwd_stress(G, oracle_mod, label, kw, dtype):
     check_bwd(G, oracle_mod, inp, TOL[dtype], "bwd_stress_" + label)
 
 
-@pytest.mark.parametrize("dtype,dk,dv", [("f32", 64, 64), ("bf16", 128, 128),
+@pytest.mark.parametrize("dtype,dk,dv", [("f32", 64, 64), ("f32", 128, 128), ("bf16", 128, 128),
                                          ("bf16", 256, 512)])
 def test_bwd_packed(G, oracle_mod, dtype, dk, dv):
     lens = [1, 0, 64, 65, 130, 7]
@@ -254,6 +256,7 @@ def check_saved(G, oracle_mod, inp, tol, label):
 
 @pytest.mark.parametrize("dtype,dk,dv,B,T,H", [
     ("f32", 64, 64, 2, 150, 2),
+    ("f32", 128, 128, 1, 200, 2),
     ("bf16", 64, 64, 1, 256, 2),
     ("bf16", 128, 128, 1, 200, 2),
     ("bf16", 256, 512, 1, 130, 2),
@@ -268,9 +271,10 @@ def test_saved_ragged(G, oracle_mod, dtype, dk, dv, B, T, H):
     ("beta_0_2", dict(beta_scale=2.0, log_alpha_scale=0.1)),
     ("strong_decay", dict(log_alpha_scale=8.0)),
 ])
-def test_saved_stress(G, oracle_mod, label, kw):
-    inp = make_inputs(1, 200, 2, 64, 64, "f32", seed=12, h0_std=0.05, backward=True, **kw)
-    check_saved(G, oracle_mod, inp, TOL["f32"], "saved_stress_" + label)
+@pytest.mark.parametrize("dk", [64, 128])
+def test_saved_stress(G, oracle_mod, label, kw, dk):
+    inp = make_inputs(1, 200, 2, dk, dk, "f32", seed=12, h0_std=0.05, backward=True, **kw)
+    check_saved(G, oracle_mod, inp, TOL["f32"], "saved_stress_%s_%d" % (label, dk))
 
 
 @pytest.mark.parametrize("label,kw", [
@@ -304,7 +308,7 @@ def test_saved_strong_decay_bf16_256_512(G, oracle_mod):
     check_saved(G, oracle_mod, inp, TOL["bf16"], "saved_strong_bf16_256")
 
 
-@pytest.mark.parametrize("dtype,dk,dv", [("f32", 64, 64), ("bf16", 256, 512)])
+@pytest.mark.parametrize("dtype,dk,dv", [("f32", 64, 64), ("f32", 128, 128), ("bf16", 256, 512)])
 def test_saved_packed(G, oracle_mod, dtype, dk, dv):
     lens = [1, 0, 64, 65, 130, 7]
     cu = torch.tensor(np.concatenate([[0], np.cumsum(lens)]), dtype=torch.int32)
@@ -435,6 +439,7 @@ def check_recurrent(G, oracle_mod, inp, tol, label):
 
 @pytest.mark.parametrize("dtype,dk,dv,B,T,H", [
     ("f32", 64, 64, 2, 150, 2),
+    ("f32", 128, 128, 2, 70, 2),
     ("bf16", 64, 64, 1, 1, 3),
     ("bf16", 128, 128, 2, 37, 2),
     ("bf16", 256, 512, 1, 70, 2),
