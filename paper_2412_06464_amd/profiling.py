@@ -4,6 +4,10 @@ counter record bench.py reads (profiles/traffic.json).
     python -m paper_2412_06464_amd.profiling stats WORKLOAD TRACE_DIR OUT.md --cmd "..."
     python -m paper_2412_06464_amd.profiling traffic WORKLOAD FETCH_DIR WRITE_DIR \
         CAL_FETCH_DIR CAL_WRITE_DIR --step-kernel KEY --cmd "..." [--md OUT.md]
+    python -m paper_2412_06464_amd.profiling summary WORKLOAD OUT.md --bench B.json \
+        --trace TRACE_DIR --pmc FETCH WRITE CAL_FETCH CAL_WRITE --step-kernel KEY --cmd ...
+    python -m paper_2412_06464_amd.profiling mfma WORKLOAD TRACE_DIR OUT.md SET1 SET2 SET3 \
+        --cmd ...   (the counter runs of MFMA_SETS)
 
 A kernel is identified by its key: base name and template arguments, e.g.
 k_prep<bf16,256,512,2,1> (the saving prep with the block prologue),
@@ -234,6 +238,55 @@ def summary(workload, out, bench_json=None, trace_dir=None, pmc=None, step_kerne
     open(out, "w").write("\n".join(lines))
 
 
+# Counter sets of the MFMA and stall profile, one rocprofv3 --pmc run each
+# (within the per-run limits: at most 8 SQ, 4 TCP, 2 TA, 2 GRBM counters).
+MFMA_SETS = (
+    "SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CU_CYCLES SQ_INSTS_MFMA "
+    "SQ_WAVE_CYCLES SQ_WAIT_INST_ANY SQ_ACTIVE_INST_VMEM GRBM_GUI_ACTIVE",
+    "SQ_WAIT_ANY SQ_ACTIVE_INST_ANY SQ_WAIT_INST_LDS SQ_ACTIVE_INST_LDS SQ_INST_LEVEL_VMEM "
+    "SQ_INSTS_VMEM_RD SQ_INSTS_VMEM_WR SQ_LEVEL_WAVES GRBM_GUI_ACTIVE",
+    "TCP_TCC_READ_REQ_LATENCY_sum TCP_TCC_READ_REQ_sum TCP_TOTAL_CACHE_ACCESSES_sum TA_BUSY_avr "
+    "GRBM_GUI_ACTIVE",
+)
+
+
+def mfma(workload, trace_dir, set_dirs, out, commands=()):
+    """MFMA use and stalls per kernel from the counter runs of MFMA_SETS and
+    the average durations of a kernel trace of the same build.  bf16 MFMA
+    FLOP = 512 x SQ_INSTS_VALU_MFMA_MOPS_BF16; 'waiting' = SQ_WAIT_INST_ANY /
+    SQ_WAVE_CYCLES (wave time in s_waitcnt), 'issuing' = SQ_ACTIVE_INST_ANY /
+    SQ_WAVE_CYCLES; L2 read latency = TCP_TCC_READ_REQ_LATENCY_sum /
+    TCP_TCC_READ_REQ_sum (cycles per L1-to-L2 read request)."""
+    dur = {kernel_key_of(r["Name"]): float(r["AverageNs"]) * 1e-9
+           for r in _csv_rows(trace_dir, "kernel_stats.csv")}
+    acc = collections.defaultdict(lambda: collections.defaultdict(list))
+    for d in set_dirs:
+        for r in _csv_rows(d, "counter_collection.csv"):
+            acc[kernel_key_of(r["Kernel_Name"])][r["Counter_Name"]].append(
+                float(r["Counter_Value"]))
+    m = {k: {c: sum(v) / len(v) for c, v in d.items()} for k, d in acc.items()}
+    lines = ["# MFMA use and stalls: %s" % workload, "",
+             "Commands (from the repository root, on one MI355X; rocprofv3 after "
+             "`cd /tmp && export TMPDIR=/tmp`):", "", "```"] + list(commands) + ["```", "",
+             mfma.__doc__.split("\n\n")[0].replace("\n    ", " ").strip() + "  Peak: 2.5 PFLOP/s "
+             "dense bf16.", "",
+             "| kernel | avg µs | bf16 MFMA GFLOP | achieved TFLOP/s | % of bf16 peak | "
+             "waiting | issuing | L2 read latency (cycles) |",
+             "|---|---|---|---|---|---|---|---|"]
+    for k in sorted(dur, key=lambda k: -dur[k]):
+        d = m.get(k, {})
+        fl = d.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) * 512
+        if not fl:
+            continue
+        t, wave = dur[k], max(d.get("SQ_WAVE_CYCLES", 0.0), 1.0)
+        lat = d.get("TCP_TCC_READ_REQ_LATENCY_sum", 0.0) / max(d.get("TCP_TCC_READ_REQ_sum", 1.0), 1.0)
+        lines.append("| `%s` | %.0f | %.1f | %.0f | %.1f%% | %.0f%% | %.0f%% | %.0f |" % (
+            k, t * 1e6, fl / 1e9, fl / t / 1e12, 100 * fl / t / 2.5e15,
+            100 * d.get("SQ_WAIT_INST_ANY", 0.0) / wave,
+            100 * d.get("SQ_ACTIVE_INST_ANY", 0.0) / wave, lat))
+    open(out, "w").write("\n".join(lines) + "\n")
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="what", required=True)
@@ -257,7 +310,16 @@ def main():
     u.add_argument("--pmc", nargs=4, metavar=("FETCH", "WRITE", "CAL_FETCH", "CAL_WRITE"))
     u.add_argument("--step-kernel")
     u.add_argument("--cmd", action="append", default=[])
+    v = sub.add_parser("mfma")
+    v.add_argument("workload")
+    v.add_argument("trace_dir")
+    v.add_argument("out")
+    v.add_argument("set_dirs", nargs=len(MFMA_SETS))
+    v.add_argument("--cmd", action="append", default=[])
     a = ap.parse_args()
+    if a.what == "mfma":
+        mfma(a.workload, a.trace_dir, a.set_dirs, a.out, a.cmd)
+        return
     if a.what == "summary":
         summary(a.workload, a.out, a.bench, a.trace, a.pmc, a.step_kernel, a.cmd)
         return
