@@ -51,7 +51,9 @@ BLOCK_WORKLOADS = {"block_bf16_b8_t4096_h6_dk256_dv512": (8, 4096, 6, 256, 512, 
 # the fused block (prologue inside the rule's kernels), fwd+bwd: the rule's
 # training workload of the same name without the prefix, plus its prologue
 FUSED_WORKLOADS = {"fusedblock_fwdbwd_bf16_b8_t4096_h6_dk256_dv512":
-                   ("fwdbwd_bf16_b8_t4096_h6_dk256_dv512", 4)}
+                   ("fwdbwd_bf16_b8_t4096_h6_dk256_dv512", 4),
+                   "fusedblock_fwdbwd_bf16_packed65536_h16_d128":
+                   ("fwdbwd_bf16_packed65536_h16_d128", 4)}
 PEAK_HBM = 8.0e12          # bytes/s, MI355X HBM3E
 PEAK_MFMA_BF16 = 2.5e15    # dense bf16 MFMA FLOP/s
 PEAK_MFMA_F32 = 157.3e12   # fp32 matrix FLOP/s
@@ -523,17 +525,19 @@ def bench_fused_block(args):
     d.update({k: rule[k].to(dev) for k in ("beta", "log_alpha", "dO", "dht")})
     B, T, H, dk, dv = w.B, w.T, w.H, w.dk, w.dv
     eps = 1e-6
+    cuh = rule.get("cu_seqlens")  # packed workloads: the same boundaries for every call
+    cu = dict(cu_seqlens=cuh.to(dev) if cuh is not None else None, cu_seqlens_host=cuh)
     # everything allocated before the timed region
     xs = (d["xq"], d["xk"], d["xv"], d["wq"], d["wk"], d["wv"])
-    f0 = gdn.gdn_block_fwd(*xs, d["beta"], d["log_alpha"], eps=eps, save=True)
+    f0 = gdn.gdn_block_fwd(*xs, d["beta"], d["log_alpha"], eps=eps, save=True, **cu)
     g0 = gdn.gdn_block_bwd_saved(*xs, f0["q"], f0["k"], f0["v"], d["beta"], d["dO"],
-                                 f0["saved"], dht=d["dht"], eps=eps)
-    p, _ = gdn.make_problem(d["xq"], d["xv"])
+                                 f0["saved"], dht=d["dht"], eps=eps, **cu)
+    p, _ = gdn.make_problem(d["xq"], d["xv"], cu["cu_seqlens"], cuh)
     ws_f = torch.empty(gdn.gdn_chunk_fwd_save_workspace_size(p), dtype=torch.uint8, device=dev)
     ws_b = torch.empty(lib.gdn_block_bwd_saved_workspace_size(ctypes.byref(p), W),
                        dtype=torch.uint8, device=dev)
     y = {k: torch.empty_like(d["x" + k]) for k in ("q", "k", "v")}
-    pk, _ = gdn.block_problem(d["xq"])
+    pk, _ = gdn.block_problem(d["xq"], cu["cu_seqlens"], cuh)
     ws_c = torch.empty(lib.gdn_conv_silu_workspace_size(ctypes.byref(pk), dv, W),
                        dtype=torch.uint8, device=dev)
     saved_u = torch.empty(gdn.gdn_chunk_saved_size(p), dtype=torch.uint8, device=dev)
@@ -551,22 +555,23 @@ def bench_fused_block(args):
         gdn.gdn_block_fwd(*xs, d["beta"], d["log_alpha"], eps=eps, save=True, o=f0["o"],
                           ht=f0["ht"], q=f0["q"], k=f0["k"], v=f0["v"],
                           saved=f0["saved"], workspace=ws_f,
-                          timer=timers[0])
+                          timer=timers[0], **cu)
         gdn.gdn_block_bwd_saved(*xs, f0["q"], f0["k"], f0["v"], d["beta"], d["dO"],
                                 f0["saved"], dht=d["dht"], eps=eps, workspace=ws_b, out=g0,
-                                timer=timers[1])
+                                timer=timers[1], **cu)
 
     def step_unfused(timers):
         for k in ("q", "k", "v"):
             gdn.gdn_conv_silu_fwd(d["x" + k], d["w" + k], l2norm=k != "v", eps=eps, y=y[k],
-                                  workspace=ws_c)
+                                  workspace=ws_c, **cu)
         gdn.gdn_chunk_fwd_save(y["q"], y["k"], y["v"], d["beta"], d["log_alpha"], o=o_u,
-                               ht=ht_u, saved=saved_u, workspace=ws_f, timer=timers[0])
+                               ht=ht_u, saved=saved_u, workspace=ws_f, timer=timers[0], **cu)
         gdn.gdn_chunk_bwd_saved(y["q"], y["k"], y["v"], d["beta"], d["dO"], saved_u,
-                                dht=d["dht"], workspace=ws_bs, out=out_u, timer=timers[1])
+                                dht=d["dht"], workspace=ws_bs, out=out_u, timer=timers[1],
+                                **cu)
         for k in ("q", "k", "v"):
             gdn.gdn_conv_silu_bwd(d["x" + k], d["w" + k], out_u["d" + k], l2norm=k != "v",
-                                  eps=eps, dx=dx_u[k], dw=dw_u[k], workspace=ws_c)
+                                  eps=eps, dx=dx_u[k], dw=dw_u[k], workspace=ws_c, **cu)
 
     stream = torch.cuda.current_stream(dev)
     timer = StepTimer(torch, stream, dev)
@@ -602,7 +607,7 @@ def bench_fused_block(args):
 
     tokens = B * T
     tokens_heads = tokens * H
-    n_states = B
+    n_states = B if cuh is None else cuh.numel() - 1
     models = fused_models(w, tokens_heads, n_states * H, False)
     dom = max(kern_ms, key=lambda k: kern_ms[k])
     kb, kf = model_for(models, dom)

@@ -176,6 +176,19 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
     pro_weights(sWl + DK, a.cwk + (size_t)h * DK * a.cw, a.cw, DK, tid, 256);
     pro_weights(sWl + 2 * DK, a.cwv + (size_t)h * DV * a.cw, a.cw, DV, tid, 256);
     const int nprev = start > pro_seq_start(a, ci) ? 3 : 0;  // chunks start 64-aligned in a sequence
+    // the chunk's rows of all three projections into L2 first, where the
+    // workgroups an XCD runs at once (two per CU, 32 CUs) keep theirs within
+    // its 4 MB L2: 64 x 67 rows x (2 dk + dv) x 2 bytes is 3.3 MB at 128/128
+    // (prep 1.29 -> 1.20 ms at 65,536 tokens x 16 heads) but 8.8 MB at
+    // 256/512, where the warmed lines are gone before they are read (0.54 ->
+    // 0.57 ms).  Their offsets from the first staged row fit 32 bits.
+    __shared__ float sWarm[64];
+    constexpr bool WARM = 64 * (CH + 3) * (2 * DK + DV) * (int)sizeof(E) <= (4 << 20);
+    if (WARM && (size_t)(CH + 3) * H * DV * sizeof(E) < (1u << 31)) {
+      pro_warm((const E*)a.xq, DK, H, h, start, len, nprev, sWarm, tid, 256);
+      pro_warm((const E*)a.xk, DK, H, h, start, len, nprev, sWarm, tid, 256);
+      pro_warm((const E*)a.xv, DV, H, h, start, len, nprev, sWarm, tid, 256);
+    }
     const int t = lane_id();
     S st;
     auto pack = [&](const float (&y)[EPV]) {
@@ -248,7 +261,8 @@ __global__ __launch_bounds__(256, 2) void k_prep(Args a) {
         }
       }
     }
-    lds_barrier();  // A and T are formed below
+    if constexpr (WARM) wait_vmcnt<0>();  // the warm-up's loads into sWarm have landed
+    lds_barrier();    // A and T are formed below
   }
 
   // a slice of raw rows into LDS, row-major (dst[t][c]) or transposed

@@ -108,6 +108,33 @@ __device__ inline void pro_weights(float4* dst, const float* w, int width, int n
   }
 }
 
+// L2 warm-up of the rows a chunk's prologue stages: one dword of every
+// 128-byte line of rows start - nprev .. start + len - 1 of x (the D channels
+// of head h), loaded straight into LDS (`sink`: 256 bytes that nothing reads),
+// so that the slice fetches that follow find their lines in L2 instead of
+// waiting on HBM one slice at a time.  As with the state passes' warm-up, the
+// statement sets m0 (which the compiler never uses in these kernels: checked on
+// the built code object), the compiler does not count these loads (its own
+// vmcnt waits only get stricter), and the caller waits vmcnt(0) before the
+// workgroup ends.  Every address lies in the sequence's rows of x.
+template <class E>
+__device__ inline void pro_warm(const E* X, int D, int H, int h, int start, int len, int nprev,
+                                float* sink, int tid, int nth) {
+  const int lpr = D * (int)sizeof(E) / 128;  // 128-byte lines per row
+  const int n = (nprev + len) * lpr;
+  const unsigned char* base =
+      reinterpret_cast<const unsigned char*>(X + ((size_t)(start - nprev) * H + h) * D);
+  const unsigned lds = (unsigned)(uintptr_t)sink;
+  const unsigned rowb = (unsigned)H * (unsigned)D * (unsigned)sizeof(E);
+  for (int i = tid; i < n; i += nth) {
+    const int r = i / lpr;
+    const unsigned off = (unsigned)r * rowb + (unsigned)(i - r * lpr) * 128u;
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, %2" ::"s"(lds), "v"(off),
+                 "s"(base)
+                 : "memory");
+  }
+}
+
 // First token of the sequence of chunk table entry ci.
 __device__ inline int pro_seq_start(const Args& a, int4 ci) {
   return a.cu ? a.cu[ci.x] : ci.x * a.T;
