@@ -47,11 +47,9 @@
  *  - Every argument check runs on the host before the first launch; a failed
  *    check returns its status and launches nothing.  A launch failure returns
  *    GDN_ERR_HIP.  No C++ exception crosses this boundary.
- *  - Supported head dims: (dk, dv) in {(64, 64), (128, 128), (256, 512)} for
- *    bfloat16 (fp32 accumulation), and (64, 64), (128, 128) for float32 (at
- *    (256, 512) in float32 the gradient kernel's q and k row staging alone
- *    would exceed a CU's 160 KB of LDS).  The block prologue and epilogue
- *    take the dims of these pairs; the fused block is bfloat16 only.
+ *  - Supported head dims: (dk, dv) in {(64, 64), (128, 128), (256, 512)},
+ *    in bfloat16 (fp32 accumulation) and in float32.  The block prologue and
+ *    epilogue take the dims of these pairs; the fused block is bfloat16 only.
  */
 #ifndef GDN_H_
 #define GDN_H_

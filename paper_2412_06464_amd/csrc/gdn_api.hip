@@ -35,11 +35,8 @@ gdn_status check_problem(const gdn_problem* p, Shape* out) {
   if (!p) return GDN_ERR_NULL;
   if (p->dtype != GDN_F32 && p->dtype != GDN_BF16) return GDN_ERR_UNSUPPORTED;
   if (p->B < 1 || p->T < 1 || p->H < 1) return GDN_ERR_SHAPE;
-  const bool ok_dims = (p->dtype == GDN_F32 && ((p->dk == 64 && p->dv == 64) ||
-                                                (p->dk == 128 && p->dv == 128))) ||
-                       (p->dtype == GDN_BF16 && ((p->dk == 64 && p->dv == 64) ||
-                                                 (p->dk == 128 && p->dv == 128) ||
-                                                 (p->dk == 256 && p->dv == 512)));
+  const bool ok_dims = (p->dk == 64 && p->dv == 64) || (p->dk == 128 && p->dv == 128) ||
+                       (p->dk == 256 && p->dv == 512);
   if (!ok_dims) return GDN_ERR_UNSUPPORTED;
   const long Ttot = (long)p->B * p->T;
   if (Ttot * (long)p->H * (p->dk > p->dv ? p->dk : p->dv) >= (1L << 40)) return GDN_ERR_SHAPE;

@@ -18,9 +18,13 @@ namespace gdn {
 
 namespace {
 
-// N consecutive elements of one row as loaded (16 bytes at most), and their
-// fp32 values.
+// N consecutive elements of one row as loaded (two 16-byte loads at most),
+// and their fp32 values.
+struct Raw32 {
+  uint4 lo, hi;
+};
 template <int BYTES> struct RawT;
+template <> struct RawT<32> { using type = Raw32; };
 template <> struct RawT<16> { using type = uint4; };
 template <> struct RawT<8> { using type = uint2; };
 template <> struct RawT<4> { using type = unsigned; };
@@ -411,6 +415,8 @@ __global__ __launch_bounds__(256) void k_norm_gate_bwd(NormArgs a) {
   do {                                                                                     \
     if ((dt) == Dt::F32 && (d) == 64) return (f).template operator()<float, 64>();         \
     if ((dt) == Dt::F32 && (d) == 128) return (f).template operator()<float, 128>();       \
+    if ((dt) == Dt::F32 && (d) == 256) return (f).template operator()<float, 256>();       \
+    if ((dt) == Dt::F32 && (d) == 512) return (f).template operator()<float, 512>();       \
     if ((dt) == Dt::BF16 && (d) == 64) return (f).template operator()<__bf16, 64>();       \
     if ((dt) == Dt::BF16 && (d) == 128) return (f).template operator()<__bf16, 128>();     \
     if ((dt) == Dt::BF16 && (d) == 256) return (f).template operator()<__bf16, 256>();     \

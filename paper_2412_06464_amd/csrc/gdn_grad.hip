@@ -38,13 +38,14 @@ namespace gdn {
 // Workgroups per (chunk, head): two at dk = 128, where the finish phase is a
 // large share of a workgroup's time and overlapping it with the other
 // workgroup's streaming pays for the second read of the dv-side operands
-// (packed dk = dv = 128: 0.92 against 1.03 ms); one at dk = 256, where the
-// two measured the same, and at dk = 64.
+// (packed dk = dv = 128: 0.92 against 1.03 ms); one at dk = 256 in bf16, where
+// the two measured the same, and at dk = 64.  fp32 at dk = 256 takes two: the
+// chunk's q and k rows over all 256 columns would need 133 KB of LDS.
 // With the fused block prologue (BLK) a workgroup needs whole rows of q and
 // k for their L2 norms, so it owns every dk column.
 template <class E, int DK, bool BLK = false>
 struct GradCfg {
-  static constexpr int HV = (DK == 128 && !BLK) ? 2 : 1;
+  static constexpr int HV = (!BLK && (DK == 128 || (DK == 256 && sizeof(E) == 4))) ? 2 : 1;
   static constexpr int NW = (HV == 1 && DK > 64) ? 8 : 4;  // waves
   static constexpr int NTH = 64 * NW;
   static constexpr int NDH = DK / HV / 16;  // dk column tiles of a workgroup

@@ -167,6 +167,8 @@ hipError_t launch_recurrent_fwd(Dt dt, int dk, int dv, const Args& a, hipStream_
       return (f).template operator()<float, 64, 64>();                                      \
     if ((dt) == Dt::F32 && (dk) == 128 && (dv) == 128)                                      \
       return (f).template operator()<float, 128, 128>();                                    \
+    if ((dt) == Dt::F32 && (dk) == 256 && (dv) == 512)                                      \
+      return (f).template operator()<float, 256, 512>();                                    \
     if ((dt) == Dt::BF16 && (dk) == 64 && (dv) == 64)                                       \
       return (f).template operator()<__bf16, 64, 64>();                                     \
     if ((dt) == Dt::BF16 && (dk) == 128 && (dv) == 128)                                     \

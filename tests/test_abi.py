@@ -69,7 +69,7 @@ def test_workspace_sizes(lib):
 
 
 @pytest.mark.parametrize("kw,code", [
-    (dict(dk=96), 3), (dict(dk=128, dv=64), 3), (dict(dtype=gdn.GDN_F32, dk=256, dv=512), 3),
+    (dict(dk=96), 3), (dict(dk=128, dv=64), 3), (dict(dtype=gdn.GDN_F32, dk=256, dv=256), 3),
     (dict(B=0), 2), (dict(T=0), 2), (dict(H=0), 2), (dict(dtype=7), 3),
 ])
 def test_bad_problem_rejected_before_launch(lib, kw, code):

@@ -65,6 +65,8 @@ def check_conv(G, blk, x, w, dy, l2norm, tol, label, cu=None):
     ("f32", 64, 2, 150, 2, 4, True),
     ("f32", 64, 1, 70, 2, 1, False),
     ("f32", 128, 1, 130, 2, 3, True),
+    ("f32", 256, 1, 130, 2, 4, True),
+    ("f32", 512, 1, 70, 1, 4, False),
     ("bf16", 128, 1, 200, 2, 3, True),
     ("bf16", 256, 1, 130, 2, 4, True),
     ("bf16", 256, 2, 64, 1, 2, True),
@@ -89,6 +91,7 @@ def test_conv_silu_packed(G, blk, dtype, d):
 
 @pytest.mark.parametrize("dtype,dv,B,T,H", [
     ("f32", 64, 2, 150, 2),
+    ("f32", 512, 1, 77, 2),
     ("bf16", 128, 1, 77, 3),
     ("bf16", 512, 2, 100, 2),
 ])

@@ -108,6 +108,7 @@ def test_fwd_f32_workload(G, oracle_mod):
 @pytest.mark.parametrize("dtype,dk,dv,B,T,H", [
     ("f32", 64, 64, 2, 200, 3),
     ("f32", 128, 128, 2, 150, 2),
+    ("f32", 256, 512, 1, 150, 2),
     ("bf16", 64, 64, 2, 200, 3),
     ("bf16", 128, 128, 2, 130, 2),
     ("bf16", 256, 512, 1, 150, 2),
@@ -131,8 +132,8 @@ def test_fwd_stress(G, oracle_mod, label, kw, dtype):
     check_fwd(G, oracle_mod, inp, TOL[dtype], "fwd_stress_" + label)
 
 
-@pytest.mark.parametrize("dtype,dk,dv", [("f32", 64, 64), ("f32", 128, 128), ("bf16", 128, 128),
-                                         ("bf16", 256, 512)])
+@pytest.mark.parametrize("dtype,dk,dv", [("f32", 64, 64), ("f32", 128, 128), ("f32", 256, 512),
+                                         ("bf16", 128, 128), ("bf16", 256, 512)])
 def test_fwd_packed(G, oracle_mod, dtype, dk, dv):
     lens = [1, 0, 64, 65, 130, 7, 128]
     cu = torch.tensor(np.concatenate([[0], np.cumsum(lens)]), dtype=torch.int32)
@@ -182,6 +183,7 @@ def test_fwd_deterministic(G):
     ("f32", 64, 64, 1, 256, 2),
     ("f32", 64, 64, 2, 150, 2),
     ("f32", 128, 128, 1, 200, 2),
+    ("f32", 256, 512, 1, 130, 2),
     ("bf16", 64, 64, 2, 150, 2),
     ("bf16", 128, 128, 1, 200, 2),
     ("bf16", 256, 512, 1, 130, 2),
@@ -204,8 +206,8 @@ def test_bwd_stress(G, oracle_mod, label, kw, dtype):
     check_bwd(G, oracle_mod, inp, TOL[dtype], "bwd_stress_" + label)
 
 
-@pytest.mark.parametrize("dtype,dk,dv", [("f32", 64, 64), ("f32", 128, 128), ("bf16", 128, 128),
-                                         ("bf16", 256, 512)])
+@pytest.mark.parametrize("dtype,dk,dv", [("f32", 64, 64), ("f32", 128, 128), ("f32", 256, 512),
+                                         ("bf16", 128, 128), ("bf16", 256, 512)])
 def test_bwd_packed(G, oracle_mod, dtype, dk, dv):
     lens = [1, 0, 64, 65, 130, 7]
     cu = torch.tensor(np.concatenate([[0], np.cumsum(lens)]), dtype=torch.int32)
@@ -282,22 +284,23 @@ def test_saved_stress(G, oracle_mod, label, kw, dk):
     ("mid_decay", dict(log_alpha_scale=0.05)),
     ("beta_0_2", dict(beta_scale=2.0, log_alpha_scale=0.1)),
 ])
-@pytest.mark.parametrize("dk,dv", [(128, 128), (256, 512)])
+@pytest.mark.parametrize("dtype,dk,dv", [("bf16", 128, 128), ("bf16", 256, 512),
+                                         ("f32", 256, 512)])
 @pytest.mark.parametrize("path", ["fwd", "bwd", "saved"])
-def test_stress_wide_heads(G, oracle_mod, path, dk, dv, label, kw):
+def test_stress_wide_heads(G, oracle_mod, path, dtype, dk, dv, label, kw):
     """Weak and intermediate decay and beta in (0, 2) at the wide head dims,
     whose kernels are separate instantiations: with e^{g_n} near 1 the
     carried state e^{g_n} S, its gradient and the <dS, S> gate term weigh as
     much as the in-chunk terms.  Four chunks, the last one ragged."""
-    inp = make_inputs(1, 200, 2, dk, dv, "bf16", seed=21, h0_std=0.05, backward=path != "fwd",
+    inp = make_inputs(1, 200, 2, dk, dv, dtype, seed=21, h0_std=0.05, backward=path != "fwd",
                       **kw)
-    name = "stress_%s_%d_%d_%s" % (path, dk, dv, label)
+    name = "stress_%s_%s_%d_%d_%s" % (path, dtype, dk, dv, label)
     if path == "fwd":
-        check_fwd(G, oracle_mod, inp, TOL["bf16"], name)
+        check_fwd(G, oracle_mod, inp, TOL[dtype], name)
     elif path == "bwd":
-        check_bwd(G, oracle_mod, inp, TOL["bf16"], name)
+        check_bwd(G, oracle_mod, inp, TOL[dtype], name)
     else:
-        check_saved(G, oracle_mod, inp, TOL["bf16"], name)
+        check_saved(G, oracle_mod, inp, TOL[dtype], name)
 
 
 def test_saved_strong_decay_bf16_256_512(G, oracle_mod):
@@ -308,7 +311,8 @@ def test_saved_strong_decay_bf16_256_512(G, oracle_mod):
     check_saved(G, oracle_mod, inp, TOL["bf16"], "saved_strong_bf16_256")
 
 
-@pytest.mark.parametrize("dtype,dk,dv", [("f32", 64, 64), ("f32", 128, 128), ("bf16", 256, 512)])
+@pytest.mark.parametrize("dtype,dk,dv", [("f32", 64, 64), ("f32", 128, 128), ("f32", 256, 512),
+                                         ("bf16", 256, 512)])
 def test_saved_packed(G, oracle_mod, dtype, dk, dv):
     lens = [1, 0, 64, 65, 130, 7]
     cu = torch.tensor(np.concatenate([[0], np.cumsum(lens)]), dtype=torch.int32)
@@ -363,6 +367,7 @@ def test_saved_equals_stateless(G, dtype, dk, dv):
 
 @pytest.mark.parametrize("dtype,dk,dv,B,T,H", [
     ("f32", 64, 64, 2, 150, 2),
+    ("f32", 256, 512, 1, 130, 2),
     ("bf16", 128, 128, 1, 200, 2),
     ("bf16", 256, 512, 1, 130, 2),
 ])
@@ -440,6 +445,7 @@ def check_recurrent(G, oracle_mod, inp, tol, label):
 @pytest.mark.parametrize("dtype,dk,dv,B,T,H", [
     ("f32", 64, 64, 2, 150, 2),
     ("f32", 128, 128, 2, 70, 2),
+    ("f32", 256, 512, 1, 40, 2),
     ("bf16", 64, 64, 1, 1, 3),
     ("bf16", 128, 128, 2, 37, 2),
     ("bf16", 256, 512, 1, 70, 2),
