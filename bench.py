@@ -18,7 +18,9 @@ L2s ("cold"); the headline is the median cold step, with p10 and p90.  K
 more steps back to back without the write give the warm figures.  The
 library records events around each of its own launches on the same stream
 (the *_timed entry points), so every kernel's duration comes from the same
-timed steps.
+timed steps.  The headline step is then captured once as a HIP graph and
+its replays timed the same way (`graph`; skipped with --no-graph): the
+figure without the host work of the calls between the kernels.
 
 Roofline.  Each kernel is credited only with the algorithmic work of its step
 of the method: the FLOP of its products at full chunk size, and the bytes of
@@ -201,6 +203,21 @@ class StepTimer:
                     per_kernel.setdefault(call + ":" + name, []).append(kms)
                 t.close()
         return step_ms, per_kernel
+
+    def run_graph(self, graph, k, cold):
+        """Times k replays of a captured step, one by one, like run()."""
+        torch = self.torch
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(k)]
+        torch.cuda.synchronize()
+        for i in range(k):
+            if cold:
+                self.flush_buf.fill_(i + 1)
+            evs[i][0].record(self.stream)
+            graph.replay()
+            evs[i][1].record(self.stream)
+        torch.cuda.synchronize()
+        return [a.elapsed_time(b) for a, b in evs]
 
 
 # ------------------------------------------------------------------ CPU baseline and parity sample
@@ -675,6 +692,8 @@ def main():
                     help="time only the headline path of a fwd+bwd workload")
     ap.add_argument("--path", choices=("saved", "stateless"), default="saved",
                     help="backward path of the headline step (the other is timed beside it)")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip timing the headline step replayed as a captured HIP graph")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy 10 times (PMC calibration)")
     args = ap.parse_args()
@@ -779,6 +798,21 @@ def main():
     steps = {"saved": step_saved, "stateless": step_stateless, "recurrent": step_recurrent}
     tc, tw, kern_ms = measure(steps[path])
     ms = tc["median"]
+    graph = None
+    if not args.no_graph:
+        # the same step captured once and replayed: the library launches
+        # kernels only, so a graph removes the per-call host work between them
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            steps[path]()
+        torch.cuda.synchronize()
+        for _ in range(args.warmup):
+            g.replay()
+        gc = percentiles(timer.run_graph(g, args.steps, True))
+        gw = percentiles(timer.run_graph(g, args.steps, False))
+        graph = {"ms_per_step": gc["median"], "value": w.B * w.T / (gc["median"] / 1e3),
+                 "cold_ms": gc, "warm_ms": gw}
+        del g
     # outputs of the headline path, for the parity sample (a decode step
     # restarts from the prefill state)
     if w.recurrent and h0_dev is not None:
@@ -857,6 +891,8 @@ def main():
         "kernels_ms": kern_ms,
         "roofline": roof,
     }
+    if graph is not None:
+        res["graph"] = graph
     if other is not None:
         res["other_path"] = other
     if not args.no_cpu_baseline:
