@@ -256,14 +256,25 @@ def mfma(workload, trace_dir, set_dirs, out, commands=()):
     FLOP = 512 x SQ_INSTS_VALU_MFMA_MOPS_BF16; 'waiting' = SQ_WAIT_INST_ANY /
     SQ_WAVE_CYCLES (wave time in s_waitcnt), 'issuing' = SQ_ACTIVE_INST_ANY /
     SQ_WAVE_CYCLES; L2 read latency = TCP_TCC_READ_REQ_LATENCY_sum /
-    TCP_TCC_READ_REQ_sum (cycles per L1-to-L2 read request)."""
+    TCP_TCC_READ_REQ_sum (cycles per L1-to-L2 read request); clock =
+    GRBM_GUI_ACTIVE / XCDs / the same dispatch's duration (median over the
+    dispatches of the three runs), and the MFMA fraction against the peak
+    scaled to that clock (the 2.5 PFLOP/s peak is at 2.4 GHz)."""
     dur = {kernel_key_of(r["Name"]): float(r["AverageNs"]) * 1e-9
            for r in _csv_rows(trace_dir, "kernel_stats.csv")}
     acc = collections.defaultdict(lambda: collections.defaultdict(list))
+    clk = collections.defaultdict(list)
     for d in set_dirs:
+        xcc = 8
+        for r in _csv_rows(d, "agent_info.csv"):
+            if r.get("Agent_Type", "").upper().endswith("GPU") and int(r.get("Num_Xcc") or 0) > 0:
+                xcc = int(r["Num_Xcc"])
         for r in _csv_rows(d, "counter_collection.csv"):
-            acc[kernel_key_of(r["Kernel_Name"])][r["Counter_Name"]].append(
-                float(r["Counter_Value"]))
+            key = kernel_key_of(r["Kernel_Name"])
+            acc[key][r["Counter_Name"]].append(float(r["Counter_Value"]))
+            ns = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+            if r["Counter_Name"] == "GRBM_GUI_ACTIVE" and ns > 0:
+                clk[key].append(float(r["Counter_Value"]) / xcc / ns)
     m = {k: {c: sum(v) / len(v) for c, v in d.items()} for k, d in acc.items()}
     lines = ["# MFMA use and stalls: %s" % workload, "",
              "Commands (from the repository root, on one MI355X; rocprofv3 after "
@@ -271,8 +282,8 @@ def mfma(workload, trace_dir, set_dirs, out, commands=()):
              mfma.__doc__.split("\n\n")[0].replace("\n    ", " ").strip() + "  Peak: 2.5 PFLOP/s "
              "dense bf16.", "",
              "| kernel | avg µs | bf16 MFMA GFLOP | achieved TFLOP/s | % of bf16 peak | "
-             "waiting | issuing | L2 read latency (cycles) |",
-             "|---|---|---|---|---|---|---|---|"]
+             "clock GHz | % of peak at that clock | waiting | issuing | L2 read latency (cycles) |",
+             "|---|---|---|---|---|---|---|---|---|---|"]
     for k in sorted(dur, key=lambda k: -dur[k]):
         d = m.get(k, {})
         fl = d.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) * 512
@@ -280,9 +291,10 @@ def mfma(workload, trace_dir, set_dirs, out, commands=()):
             continue
         t, wave = dur[k], max(d.get("SQ_WAVE_CYCLES", 0.0), 1.0)
         lat = d.get("TCP_TCC_READ_REQ_LATENCY_sum", 0.0) / max(d.get("TCP_TCC_READ_REQ_sum", 1.0), 1.0)
-        lines.append("| `%s` | %.0f | %.1f | %.0f | %.1f%% | %.0f%% | %.0f%% | %.0f |" % (
-            k, t * 1e6, fl / 1e9, fl / t / 1e12, 100 * fl / t / 2.5e15,
-            100 * d.get("SQ_WAIT_INST_ANY", 0.0) / wave,
+        ghz = sorted(clk[k])[len(clk[k]) // 2] if clk.get(k) else float("nan")
+        lines.append("| `%s` | %.0f | %.1f | %.0f | %.1f%% | %.2f | %.1f%% | %.0f%% | %.0f%% | %.0f |" % (
+            k, t * 1e6, fl / 1e9, fl / t / 1e12, 100 * fl / t / 2.5e15, ghz,
+            100 * fl / t / (2.5e15 * ghz / 2.4), 100 * d.get("SQ_WAIT_INST_ANY", 0.0) / wave,
             100 * d.get("SQ_ACTIVE_INST_ANY", 0.0) / wave, lat))
     open(out, "w").write("\n".join(lines) + "\n")
 
