@@ -173,3 +173,53 @@ def test_decode_steps_replay_match_eager(G):
         assert_same({"o": o, "ht": state}, {"o": o2, "ht": st2}, "token %d" % r)
         ref_state.copy_(st2)
     del g
+
+
+def block_inputs(B, T, H, dk, dv, seed):
+    from paper_2412_06464_amd.inputs import make_block_inputs
+    rule = make_inputs(B, T, H, dk, dv, "bf16", seed=seed, h0_std=0.02, backward=True)
+    blk = make_block_inputs(B, T, H, dk, dv, "bf16", seed=seed + 1000, width=4)
+    out = {k: blk[k] for k in ("xq", "xk", "xv", "wq", "wk", "wv")}
+    out.update({k: rule[k] for k in ("beta", "log_alpha", "h0", "dO", "dht")})
+    return {k: v.cuda() for k, v in out.items()}
+
+
+@pytest.mark.parametrize("dk,dv", [(64, 64), (256, 512)])
+def test_fused_block_training_step_replays_match_eager(G, dk, dv):
+    """The fused block's saving forward and saved backward (with the
+    fix-up and the weight-gradient sums) captured as one graph."""
+    say("graph_fused_block", dk, dv)
+    B, T, H = 1, 200, 2
+    d = block_inputs(B, T, H, dk, dv, seed=35)
+    x = [d[n] for n in ("xq", "xk", "xv", "wq", "wk", "wv")]
+    f = G.gdn_block_fwd(*x, d["beta"], d["log_alpha"], h0=d["h0"], save=True)
+    out = G.gdn_block_bwd_saved(*x, f["q"], f["k"], f["v"], d["beta"], d["dO"], f["saved"],
+                                dht=d["dht"])
+    p, _ = G.make_problem(d["xq"], d["xv"], None, None)
+    ws_f = torch.empty(G.gdn_chunk_fwd_save_workspace_size(p), dtype=torch.uint8, device="cuda")
+    lib = G.load_library()
+    import ctypes
+    ws_b = torch.empty(lib.gdn_block_bwd_saved_workspace_size(ctypes.byref(p), 4),
+                       dtype=torch.uint8, device="cuda")
+
+    def step():
+        G.gdn_block_fwd(*x, d["beta"], d["log_alpha"], h0=d["h0"], save=True, o=f["o"],
+                        ht=f["ht"], q=f["q"], k=f["k"], v=f["v"], saved=f["saved"],
+                        workspace=ws_f)
+        G.gdn_block_bwd_saved(*x, f["q"], f["k"], f["v"], d["beta"], d["dO"], f["saved"],
+                              dht=d["dht"], workspace=ws_b, out=out)
+
+    step()
+    g = capture(step)
+    for r in range(REPLAYS):
+        refill(d, block_inputs(B, T, H, dk, dv, seed=80 + r))
+        g.replay()
+        torch.cuda.synchronize()
+        f2 = G.gdn_block_fwd(*x, d["beta"], d["log_alpha"], h0=d["h0"], save=True)
+        ref = G.gdn_block_bwd_saved(*x, f2["q"], f2["k"], f2["v"], d["beta"], d["dO"],
+                                    f2["saved"], dht=d["dht"])
+        torch.cuda.synchronize()
+        assert_same({k: f[k] for k in ("o", "ht", "q", "k", "v")},
+                    {k: f2[k] for k in ("o", "ht", "q", "k", "v")}, "replay %d fwd" % r)
+        assert_same({k: out[k] for k in ref}, ref, "replay %d bwd" % r)
+    del g
