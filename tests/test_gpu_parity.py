@@ -656,3 +656,52 @@ def test_nan_stays_in_its_unit(G, dtype, dk, dv, where):
             y[n0, h0] = 0
         assert torch.equal(x, y), name
     assert hit
+
+
+# ------------------------------------------------------------------ seeded random cases
+
+SPECIAL_LENGTHS = (0, 1, 2, 63, 64, 65, 127, 128, 129)
+DIMS = (("f32", 64, 64), ("f32", 128, 128), ("f32", 256, 512),
+        ("bf16", 64, 64), ("bf16", 128, 128), ("bf16", 256, 512))
+
+
+def random_case(seed):
+    """A seeded random problem: dims and dtype by turn; packed (0 to 6
+    sequences, lengths drawn from chunk-boundary cases or uniformly) or dense
+    (B up to 3, T up to 300); 1 to 3 heads; default, intermediate or weak
+    decay; beta up to 1 or up to 2; with or without an initial state."""
+    rng = np.random.default_rng(7000 + seed)
+    dtype, dk, dv = DIMS[seed % len(DIMS)]
+    cap = 300 if dk < 256 else 160
+    H = int(rng.integers(1, 4))
+    kw = dict(log_alpha_scale=float(rng.choice([1.0, 0.05, 0.01])),
+              beta_scale=float(rng.choice([1.0, 2.0])),
+              h0_std=0.05 if rng.random() < 0.5 else None)
+    if seed % 2 == 0:
+        n = int(rng.integers(1, 7))
+        lens = [int(rng.choice(SPECIAL_LENGTHS)) if rng.random() < 0.5 else
+                int(rng.integers(0, cap)) for _ in range(n)]
+        if sum(lens) == 0:
+            lens[-1] = 1
+        cu = torch.tensor(np.concatenate([[0], np.cumsum(lens)]), dtype=torch.int32)
+        inp = make_inputs(1, int(cu[-1]), H, dk, dv, dtype, seed=seed, backward=True,
+                          cu_seqlens=cu, **kw)
+        shape = "packed %s" % lens
+    else:
+        B, T = int(rng.integers(1, 4)), int(rng.integers(1, cap))
+        inp = make_inputs(B, T, H, dk, dv, dtype, seed=seed, backward=True, **kw)
+        shape = "dense B%d T%d" % (B, T)
+    label = "random%d %s %d/%d H%d %s %s" % (seed, dtype, dk, dv, H, shape,
+                                            {k: v for k, v in kw.items() if v is not None})
+    return inp, dtype, label
+
+
+@pytest.mark.parametrize("seed", range(36))
+def test_random_cases_all_paths(G, oracle_mod, seed):
+    """Every path (forward, stateless and saved backward, token-by-token
+    forward) on a seeded random problem against the oracle."""
+    inp, dtype, label = random_case(seed)
+    check_fwd(G, oracle_mod, inp, TOL[dtype], label)
+    check_bwd(G, oracle_mod, inp, TOL[dtype], label)
+    check_saved(G, oracle_mod, inp, TOL[dtype], label)
+    check_recurrent(G, oracle_mod, inp, TOL[dtype], label)
