@@ -179,3 +179,29 @@ def test_fused_block_full_size_sampled(G, refs):
     say("fused full size", {k: "%.3g" % v for k, v in errs.items()})
     bad = {k: v for k, v in errs.items() if not v <= TOL}
     assert not bad, bad
+
+
+@pytest.mark.parametrize("seed", range(9))
+def test_fused_block_random(G, refs, seed):
+    """Seeded random fused-block problems: dims by turn, convolution width 1
+    to 4, packed (lengths from chunk-boundary and convolution-halo cases, or
+    uniform) or dense, 1 to 3 heads, with or without an initial state."""
+    rng = np.random.default_rng(9000 + seed)
+    dk, dv = ((64, 64), (128, 128), (256, 512))[seed % 3]
+    width, H = int(rng.integers(1, 5)), int(rng.integers(1, 4))
+    h0_std = 0.02 if rng.random() < 0.5 else None
+    cap = 260 if dk < 256 else 150
+    if rng.random() < 0.5:
+        lens = [int(rng.choice((1, 2, 3, 4, 63, 64, 65, 67))) if rng.random() < 0.5 else
+                int(rng.integers(1, cap)) for _ in range(int(rng.integers(1, 6)))]
+        if max(lens) == 1:  # a zero entry state: dlog_alpha is zero by cancellation
+            h0_std = 0.02
+        cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+        inp = fused_inputs(1, int(cu[-1]), H, dk, dv, seed=100 + seed, width=width, cu=cu,
+                           h0_std=h0_std)
+    else:
+        B, T = int(rng.integers(1, 3)), int(rng.integers(1, cap))
+        if T == 1:
+            h0_std = 0.02
+        inp = fused_inputs(B, T, H, dk, dv, seed=100 + seed, width=width, h0_std=h0_std)
+    compare(G, refs, inp, "fused_random%d" % seed)

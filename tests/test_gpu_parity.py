@@ -683,12 +683,16 @@ def random_case(seed):
                 int(rng.integers(0, cap)) for _ in range(n)]
         if sum(lens) == 0:
             lens[-1] = 1
+        if max(lens) <= 1:  # dlog_alpha would be zero by cancellation
+            kw["h0_std"] = 0.05
         cu = torch.tensor(np.concatenate([[0], np.cumsum(lens)]), dtype=torch.int32)
         inp = make_inputs(1, int(cu[-1]), H, dk, dv, dtype, seed=seed, backward=True,
                           cu_seqlens=cu, **kw)
         shape = "packed %s" % lens
     else:
         B, T = int(rng.integers(1, 4)), int(rng.integers(1, cap))
+        if T == 1:  # dlog_alpha would be zero by cancellation
+            kw["h0_std"] = 0.05
         inp = make_inputs(B, T, H, dk, dv, dtype, seed=seed, backward=True, **kw)
         shape = "dense B%d T%d" % (B, T)
     label = "random%d %s %d/%d H%d %s %s" % (seed, dtype, dk, dv, H, shape,
@@ -705,3 +709,35 @@ def test_random_cases_all_paths(G, oracle_mod, seed):
     check_bwd(G, oracle_mod, inp, TOL[dtype], label)
     check_saved(G, oracle_mod, inp, TOL[dtype], label)
     check_recurrent(G, oracle_mod, inp, TOL[dtype], label)
+
+
+@pytest.mark.parametrize("dtype,dk,dv,packed", [("f32", 64, 64, False), ("bf16", 256, 512, False),
+                                                ("bf16", 128, 128, True)])
+def test_one_token_sequences_without_state(G, oracle_mod, dtype, dk, dv, packed):
+    """Sequences of at most one token and no initial state: the entry state is
+    zero, so every term of dlog_alpha cancels and its exact value is zero
+    (the oracle returns exact zeros).  The kernels form those terms in fp32
+    and leave their rounding; the relative metric has no scale there, so the
+    residue is bounded by the tolerance times the size of the terms that
+    cancel (that of dbeta, whose terms are the same products of k, v and the
+    state gradient).  Every other gradient is compared as usual."""
+    if packed:
+        cu = torch.tensor([0, 1, 1, 2, 3], dtype=torch.int32)
+        inp = make_inputs(1, 3, 2, dk, dv, dtype, seed=91, backward=True, cu_seqlens=cu)
+    else:
+        inp = make_inputs(2, 1, 2, dk, dv, dtype, seed=91, backward=True)
+    d = to_dev(inp)
+    kw = dict(cu_seqlens=inp.get("cu_seqlens"))
+    ref = oracle_mod.bwd(inp["q"], inp["k"], inp["v"], inp["beta"], inp["log_alpha"], inp["dO"],
+                         dht=inp["dht"], **kw)
+    assert not np.any(np.asarray(ref["dlog_alpha"])), "the oracle's dlog_alpha is not zero"
+    scale = float(np.abs(np.asarray(ref["dbeta"])).max())
+    assert scale > 0
+    for label, r in (("stateless", run_bwd(G, d)), ("saved", run_saved(G, d)[2])):
+        say("one_token", dtype, dk, dv, packed, label)
+        for name in ("dq", "dk", "dv", "dbeta", "dh0"):
+            e = rel_err(f64(r[name]).reshape(ref[name].shape), ref[name])
+            assert e <= TOL[dtype], (label, name, e)
+        resid = float(np.abs(f64(r["dlog_alpha"])).max())
+        say("one_token", label, "dlog_alpha residue %.3g, scale %.3g" % (resid, scale))
+        assert resid <= TOL[dtype] * scale, (label, resid, scale)
