@@ -78,18 +78,20 @@ def path_flops(w, tokens_heads):
     return f * tokens_heads
 
 
-def path_bytes(w, tokens_heads, n_states, has_h0):
+def path_bytes(w, tokens_heads, n_states, has_h0, saved=True):
     """Algorithmic HBM bytes per step: every call reads its inputs and writes
     its outputs once.  Forward (2 dk + 2 dv) e + 8 per token-head (q, k, v, o,
     beta, log_alpha); backward (4 dk + 3 dv) e + 16 (q, k, v, dO in; dq, dk, dv
     out; gates in, gate gradients out); plus the fp32 states of every
-    (sequence, head): ht, h0 if given, and dht, dh0 for the backward."""
+    (sequence, head): h0 if given and ht for the forward, dht and dh0 for the
+    backward, and h0 again for the stateless backward (the saved backward
+    takes its states from the saved buffer)."""
     e = 4 if w.dtype == "f32" else 2
     dk, dv = w.dk, w.dv
     st = n_states * w.H * dk * dv * 4
     b = ((2 * dk + 2 * dv) * e + 8) * tokens_heads + st * (2 if has_h0 else 1)
     if w.backward:
-        b += ((4 * dk + 3 * dv) * e + 16) * tokens_heads + st * (3 if has_h0 else 2)
+        b += ((4 * dk + 3 * dv) * e + 16) * tokens_heads + st * (3 if has_h0 and not saved else 2)
     return b
 
 
@@ -863,7 +865,7 @@ def main():
         nbytes, flops = models["k_recurrent"]
     else:
         flops = path_flops(w, tokens_heads)
-        nbytes = path_bytes(w, tokens_heads, n_states, has_h0)
+        nbytes = path_bytes(w, tokens_heads, n_states, has_h0, saved=path == "saved")
     res = {
         "metric": METRIC if w.backward else (METRIC_RECURRENT if w.recurrent else METRIC_FWD),
         "value": tokens / (ms / 1e3),
