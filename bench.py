@@ -503,6 +503,10 @@ def fused_models(w, tokens_heads, n_units, has_h0):
     m["k_grad_block"] = m["k_grad"]
     m["k_block_fixup"] = (0, 0)
     m["k_conv_bwd"] = (2 * w.dv * 2 * tokens_heads, 0)
+    # at dk >= 128 the backward runs the plain gradient kernel (its dq, dk
+    # are intermediates there) and then the convolution backward of q and k,
+    # which reads xq, xk and writes dxq, dxk
+    m["k_conv_bwd_qk"] = (4 * w.dk * 2 * tokens_heads, 0)
     return m
 
 
@@ -514,11 +518,12 @@ def fused_step_bytes(w, tokens_heads, n_states, has_h0):
     the projections for q, k, v; the weights are a few kB).  Kept off HBM
     against the unfused composition, per token-head (e = 2): the read of the
     rule's q, k, v by the prep (the prologue wrote them; the fused prep writes
-    them once, for the backward) (2 dk + dv) e, and in the backward the rule's
-    dq and dk written and read back 4 dk e."""
+    them once, for the backward) (2 dk + dv) e, and at dk = 64, where the
+    prologue's backward runs inside the gradient kernel, the rule's dq and dk
+    written and read back 4 dk e."""
     e = 2
-    return (path_bytes(w, tokens_heads, n_states, has_h0),
-            (6 * w.dk + w.dv) * e * tokens_heads)
+    kept = 2 * w.dk + w.dv + (4 * w.dk if w.dk < 128 else 0)
+    return (path_bytes(w, tokens_heads, n_states, has_h0), kept * e * tokens_heads)
 
 
 def bench_fused_block(args):

@@ -289,7 +289,12 @@ gdn_status gdn_block_fwd_save(const gdn_problem *p,
  * (optional), dh0 (optional) as gdn_chunk_bwd_saved returns them.  Reads
  * the same prologue, the rule's q, k, v that gdn_block_fwd_save wrote, beta,
  * dO, dht (or NULL) and `saved` (unchanged).  `workspace` holds
- * gdn_block_bwd_saved_workspace_size(p, width) bytes. */
+ * gdn_block_bwd_saved_workspace_size(p, width) bytes.  At dk = 64 the
+ * prologue's backward of q and k runs inside the gradient kernel; at
+ * dk >= 128, where that kernel holds one workgroup per CU, the gradient
+ * kernel writes the rule's dq, dk into the workspace and the convolution
+ * backward of q and k follows (the faster of the two forms measured at each
+ * size; the results agree to rounding). */
 size_t gdn_block_bwd_saved_workspace_size(const gdn_problem *p, int width);
 gdn_status gdn_block_bwd_saved(const gdn_problem *p,
                                const gdn_block_prologue *pro, const void *q,
@@ -389,6 +394,12 @@ gdn_status gdn_recurrent_fwd_timed(const gdn_problem *p, const void *q,
  * for an unknown sequence.  Nothing is launched or dereferenced. */
 int32_t gdn_debug_audit(int32_t sequence, uint64_t present);
 const char *gdn_debug_audit_field(int32_t index);
+
+/* Which form gdn_block_bwd_saved runs, for tests of both at every size:
+ * 0 by dk (the default), 1 the prologue's backward inside the gradient
+ * kernel, 2 the gradient kernel then the convolution backward of q and k.
+ * Process-wide; returns the previous mode, or -1 for an unknown one. */
+int32_t gdn_debug_block_bwd(int32_t mode);
 
 /* Human-readable name of a status. */
 const char *gdn_status_string(gdn_status s);

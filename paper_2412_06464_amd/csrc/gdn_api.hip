@@ -1,6 +1,7 @@
 // C ABI of libgdn: argument validation, workspace carve-up and launch
 // sequencing.  Every check runs before the first launch; nothing here
 // allocates, frees or synchronises.
+#include <atomic>
 #include <stdint.h>
 #include <string.h>
 
@@ -255,10 +256,30 @@ void fill_prologue(const gdn_block_prologue* b, Args* a) {
 // then the rule's dv (the v prologue's input gradient), the q and k
 // prologue's side buffers and per-chunk weight gradients, and the v
 // prologue's per-chunk weight gradients.
+// Backward of the fused block at dk >= 128: the gradient kernel with the
+// prologue's backward inside holds one workgroup per CU there, and the plain
+// gradient kernel followed by the standalone convolution backward of q and k
+// measured faster; at dk = 64 the fused kernel is the faster.  A test can
+// force either form (gdn_debug_block_bwd).
+std::atomic<int> block_bwd_mode{0};  // 0: by dk, 1: fused, 2: composed
+
+bool block_bwd_composed(const gdn_problem* p) {
+  const int m = block_bwd_mode.load();
+  return m == 2 || (m == 0 && p->dk >= 128);
+}
+
+// dyqk (when given) receives the two buffers of the composed form's rule
+// gradients dq, dk.
 size_t carve_block_bwd(const gdn_problem* p, const Shape& s, int width, unsigned char* base,
-                       Args* a, gdn::ConvArgs* cv) {
+                       Args* a, gdn::ConvArgs* cv, unsigned char** dyqk = nullptr) {
   Carver c{base, carve(p, s, Use::BwdSaved, base, a)};
   const size_t NCH = (size_t)s.NC * p->H, NS = (size_t)((s.NC + 255) / 256);
+  unsigned char* dyq = c.take((size_t)s.Ttot * p->H * p->dk * s.esz);
+  unsigned char* dyk = c.take((size_t)s.Ttot * p->H * p->dk * s.esz);
+  if (dyqk) {
+    dyqk[0] = dyq;
+    dyqk[1] = dyk;
+  }
   unsigned char* dyv = c.take((size_t)s.Ttot * p->H * p->dv * s.esz);
   unsigned char* head = c.take(2 * NCH * 3 * p->dk * sizeof(float));
   unsigned char* tail = c.take(2 * NCH * 3 * p->dk * sizeof(float));
@@ -709,7 +730,9 @@ gdn_status gdn_block_bwd_saved_timed(const gdn_problem* p, const gdn_block_prolo
   gdn::ConvArgs cv;
   memset(&cv, 0, sizeof cv);
   fill_common(p, s, &a);
-  carve_block_bwd(p, s, pro->width, (unsigned char*)workspace, &a, &cv);
+  unsigned char* dyqk[2];
+  carve_block_bwd(p, s, pro->width, (unsigned char*)workspace, &a, &cv, dyqk);
+  const bool composed = block_bwd_composed(p);
   Carver c{(unsigned char*)const_cast<void*>(saved)};
   carve_saved(p, s, c, &a);
   fill_prologue(pro, &a);
@@ -739,9 +762,35 @@ gdn_status gdn_block_bwd_saved_timed(const gdn_problem* p, const gdn_block_prolo
   cv.w = pro->wv;
   cv.dx = dxv;
   cv.dw = dwv;
+  // the composed form: the rule's dq, dk into the workspace, then the
+  // convolution backward of q and k (with L2) on them; the per-chunk weight
+  // partials of q and k reuse the fused form's buffers
+  gdn::ConvArgs cq = cv, ck = cv;
+  if (composed) {
+    a.dq = dyqk[0];
+    a.dk = dyqk[1];
+    const size_t per = (size_t)s.NC * p->H * p->dk * pro->width;
+    cq.l2 = ck.l2 = 1;
+    cq.x = pro->xq;
+    cq.w = pro->wq;
+    cq.dy = dyqk[0];
+    cq.dx = dxq;
+    cq.dw = dwq;
+    cq.part = a.bpart;
+    cq.tmp = a.btmp;
+    ck.x = pro->xk;
+    ck.w = pro->wk;
+    ck.dy = dyqk[1];
+    ck.dx = dxk;
+    ck.dw = dwk;
+    ck.part = a.bpart + per;
+    ck.tmp = a.btmp;
+  }
   TimingGuard tg(timing);
-  const hipError_t e =
-      gdn::launch_block_bwd_saved(p->dk, p->dv, a, cv, (hipStream_t)stream, tg.get());
+  const hipError_t e = gdn::launch_block_bwd_saved(p->dk, p->dv, a, cv,
+                                                   composed ? &cq : nullptr,
+                                                   composed ? &ck : nullptr,
+                                                   (hipStream_t)stream, tg.get());
   return e == hipSuccess ? GDN_OK : GDN_ERR_HIP;
 }
 
@@ -895,6 +944,11 @@ const char* gdn_status_string(gdn_status s) {
     case GDN_ERR_VALUE: return "GDN_ERR_VALUE: a scalar argument is out of range";
   }
   return "GDN: unknown status";
+}
+
+int gdn_debug_block_bwd(int mode) {
+  if (mode < 0 || mode > 2) return -1;
+  return block_bwd_mode.exchange(mode);
 }
 
 int gdn_debug_audit(int sequence, uint64_t present) {

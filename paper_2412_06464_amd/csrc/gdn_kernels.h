@@ -156,7 +156,8 @@ hipError_t launch_bwd_saved(Dt dt, int dk, int dv, const Args& a, hipStream_t s,
 // backward with the q and k prologue folded into the gradient kernel, then
 // the v prologue's backward (cv, on the rule's dv).
 hipError_t launch_block_bwd_saved(int dk, int dv, const Args& a, const ConvArgs& cv,
-                                  hipStream_t s, Timing* t);
+                                  const ConvArgs* cq, const ConvArgs* ck, hipStream_t s,
+                                  Timing* t);
 hipError_t launch_recurrent_fwd(Dt dt, int dk, int dv, const Args& a, hipStream_t s, Timing* t);
 
 // Call a lambda templated on (element type, dk, dv) for the supported

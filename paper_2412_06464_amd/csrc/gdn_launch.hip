@@ -183,7 +183,8 @@ hipError_t launch_bwd_saved(Dt dt, int dk, int dv, const Args& a, hipStream_t s,
 // across chunk boundaries and sums dw, and the v prologue's backward runs
 // on the rule's dv.
 hipError_t launch_block_bwd_saved(int dk, int dv, const Args& a, const ConvArgs& cv,
-                                  hipStream_t s, Timing* t) {
+                                  const ConvArgs* cq, const ConvArgs* ck, hipStream_t s,
+                                  Timing* t) {
   if (audit(Seq::BlockBwdSaved, a) >= 0) return hipErrorInvalidValue;
   hipError_t e;
   if ((e = timed(t, "k_chunk_table", s, [&] { return launch_chunk_table(a, s); })) != hipSuccess)
@@ -191,12 +192,25 @@ hipError_t launch_block_bwd_saved(int dk, int dv, const Args& a, const ConvArgs&
   if ((e = timed(t, "k_bwd_seq", s, [&] { return launch_bwd_seq(Dt::BF16, dk, dv, a, s); })) !=
       hipSuccess)
     return e;
-  if ((e = timed(t, "k_grad_block", s,
-                 [&] { return launch_grad(Dt::BF16, dk, dv, a, s, true); })) != hipSuccess)
-    return e;
-  if ((e = timed(t, "k_block_fixup", s, [&] { return launch_block_fixup(dk, a, s); })) !=
-      hipSuccess)
-    return e;
+  if (cq && ck) {  // composed: the rule's dq, dk, then the prologue's backward of q and k
+    if (!a.dq || !a.dk || !cq->dy || !ck->dy || !cq->part || !ck->part || !cq->tmp)
+      return hipErrorInvalidValue;
+    if ((e = timed(t, "k_grad", s, [&] { return launch_grad(Dt::BF16, dk, dv, a, s, false); })) !=
+        hipSuccess)
+      return e;
+    if ((e = timed(t, "k_conv_bwd_qk", s, [&] {
+           hipError_t r = launch_conv_bwd(Dt::BF16, dk, *cq, s);
+           return r == hipSuccess ? launch_conv_bwd(Dt::BF16, dk, *ck, s) : r;
+         })) != hipSuccess)
+      return e;
+  } else {
+    if ((e = timed(t, "k_grad_block", s,
+                   [&] { return launch_grad(Dt::BF16, dk, dv, a, s, true); })) != hipSuccess)
+      return e;
+    if ((e = timed(t, "k_block_fixup", s, [&] { return launch_block_fixup(dk, a, s); })) !=
+        hipSuccess)
+      return e;
+  }
   return timed(t, "k_conv_bwd", s, [&] { return launch_conv_bwd(Dt::BF16, dv, cv, s); });
 }
 

@@ -30,7 +30,7 @@ EXPORTS = ("gdn_chunk_fwd", "gdn_chunk_bwd", "gdn_chunk_fwd_workspace_size",
            "gdn_block_fwd", "gdn_block_fwd_save", "gdn_block_bwd_saved",
            "gdn_block_bwd_saved_workspace_size", "gdn_block_fwd_timed",
            "gdn_block_fwd_save_timed", "gdn_block_bwd_saved_timed", "gdn_debug_audit",
-           "gdn_debug_audit_field")
+           "gdn_debug_audit_field", "gdn_debug_block_bwd")
 # bytes of the library's static workspace behind gdn_chunk_fwd_noalloc
 NOALLOC_SCRATCH_BYTES = 64 << 20
 
@@ -172,6 +172,8 @@ def load_library():
         lib.gdn_debug_audit.restype = ctypes.c_int32
         lib.gdn_debug_audit_field.argtypes = [ctypes.c_int32]
         lib.gdn_debug_audit_field.restype = ctypes.c_char_p
+        lib.gdn_debug_block_bwd.argtypes = [ctypes.c_int32]
+        lib.gdn_debug_block_bwd.restype = ctypes.c_int32
         lib.gdn_status_string.argtypes = [ctypes.c_int]
         lib.gdn_status_string.restype = ctypes.c_char_p
         _lib = lib

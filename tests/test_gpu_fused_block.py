@@ -205,3 +205,24 @@ def test_fused_block_random(G, refs, seed):
             h0_std = 0.02
         inp = fused_inputs(B, T, H, dk, dv, seed=100 + seed, width=width, h0_std=h0_std)
     compare(G, refs, inp, "fused_random%d" % seed)
+
+
+@pytest.mark.parametrize("mode", [1, 2])
+@pytest.mark.parametrize("dk,dv,packed", [(64, 64, False), (64, 64, True), (128, 128, False),
+                                          (128, 128, True), (256, 512, False), (256, 512, True)])
+def test_fused_block_both_backward_forms(G, refs, mode, dk, dv, packed):
+    """The saved backward's two forms at every size: the prologue's backward
+    of q and k inside the gradient kernel (1) and the gradient kernel then
+    the convolution backward (2); by default dk picks one."""
+    lib = G.load_library()
+    if packed:
+        lens = [1, 2, 65, 64, 70]
+        cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+        inp = fused_inputs(1, int(cu[-1]), 2, dk, dv, seed=41, cu=cu)
+    else:
+        inp = fused_inputs(2, 150, 2, dk, dv, seed=41)
+    prev = lib.gdn_debug_block_bwd(mode)
+    try:
+        compare(G, refs, inp, "fused_form%d_%d_%d%s" % (mode, dk, dv, "_packed" if packed else ""))
+    finally:
+        lib.gdn_debug_block_bwd(prev)
